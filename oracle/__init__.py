@@ -1,0 +1,118 @@
+"""Double-precision CPU oracle for the Sliding Window Recurrence.
+
+TEST INFRASTRUCTURE ONLY: the plain, slow, obviously correct checker the GPU
+library is compared against.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import it.  It shares no code with the
+HIP library (``paper_2512_13921_amd``) and never imports it.
+
+The arithmetic lives in ``swr_oracle.c`` (see its header for the definition and
+the paper passages it follows); this module only marshals numpy arrays.
+
+Tensor layout at this level is the library's: ``x, b, c, y, dy, ...`` are
+``[B, T, H, D]``; ``a`` is ``[B, T, H]`` (decay shared by a head's D channels,
+Sec. 5) or ``[B, T, H, D]`` (per-channel decay).  Inputs of any float dtype are
+converted to float64 first.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+RESIDUAL = 1
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if _build.is_stale():
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        i64 = ctypes.c_int64
+        ci = ctypes.c_int
+        for name, nin, nout in (("swr_oracle_forward_slice", 4, 1),
+                                ("swr_oracle_backward_slice", 5, 4),
+                                ("swr_oracle_forward", 4, 1),
+                                ("swr_oracle_backward", 5, 4)):
+            fn = getattr(lib, name)
+            lead = [i64] if not name.endswith("_slice") else []
+            fn.argtypes = lead + [i64, i64, i64, ci, ci] + [dp] * (nin + nout)
+            fn.restype = ci
+        lib.swr_oracle_max_threads.restype = ci
+        _lib = lib
+    return _lib
+
+
+def _ptr(arr):
+    return arr.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _c64(arr):
+    return np.ascontiguousarray(arr, dtype=np.float64)
+
+
+def max_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().swr_oracle_max_threads())
+
+
+def forward_slices(x, a, b, c, block, residual=False):
+    """Forward on independent slices: x, b, c are [S, T, D]; a is [S, T] or [S, T, D]."""
+    lib = _load()
+    x, a, b, c = _c64(x), _c64(a), _c64(b), _c64(c)
+    S, T, D = x.shape
+    apc = int(a.ndim == 3)
+    y = np.empty((S, T, D), np.float64)
+    rc = lib.swr_oracle_forward(S, T, D, int(block), apc, RESIDUAL if residual else 0,
+                                _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle forward rejected its arguments")
+    return y
+
+
+def backward_slices(x, a, b, c, dy, block, residual=False):
+    """Backward on independent slices; returns (dx, da, db, dc) with da shaped like a."""
+    lib = _load()
+    x, a, b, c, dy = _c64(x), _c64(a), _c64(b), _c64(c), _c64(dy)
+    S, T, D = x.shape
+    apc = int(a.ndim == 3)
+    dx, db, dc = (np.empty((S, T, D), np.float64) for _ in range(3))
+    da = np.empty(a.shape, np.float64)
+    rc = lib.swr_oracle_backward(S, T, D, int(block), apc, RESIDUAL if residual else 0,
+                                 _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
+                                 _ptr(dx), _ptr(da), _ptr(db), _ptr(dc))
+    if rc != 0:
+        raise ValueError("oracle backward rejected its arguments")
+    return dx, da, db, dc
+
+
+def _to_slices(t):
+    # [B, T, H, ...] -> [B*H, T, ...]
+    t = np.asarray(t)
+    B, T, H = t.shape[:3]
+    return np.moveaxis(t, 2, 1).reshape((B * H, T) + t.shape[3:])
+
+
+def _from_slices(t, B, H):
+    S, T = t.shape[:2]
+    return np.moveaxis(t.reshape((B, H, T) + t.shape[2:]), 1, 2)
+
+
+def forward(x, a, b, c, block, residual=False):
+    """y = SWR(x, a, b, c) for [B, T, H, D] tensors (a: [B, T, H] or [B, T, H, D])."""
+    B, T, H, D = np.shape(x)
+    y = forward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c),
+                       block, residual)
+    return _from_slices(y, B, H)
+
+
+def backward(x, a, b, c, dy, block, residual=False):
+    """(dx, da, db, dc) for [B, T, H, D] tensors; da has the shape of a."""
+    B, T, H, D = np.shape(x)
+    outs = backward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c),
+                           _to_slices(dy), block, residual)
+    return tuple(_from_slices(o, B, H) for o in outs)

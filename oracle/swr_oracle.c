@@ -1,0 +1,154 @@
+/*
+ * swr_oracle.c -- plain double-precision CPU oracle for the Sliding Window
+ * Recurrence (test infrastructure only; see swr_oracle.h for the definition,
+ * the layouts and who may use this file).
+ *
+ * Nothing here is blocked, fused or reordered: the forward walks every block's
+ * window token by token (the recurrence of Sec. 3, eq. (2.1), restarted from
+ * zero state at the start of the previous block, which is what the truncation
+ * T ~ I_b of Sec. 4.2 keeps), and the backward walks the same windows in
+ * reverse, accumulating the chain rule of that loop.
+ */
+#include "swr_oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Decay coefficient of token m, channel mu. */
+static double decay(const double* a, int a_per_channel, int64_t D, int64_t m, int64_t mu) {
+    return a_per_channel ? a[m * D + mu] : a[m];
+}
+
+static int bad_args(int64_t T, int64_t D, int64_t block) {
+    return T < 0 || D < 1 || block < 1;
+}
+
+int swr_oracle_forward_slice(int64_t T, int64_t D, int64_t block, int a_per_channel,
+                             int flags, const double* x, const double* a,
+                             const double* b, const double* c, double* y) {
+    if (bad_args(T, D, block)) return -1;
+    if (T == 0) return 0;
+    if (!x || !a || !b || !c || !y) return -1;
+    double* s = (double*)malloc((size_t)D * sizeof(double));
+    if (!s) return -1;
+    const int64_t nblocks = (T + block - 1) / block;
+    for (int64_t tau = 0; tau < nblocks; ++tau) {
+        /* Window of block tau: the previous block (if any) and block tau itself. */
+        const int64_t first = tau * block;
+        const int64_t start = (tau > 0 ? tau - 1 : 0) * block;
+        const int64_t end = (first + block < T) ? first + block : T;
+        for (int64_t mu = 0; mu < D; ++mu) s[mu] = 0.0;
+        for (int64_t m = start; m < end; ++m) {
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu;
+                s[mu] = decay(a, a_per_channel, D, m, mu) * s[mu] + b[e] * x[e];
+                if (m >= first) {
+                    y[e] = c[e] * s[mu];
+                    if (flags & SWR_ORACLE_RESIDUAL) y[e] += x[e];
+                }
+            }
+        }
+    }
+    free(s);
+    return 0;
+}
+
+int swr_oracle_backward_slice(int64_t T, int64_t D, int64_t block, int a_per_channel,
+                              int flags, const double* x, const double* a,
+                              const double* b, const double* c, const double* dy,
+                              double* dx, double* da, double* db, double* dc) {
+    if (bad_args(T, D, block)) return -1;
+    if (T == 0) return 0;
+    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return -1;
+    const int64_t win = 2 * block; /* longest window */
+    double* du = (double*)calloc((size_t)(T * D), sizeof(double));
+    double* pre = (double*)malloc((size_t)(win * D) * sizeof(double));
+    double* post = (double*)malloc((size_t)(win * D) * sizeof(double));
+    double* lam = (double*)malloc((size_t)D * sizeof(double));
+    if (!du || !pre || !post || !lam) {
+        free(du); free(pre); free(post); free(lam);
+        return -1;
+    }
+    memset(da, 0, (size_t)(a_per_channel ? T * D : T) * sizeof(double));
+
+    const int64_t nblocks = (T + block - 1) / block;
+    for (int64_t tau = 0; tau < nblocks; ++tau) {
+        const int64_t first = tau * block;
+        const int64_t start = (tau > 0 ? tau - 1 : 0) * block;
+        const int64_t end = (first + block < T) ? first + block : T;
+        /* Re-run the window, keeping each step's incoming and outgoing state. */
+        for (int64_t mu = 0; mu < D; ++mu) lam[mu] = 0.0; /* lam doubles as the state here */
+        for (int64_t m = start; m < end; ++m) {
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu, w = (m - start) * D + mu;
+                pre[w] = lam[mu];
+                lam[mu] = decay(a, a_per_channel, D, m, mu) * lam[mu] + b[e] * x[e];
+                post[w] = lam[mu];
+            }
+        }
+        /* Reverse sweep: lam is d(loss)/d(state after step m). */
+        for (int64_t mu = 0; mu < D; ++mu) lam[mu] = 0.0;
+        for (int64_t m = end - 1; m >= start; --m) {
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu, w = (m - start) * D + mu;
+                if (m >= first) {            /* y_m = c_m * state_m belongs to this window */
+                    lam[mu] += c[e] * dy[e];
+                    dc[e] = dy[e] * post[w];
+                }
+                du[e] += lam[mu];            /* d state_m / d u_m = 1          */
+                if (a_per_channel)           /* d state_m / d a_m = state_{m-1} */
+                    da[e] += lam[mu] * pre[w];
+                else
+                    da[m] += lam[mu] * pre[w];
+                lam[mu] *= decay(a, a_per_channel, D, m, mu); /* d state_m / d state_{m-1} */
+            }
+        }
+    }
+    /* u = b * x: chain rule into the two gates; the residual adds dy to dx. */
+    for (int64_t e = 0; e < T * D; ++e) {
+        dx[e] = b[e] * du[e];
+        if (flags & SWR_ORACLE_RESIDUAL) dx[e] += dy[e];
+        db[e] = x[e] * du[e];
+    }
+    free(du); free(pre); free(post); free(lam);
+    return 0;
+}
+
+int swr_oracle_forward(int64_t S, int64_t T, int64_t D, int64_t block, int a_per_channel,
+                       int flags, const double* x, const double* a, const double* b,
+                       const double* c, double* y) {
+    if (S < 0 || bad_args(T, D, block)) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_forward_slice(T, D, block, a_per_channel, flags, x + s * n, a + s * na,
+                                        b + s * n, c + s * n, y + s * n) != 0;
+    return err ? -1 : 0;
+}
+
+int swr_oracle_backward(int64_t S, int64_t T, int64_t D, int64_t block, int a_per_channel,
+                        int flags, const double* x, const double* a, const double* b,
+                        const double* c, const double* dy, double* dx, double* da,
+                        double* db, double* dc) {
+    if (S < 0 || bad_args(T, D, block)) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_backward_slice(T, D, block, a_per_channel, flags, x + s * n,
+                                         a + s * na, b + s * n, c + s * n, dy + s * n,
+                                         dx + s * n, da + s * na, db + s * n, dc + s * n) != 0;
+    return err ? -1 : 0;
+}
+
+int swr_oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

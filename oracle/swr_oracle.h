@@ -1,0 +1,70 @@
+/*
+ * swr_oracle.h -- reference (oracle) implementation of the Sliding Window
+ * Recurrence, forward and backward, in plain C and double precision.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library is the slow, obviously correct
+ * checker that the GPU path is compared against.  Only the test-suite, the
+ * smoke check and the CPU-baseline leg of the benchmark may load it.  It shares
+ * no code, header, table or helper with the HIP library.
+ *
+ * What it computes (Sliding Window Recurrences, Sec. 4.2, eqs. for the
+ * truncated operator  L~ = calL + G Z_b R  and its block-bidiagonal form):
+ * for one (batch, head) slice with T tokens, D channels and block size l,
+ * token i (0-based) sits in block tau(i) = floor(i / l) and its window starts at
+ * s(i) = l * max(tau(i) - 1, 0).  The state is the scalar recurrence of
+ * Sec. 3, eq. (2.1),  h_m = a_m h_{m-1} + u_m,  restarted from zero state at s(i):
+ *
+ *     h~_i = sum_{j = s(i)}^{i} ( prod_{m = j+1}^{i} a_m ) * u_j ,   u = b (*) x
+ *     y_i  = c_i (*) h~_i      (+ x_i when the residual flag is set, Sec. 5
+ *                               "post-gate with residual")
+ *
+ * The forward is literally that restarted loop, one block at a time.  The
+ * backward is the exact reverse-mode adjoint of the same loop (the paper gives
+ * no backward pass; this is the gradient of the truncated forward).
+ *
+ * Layouts (per slice, row-major doubles): x, b, c, y, dy, dx, db, dc are
+ * [T][D].  a and da are [T] when the decay is shared by the head's D channels
+ * (the paper's Phalanx parametrisation, Sec. 5), or [T][D] when per-channel.
+ * A last block shorter than l is allowed (equivalent to zero-padding the
+ * inputs at the end, Sec. 3.2 assumes n = b*l "for simplicity").
+ */
+#ifndef SWR_ORACLE_H
+#define SWR_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SWR_ORACLE_RESIDUAL 1
+
+/* One slice.  Returns 0, or -1 on a bad argument (T < 0, D < 1, block < 1, NULL). */
+int swr_oracle_forward_slice(int64_t T, int64_t D, int64_t block, int a_per_channel,
+                             int flags, const double* x, const double* a,
+                             const double* b, const double* c, double* y);
+
+/* Gradients of the slice's forward w.r.t. x, a, b, c given dy.  Outputs are
+ * overwritten.  da has the shape of a. */
+int swr_oracle_backward_slice(int64_t T, int64_t D, int64_t block, int a_per_channel,
+                              int flags, const double* x, const double* a,
+                              const double* b, const double* c, const double* dy,
+                              double* dx, double* da, double* db, double* dc);
+
+/* S independent slices stored back to back ([S][T][D], a as [S][T] or
+ * [S][T][D]); slices run in parallel over OpenMP threads.  Returns 0 or -1. */
+int swr_oracle_forward(int64_t S, int64_t T, int64_t D, int64_t block, int a_per_channel,
+                       int flags, const double* x, const double* a, const double* b,
+                       const double* c, double* y);
+int swr_oracle_backward(int64_t S, int64_t T, int64_t D, int64_t block, int a_per_channel,
+                        int flags, const double* x, const double* a, const double* b,
+                        const double* c, const double* dy, double* dx, double* da,
+                        double* db, double* dc);
+
+/* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
+int swr_oracle_max_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

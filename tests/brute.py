@@ -1,0 +1,145 @@
+"""Brute-force constructions used to pin the oracle (tiny inputs only).
+
+Each function re-derives the Sliding Window Recurrence from a *different*
+statement in the paper than the oracle's restarted loop, so that a mistake in
+either shows up as a disagreement:
+
+* ``dense_L``          -- the transfer operator entry by entry, L_ij = a_{i:j+1}
+                          (Sec. 3, eqs. (2.2)-(2.3) and the entry formula after them).
+* ``dense_L_neumann``  -- the same operator as the finite Neumann series
+                          sum_k (AZ)^k (Sec. 3, eq. (2.3)).
+* ``dense_Ltilde``     -- the jagged operator assembled from its hierarchical
+                          pieces, calL + G Z_b R (Sec. 4.2, truncated
+                          factorisation), with each L_t = (I - A_t Z)^{-1}
+                          obtained by a linear solve (Sec. 3.2, intra-block
+                          operator), g_t the block's cumulative products and
+                          r_t^T = e_l^T L_t (Sec. 3.2, carrier definitions).
+* ``window_sum``       -- the explicit sum of decay products over each token's
+                          window.
+* ``torch_forward``    -- a differentiable float64 torch version of
+                          ``window_sum`` whose autograd gradients pin the
+                          oracle's backward.
+Everything is float64.  Sizes must be tiny (the dense builders are O(T^2)).
+"""
+import numpy as np
+
+
+def decay_product(a, i, j):
+    """a_{i:j+1} = a_i a_{i-1} ... a_{j+1}; 1 when j == i; 0 when j > i."""
+    if j > i:
+        return 0.0
+    p = 1.0
+    for m in range(j + 1, i + 1):
+        p *= a[m]
+    return p
+
+
+def dense_L(a):
+    """Full (untruncated) transfer operator, entry by entry."""
+    a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    L = np.zeros((n, n))
+    for i in range(n):
+        for j in range(i + 1):
+            L[i, j] = decay_product(a, i, j)
+    return L
+
+
+def dense_L_neumann(a):
+    """Full transfer operator as I + AZ + (AZ)^2 + ... + (AZ)^{n-1}."""
+    a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    AZ = np.diag(a) @ np.eye(n, k=-1)
+    L = np.zeros((n, n))
+    P = np.eye(n)
+    for _ in range(n):
+        L += P
+        P = P @ AZ
+    return L
+
+
+def window_start(i, block):
+    return block * max(i // block - 1, 0)
+
+
+def dense_Ltilde(a, block):
+    """Jagged-window operator calL + G Z_b R for a (1-D) decay sequence.
+
+    A last block shorter than ``block`` is handled by zero-padding to a whole
+    number of blocks and truncating the result (the padding sits after every
+    real token, so it cannot reach them)."""
+    a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    nb = -(-n // block)
+    N = nb * block
+    ap = np.zeros(N)
+    ap[:n] = a
+    calL = np.zeros((N, N))
+    G = np.zeros((N, nb))
+    R = np.zeros((nb, N))
+    Zl = np.eye(block, k=-1)
+    for t in range(nb):
+        sl = slice(t * block, (t + 1) * block)
+        at = ap[sl]
+        Lt = np.linalg.solve(np.eye(block) - np.diag(at) @ Zl, np.eye(block))
+        calL[sl, sl] = Lt
+        G[sl, t] = np.cumprod(at)            # (a_{t,1}, a_{t,2:1}, ..., a_{t,l:1})
+        R[t, sl] = Lt[block - 1, :]          # e_l^T L_t
+    Zb = np.eye(nb, k=-1)
+    Lt_full = calL + G @ Zb @ R
+    return Lt_full[:n, :n]
+
+
+def window_sum(a, u, block):
+    """h~_i = sum_{j=s(i)}^{i} a_{i:j+1} u_j for u of shape [T, D] and a of
+    shape [T] (shared decay) or [T, D] (per-channel decay)."""
+    a = np.asarray(a, np.float64)
+    u = np.asarray(u, np.float64)
+    T, D = u.shape
+    h = np.zeros((T, D))
+    for i in range(T):
+        for j in range(window_start(i, block), i + 1):
+            for mu in range(D):
+                aa = a if a.ndim == 1 else a[:, mu]
+                h[i, mu] += decay_product(aa, i, j) * u[j, mu]
+    return h
+
+
+def swr_slice(x, a, b, c, block, residual=False):
+    """Forward of one slice through the explicit window sum."""
+    x = np.asarray(x, np.float64)
+    h = window_sum(a, np.asarray(b, np.float64) * x, block)
+    y = np.asarray(c, np.float64) * h
+    return y + x if residual else y
+
+
+def torch_forward(x, a, b, c, block, residual=False, truncated=True):
+    """Differentiable float64 forward of one slice (torch CPU), built from the
+    explicit products.  ``truncated=False`` gives the untruncated recurrence."""
+    import torch
+    T, D = x.shape
+    u = b * x
+    rows = []
+    for i in range(T):
+        j0 = window_start(i, block) if truncated else 0
+        acc = torch.zeros(D, dtype=torch.float64)
+        for j in range(j0, i + 1):
+            if a.dim() == 1:
+                w = torch.prod(a[j + 1:i + 1]) if i > j else torch.ones((), dtype=torch.float64)
+            else:
+                w = torch.prod(a[j + 1:i + 1], dim=0) if i > j else torch.ones(D, dtype=torch.float64)
+            acc = acc + w * u[j]
+        rows.append(acc)
+    h = torch.stack(rows)
+    y = c * h
+    return y + x if residual else y
+
+
+def torch_grads(x, a, b, c, dy, block, residual=False, truncated=True):
+    """(dx, da, db, dc) of sum(dy * forward) by torch autograd, as numpy."""
+    import torch
+    ts = [torch.tensor(np.asarray(v, np.float64), requires_grad=True) for v in (x, a, b, c)]
+    y = torch_forward(*ts, block, residual=residual, truncated=truncated)
+    (y * torch.tensor(np.asarray(dy, np.float64))).sum().backward()
+    # a leaf that no product touched (T = 1) gets no .grad: its gradient is 0
+    return tuple(t.grad.numpy() if t.grad is not None else np.zeros(t.shape) for t in ts)
