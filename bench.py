@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Benchmark of the Sliding Window Recurrence hot path on one MI355X.
+
+One step = one forward (swr_forward) and one backward (swr_backward) pass over
+the whole workload, inputs already resident in HBM.  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+
+Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
+durations come from HIP events recorded on the stream the kernels run on.
+The roofline entry reports the dominant kernel's algorithmic HBM bytes per
+launch (every input read once, every output written once) divided by its
+average duration, against the MI355X's 8 TB/s.  The CPU baseline times the
+double-precision oracle on a bounded sample of the same workload on this
+machine's host cores.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+METRIC = "SWR fwd+bwd tokens/sec and achieved HBM GB/s at B=8,H=16,d=128,T=16384"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak
+BF16_MFMA_PEAK_TFLOPS = 2500.0 # dense bf16 MFMA peak
+F32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(cfg, backward):
+    """HBM bytes one launch must move: inputs read once, outputs written once."""
+    e = 2 if cfg.dtype == "bf16" else 4
+    th = cfg.B * cfg.T * cfg.H
+    if backward:   # x, b, c, dy, a in; dx, db, dc out; da out in fp32
+        return th * (e * (7 * cfg.D + 1) + 4)
+    return th * e * (4 * cfg.D + 1)   # x, b, c, a in; y out
+
+
+def contraction_flops(cfg, backward):
+    """Dense flops of the intra-block contractions (16x16 sub-block tiles):
+    2 * 16 * D per token-head per contraction; the backward runs three
+    (forward recompute, reverse solve, look-ahead reverse solve)."""
+    per = 2 * 16 * cfg.D * cfg.B * cfg.T * cfg.H
+    return per * (3 if backward else 1)
+
+
+def to_device(arr, dtype):
+    import torch
+    if dtype == "bf16":
+        bits = W.f32_to_bf16_bits(arr).view(np.int16)
+        return torch.from_numpy(bits).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
+
+
+def cpu_baseline(cfg, prob, budget_s=10.0):
+    """Oracle throughput on whole (batch, head) slices of the workload, in
+    tokens/s of the full job (a token carries all H heads)."""
+    import oracle
+    threads = oracle.max_threads()
+    nslices = cfg.B * cfg.H
+    batch = max(1, min(threads, nslices))
+    done, elapsed = 0, 0.0
+    order = np.random.default_rng(0).permutation(nslices)
+    while done < nslices and (elapsed < budget_s or done == 0):
+        idx = order[done:done + batch]
+        bi, hi = idx // cfg.H, idx % cfg.H
+
+        def take(t):
+            return np.ascontiguousarray(np.asarray(t)[bi, :, hi], dtype=np.float64)
+
+        xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
+        t0 = time.perf_counter()
+        oracle.forward_slices(xs, as_, bs, cs, cfg.block)
+        oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
+        elapsed += time.perf_counter() - t0
+        done += len(idx)
+    token_heads = done * cfg.T
+    return {
+        "value": token_heads / cfg.H / elapsed,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{done} of {nslices} (batch, head) slices at full T={cfg.T}, forward+backward, "
+                  f"float64, OpenMP over slices; {elapsed:.1f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=W.HEADLINE, choices=sorted(W.CONFIGS))
+    ap.add_argument("--run-len", type=int, default=0, help="tokens per workgroup run (0 = library default)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the SWR hot path here runs on a single MI355X "
+              "and has no multi-GPU path (use --gpus 1).", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2512_13921_amd as swr
+
+    if not torch.cuda.is_available():
+        print("no GPU visible: bench.py needs an MI355X", file=sys.stderr)
+        return 1
+    swr.load()
+
+    cfg = W.CONFIGS[args.config]
+    if not cfg.backward:
+        cfg = cfg.with_(backward=True)
+    log(f"[bench] workload {cfg.name}: generating inputs")
+    prob = W.generate(cfg)
+    x, a, b, c, dy = (to_device(getattr(prob, n), cfg.dtype) for n in ("x", "a", "b", "c", "dy"))
+    y = torch.empty_like(x)
+    dx, db, dc = (torch.empty_like(x) for _ in range(3))
+    da = torch.empty(a.shape, dtype=torch.float32, device=a.device)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        swr.swr_forward(x, a, b, c, cfg.block, y=y, run_len=args.run_len)
+        if ev is not None:
+            ev[1].record(stream)
+        swr.swr_backward(x, a, b, c, dy, cfg.block, outputs=(dx, da, db, dc), run_len=args.run_len)
+        if ev is not None:
+            ev[2].record(stream)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+
+    fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    bwd_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    total_ms = float(events[0][0].elapsed_time(events[-1][2]))
+    ms_per_step = total_ms / args.steps
+    tokens = cfg.B * cfg.T
+    value = tokens / (ms_per_step * 1e-3)
+
+    fb, bb = algorithmic_bytes(cfg, False), algorithmic_bytes(cfg, True)
+    f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
+    dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
+    dom_gbs = b_gbs if dominant_bwd else f_gbs
+    mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
+
+    run_len, fwg, bwg = swr.swr_launch_info(swr.make_problem(
+        cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
+        x.stride()[:3], a.stride(), False, args.run_len))
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded host draws, rounded to the I/O dtype)",
+        "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
+                   "block": cfg.block, "global_batch": cfg.B, "seq_len": cfg.T,
+                   "parallelism": "single GPU", "run_len": run_len, "workgroups": fwg},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "swr_bwd_kernel" if dominant_bwd else "swr_fwd_kernel",
+            "achieved": dom_gbs,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": dom_gbs / HBM_PEAK_GBS,
+            "traffic": None,
+        },
+        "kernels": {
+            "forward": {"ms": float(fwd_ms.mean()), "ms_min": float(fwd_ms.min()),
+                        "algorithmic_bytes": fb, "GB/s": f_gbs, "frac_hbm": f_gbs / HBM_PEAK_GBS,
+                        "mfma_tflops": contraction_flops(cfg, False) / (fwd_ms.mean() * 1e-3) / 1e12,
+                        "tokens_per_s": tokens / (fwd_ms.mean() * 1e-3)},
+            "backward": {"ms": float(bwd_ms.mean()), "ms_min": float(bwd_ms.min()),
+                         "algorithmic_bytes": bb, "GB/s": b_gbs, "frac_hbm": b_gbs / HBM_PEAK_GBS,
+                         "mfma_tflops": contraction_flops(cfg, True) / (bwd_ms.mean() * 1e-3) / 1e12,
+                         "tokens_per_s": tokens / (bwd_ms.mean() * 1e-3)},
+            "mfma_peak_tflops": mfma_peak,
+            "wall_s_timed": t_wall,
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(cfg, prob)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

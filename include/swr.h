@@ -1,0 +1,119 @@
+/*
+ * swr.h -- C ABI of the MI355X (gfx950) Sliding Window Recurrence library.
+ *
+ * The operation (Sliding Window Recurrences, Sec. 4.2: the jagged-window
+ * truncation T ~ I_b of the hierarchical decomposition, computed by the Block
+ * Two-Pass algorithm, Alg. "Block Two-Pass"): for every batch b and head h,
+ * with l = block and token i (0-based) in block tau = floor(i / l),
+ *
+ *     u_i  = b_i (*) x_i                                   (pre-gate, Sec. 5)
+ *     h~_i = sum_{j = l*max(tau-1,0)}^{i} ( prod_{m=j+1}^{i} a_m ) u_j
+ *     y_i  = c_i (*) h~_i   (+ x_i if SWR_FLAG_RESIDUAL)   (post-gate, Sec. 5)
+ *
+ * i.e. the diagonal linear recurrence h_i = a_i h_{i-1} + u_i (Sec. 3,
+ * eq. (2.1)) whose state is restarted from zero at the start of the previous
+ * block: every token sees its own block and the block before it (lags up to
+ * l on a block's first token, up to 2l-1 on its last).  The decay a_i is one
+ * scalar per token and head, shared by the head's D channels (Sec. 4.2.2 and
+ * Sec. 5, "Featurization"), which makes the intra-block solve a matrix
+ * product.  A last block shorter than l behaves as if the inputs were
+ * zero-padded at the end.  The initial state is zero.
+ *
+ * swr_backward returns the exact gradients of that (truncated) forward.
+ *
+ * Tensor layout.  x, b, c, y, dy, dx, db, dc are [B, T, H, D] with the channel
+ * dimension D contiguous (stride 1) and element strides sx_b, sx_t, sx_h for
+ * the other three dimensions (shared by all eight tensors).  a is [B, T, H]
+ * with strides sa_b, sa_t, sa_h; da uses the same strides as a but is always
+ * float32.  Element type of x, a, b, c, y, dy, dx, db, dc is `dtype`;
+ * accumulation is always float32.
+ *
+ * Ownership.  Every pointer is device memory owned by the caller.  The library
+ * allocates no memory, needs no workspace and keeps no mutable global state;
+ * calls from several host threads are safe.  Outputs are fully overwritten.
+ *
+ * Asynchrony.  Work is enqueued on `stream` (a hipStream_t passed as void*;
+ * NULL = the default stream) and the call returns without waiting.  A fault
+ * inside a kernel surfaces at the caller's next synchronisation.
+ *
+ * Errors.  Arguments are validated before any HIP runtime call; a failed
+ * validation returns a negative SWR_ERR_* code and touches nothing.
+ * SWR_ERR_HIP means the kernel launch itself failed.
+ */
+#ifndef SWR_H
+#define SWR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SWR_ABI_VERSION 1
+
+typedef enum swr_status {
+    SWR_OK = 0,
+    SWR_ERR_NULL = -1,        /* a required pointer is NULL                              */
+    SWR_ERR_SHAPE = -2,       /* negative B, T or H, D < 1, or overlapping strides        */
+    SWR_ERR_DTYPE = -3,       /* dtype is not one of swr_dtype_t                          */
+    SWR_ERR_BLOCK = -4,       /* block is not 16, 32, 64 or 128                           */
+    SWR_ERR_ALIGN = -5,       /* a pointer or stride breaks the vector alignment          */
+    SWR_ERR_ALIAS = -6,       /* an output overlaps an input or another output            */
+    SWR_ERR_UNSUPPORTED = -7, /* D not in {16, 32, 64, 128}, unknown flags, run_len bad   */
+    SWR_ERR_HIP = -8,         /* the HIP runtime rejected the launch                      */
+    SWR_ERR_VERSION = -9      /* problem->abi_version != SWR_ABI_VERSION                  */
+} swr_status_t;
+
+typedef enum swr_dtype {
+    SWR_DTYPE_F32 = 0,        /* IEEE float32                                            */
+    SWR_DTYPE_BF16 = 1        /* bfloat16; outputs are rounded to nearest even            */
+} swr_dtype_t;
+
+/* y += x in the forward and dx += dy in the backward (Phalanx post-gate with
+ * residual, Sec. 5). */
+#define SWR_FLAG_RESIDUAL 1u
+
+typedef struct swr_problem {
+    int32_t abi_version;   /* must be SWR_ABI_VERSION                                     */
+    int32_t dtype;         /* swr_dtype_t of every tensor except da                       */
+    int64_t B, T, H, D;    /* batch, tokens, heads, channels per head; B, T or H may be 0 */
+    int64_t block;         /* l, the block (= window unit) length: 16, 32, 64 or 128       */
+    uint32_t flags;        /* SWR_FLAG_* bits                                              */
+    int32_t reserved;      /* must be 0                                                    */
+    int64_t sx_b, sx_t, sx_h;  /* element strides of the [B,T,H,D] tensors (channel = 1) */
+    int64_t sa_b, sa_t, sa_h;  /* element strides of a and da                            */
+    int64_t run_len;       /* tokens per workgroup run: 0 = automatic, else a positive
+                              multiple of max(64, block); a tuning knob that does not
+                              change results beyond float32 rounding order              */
+} swr_problem_t;
+
+/* Forward: y = SWR(x, a, b, c).  Alignment: x, b, c, y and every sx_* must be
+ * multiples of min(16 bytes, D/16 elements) (i.e. each lane's slice of a row is
+ * a naturally aligned vector); a needs the alignment of one element. */
+int swr_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                const void* c, void* y, void* stream);
+
+/* Backward: given dy = dL/dy, writes dx, da (float32, [B,T,H] at a's strides),
+ * db and dc.  Inputs are those of the forward; nothing from the forward pass is
+ * saved or needed (the kernel recomputes what it uses). */
+int swr_backward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                 const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
+                 void* stream);
+
+/* Static English description of a status code (never NULL). */
+const char* swr_error_string(int code);
+
+/* SWR_ABI_VERSION of the built library. */
+int swr_abi_version(void);
+
+/* Resolved launch shape for a problem (for reports and tests): the run length
+ * in tokens that `run_len == 0` selects, and the number of workgroups the
+ * forward and backward launch.  Returns an SWR_ERR_* code for a problem that
+ * swr_forward would reject on shape grounds; pointers are not inspected. */
+int swr_launch_info(const swr_problem_t* problem, int64_t* run_len, int64_t* fwd_workgroups,
+                    int64_t* bwd_workgroups);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SWR_H */

@@ -1,0 +1,218 @@
+// swr_api.cpp -- C ABI of the Sliding Window Recurrence library: argument
+// validation (done entirely before any HIP runtime call), launch-shape
+// selection and dispatch to the gfx950 kernels.
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/swr.h"
+#include "swr_launch.h"
+
+namespace {
+
+constexpr int64_t kMaxWorkgroups = 0x7fffffffLL;
+constexpr int64_t kMaxExtent = (int64_t)1 << 62;
+// Default number of workgroups to aim for: a few per compute unit of the
+// MI355X (256 CUs), so that runs are long (few halo re-reads) while the grid
+// still fills the chip with some slack for uneven progress.
+constexpr int64_t kTargetWorkgroups = 1024;
+
+struct Dim {
+    int64_t size, stride;
+};
+
+// Largest element offset of a strided tensor, or -1 on overflow / bad stride.
+int64_t max_offset(const Dim* d, int nd) {
+    int64_t off = 0;
+    for (int i = 0; i < nd; ++i) {
+        if (d[i].size <= 1) continue;
+        if (d[i].stride < 0) return -1;
+        if (d[i].stride > 0 && (d[i].size - 1) > kMaxExtent / d[i].stride) return -1;
+        off += (d[i].size - 1) * d[i].stride;
+        if (off > kMaxExtent) return -1;
+    }
+    return off;
+}
+
+// True when distinct index tuples never map to the same element.
+bool non_overlapping(Dim* d, int nd) {
+    std::sort(d, d + nd, [](const Dim& p, const Dim& q) { return p.stride < q.stride; });
+    int64_t need = 1;   // smallest stride the next (larger-stride) dimension may have
+    for (int i = 0; i < nd; ++i) {
+        if (d[i].size <= 1) continue;
+        if (d[i].stride < need) return false;
+        need = d[i].stride * d[i].size;
+    }
+    return true;
+}
+
+struct Resolved {
+    bool empty;
+    int es;             // bytes per I/O element
+    int cpl;            // channels per lane = D / 16
+    int nw;             // waves per workgroup
+    int64_t step;       // tokens per workgroup step
+    int64_t run_len, nruns, nwork;
+    int64_t xspan;      // bytes spanned by one [B,T,H,D] tensor
+    int64_t aspan;      // elements spanned by a / da
+};
+
+int resolve(const swr_problem_t* p, Resolved* r) {
+    if (!p) return SWR_ERR_NULL;
+    if (p->abi_version != SWR_ABI_VERSION) return SWR_ERR_VERSION;
+    if (p->dtype != SWR_DTYPE_F32 && p->dtype != SWR_DTYPE_BF16) return SWR_ERR_DTYPE;
+    if (p->B < 0 || p->T < 0 || p->H < 0 || p->D < 1) return SWR_ERR_SHAPE;
+    if (p->block != 16 && p->block != 32 && p->block != 64 && p->block != 128) return SWR_ERR_BLOCK;
+    if (p->D != 16 && p->D != 32 && p->D != 64 && p->D != 128) return SWR_ERR_UNSUPPORTED;
+    if ((p->flags & ~SWR_FLAG_RESIDUAL) != 0 || p->reserved != 0) return SWR_ERR_UNSUPPORTED;
+
+    r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
+    r->cpl = (int)(p->D / 16);
+    r->nw = swr::waves_for_block(p->block);
+    r->step = (int64_t)r->nw * 16;
+    if (p->run_len < 0 || (p->run_len > 0 && p->run_len % r->step != 0)) return SWR_ERR_UNSUPPORTED;
+
+    r->empty = p->B == 0 || p->T == 0 || p->H == 0;
+    r->xspan = r->aspan = 0;
+    if (!r->empty) {   // strides of an empty tensor are meaningless
+        Dim xd[4] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}, {p->D, 1}};
+        Dim ad[3] = {{p->B, p->sa_b}, {p->T, p->sa_t}, {p->H, p->sa_h}};
+        const int64_t xo = max_offset(xd, 4), ao = max_offset(ad, 3);
+        if (xo < 0 || ao < 0) return SWR_ERR_SHAPE;
+        if (!non_overlapping(xd, 4) || !non_overlapping(ad, 3)) return SWR_ERR_SHAPE;
+        r->xspan = (xo + 1) * r->es;
+        r->aspan = ao + 1;
+    }
+    const int64_t seqs = p->B * p->H;
+    const int64_t nsteps = (p->T + r->step - 1) / r->step;
+    if (p->run_len > 0) {
+        r->run_len = p->run_len;
+    } else if (r->empty) {
+        r->run_len = r->step;
+    } else {
+        const int64_t want = (kTargetWorkgroups + seqs - 1) / seqs;
+        const int64_t runs = std::max<int64_t>(1, std::min(nsteps, want));
+        r->run_len = ((nsteps + runs - 1) / runs) * r->step;
+    }
+    r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
+    if (!r->empty && r->nruns > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
+    r->nwork = seqs * r->nruns;
+    return SWR_OK;
+}
+
+int check_strides_aligned(const swr_problem_t* p, const Resolved& r) {
+    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);   // bytes per lane row vector
+    const Dim xd[3] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}};
+    for (const Dim& d : xd)
+        if (d.size > 1 && (d.stride * r.es) % vb != 0) return SWR_ERR_ALIGN;
+    return SWR_OK;
+}
+
+bool aligned(const void* ptr, int64_t bytes) { return ((uintptr_t)ptr % (uintptr_t)bytes) == 0; }
+
+struct Span {
+    uintptr_t lo, hi;   // [lo, hi)
+};
+
+Span span(const void* p, int64_t bytes) { return {(uintptr_t)p, (uintptr_t)p + (uintptr_t)bytes}; }
+
+bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
+
+swr::Params make_params(const swr_problem_t* p, const Resolved& r) {
+    swr::Params k{};
+    k.B = p->B; k.T = p->T; k.H = p->H;
+    k.sx_b = p->sx_b; k.sx_t = p->sx_t; k.sx_h = p->sx_h;
+    k.sa_b = p->sa_b; k.sa_t = p->sa_t; k.sa_h = p->sa_h;
+    k.block = (int32_t)p->block;
+    k.residual = (p->flags & SWR_FLAG_RESIDUAL) ? 1 : 0;
+    k.run_len = r.run_len;
+    k.nruns = r.nruns;
+    k.nwork = r.nwork;
+    return k;
+}
+
+}  // namespace
+
+extern "C" {
+
+int swr_abi_version(void) { return SWR_ABI_VERSION; }
+
+const char* swr_error_string(int code) {
+    switch (code) {
+        case SWR_OK: return "success";
+        case SWR_ERR_NULL: return "a required pointer is NULL";
+        case SWR_ERR_SHAPE: return "invalid shape or strides (negative size, D < 1, overlapping or overflowing strides)";
+        case SWR_ERR_DTYPE: return "unknown dtype";
+        case SWR_ERR_BLOCK: return "block must be 16, 32, 64 or 128";
+        case SWR_ERR_ALIGN: return "pointer or stride not aligned to the per-lane vector width";
+        case SWR_ERR_ALIAS: return "an output overlaps an input or another output";
+        case SWR_ERR_UNSUPPORTED: return "unsupported: D must be 16, 32, 64 or 128; unknown flags; or bad run_len";
+        case SWR_ERR_HIP: return "the HIP runtime rejected the kernel launch";
+        case SWR_ERR_VERSION: return "ABI version mismatch";
+        default: return "unknown status code";
+    }
+}
+
+int swr_launch_info(const swr_problem_t* problem, int64_t* run_len, int64_t* fwd_workgroups,
+                    int64_t* bwd_workgroups) {
+    Resolved r;
+    const int rc = resolve(problem, &r);
+    if (rc != SWR_OK) return rc;
+    if (run_len) *run_len = r.run_len;
+    if (fwd_workgroups) *fwd_workgroups = r.nwork;
+    if (bwd_workgroups) *bwd_workgroups = r.nwork;
+    return SWR_OK;
+}
+
+int swr_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                const void* c, void* y, void* stream) {
+    Resolved r;
+    int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    if (r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !y) return SWR_ERR_NULL;
+    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
+    for (const void* q : {x, b, c, (const void*)y})
+        if (!aligned(q, vb)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es)) return SWR_ERR_ALIGN;
+    if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    const Span sy = span(y, r.xspan);
+    for (const Span& s : {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es)})
+        if (overlap(sy, s)) return SWR_ERR_ALIAS;
+
+    swr::Params k = make_params(p, r);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.y = y;
+    return swr::launch(k, p->dtype, (int)p->D, r.nw, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+int swr_backward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                 const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
+                 void* stream) {
+    Resolved r;
+    int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    if (r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return SWR_ERR_NULL;
+    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
+    for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
+        if (!aligned(q, vb)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es) || !aligned(da, 4)) return SWR_ERR_ALIGN;
+    if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    const Span outs[4] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan),
+                          span(da, r.aspan * 4)};
+    const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
+                         span(a, r.aspan * r.es)};
+    for (int i = 0; i < 4; ++i) {
+        for (const Span& s : ins)
+            if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
+    }
+
+    swr::Params k = make_params(p, r);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
+    k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+    return swr::launch(k, p->dtype, (int)p->D, r.nw, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+}  // extern "C"

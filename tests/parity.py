@@ -1,0 +1,60 @@
+"""Helpers shared by the GPU parity tests: moving seeded inputs to the device,
+calling the library through its binding, and the error metric.
+
+Error metric (one number per output tensor Z, against the oracle's float64
+result R on the same rounded inputs):  e_i = |Z_i - R_i| / max(|R_i|, rms(R)).
+It is relative for elements of typical size and absolute (in units of the
+tensor's RMS) for elements near zero, where a relative error means nothing.
+"""
+import numpy as np
+
+import workloads as W
+
+# fp32 I/O: relative 1e-5 (scaled as above).
+TOL_F32_MAX = 1e-5
+# bf16 I/O, fp32 accumulation: max 2e-2 and mean 5e-3 in the scaled metric.
+# (Rounding a correct result to bf16 alone gives up to 2^-9 ~ 2e-3 here.)
+TOL_BF16_MAX = 2e-2
+TOL_BF16_MEAN = 5e-3
+
+
+def torch_dtype(dtype):
+    import torch
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def to_device(arr_f32, dtype, device="cuda"):
+    """A device tensor holding exactly the (already rounded) float32 values."""
+    import torch
+    if dtype == "bf16":
+        bits = W.f32_to_bf16_bits(arr_f32).view(np.int16)
+        return torch.from_numpy(bits).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(arr_f32, np.float32)).to(device)
+
+
+def to_host(t):
+    """float64 numpy copy of a device tensor (exact for bf16 and fp32)."""
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def error_stats(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return dict(max_e=0.0, mean_e=0.0, max_abs=0.0, mean_abs=0.0, rms=0.0)
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    denom = np.maximum(np.abs(ref), rms if rms > 0 else 1.0)
+    diff = np.abs(got - ref)
+    e = diff / denom
+    return dict(max_e=float(e.max()), mean_e=float(e.mean()), max_abs=float(diff.max()),
+                mean_abs=float(diff.mean()), rms=rms, nonfinite=int((~np.isfinite(got)).sum()))
+
+
+def assert_close(got, ref, dtype, what=""):
+    st = error_stats(got, ref)
+    assert st["nonfinite"] == 0, f"{what}: non-finite values {st}"
+    if dtype == "f32":
+        assert st["max_e"] <= TOL_F32_MAX, f"{what}: {st}"
+    else:
+        assert st["max_e"] <= TOL_BF16_MAX and st["mean_e"] <= TOL_BF16_MEAN, f"{what}: {st}"
+    return st
