@@ -55,6 +55,24 @@ def contraction_flops(cfg, backward):
     return per * (3 if backward else 1)
 
 
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch measured with rocprofv3 counters for this kernel and
+    workload, as recorded in profiles/, or None when the kernel source has
+    changed since the counters were taken."""
+    import hashlib
+    import re
+    src = os.path.join(ROOT, "paper_2512_13921_amd", "csrc", "swr_kernels.hip")
+    prof = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
+    if not os.path.exists(prof):
+        return None
+    m = re.search(r"<!-- traffic: (\{.*\}) -->", open(prof).read())
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    return rec if rec.get("kernel_sha256") == sha else None
+
+
 def to_device(arr, dtype):
     import torch
     if dtype == "bf16":
@@ -65,15 +83,18 @@ def to_device(arr, dtype):
 
 def cpu_baseline(cfg, prob, budget_s=10.0):
     """Oracle throughput on whole (batch, head) slices of the workload, in
-    tokens/s of the full job (a token carries all H heads)."""
+    tokens/s of the full job (a token carries all H heads).  Slices are taken
+    in a fixed shuffled order and revisited until about budget_s seconds of
+    oracle time have been spent."""
     import oracle
     threads = oracle.max_threads()
     nslices = cfg.B * cfg.H
     batch = max(1, min(threads, nslices))
-    done, elapsed = 0, 0.0
     order = np.random.default_rng(0).permutation(nslices)
-    while done < nslices and (elapsed < budget_s or done == 0):
-        idx = order[done:done + batch]
+    done, elapsed, passes = 0, 0.0, 0
+    pos = 0
+    while elapsed < budget_s or done == 0:
+        idx = order[pos:pos + batch]
         bi, hi = idx // cfg.H, idx % cfg.H
 
         def take(t):
@@ -85,14 +106,17 @@ def cpu_baseline(cfg, prob, budget_s=10.0):
         oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
         elapsed += time.perf_counter() - t0
         done += len(idx)
+        pos += len(idx)
+        if pos >= nslices:
+            pos, passes = 0, passes + 1
     token_heads = done * cfg.T
     return {
         "value": token_heads / cfg.H / elapsed,
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"{done} of {nslices} (batch, head) slices at full T={cfg.T}, forward+backward, "
-                  f"float64, OpenMP over slices; {elapsed:.1f} s",
+        "sample": f"{done} (batch, head) slices of {nslices} (full T={cfg.T}; {passes} full passes), "
+                  f"forward+backward in float64, OpenMP over slices; {elapsed:.1f} s of oracle time",
     }
 
 
@@ -166,11 +190,26 @@ def main():
     f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
     dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
     dom_gbs = b_gbs if dominant_bwd else f_gbs
+    dom_kernel = "swr_bwd_kernel" if dominant_bwd else "swr_fwd_kernel"
+    traffic = recorded_traffic(dom_kernel, cfg.name)
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
 
     run_len, fwg, bwg = swr.swr_launch_info(swr.make_problem(
         cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
         x.stride()[:3], a.stride(), False, args.run_len))
+
+    # Reference: a plain device-to-device copy of one [B,T,H,D] tensor (read + write).
+    cbuf = torch.empty_like(x)
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(3):
+        cbuf.copy_(x)
+    ce[0].record(stream)
+    for _ in range(10):
+        cbuf.copy_(x)
+    ce[1].record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * x.numel() * x.element_size() * 10 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
+    del cbuf
 
     out = {
         "metric": METRIC,
@@ -190,12 +229,15 @@ def main():
                    "parallelism": "single GPU", "run_len": run_len, "workgroups": fwg},
         "roofline": {
             "bound": "hbm",
-            "kernel": "swr_bwd_kernel" if dominant_bwd else "swr_fwd_kernel",
+            "kernel": dom_kernel,
             "achieved": dom_gbs,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": dom_gbs / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": None if traffic is None else traffic["traffic_bytes"] / 1e9,
+            "traffic_unit": "GB per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+            "traffic_vs_algorithmic": None if traffic is None else
+                traffic["traffic_bytes"] / (bb if dominant_bwd else fb),
         },
         "kernels": {
             "forward": {"ms": float(fwd_ms.mean()), "ms_min": float(fwd_ms.min()),
@@ -207,6 +249,7 @@ def main():
                          "mfma_tflops": contraction_flops(cfg, True) / (bwd_ms.mean() * 1e-3) / 1e12,
                          "tokens_per_s": tokens / (bwd_ms.mean() * 1e-3)},
             "mfma_peak_tflops": mfma_peak,
+            "copy_GB/s": copy_gbs,
             "wall_s_timed": t_wall,
         },
         "cpu_baseline": None,

@@ -73,6 +73,29 @@ struct IoF32 {
     static constexpr int ES = 4;
 };
 
+// ---------------------------------------------------------------------------
+// Buffer access
+// ---------------------------------------------------------------------------
+//
+// Every tensor access is a raw buffer load or store: a scalar resource (base
+// address of the rows this wave touches in the current step) plus a 32-bit
+// per-lane byte offset.  A lane whose row lies outside the valid token range
+// passes an offset past the resource's record count, so the hardware returns
+// zeros for the load and drops the store; no branches are needed.
+
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBufferWord3 = 0x00020000;        // raw buffer, 32-bit data format (gfx9 family)
+constexpr int kNumRecords = 0x7fffffff;         // every offset below 2^31 - 1 is in range
+constexpr uint32_t kOutOfRange = 0x80000000u;   // an offset the range check rejects
+
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, kNumRecords, kBufferWord3);
+}
+
+__device__ inline uint32_t in_range(bool ok, uint32_t off) { return ok ? off : kOutOfRange; }
+
 // One lane's CPL consecutive channels of one token row, kept as raw bits.
 template <class IO, int CPL>
 struct Row {
@@ -84,18 +107,18 @@ struct Row {
 #pragma unroll
         for (int i = 0; i < NWORDS; ++i) w[i] = 0;
     }
-    __device__ void load(const void* p) {
+    __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
         if constexpr (BYTES == 2) {
-            w[0] = *(const uint16_t*)p;
+            w[0] = (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
         } else if constexpr (BYTES == 4) {
-            w[0] = *(const uint32_t*)p;
+            w[0] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
         } else if constexpr (BYTES == 8) {
-            uint2 v = *(const uint2*)p;
+            const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
             w[0] = v.x; w[1] = v.y;
         } else {
 #pragma unroll
             for (int i = 0; i < BYTES / 16; ++i) {
-                uint4 v = ((const uint4*)p)[i];
+                const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(off + 16 * i), 0, 0);
                 w[4 * i + 0] = v.x; w[4 * i + 1] = v.y; w[4 * i + 2] = v.z; w[4 * i + 3] = v.w;
             }
         }
@@ -113,43 +136,43 @@ struct Row {
 
 // Packs CPL floats to the I/O type and stores them as one vector.
 template <class IO, int CPL>
-__device__ inline void store_row(void* p, const float (&v)[CPL]) {
+__device__ inline void store_row(__amdgpu_buffer_rsrc_t r, uint32_t off, const float (&v)[CPL]) {
+    constexpr int BYTES = CPL * IO::ES;
+    uint32_t w[BYTES >= 4 ? BYTES / 4 : 1];
     if constexpr (IO::ES == 2) {
         if constexpr (CPL == 1) {
-            *(uint16_t*)p = (uint16_t)IoBf16::from_f32(v[0]);
+            __builtin_amdgcn_raw_buffer_store_b16((short)IoBf16::from_f32(v[0]), r, (int)off, 0, 0);
+            return;
         } else {
-            uint32_t w[CPL / 2];
 #pragma unroll
             for (int i = 0; i < CPL / 2; ++i)
                 w[i] = IoBf16::from_f32(v[2 * i]) | (IoBf16::from_f32(v[2 * i + 1]) << 16);
-            if constexpr (CPL == 2) {
-                *(uint32_t*)p = w[0];
-            } else if constexpr (CPL == 4) {
-                *(uint2*)p = make_uint2(w[0], w[1]);
-            } else {
-                *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
-            }
         }
     } else {
-        if constexpr (CPL == 1) {
-            *(float*)p = v[0];
-        } else if constexpr (CPL == 2) {
-            *(float2*)p = make_float2(v[0], v[1]);
-        } else {
 #pragma unroll
-            for (int i = 0; i < CPL / 4; ++i)
-                ((float4*)p)[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
-        }
+        for (int i = 0; i < CPL; ++i) w[i] = __builtin_bit_cast(uint32_t, v[i]);
+    }
+    if constexpr (BYTES == 4) {
+        __builtin_amdgcn_raw_buffer_store_b32((int)w[0], r, (int)off, 0, 0);
+    } else if constexpr (BYTES == 8) {
+        __builtin_amdgcn_raw_buffer_store_b64(i32x2{(int)w[0], (int)w[1]}, r, (int)off, 0, 0);
+    } else if constexpr (BYTES >= 16) {
+#pragma unroll
+        for (int i = 0; i < BYTES / 16; ++i)
+            __builtin_amdgcn_raw_buffer_store_b128(
+                i32x4{(int)w[4 * i], (int)w[4 * i + 1], (int)w[4 * i + 2], (int)w[4 * i + 3]}, r,
+                (int)(off + 16 * i), 0, 0);
     }
 }
 
 template <class IO>
-__device__ inline float load_scalar(const void* p) {
+__device__ inline float load_scalar(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     if constexpr (IO::ES == 2)
-        return IoBf16::to_f32(*(const uint16_t*)p);
+        return IoBf16::to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0));
     else
-        return *(const float*)p;
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
 }
+
 
 // ---------------------------------------------------------------------------
 // Cross-lane helpers (a DPP "row" is 16 lanes on CDNA)
@@ -321,6 +344,27 @@ __device__ inline Decay build_decay(float a_n, int grp, int n) {
 }
 
 // ---------------------------------------------------------------------------
+// Addressing
+// ---------------------------------------------------------------------------
+
+// Row t of one [B, T, H, D] tensor of this workgroup's (batch, head) sits at
+// base + t * rs; a lane adds its own 32-bit offset (its row within the
+// sub-block and its channel slice).  Keeping base and t * rs uniform lets
+// every access use a scalar base plus one vector register of offset.
+struct Lanes {
+    int lane, wv, grp, n;
+};
+
+__device__ inline Lanes lanes() {
+    Lanes L;
+    L.lane = threadIdx.x & 63;
+    L.wv = __builtin_amdgcn_readfirstlane((int)threadIdx.x) >> 6;   // uniform per wave
+    L.grp = L.lane >> 4;
+    L.n = L.lane & 15;
+    return L;
+}
+
+// ---------------------------------------------------------------------------
 // Forward
 // ---------------------------------------------------------------------------
 
@@ -328,24 +372,28 @@ template <class IO, int CPL, int NW>
 __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
     constexpr int D = CPL * SB;
     constexpr int STEP = NW * SB;
+    constexpr int ES = IO::ES;
     __shared__ float s_wl[2][NW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[2][NW];       // each sub-block's decay product
 
-    const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
-    const int grp = lane >> 4, n = lane & 15;
+    const Lanes ln = lanes();
+    const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work(p);
     const int l = p.block;
     const int S = l / SB;              // sub-blocks per block
     const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);  // first token read
     const int64_t halo = wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
-    const char* xp = (const char*)p.x + (wk.b * p.sx_b + wk.h * p.sx_h + n * CPL) * IO::ES;
-    const char* bp = (const char*)p.b + (wk.b * p.sx_b + wk.h * p.sx_h + n * CPL) * IO::ES;
-    const char* cp = (const char*)p.c + (wk.b * p.sx_b + wk.h * p.sx_h + n * CPL) * IO::ES;
-    char* yp = (char*)p.y + (wk.b * p.sx_b + wk.h * p.sx_h + n * CPL) * IO::ES;
-    const char* ap = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * IO::ES;
-    const int64_t rs = p.sx_t * IO::ES;   // row stride in bytes
+    const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    const char* xb = (const char*)p.x + xo;
+    const char* bb = (const char*)p.b + xo;
+    const char* cb = (const char*)p.c + xo;
+    char* yb = (char*)p.y + xo;
+    const char* ab = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * ES;
+    const int64_t rs = p.sx_t * ES;    // row stride in bytes
+    const int64_t as = p.sa_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
 
     float e[CPL], s[CPL];   // carriers at the start of the step: full and block-restarted
 #pragma unroll
@@ -353,24 +401,24 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
 
     int buf = 0;
     for (int64_t t0 = wk.t_begin - halo * STEP; t0 < wk.t_end; t0 += STEP, buf ^= 1) {
-        const int64_t r0 = t0 + wv * SB;          // first token of this wave's sub-block
+        const int64_t r0 = t0 + wv * SB;          // first token of this wave's sub-block (uniform)
         const int64_t tr0 = r0 + 4 * grp;         // first of this lane's four tokens
 
         // ---- loads -------------------------------------------------------
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                     rc = rsrc(cb + r0 * rs), ry = rsrc(yb + r0 * rs);
         Row<IO, CPL> xr[4], br[4], cr[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t t = tr0 + r;
-            if (t >= t_lo && t < wk.t_end) {
-                xr[r].load(xp + t * rs);
-                br[r].load(bp + t * rs);
-            } else {
-                xr[r].zero(); br[r].zero();
-            }
-            if (t >= wk.t_begin && t < wk.t_end) cr[r].load(cp + t * rs); else cr[r].zero();
+            const uint32_t o = loff + (uint32_t)(r * rs);
+            const uint32_t ox = in_range(t >= t_lo && t < wk.t_end, o);
+            xr[r].load(rx, ox);
+            br[r].load(rb, ox);
+            cr[r].load(rc, in_range(t >= wk.t_begin && t < wk.t_end, o));
         }
         const int64_t ta = r0 + n;
-        const float a_n = (ta >= t_lo && ta < wk.t_end) ? load_scalar<IO>(ap + ta * p.sa_t * IO::ES) : 0.0f;
+        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
 
         // ---- local solve W = L U on the matrix cores ---------------------
         const Decay dk = build_decay(a_n, grp, n);
@@ -417,16 +465,14 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t t = tr0 + r;
-            if (t >= wk.t_begin && t < wk.t_end) {
-                float yv[CPL];
+            float yv[CPL];
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) {
-                    const float hv = W[m][r] + dk.G[r] * ein[m];
-                    yv[m] = cr[r].get(m) * hv;
-                    if (p.residual) yv[m] += xr[r].get(m);
-                }
-                store_row<IO, CPL>(yp + t * rs, yv);
+            for (int m = 0; m < CPL; ++m) {
+                const float hv = W[m][r] + dk.G[r] * ein[m];
+                yv[m] = cr[r].get(m) * hv;
+                if (p.residual) yv[m] += xr[r].get(m);
             }
+            store_row<IO, CPL>(ry, in_range(t >= wk.t_begin && t < wk.t_end, loff + (uint32_t)(r * rs)), yv);
         }
     }
 }
@@ -435,258 +481,342 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
 // Backward
 // ---------------------------------------------------------------------------
 
+// Operand A of the reverse solve D = L^T dh: this lane holds
+// L[4*grp + q][n] = a_{n+1} ... a_{4 grp + q} (1 on the diagonal, 0 below),
+// a suffix product along the row, built like the forward operator.
+__device__ inline void build_decay_transposed(float a_n, int grp, int n, float (&LT)[4]) {
+    const float a_next = dpp<DPP_ROW_SHL + 1>(a_n, 1.0f);   // a of token n+1
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int rho = 4 * grp + q;
+        const float v = row_suffix_prod(n < rho ? a_next : 1.0f);
+        LT[q] = n <= rho ? v : 0.0f;
+    }
+}
+
+// Gradient of the truncated forward.  du = L~^T dh with dh = c * dy is itself a
+// block two-pass run backwards: du_t = L_t^T dh_t + r_t C_{t+1}, where
+// r_t = e_l^T L_t and C_{t+1} = g_{t+1}^T dh_{t+1} comes from the next block.
+// The decay gradient of token k (block t) collects, over the channels, the
+// state entering step k times the adjoint leaving it, for the two windows
+// that contain k:  da_k = sum_mu [ w_{t,k-1} du_k + g_{t,k-1} v_{t-1} D_{t,k} ]
+// with w the block-restarted local state, D_t = L_t^T dh_t and v_{t-1} the
+// previous block's carrier (w_{t,-1} = 0, g_{t,-1} = 1).
+//
+// Register budget: the step's look-ahead tiles (c, dy of the next step) are
+// handed to the next step through a wave-private LDS slot (two slots used in
+// turn), and the epilogue runs over the channels in NPASS passes, each
+// recomputing its part of W = L u and D = L^T dh on the matrix cores, so that
+// only one pass's accumulators are live at a time.  In pass ps lane n owns
+// channels ps*16*CH + n*CH .. + CH-1, so every load and store instruction
+// covers 16*CH contiguous channels of a row (whole memory sectors).
+template <class IO, int CPL, int NW>
+struct BwdShape {
+    static constexpr int NPASS = CPL >= 4 ? 2 : 1;      // epilogue passes
+    static constexpr int CH = CPL / NPASS;               // channels per lane per pass
+    static constexpr int HWD = Row<IO, CH>::NWORDS;      // words of one lane's pass slice
+    static constexpr int NWD = NPASS * HWD;
+    static constexpr int HAND_BYTES = 2 * NW * 2 * 4 * NWD * 64 * 4;
+    // Hand over through LDS when both slots fit beside the carrier buffers;
+    // otherwise the next step re-reads c and dy from global memory.
+    static constexpr bool HAND_LDS = HAND_BYTES <= 128 * 1024;
+};
+
 template <class IO, int CPL, int NW>
 __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
     constexpr int D = CPL * SB;
     constexpr int STEP = NW * SB;
+    constexpr int ES = IO::ES;
+    using Sh = BwdShape<IO, CPL, NW>;
+    using RH = Row<IO, Sh::CH>;
+    constexpr int NPASS = Sh::NPASS, CH = Sh::CH, HWD = Sh::HWD, NWD = Sh::NWD;
+    constexpr int PIECE = 16 * CH;                       // channels covered by one pass
     __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve
     __shared__ float s_c[2][NW];        // decay product of each sub-block
     __shared__ float s_df[3][NW][D];    // a_0 * first row of each sub-block's L^T dh
     __shared__ float s_cf[3][NW];       // decay products for the reverse carriers
+    // Wave-private hand-over of the look-ahead's c and dy tiles: [slot][wave][c|dy][row][word][lane].
+    __shared__ uint32_t s_hand[Sh::HAND_LDS ? 2 : 1][Sh::HAND_LDS ? NW : 1][2][4][NWD][64];
 
-    const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
-    const int grp = lane >> 4, n = lane & 15;
+    const Lanes ln = lanes();
+    const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work(p);
     const int l = p.block;
     const int S = l / SB;
     const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);
-    const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // last token (excl.) of the look-ahead
+    const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the look-ahead
 
-    const int64_t off = (wk.b * p.sx_b + wk.h * p.sx_h + n * CPL) * IO::ES;
-    const char* xp = (const char*)p.x + off;
-    const char* bp = (const char*)p.b + off;
-    const char* cp = (const char*)p.c + off;
-    const char* dyp = (const char*)p.dy + off;
-    char* dxp = (char*)p.dx + off;
-    char* dbp = (char*)p.db + off;
-    char* dcp = (char*)p.dc + off;
-    const char* ap = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * IO::ES;
-    float* dap = p.da + (wk.b * p.sa_b + wk.h * p.sa_h);
-    const int64_t rs = p.sx_t * IO::ES;
-    const int64_t as = p.sa_t * IO::ES;
+    const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    const char* xb = (const char*)p.x + xo;
+    const char* bb = (const char*)p.b + xo;
+    const char* cb = (const char*)p.c + xo;
+    const char* dyb = (const char*)p.dy + xo;
+    char* dxb = (char*)p.dx + xo;
+    char* dbb = (char*)p.db + xo;
+    char* dcb = (char*)p.dc + xo;
+    const int64_t ao = wk.b * p.sa_b + wk.h * p.sa_h;
+    const char* ab = (const char*)p.a + ao * ES;
+    char* dab = (char*)(p.da + ao);
+    const int64_t rs = p.sx_t * ES;
+    const int64_t as = p.sa_t * ES;
+    const int64_t das = p.sa_t * 4;
+    // Byte offset of this lane's slice in pass 0 of row 4*grp; pass ps adds ps*PIECE channels.
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CH * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das;
+    const int base = lane & 48;   // first lane of this 16-lane row
+    auto chan = [&](int ps, int j) { return ps * PIECE + n * CH + j; };   // channel of slot (ps, j)
 
-    float e[CPL], s[CPL];
+    float e[CPL], s[CPL];   // forward carriers at the step start (full, block-restarted)
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
 
     // The sweep starts one step early (the halo step): it recovers the forward
-    // carrier entering the run and the look-ahead of the run's first step.
+    // carrier entering the run and the look-ahead for the run's first step.
     int k = 0;
     for (int64_t t0 = wk.t_begin - STEP; t0 < wk.t_end; t0 += STEP, ++k) {
         const int bw = k & 1, bc = k % 3, bn = (k + 1) % 3;
+        const int hs = Sh::HAND_LDS ? (k & 1) : 0;          // slot holding this step's c, dy
         const int64_t r0 = t0 + wv * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const bool out_step = t0 >= wk.t_begin;
 
-        // ---- loads: this step's x, b, c, dy, a and the next step's c, dy, a --
-        Row<IO, CPL> xr[4], br[4], cr[4], dyr[4], cn[4], dyn[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t t = tr0 + r;
-            if (t >= t_lo && t < wk.t_end) {
-                xr[r].load(xp + t * rs);
-                br[r].load(bp + t * rs);
-            } else {
-                xr[r].zero(); br[r].zero();
-            }
-            if (out_step && t >= wk.t_begin && t < wk.t_end) {
-                cr[r].load(cp + t * rs);
-                dyr[r].load(dyp + t * rs);
-            } else {
-                cr[r].zero(); dyr[r].zero();
-            }
-            const int64_t tn = t + STEP;
-            if (tn >= wk.t_begin && tn < t_la) {
-                cn[r].load(cp + tn * rs);
-                dyn[r].load(dyp + tn * rs);
-            } else {
-                cn[r].zero(); dyn[r].zero();
-            }
-        }
-        const int64_t ta = r0 + n;
-        const float a_n = (ta >= t_lo && ta < wk.t_end) ? load_scalar<IO>(ap + ta * as) : 0.0f;
-        const int64_t tan_ = ta + STEP;
-        const float a_nn = (tan_ >= wk.t_begin && tan_ < t_la) ? load_scalar<IO>(ap + tan_ * as) : 0.0f;
-
-        // ---- look-ahead: reverse local solve of the next step's sub-block ----
-        // Only its first row is used here (the reverse carrier entering this
-        // step's last block); the full solve is redone when that step comes.
+        // ---- loads: this step's x, b, a and the next step's c, dy, a ---------
+        RH xr[NPASS][4], br[NPASS][4];
         {
-            // A operand: L^T, i.e. this lane holds L[4*grp + q][n] = a_{n+1} ... a_{4 grp + q}.
-            const float a_next = dpp<DPP_ROW_SHL + 1>(a_nn, 1.0f);   // a of token n+1
-            float LT[4];
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs);
+            const __amdgpu_buffer_rsrc_t rcn = rsrc(cb + (r0 + STEP) * rs), rdyn = rsrc(dyb + (r0 + STEP) * rs);
+            RH cn[NPASS][4], dyn[NPASS][4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int rho = 4 * grp + q;
-                const float v = row_suffix_prod(n < rho ? a_next : 1.0f);
-                LT[q] = n <= rho ? v : 0.0f;
+            for (int r = 0; r < 4; ++r) {
+                const int64_t t = tr0 + r, tn = t + STEP;
+                const bool okx = t >= t_lo && t < wk.t_end;
+                const bool okn = tn >= wk.t_begin && tn < t_la;
+#pragma unroll
+                for (int ps = 0; ps < NPASS; ++ps) {
+                    const uint32_t o = loff + (uint32_t)(r * rs + ps * PIECE * ES);
+                    xr[ps][r].load(rx, in_range(okx, o));
+                    br[ps][r].load(rb, in_range(okx, o));
+                    cn[ps][r].load(rcn, in_range(okn, o));
+                    dyn[ps][r].load(rdyn, in_range(okn, o));
+                }
             }
+            const int64_t tan_ = r0 + n + STEP;
+            const float a_nn = load_scalar<IO>(rsrc(ab + (r0 + STEP) * as),
+                                               in_range(tan_ >= wk.t_begin && tan_ < t_la, aoff));
+
+            // ---- look-ahead: first row of the next step's reverse solve ------
+            // It feeds the reverse carrier entering this step's last block.
+            float LT[4];
+            build_decay_transposed(a_nn, grp, n, LT);
             const typename Contract<IO>::A At = Contract<IO>::prep(LT);
             const float cn_ = shfl(row_prefix_prod(a_nn), 15);
             const float a0 = shfl(a_nn, 0);
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                float dh[4];
+            for (int ps = 0; ps < NPASS; ++ps)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) dh[q] = dyn[q].get(m) * cn[q].get(m);
-                const f32x4 Dn = Contract<IO>::run(At, dh);
-                if (grp == 0) s_df[bn][wv][n * CPL + m] = a0 * Dn[0];
-            }
+                for (int j = 0; j < CH; ++j) {
+                    float dh[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) dh[q] = dyn[ps][q].get(j) * cn[ps][q].get(j);
+                    const f32x4 Dn = Contract<IO>::run(At, dh);
+                    if (grp == 0) s_df[bn][wv][chan(ps, j)] = a0 * Dn[0];
+                }
             if (lane == 0) s_cf[bn][wv] = cn_;
-        }
-
-        // ---- this step: forward recompute and reverse local solve -----------
-        const Decay dk = build_decay(a_n, grp, n);
-        f32x4 W[CPL], Dl[CPL];
-        {
-            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+            if constexpr (Sh::HAND_LDS) {
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) {
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+                        for (int i = 0; i < HWD; ++i) {
+                            s_hand[hs ^ 1][wv][0][r][ps * HWD + i][lane] = cn[ps][r].w[i];
+                            s_hand[hs ^ 1][wv][1][r][ps * HWD + i][lane] = dyn[ps][r].w[i];
+                        }
+            }
+        }
+        const int64_t ta = r0 + n;
+        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
+
+        // ---- forward recompute: last local row W[15] of each channel ---------
+        const Decay dk = build_decay(a_n, grp, n);
+        const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+            for (int j = 0; j < CH; ++j) {
                 float u[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * br[q].get(m);
-                W[m] = Contract<IO>::run(A, u);
+                for (int q = 0; q < 4; ++q) u[q] = xr[ps][q].get(j) * br[ps][q].get(j);
+                const f32x4 W = Contract<IO>::run(A, u);
+                if (grp == 3) s_wl[bw][wv][chan(ps, j)] = W[3];
             }
-        }
-        {
-            const float a_next = dpp<DPP_ROW_SHL + 1>(a_n, 1.0f);
-            float LT[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int rho = 4 * grp + q;
-                const float v = row_suffix_prod(n < rho ? a_next : 1.0f);
-                LT[q] = n <= rho ? v : 0.0f;
-            }
-            const typename Contract<IO>::A At = Contract<IO>::prep(LT);
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                float dh[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) dh[q] = dyr[q].get(m) * cr[q].get(m);   // dh = dy * c
-                Dl[m] = Contract<IO>::run(At, dh);
-            }
-        }
-
-        if (grp == 3) {
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) s_wl[bw][wv][n * CPL + m] = W[m][3];
-        }
         if (lane == 63) s_c[bw][wv] = dk.c;
         __syncthreads();
 
-        // ---- forward carriers (as in the forward kernel) ---------------------
-        float ein[CPL], sin_[CPL];
+        if (!out_step) {
+            // Halo step: only advance the forward carriers.
+#pragma unroll 1
+            for (int r = 0; r < NW; ++r) {
+                if (r % S == 0) {
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; sin_[m] = 0.f; }
-        for (int r = 0; r < NW; ++r) {
-            if (r % S == 0) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
-            }
-            if (r == wv) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) { ein[m] = e[m]; sin_[m] = s[m]; }
-            }
-            const float c_ = s_c[bw][r];
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                const float wl = s_wl[bw][r][n * CPL + m];
-                e[m] = c_ * e[m] + wl;
-                s[m] = c_ * s[m] + wl;
-            }
-        }
-        if (!out_step) continue;
-
-        // ---- reverse carriers: from the end of the next step's first block --
-        // back to this wave's sub-block.  eps is the full adjoint entering a
-        // sub-block from the right, pr the one restarted at the block's end.
-        float eps[CPL], pr[CPL], epsin[CPL], prin[CPL];
-#pragma unroll
-        for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; epsin[m] = 0.f; prin[m] = 0.f; }
-        for (int r = S - 1; r >= 0; --r) {
-            if (r % S == S - 1) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
-            }
-            const float c_ = s_cf[bn][r];
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                const float df = s_df[bn][r][n * CPL + m];
-                eps[m] = c_ * eps[m] + df;
-                pr[m] = c_ * pr[m] + df;
-            }
-        }
-        for (int r = NW - 1; r >= wv; --r) {
-            if (r % S == S - 1) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
-            }
-            if (r == wv) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) { epsin[m] = eps[m]; prin[m] = pr[m]; }
-            } else {
-                const float c_ = s_cf[bc][r];
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) {
-                    const float df = s_df[bc][r][n * CPL + m];
-                    eps[m] = c_ * eps[m] + df;
-                    pr[m] = c_ * pr[m] + df;
+                    for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
+                const float c_ = s_c[bw][r];
+#pragma unroll
+                for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+                    for (int j = 0; j < CH; ++j) {
+                        const float wl = s_wl[bw][r][chan(ps, j)];
+                        e[ps * CH + j] = c_ * e[ps * CH + j] + wl;
+                        s[ps * CH + j] = c_ * s[ps * CH + j] + wl;
+                    }
             }
+            continue;
         }
 
-        // ---- gradients ---------------------------------------------------------
-        // r_q[k] = L[15][k] (last row of the sub-block operator) for this lane's rows.
-        const int base = lane & 48;
-        float R[4], Gsh[4];
+        // ---- per-step constants of the epilogue -----------------------------
+        float LTc[4];
+        build_decay_transposed(a_n, grp, n, LTc);
+        const typename Contract<IO>::A Atc = Contract<IO>::prep(LTc);
+        float Rr[4], Gsh[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) R[r] = shfl(dk.L[r], base + 15);
-        // G[k-1] with G[-1] = 1: the decay product before each row.
+        for (int r = 0; r < 4; ++r) Rr[r] = shfl(dk.L[r], base + 15);   // r_q = L[15][.] at this lane's rows
         {
-            const float gprev = shfl(dk.G[3], (lane - 16) & 63);   // G[4 grp - 1] from the row group above
+            const float gprev = shfl(dk.G[3], (lane - 16) & 63);      // G[k-1], G[-1] = 1
             Gsh[0] = grp == 0 ? 1.0f : gprev;
             Gsh[1] = dk.G[0]; Gsh[2] = dk.G[1]; Gsh[3] = dk.G[2];
         }
-        // Local state of the row above each of this lane's rows (0 above row 0).
-        float wup[CPL];
+        float da_acc[4] = {0.f, 0.f, 0.f, 0.f};
+        const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * rs),
+                                     rdc = rsrc(dcb + r0 * rs);
+
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) {
-            const float v = shfl(W[m][3], (lane - 16) & 63);
-            wup[m] = grp == 0 ? 0.0f : v;
+        for (int ps = 0; ps < NPASS; ++ps) {
+            const int m0 = ps * CH;
+            // c and dy of this step for the pass's channels.
+            RH cr[4], dyr[4];
+            if constexpr (Sh::HAND_LDS) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < HWD; ++i) {
+                        cr[r].w[i] = s_hand[hs][wv][0][r][ps * HWD + i][lane];
+                        dyr[r].w[i] = s_hand[hs][wv][1][r][ps * HWD + i][lane];
+                    }
+            } else {
+                const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs + ps * PIECE * ES));
+                    cr[r].load(rc, o);
+                    dyr[r].load(rdy, o);
+                }
+            }
+
+            // Forward carriers entering this wave's sub-block, and their update.
+            float ein[CH], sin_[CH];
+#pragma unroll
+            for (int j = 0; j < CH; ++j) { ein[j] = 0.f; sin_[j] = 0.f; }
+#pragma unroll 1
+            for (int r = 0; r < NW; ++r) {
+                if (r % S == 0) {
+#pragma unroll
+                    for (int j = 0; j < CH; ++j) { e[m0 + j] = s[m0 + j]; s[m0 + j] = 0.f; }
+                }
+                if (r == wv) {
+#pragma unroll
+                    for (int j = 0; j < CH; ++j) { ein[j] = e[m0 + j]; sin_[j] = s[m0 + j]; }
+                }
+                const float c_ = s_c[bw][r];
+#pragma unroll
+                for (int j = 0; j < CH; ++j) {
+                    const float wl = s_wl[bw][r][chan(ps, j)];
+                    e[m0 + j] = c_ * e[m0 + j] + wl;
+                    s[m0 + j] = c_ * s[m0 + j] + wl;
+                }
+            }
+            // Reverse carriers: from the end of the next step's first block back
+            // to this wave's sub-block.  eps is the full adjoint entering a
+            // sub-block from the right, pr the one restarted at its block's end.
+            float eps[CH], pr[CH];
+#pragma unroll
+            for (int j = 0; j < CH; ++j) { eps[j] = 0.f; pr[j] = 0.f; }
+#pragma unroll 1
+            for (int r = S - 1; r >= 0; --r) {
+                const float c_ = s_cf[bn][r];
+#pragma unroll
+                for (int j = 0; j < CH; ++j) pr[j] = c_ * pr[j] + s_df[bn][r][chan(ps, j)];
+            }
+#pragma unroll 1
+            for (int r = NW - 1; r >= wv; --r) {
+                if (r % S == S - 1) {
+#pragma unroll
+                    for (int j = 0; j < CH; ++j) { eps[j] = pr[j]; pr[j] = 0.f; }
+                }
+                if (r > wv) {
+                    const float c_ = s_cf[bc][r];
+#pragma unroll
+                    for (int j = 0; j < CH; ++j) {
+                        const float df = s_df[bc][r][chan(ps, j)];
+                        eps[j] = c_ * eps[j] + df;
+                        pr[j] = c_ * pr[j] + df;
+                    }
+                }
+            }
+
+            // Recompute this pass's tiles: W = L (b*x) and D = L^T (c*dy).
+            f32x4 W[CH], Dl[CH];
+            float wup[CH];   // local state of the row above this lane's first row (0 above row 0)
+#pragma unroll
+            for (int j = 0; j < CH; ++j) {
+                float u[4], dh[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    u[q] = xr[ps][q].get(j) * br[ps][q].get(j);
+                    dh[q] = dyr[q].get(j) * cr[q].get(j);
+                }
+                W[j] = Contract<IO>::run(A, u);
+                Dl[j] = Contract<IO>::run(Atc, dh);
+                const float v = shfl(W[j][3], (lane - 16) & 63);
+                wup[j] = grp == 0 ? 0.0f : v;
+            }
+
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t t = tr0 + r;
+                float vdx[CH], vdb[CH], vdc[CH];
+                float acc = 0.f, acc2 = 0.f;
+#pragma unroll
+                for (int j = 0; j < CH; ++j) {
+                    const float hv = W[j][r] + dk.G[r] * ein[j];           // jagged-window state
+                    const float dyv = dyr[r].get(j);
+                    vdc[j] = dyv * hv;
+                    const float du = Dl[j][r] + Rr[r] * eps[j];            // adjoint of u
+                    const float dblk = Dl[j][r] + Rr[r] * pr[j];           // ... from this block's rows
+                    vdx[j] = br[ps][r].get(j) * du;
+                    if (p.residual) vdx[j] += dyv;
+                    vdb[j] = xr[ps][r].get(j) * du;
+                    const float wprev = r == 0 ? wup[j] : W[j][r - 1];
+                    acc += wprev * du;
+                    acc2 += sin_[j] * du + (ein[j] - sin_[j]) * dblk;
+                }
+                da_acc[r] += acc + Gsh[r] * acc2;
+                const uint32_t o = in_range(t >= wk.t_begin && t < wk.t_end,
+                                            loff + (uint32_t)(r * rs + ps * PIECE * ES));
+                store_row<IO, CH>(rdx, o, vdx);
+                store_row<IO, CH>(rdb, o, vdb);
+                store_row<IO, CH>(rdc, o, vdc);
+            }
         }
-        float da_part[4];
+        const __amdgpu_buffer_rsrc_t rda = rsrc(dab + r0 * das);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+            const float tot = row_sum(da_acc[r]);
             const int64_t t = tr0 + r;
-            float vdx[CPL], vdb[CPL], vdc[CPL];
-            float acc = 0.f, acc2 = 0.f;
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                const float hv = W[m][r] + dk.G[r] * ein[m];           // jagged-window state
-                const float dyv = dyr[r].get(m);
-                vdc[m] = dyv * hv;
-                const float du = Dl[m][r] + R[r] * epsin[m];           // adjoint of u
-                const float dblk = Dl[m][r] + R[r] * prin[m];          // ... from this block's rows only
-                vdx[m] = br[r].get(m) * du;
-                if (p.residual) vdx[m] += dyv;
-                vdb[m] = xr[r].get(m) * du;
-                const float wprev = r == 0 ? wup[m] : W[m][r - 1];
-                acc += wprev * du;
-                acc2 += sin_[m] * du + (ein[m] - sin_[m]) * dblk;
-            }
-            da_part[r] = acc + Gsh[r] * acc2;
-            if (t >= wk.t_begin && t < wk.t_end) {
-                store_row<IO, CPL>(dxp + t * rs, vdx);
-                store_row<IO, CPL>(dbp + t * rs, vdb);
-                store_row<IO, CPL>(dcp + t * rs, vdc);
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float tot = row_sum(da_part[r]);
-            const int64_t t = tr0 + r;
-            if (n == 0 && t >= wk.t_begin && t < wk.t_end) dap[t * p.sa_t] = tot;
+            __builtin_amdgcn_raw_buffer_store_b32(
+                __builtin_bit_cast(int, tot), rda,
+                (int)in_range(n == 0 && t >= wk.t_begin && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, 0);
         }
     }
 }
