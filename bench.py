@@ -39,12 +39,16 @@ def log(msg):
 
 
 def algorithmic_bytes(cfg, backward):
-    """HBM bytes one launch must move: inputs read once, outputs written once."""
+    """HBM bytes one launch must move: inputs read once, outputs written once.
+    The block carriers (4*D bytes per block per (batch, head), written by the
+    forward and read by the backward: 4*D/block bytes per token-head) are part
+    of the algorithm's state and are counted."""
     e = 2 if cfg.dtype == "bf16" else 4
     th = cfg.B * cfg.T * cfg.H
-    if backward:   # x, b, c, dy, a in; dx, db, dc out; da out in fp32
-        return th * (e * (7 * cfg.D + 1) + 4)
-    return th * e * (4 * cfg.D + 1)   # x, b, c, a in; y out
+    carriers = th * 4 * cfg.D // cfg.block
+    if backward:   # x, b, c, dy, a, carriers in; dx, db, dc out; da out in fp32
+        return th * (e * (7 * cfg.D + 1) + 4) + carriers
+    return th * e * (4 * cfg.D + 1) + carriers   # x, b, c, a in; y, carriers out
 
 
 def contraction_flops(cfg, backward):
@@ -152,16 +156,18 @@ def main():
     y = torch.empty_like(x)
     dx, db, dc = (torch.empty_like(x) for _ in range(3))
     da = torch.empty(a.shape, dtype=torch.float32, device=a.device)
+    carriers = torch.empty(swr.carrier_shape(x, cfg.block), dtype=torch.float32, device=x.device)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        swr.swr_forward(x, a, b, c, cfg.block, y=y, run_len=args.run_len)
+        swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len)
         if ev is not None:
             ev[1].record(stream)
-        swr.swr_backward(x, a, b, c, dy, cfg.block, outputs=(dx, da, db, dc), run_len=args.run_len)
+        swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
+                         run_len=args.run_len)
         if ev is not None:
             ev[2].record(stream)
 

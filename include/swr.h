@@ -21,6 +21,15 @@
  *
  * swr_backward returns the exact gradients of that (truncated) forward.
  *
+ * Block carriers.  For every block t the forward can save the carrier
+ * v_t = w_{t,l}, the last state of the block's local solve started from zero
+ * (the "effective input" that the Block Two-Pass algorithm hands to block
+ * t+1; the paper suggests checkpointing only this carrier).  They are D
+ * float32 values per block: a [B][H][ceil(T/block)][D] array, contiguous,
+ * 0.4% of the forward's traffic at D = 128, block = 128.  swr_backward reads
+ * them instead of re-reading the previous block's x, b and a; swr_carriers
+ * recomputes them for callers that did not keep them.
+ *
  * Tensor layout.  x, b, c, y, dy, dx, db, dc are [B, T, H, D] with the channel
  * dimension D contiguous (stride 1) and element strides sx_b, sx_t, sx_h for
  * the other three dimensions (shared by all eight tensors).  a is [B, T, H]
@@ -59,7 +68,8 @@ typedef enum swr_status {
     SWR_ERR_BLOCK = -4,       /* block is not 16, 32, 64 or 128                           */
     SWR_ERR_ALIGN = -5,       /* a pointer or stride breaks the vector alignment          */
     SWR_ERR_ALIAS = -6,       /* an output overlaps an input or another output            */
-    SWR_ERR_UNSUPPORTED = -7, /* D not in {16, 32, 64, 128}, unknown flags, run_len bad   */
+    SWR_ERR_UNSUPPORTED = -7, /* D not in {16, 32, 64, 128}, unknown flags, bad run_len,
+                                 or strides/sizes beyond the kernels' 32-bit offsets       */
     SWR_ERR_HIP = -8,         /* the HIP runtime rejected the launch                      */
     SWR_ERR_VERSION = -9      /* problem->abi_version != SWR_ABI_VERSION                  */
 } swr_status_t;
@@ -89,16 +99,28 @@ typedef struct swr_problem {
 
 /* Forward: y = SWR(x, a, b, c).  Alignment: x, b, c, y and every sx_* must be
  * multiples of min(16 bytes, D/16 elements) (i.e. each lane's slice of a row is
- * a naturally aligned vector); a needs the alignment of one element. */
+ * a naturally aligned vector); a needs the alignment of one element.
+ * carriers: NULL, or swr_carrier_elems(problem) float32 values (16-byte
+ * aligned) that receive the block carriers for swr_backward. */
 int swr_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
-                const void* c, void* y, void* stream);
+                const void* c, void* y, float* carriers, void* stream);
+
+/* Block carriers alone (what swr_forward writes to `carriers`), from x, a, b. */
+int swr_carriers(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                 float* carriers, void* stream);
 
 /* Backward: given dy = dL/dy, writes dx, da (float32, [B,T,H] at a's strides),
- * db and dc.  Inputs are those of the forward; nothing from the forward pass is
- * saved or needed (the kernel recomputes what it uses). */
+ * db and dc.  x, a, b, c are the forward's inputs and `carriers` the block
+ * carriers of those same inputs (from swr_forward or swr_carriers; required).
+ * Nothing else from the forward is needed: the kernel recomputes the local
+ * solves it uses. */
 int swr_backward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
-                 const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
-                 void* stream);
+                 const void* c, const void* dy, const float* carriers, void* dx, float* da,
+                 void* db, void* dc, void* stream);
+
+/* Number of float32 block carriers of a problem, B * H * ceil(T / block) * D,
+ * or a negative SWR_ERR_* code for a problem with invalid shape fields. */
+int64_t swr_carrier_elems(const swr_problem_t* problem);
 
 /* Static English description of a status code (never NULL). */
 const char* swr_error_string(int code);

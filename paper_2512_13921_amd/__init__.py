@@ -9,15 +9,17 @@ GPU, the calls raise.
 Layouts: ``x, b, c, y, dy, dx, db, dc`` are ``[B, T, H, D]`` (channels
 contiguous, all with the same strides); ``a`` is ``[B, T, H]`` in the same
 dtype; ``da`` is float32 with ``a``'s shape.  Supported dtypes: float32 and
-bfloat16.
+bfloat16.  The block carriers that the forward saves for the backward are a
+float32 ``[B, H, ceil(T / block), D]`` tensor (``carrier_shape``).
 """
 import ctypes
 import os
 
 from . import build as _build
 
-__all__ = ["SwrError", "swr_forward", "swr_backward", "swr_error_string", "swr_abi_version",
-           "swr_launch_info", "SWRFunction", "library_path", "load"]
+__all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error_string",
+           "swr_abi_version", "swr_launch_info", "swr_carrier_elems", "carrier_shape",
+           "SWRFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
 SWR_DTYPE_F32 = 0
@@ -61,10 +63,14 @@ def load():
         lib = ctypes.CDLL(_build.LIB)
         P = ctypes.POINTER(SwrProblem)
         vp = ctypes.c_void_p
-        lib.swr_forward.argtypes = [P, vp, vp, vp, vp, vp, vp]
+        lib.swr_forward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
         lib.swr_forward.restype = ctypes.c_int
-        lib.swr_backward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.swr_carriers.argtypes = [P, vp, vp, vp, vp, vp]
+        lib.swr_carriers.restype = ctypes.c_int
+        lib.swr_backward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.swr_backward.restype = ctypes.c_int
+        lib.swr_carrier_elems.argtypes = [P]
+        lib.swr_carrier_elems.restype = ctypes.c_int64
         lib.swr_error_string.argtypes = [ctypes.c_int]
         lib.swr_error_string.restype = ctypes.c_char_p
         lib.swr_abi_version.restype = ctypes.c_int
@@ -108,6 +114,20 @@ def swr_launch_info(problem: SwrProblem):
     if rc != 0:
         raise SwrError(rc, "swr_launch_info")
     return r.value, f.value, b.value
+
+
+def swr_carrier_elems(problem: SwrProblem) -> int:
+    """Number of float32 block carriers of a problem."""
+    n = int(load().swr_carrier_elems(ctypes.byref(problem)))
+    if n < 0:
+        raise SwrError(n, "swr_carrier_elems")
+    return n
+
+
+def carrier_shape(x, block):
+    """Shape [B, H, ceil(T / block), D] of the block-carrier tensor for x."""
+    B, T, H, D = x.shape
+    return (B, H, -(-T // block), D)
 
 
 # ----------------------------------------------------------------------------- torch marshalling
@@ -157,8 +177,23 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def swr_forward(x, a, b, c, block, residual=False, y=None, run_len=0, stream=None):
-    """y = SWR(x, a, b, c) on the GPU (see ``include/swr.h``).  Returns y."""
+def _carrier_tensor(x, block, carriers):
+    torch = _torch()
+    shape = carrier_shape(x, block)
+    if carriers is None:
+        return torch.empty(shape, dtype=torch.float32, device=x.device)
+    if (tuple(carriers.shape) != shape or carriers.dtype != torch.float32
+            or not carriers.is_contiguous() or carriers.device != x.device):
+        raise ValueError(f"carriers must be a contiguous float32 tensor of shape {shape}")
+    return carriers
+
+
+def swr_forward(x, a, b, c, block, residual=False, y=None, carriers=None, save_carriers=False,
+                run_len=0, stream=None):
+    """y = SWR(x, a, b, c) on the GPU (see ``include/swr.h``).
+
+    Returns y, or (y, carriers) when ``save_carriers`` is true or a carrier
+    tensor is passed in (it is filled)."""
     torch = _torch()
     problem = _problem_from(x, a, block, residual, run_len)
     _same_layout(x, b, c)
@@ -166,18 +201,38 @@ def swr_forward(x, a, b, c, block, residual=False, y=None, run_len=0, stream=Non
         y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
     else:
         _same_layout(x, y)
+    want_v = save_carriers or carriers is not None
+    v = _carrier_tensor(x, block, carriers) if want_v else None
     rc = load().swr_forward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y),
-                            _stream(stream, x.device))
+                            _ptr(v) if want_v else None, _stream(stream, x.device))
     if rc != 0:
         raise SwrError(rc, "swr_forward")
-    return y
+    return (y, v) if want_v else y
 
 
-def swr_backward(x, a, b, c, dy, block, residual=False, outputs=None, run_len=0, stream=None):
-    """(dx, da, db, dc) of the SWR forward given dy (see ``include/swr.h``)."""
+def swr_carriers(x, a, b, block, carriers=None, run_len=0, stream=None):
+    """The block carriers swr_forward would save, computed from x, a, b alone."""
+    problem = _problem_from(x, a, block, False, run_len)
+    _same_layout(x, b)
+    v = _carrier_tensor(x, block, carriers)
+    rc = load().swr_carriers(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(v),
+                             _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_carriers")
+    return v
+
+
+def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, run_len=0,
+                 stream=None):
+    """(dx, da, db, dc) of the SWR forward given dy and the forward's block
+    carriers (see ``include/swr.h``)."""
     torch = _torch()
     problem = _problem_from(x, a, block, residual, run_len)
     _same_layout(x, b, c, dy)
+    if carriers is None:
+        raise ValueError("swr_backward needs the forward's block carriers: "
+                         "swr_forward(..., save_carriers=True) or swr_carriers(x, a, b, block)")
+    carriers = _carrier_tensor(x, block, carriers)
     if outputs is None:
         dx, db, dc = (torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
                       for _ in range(3))
@@ -188,7 +243,8 @@ def swr_backward(x, a, b, c, dy, block, residual=False, outputs=None, run_len=0,
         if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
             raise ValueError("da must be float32 with the shape and strides of a")
     rc = load().swr_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
-                             _ptr(dx), _ptr(da), _ptr(db), _ptr(dc), _stream(stream, x.device))
+                             _ptr(carriers), _ptr(dx), _ptr(da), _ptr(db), _ptr(dc),
+                             _stream(stream, x.device))
     if rc != 0:
         raise SwrError(rc, "swr_backward")
     return dx, da, db, dc
@@ -204,15 +260,16 @@ def _autograd_function():
         @staticmethod
         def forward(ctx, x, a, b, c, block, residual=False):
             ctx.block, ctx.residual = block, residual
-            ctx.save_for_backward(x, a, b, c)
-            return swr_forward(x, a, b, c, block, residual)
+            y, v = swr_forward(x, a, b, c, block, residual, save_carriers=True)
+            ctx.save_for_backward(x, a, b, c, v)     # the carriers are the only extra state
+            return y
 
         @staticmethod
         def backward(ctx, dy):
-            x, a, b, c = ctx.saved_tensors
+            x, a, b, c, v = ctx.saved_tensors
             dy = dy if dy.stride() == x.stride() else torch.empty_strided(
                 x.shape, x.stride(), dtype=x.dtype, device=x.device).copy_(dy)
-            dx, da, db, dc = swr_backward(x, a, b, c, dy, ctx.block, ctx.residual)
+            dx, da, db, dc = swr_backward(x, a, b, c, dy, v, ctx.block, ctx.residual)
             return dx, da.to(a.dtype), db, dc, None, None
 
     return _SWRFunction

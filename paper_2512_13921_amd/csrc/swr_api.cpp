@@ -50,11 +50,14 @@ struct Resolved {
     bool empty;
     int es;             // bytes per I/O element
     int cpl;            // channels per lane = D / 16
-    int nw;             // waves per workgroup
+    int nw;             // waves per backward workgroup
+    int nw_fwd;         // waves per forward workgroup
     int64_t step;       // tokens per workgroup step
     int64_t run_len, nruns, nwork;
     int64_t xspan;      // bytes spanned by one [B,T,H,D] tensor
     int64_t aspan;      // elements spanned by a / da
+    int64_t nblocks;    // blocks per sequence
+    int64_t carriers;   // float32 carriers of the whole problem
 };
 
 int resolve(const swr_problem_t* p, Resolved* r) {
@@ -68,8 +71,9 @@ int resolve(const swr_problem_t* p, Resolved* r) {
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
     r->cpl = (int)(p->D / 16);
-    r->nw = swr::waves_for_block(p->block);
-    r->step = (int64_t)r->nw * 16;
+    r->nw = swr::bwd_waves_for_block(p->block);
+    r->nw_fwd = swr::fwd_waves_for_block(p->block);
+    r->step = (int64_t)std::max(r->nw, r->nw_fwd) * 16;   // both sweeps' steps divide a run
     if (p->run_len < 0 || (p->run_len > 0 && p->run_len % r->step != 0)) return SWR_ERR_UNSUPPORTED;
 
     r->empty = p->B == 0 || p->T == 0 || p->H == 0;
@@ -97,6 +101,17 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
     if (!r->empty && r->nruns > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
     r->nwork = seqs * r->nruns;
+    r->nblocks = (p->T + p->block - 1) / p->block;
+    r->carriers = seqs * r->nblocks * p->D;
+    if (!r->empty) {
+        // The kernels address a lane's data with 32-bit byte offsets from a
+        // per-step base: 16 rows of x-like tensors, 16 tokens of a / da, and a
+        // (batch, head)'s carrier array must stay below 2^31 bytes.
+        const int64_t lim = 0x7fffffffLL;
+        if (p->sx_t > (lim - p->D * r->es) / (16 * r->es)) return SWR_ERR_UNSUPPORTED;
+        if (p->sa_t > lim / (16 * 4)) return SWR_ERR_UNSUPPORTED;
+        if (r->nblocks > lim / (p->D * 4)) return SWR_ERR_UNSUPPORTED;
+    }
     return SWR_OK;
 }
 
@@ -128,6 +143,7 @@ swr::Params make_params(const swr_problem_t* p, const Resolved& r) {
     k.run_len = r.run_len;
     k.nruns = r.nruns;
     k.nwork = r.nwork;
+    k.nblocks = r.nblocks;
     return k;
 }
 
@@ -164,44 +180,76 @@ int swr_launch_info(const swr_problem_t* problem, int64_t* run_len, int64_t* fwd
     return SWR_OK;
 }
 
-int swr_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
-                const void* c, void* y, void* stream) {
+int64_t swr_carrier_elems(const swr_problem_t* problem) {
+    Resolved r;
+    const int rc = resolve(problem, &r);
+    return rc != SWR_OK ? rc : r.carriers;
+}
+
+namespace {
+
+// Shared by swr_forward (y != NULL) and swr_carriers (y == NULL).
+int forward_impl(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                 const void* c, void* y, float* carriers, void* stream) {
     Resolved r;
     int rc = resolve(p, &r);
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
-    if (!x || !a || !b || !c || !y) return SWR_ERR_NULL;
+    if (!x || !a || !b || (y && !c)) return SWR_ERR_NULL;
     const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
     for (const void* q : {x, b, c, (const void*)y})
-        if (!aligned(q, vb)) return SWR_ERR_ALIGN;
-    if (!aligned(a, r.es)) return SWR_ERR_ALIGN;
+        if (q && !aligned(q, vb)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
-    const Span sy = span(y, r.xspan);
-    for (const Span& s : {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es)})
-        if (overlap(sy, s)) return SWR_ERR_ALIAS;
+    const Span ins[4] = {span(x, r.xspan), span(b, r.xspan), span(c, c ? r.xspan : 0),
+                         span(a, r.aspan * r.es)};
+    const Span sy = span(y, y ? r.xspan : 0), sv = span(carriers, carriers ? r.carriers * 4 : 0);
+    for (const Span& s : ins)
+        if (overlap(sy, s) || overlap(sv, s)) return SWR_ERR_ALIAS;
+    if (overlap(sy, sv)) return SWR_ERR_ALIAS;
 
     swr::Params k = make_params(p, r);
-    k.x = x; k.a = a; k.b = b; k.c = c; k.y = y;
-    return swr::launch(k, p->dtype, (int)p->D, r.nw, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
+    return swr::launch(k, p->dtype, (int)p->D, r.nw_fwd, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+}  // namespace
+
+int swr_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                const void* c, void* y, float* carriers, void* stream) {
+    Resolved r;
+    const int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    if (!r.empty && !y) return SWR_ERR_NULL;
+    return forward_impl(p, x, a, b, c, y, carriers, stream);
+}
+
+int swr_carriers(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                 float* carriers, void* stream) {
+    Resolved r;
+    const int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    if (!r.empty && !carriers) return SWR_ERR_NULL;
+    return forward_impl(p, x, a, b, nullptr, nullptr, carriers, stream);
 }
 
 int swr_backward(const swr_problem_t* p, const void* x, const void* a, const void* b,
-                 const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
-                 void* stream) {
+                 const void* c, const void* dy, const float* carriers, void* dx, float* da,
+                 void* db, void* dc, void* stream) {
     Resolved r;
     int rc = resolve(p, &r);
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
-    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return SWR_ERR_NULL;
+    if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc) return SWR_ERR_NULL;
     const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
     for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
         if (!aligned(q, vb)) return SWR_ERR_ALIGN;
-    if (!aligned(a, r.es) || !aligned(da, 4)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es) || !aligned(da, 4) || !aligned(carriers, 16)) return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     const Span outs[4] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan),
                           span(da, r.aspan * 4)};
-    const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
-                         span(a, r.aspan * r.es)};
+    const Span ins[6] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
+                         span(a, r.aspan * r.es), span(carriers, r.carriers * 4)};
     for (int i = 0; i < 4; ++i) {
         for (const Span& s : ins)
             if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
@@ -212,6 +260,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     swr::Params k = make_params(p, r);
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+    k.carriers = const_cast<float*>(carriers);
     return swr::launch(k, p->dtype, (int)p->D, r.nw, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 

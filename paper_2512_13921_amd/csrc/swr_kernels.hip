@@ -394,13 +394,20 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
     const int64_t as = p.sa_t * ES;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const bool want_y = p.y != nullptr;            // false: only the block carriers are produced
+    float* const vb = p.carriers ? p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D : nullptr;
+    const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
 
     float e[CPL], s[CPL];   // carriers at the start of the step: full and block-restarted
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
 
+    // Sweep to the end of the run's last block: when the sequence ends inside a
+    // block, the step holding that block's last sub-block still computes its
+    // carrier (its rows past the end are masked, so it moves no data).
+    const int64_t t_stop = ((wk.t_end + l - 1) / l) * l;
     int buf = 0;
-    for (int64_t t0 = wk.t_begin - halo * STEP; t0 < wk.t_end; t0 += STEP, buf ^= 1) {
+    for (int64_t t0 = wk.t_begin - halo * STEP; t0 < t_stop; t0 += STEP, buf ^= 1) {
         const int64_t r0 = t0 + wv * SB;          // first token of this wave's sub-block (uniform)
         const int64_t tr0 = r0 + 4 * grp;         // first of this lane's four tokens
 
@@ -415,10 +422,13 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
             const uint32_t ox = in_range(t >= t_lo && t < wk.t_end, o);
             xr[r].load(rx, ox);
             br[r].load(rb, ox);
-            cr[r].load(rc, in_range(t >= wk.t_begin && t < wk.t_end, o));
+            cr[r].load(rc, in_range(want_y && t >= wk.t_begin && t < wk.t_end, o));
         }
         const int64_t ta = r0 + n;
-        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
+        // Past the end of the sequence the decay is 1 (and u = 0), so the
+        // carrier of a partial last block is the state at its last token.
+        const float a_n = ta >= p.T ? 1.0f
+                          : load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
 
         // ---- local solve W = L U on the matrix cores ---------------------
         const Decay dk = build_decay(a_n, grp, n);
@@ -440,11 +450,14 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
         if (lane == 63) s_c[buf][wv] = dk.c;
         __syncthreads();
 
-        float ein[CPL];
+        // A step need not start at a block boundary: phase of its first sub-block.
+        const int ph = (int)((t0 / SB) % S);
+        float ein[CPL], vout[CPL];
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) ein[m] = 0.f;
+        for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
+#pragma unroll 1
         for (int r = 0; r < NW; ++r) {
-            if (r % S == 0) {   // a block starts: its carry-in is the previous block's v
+            if ((ph + r) % S == 0) {   // a block starts: its carry-in is the previous block's v
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -459,7 +472,20 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
                 e[m] = cr_ * e[m] + wl;
                 s[m] = cr_ * s[m] + wl;
             }
+            if (r == wv) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) vout[m] = s[m];
+            }
         }
+        // The wave holding a block's last sub-block saves that block's carrier
+        // v_t (its block-restarted end state) for the backward.
+        if (vb && (ph + wv) % S == S - 1) {
+            const int64_t blk = r0 / l;
+            const int64_t t_blk = blk * l;   // first token of the block (it may end past T)
+            store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
+                                               (uint32_t)(blk * D + n * CPL) * 4u), vout);
+        }
+        if (!want_y) continue;
 
         // ---- rank-one injection, read-out gate, store ----------------------
 #pragma unroll
@@ -501,50 +527,35 @@ __device__ inline void build_decay_transposed(float a_n, int grp, int n, float (
 // state entering step k times the adjoint leaving it, for the two windows
 // that contain k:  da_k = sum_mu [ w_{t,k-1} du_k + g_{t,k-1} v_{t-1} D_{t,k} ]
 // with w the block-restarted local state, D_t = L_t^T dh_t and v_{t-1} the
-// previous block's carrier (w_{t,-1} = 0, g_{t,-1} = 1).
+// previous block's carrier (w_{t,-1} = 0, g_{t,-1} = 1).  Writing it with the
+// jagged-window state H entering row k (H_{-1} = the carrier entering the
+// sub-block) and the restarted reverse carrier p:
+//     da_k = sum_mu H_{k-1} du_k  -  g_{k-1} r_k sum_mu (e - s)(eps - p)
+// where (e, s) / (eps, p) are the forward / reverse carriers entering the
+// sub-block; the second sum is one number per sub-block and lane.
 //
-// Register budget: the step's look-ahead tiles (c, dy of the next step) are
-// handed to the next step through a wave-private LDS slot (two slots used in
-// turn), and the epilogue runs over the channels in NPASS passes, each
-// recomputing its part of W = L u and D = L^T dh on the matrix cores, so that
-// only one pass's accumulators are live at a time.  In pass ps lane n owns
-// channels ps*16*CH + n*CH .. + CH-1, so every load and store instruction
-// covers 16*CH contiguous channels of a row (whole memory sectors).
-template <class IO, int CPL, int NW>
-struct BwdShape {
-    static constexpr int NPASS = CPL >= 4 ? 2 : 1;      // epilogue passes
-    static constexpr int CH = CPL / NPASS;               // channels per lane per pass
-    static constexpr int HWD = Row<IO, CH>::NWORDS;      // words of one lane's pass slice
-    static constexpr int NWD = NPASS * HWD;
-    static constexpr int HAND_BYTES = 2 * NW * 2 * 4 * NWD * 64 * 4;
-    // Hand over through LDS when both slots fit beside the carrier buffers;
-    // otherwise the next step re-reads c and dy from global memory.
-    static constexpr bool HAND_LDS = HAND_BYTES <= 128 * 1024;
-};
-
+// Schedule: a workgroup sweeps its run from the last step to the first.  The
+// reverse carriers then arrive from the step processed before, and the
+// forward carrier entering each step is the previous block's carrier v,
+// saved by the forward pass (the paper's "checkpoint only the carrier").
+// Only the run's end needs a halo: the first block after the run (c, dy, a)
+// gives the reverse carrier entering it.  Nothing is read twice.
 template <class IO, int CPL, int NW>
 __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
     constexpr int D = CPL * SB;
     constexpr int STEP = NW * SB;
     constexpr int ES = IO::ES;
-    using Sh = BwdShape<IO, CPL, NW>;
-    using RH = Row<IO, Sh::CH>;
-    constexpr int NPASS = Sh::NPASS, CH = Sh::CH, HWD = Sh::HWD, NWD = Sh::NWD;
-    constexpr int PIECE = 16 * CH;                       // channels covered by one pass
-    __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve
+    using R_ = Row<IO, CPL>;
+    __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve L u
+    __shared__ float s_df[2][NW][D];    // a_0 * first row of each sub-block's L^T dh
     __shared__ float s_c[2][NW];        // decay product of each sub-block
-    __shared__ float s_df[3][NW][D];    // a_0 * first row of each sub-block's L^T dh
-    __shared__ float s_cf[3][NW];       // decay products for the reverse carriers
-    // Wave-private hand-over of the look-ahead's c and dy tiles: [slot][wave][c|dy][row][word][lane].
-    __shared__ uint32_t s_hand[Sh::HAND_LDS ? 2 : 1][Sh::HAND_LDS ? NW : 1][2][4][NWD][64];
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work(p);
     const int l = p.block;
     const int S = l / SB;
-    const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);
-    const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the look-ahead
+    const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the halo block
 
     const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
     const char* xb = (const char*)p.x + xo;
@@ -557,128 +568,201 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
     const int64_t ao = wk.b * p.sa_b + wk.h * p.sa_h;
     const char* ab = (const char*)p.a + ao * ES;
     char* dab = (char*)(p.da + ao);
+    const float* vb = p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D;
     const int64_t rs = p.sx_t * ES;
     const int64_t as = p.sa_t * ES;
     const int64_t das = p.sa_t * 4;
-    // Byte offset of this lane's slice in pass 0 of row 4*grp; pass ps adds ps*PIECE channels.
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CH * ES);
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das;
     const int base = lane & 48;   // first lane of this 16-lane row
-    auto chan = [&](int ps, int j) { return ps * PIECE + n * CH + j; };   // channel of slot (ps, j)
 
-    float e[CPL], s[CPL];   // forward carriers at the step start (full, block-restarted)
+    // Reverse carriers at the end of the step about to be processed: the
+    // full adjoint entering from the right (eps) and the one restarted at the
+    // end of the current block (pr).
+    float eps[CPL], pr[CPL];
 #pragma unroll
-    for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
+    for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; }
+    int buf = 0;
 
-    // The sweep starts one step early (the halo step): it recovers the forward
-    // carrier entering the run and the look-ahead for the run's first step.
-    int k = 0;
-    for (int64_t t0 = wk.t_begin - STEP; t0 < wk.t_end; t0 += STEP, ++k) {
-        const int bw = k & 1, bc = k % 3, bn = (k + 1) % 3;
-        const int hs = Sh::HAND_LDS ? (k & 1) : 0;          // slot holding this step's c, dy
-        const int64_t r0 = t0 + wv * SB;
+    // ---- halo: the first block after the run -----------------------------------
+    if (wk.t_end < p.T) {
+        const int64_t r0 = wk.t_end + wv * SB;
         const int64_t tr0 = r0 + 4 * grp;
-        const bool out_step = t0 >= wk.t_begin;
-
-        // ---- loads: this step's x, b, a and the next step's c, dy, a ---------
-        RH xr[NPASS][4], br[NPASS][4];
-        {
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs);
-            const __amdgpu_buffer_rsrc_t rcn = rsrc(cb + (r0 + STEP) * rs), rdyn = rsrc(dyb + (r0 + STEP) * rs);
-            RH cn[NPASS][4], dyn[NPASS][4];
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+        R_ cr[4], dyr[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t t = tr0 + r, tn = t + STEP;
-                const bool okx = t >= t_lo && t < wk.t_end;
-                const bool okn = tn >= wk.t_begin && tn < t_la;
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(tr0 + r < t_la, loff + (uint32_t)(r * rs));
+            cr[r].load(rc, o);
+            dyr[r].load(rdy, o);
+        }
+        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < t_la, aoff));
+        float LT[4];
+        build_decay_transposed(a_n, grp, n, LT);
+        const typename Contract<IO>::A At = Contract<IO>::prep(LT);
+        const float a0 = shfl(a_n, 0);
 #pragma unroll
-                for (int ps = 0; ps < NPASS; ++ps) {
-                    const uint32_t o = loff + (uint32_t)(r * rs + ps * PIECE * ES);
-                    xr[ps][r].load(rx, in_range(okx, o));
-                    br[ps][r].load(rb, in_range(okx, o));
-                    cn[ps][r].load(rcn, in_range(okn, o));
-                    dyn[ps][r].load(rdyn, in_range(okn, o));
-                }
+        for (int m = 0; m < CPL; ++m) {
+            float dh[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) dh[q] = dyr[q].get(m) * cr[q].get(m);
+            const f32x4 Dn = Contract<IO>::run(At, dh);
+            if (grp == 0) s_df[buf][wv][n * CPL + m] = a0 * Dn[0];
+        }
+        const float cq = shfl(row_prefix_prod(a_n), 15);
+        if (lane == 0) s_c[buf][wv] = cq;
+        __syncthreads();
+#pragma unroll 1
+        for (int r = NW - 1; r >= 0; --r) {
+            if (r % S == S - 1) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
-            const int64_t tan_ = r0 + n + STEP;
-            const float a_nn = load_scalar<IO>(rsrc(ab + (r0 + STEP) * as),
-                                               in_range(tan_ >= wk.t_begin && tan_ < t_la, aoff));
-
-            // ---- look-ahead: first row of the next step's reverse solve ------
-            // It feeds the reverse carrier entering this step's last block.
-            float LT[4];
-            build_decay_transposed(a_nn, grp, n, LT);
-            const typename Contract<IO>::A At = Contract<IO>::prep(LT);
-            const float cn_ = shfl(row_prefix_prod(a_nn), 15);
-            const float a0 = shfl(a_nn, 0);
+            const float c_ = s_c[buf][r];
 #pragma unroll
-            for (int ps = 0; ps < NPASS; ++ps)
-#pragma unroll
-                for (int j = 0; j < CH; ++j) {
-                    float dh[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) dh[q] = dyn[ps][q].get(j) * cn[ps][q].get(j);
-                    const f32x4 Dn = Contract<IO>::run(At, dh);
-                    if (grp == 0) s_df[bn][wv][chan(ps, j)] = a0 * Dn[0];
-                }
-            if (lane == 0) s_cf[bn][wv] = cn_;
-            if constexpr (Sh::HAND_LDS) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-#pragma unroll
-                    for (int ps = 0; ps < NPASS; ++ps)
-#pragma unroll
-                        for (int i = 0; i < HWD; ++i) {
-                            s_hand[hs ^ 1][wv][0][r][ps * HWD + i][lane] = cn[ps][r].w[i];
-                            s_hand[hs ^ 1][wv][1][r][ps * HWD + i][lane] = dyn[ps][r].w[i];
-                        }
+            for (int m = 0; m < CPL; ++m) {
+                const float df = s_df[buf][r][n * CPL + m];
+                eps[m] = c_ * eps[m] + df;
+                pr[m] = c_ * pr[m] + df;
             }
         }
-        const int64_t ta = r0 + n;
-        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
+        buf ^= 1;
+    }
 
-        // ---- forward recompute: last local row W[15] of each channel ---------
-        const Decay dk = build_decay(a_n, grp, n);
-        const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+    const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
+        const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
+        const int64_t r0 = t0 + wv * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+
+        // ---- loads ---------------------------------------------------------------
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                     rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+        R_ xr[4], br[4], dyr[4];
+        float dh[4][CPL];
+        {
+            R_ cr[4];
 #pragma unroll
-        for (int ps = 0; ps < NPASS; ++ps)
-#pragma unroll
-            for (int j = 0; j < CH; ++j) {
-                float u[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) u[q] = xr[ps][q].get(j) * br[ps][q].get(j);
-                const f32x4 W = Contract<IO>::run(A, u);
-                if (grp == 3) s_wl[bw][wv][chan(ps, j)] = W[3];
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+                xr[r].load(rx, o);
+                br[r].load(rb, o);
+                cr[r].load(rc, o);
+                dyr[r].load(rdy, o);
             }
-        if (lane == 63) s_c[bw][wv] = dk.c;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);   // dh = dy * c
+        }
+        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+        // Carrier of the block before this step (zero before the sequence start).
+        float vprev[CPL];
+        {
+            Row<IoF32, CPL> vr;
+            const int64_t blk = t0 / l - 1;
+            vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
+        }
+
+        // ---- local solves: W = L (b*x) and Dl = L^T (c*dy) ---------------------------
+        const Decay dk = build_decay(a_n, grp, n);
+        f32x4 W[CPL], Dl[CPL];
+        {
+            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+            float LT[4];
+            build_decay_transposed(a_n, grp, n, LT);
+            const typename Contract<IO>::A At = Contract<IO>::prep(LT);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                float u[4], d4[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    u[q] = xr[q].get(m) * br[q].get(m);
+                    d4[q] = dh[q][m];
+                }
+                W[m] = Contract<IO>::run(A, u);
+                Dl[m] = Contract<IO>::run(At, d4);
+            }
+        }
+        const float a0 = shfl(a_n, 0);
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_wl[buf][wv][n * CPL + m] = W[m][3];
+        }
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_df[buf][wv][n * CPL + m] = a0 * Dl[m][0];
+        }
+        if (lane == 63) s_c[buf][wv] = dk.c;
         __syncthreads();
 
-        if (!out_step) {
-            // Halo step: only advance the forward carriers.
+        // ---- forward carriers entering this wave's sub-block ---------------------------
+        float ein[CPL], sin_[CPL];
+        {
+            float e[CPL], s[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
 #pragma unroll 1
-            for (int r = 0; r < NW; ++r) {
+            for (int r = 0; r < wv; ++r) {
                 if (r % S == 0) {
 #pragma unroll
                     for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
-                const float c_ = s_c[bw][r];
+                const float c_ = s_c[buf][r];
 #pragma unroll
-                for (int ps = 0; ps < NPASS; ++ps)
-#pragma unroll
-                    for (int j = 0; j < CH; ++j) {
-                        const float wl = s_wl[bw][r][chan(ps, j)];
-                        e[ps * CH + j] = c_ * e[ps * CH + j] + wl;
-                        s[ps * CH + j] = c_ * s[ps * CH + j] + wl;
-                    }
+                for (int m = 0; m < CPL; ++m) {
+                    const float wl = s_wl[buf][r][n * CPL + m];
+                    e[m] = c_ * e[m] + wl;
+                    s[m] = c_ * s[m] + wl;
+                }
             }
-            continue;
+            if (wv % S == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+            }
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { ein[m] = e[m]; sin_[m] = s[m]; }
         }
 
-        // ---- per-step constants of the epilogue -----------------------------
-        float LTc[4];
-        build_decay_transposed(a_n, grp, n, LTc);
-        const typename Contract<IO>::A Atc = Contract<IO>::prep(LTc);
+        // ---- reverse carriers: capture at this sub-block, carry to the previous step ---
+        float epsin[CPL], kd = 0.f;
+#pragma unroll 1
+        for (int r = NW - 1; r >= 0; --r) {
+            if (r % S == S - 1) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
+            }
+            if (r == wv) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) {
+                    epsin[m] = eps[m];
+                    kd += (ein[m] - sin_[m]) * (eps[m] - pr[m]);
+                }
+            }
+            const float c_ = s_c[buf][r];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float df = s_df[buf][r][n * CPL + m];
+                eps[m] = c_ * eps[m] + df;
+                pr[m] = c_ * pr[m] + df;
+            }
+        }
+
+        // ---- gradients -------------------------------------------------------------------
+        // H = W + g * e_in: the jagged-window state of each row.
+#pragma unroll
+        for (int m = 0; m < CPL; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) W[m][r] += dk.G[r] * ein[m];
+        float hup[CPL];   // state entering this lane's first row
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            const float v = shfl(W[m][3], (lane - 16) & 63);
+            hup[m] = grp == 0 ? ein[m] : v;
+        }
         float Rr[4], Gsh[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) Rr[r] = shfl(dk.L[r], base + 15);   // r_q = L[15][.] at this lane's rows
@@ -687,136 +771,31 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
             Gsh[0] = grp == 0 ? 1.0f : gprev;
             Gsh[1] = dk.G[0]; Gsh[2] = dk.G[1]; Gsh[3] = dk.G[2];
         }
-        float da_acc[4] = {0.f, 0.f, 0.f, 0.f};
         const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * rs),
-                                     rdc = rsrc(dcb + r0 * rs);
-
-#pragma unroll
-        for (int ps = 0; ps < NPASS; ++ps) {
-            const int m0 = ps * CH;
-            // c and dy of this step for the pass's channels.
-            RH cr[4], dyr[4];
-            if constexpr (Sh::HAND_LDS) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-#pragma unroll
-                    for (int i = 0; i < HWD; ++i) {
-                        cr[r].w[i] = s_hand[hs][wv][0][r][ps * HWD + i][lane];
-                        dyr[r].w[i] = s_hand[hs][wv][1][r][ps * HWD + i][lane];
-                    }
-            } else {
-                const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs + ps * PIECE * ES));
-                    cr[r].load(rc, o);
-                    dyr[r].load(rdy, o);
-                }
-            }
-
-            // Forward carriers entering this wave's sub-block, and their update.
-            float ein[CH], sin_[CH];
-#pragma unroll
-            for (int j = 0; j < CH; ++j) { ein[j] = 0.f; sin_[j] = 0.f; }
-#pragma unroll 1
-            for (int r = 0; r < NW; ++r) {
-                if (r % S == 0) {
-#pragma unroll
-                    for (int j = 0; j < CH; ++j) { e[m0 + j] = s[m0 + j]; s[m0 + j] = 0.f; }
-                }
-                if (r == wv) {
-#pragma unroll
-                    for (int j = 0; j < CH; ++j) { ein[j] = e[m0 + j]; sin_[j] = s[m0 + j]; }
-                }
-                const float c_ = s_c[bw][r];
-#pragma unroll
-                for (int j = 0; j < CH; ++j) {
-                    const float wl = s_wl[bw][r][chan(ps, j)];
-                    e[m0 + j] = c_ * e[m0 + j] + wl;
-                    s[m0 + j] = c_ * s[m0 + j] + wl;
-                }
-            }
-            // Reverse carriers: from the end of the next step's first block back
-            // to this wave's sub-block.  eps is the full adjoint entering a
-            // sub-block from the right, pr the one restarted at its block's end.
-            float eps[CH], pr[CH];
-#pragma unroll
-            for (int j = 0; j < CH; ++j) { eps[j] = 0.f; pr[j] = 0.f; }
-#pragma unroll 1
-            for (int r = S - 1; r >= 0; --r) {
-                const float c_ = s_cf[bn][r];
-#pragma unroll
-                for (int j = 0; j < CH; ++j) pr[j] = c_ * pr[j] + s_df[bn][r][chan(ps, j)];
-            }
-#pragma unroll 1
-            for (int r = NW - 1; r >= wv; --r) {
-                if (r % S == S - 1) {
-#pragma unroll
-                    for (int j = 0; j < CH; ++j) { eps[j] = pr[j]; pr[j] = 0.f; }
-                }
-                if (r > wv) {
-                    const float c_ = s_cf[bc][r];
-#pragma unroll
-                    for (int j = 0; j < CH; ++j) {
-                        const float df = s_df[bc][r][chan(ps, j)];
-                        eps[j] = c_ * eps[j] + df;
-                        pr[j] = c_ * pr[j] + df;
-                    }
-                }
-            }
-
-            // Recompute this pass's tiles: W = L (b*x) and D = L^T (c*dy).
-            f32x4 W[CH], Dl[CH];
-            float wup[CH];   // local state of the row above this lane's first row (0 above row 0)
-#pragma unroll
-            for (int j = 0; j < CH; ++j) {
-                float u[4], dh[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    u[q] = xr[ps][q].get(j) * br[ps][q].get(j);
-                    dh[q] = dyr[q].get(j) * cr[q].get(j);
-                }
-                W[j] = Contract<IO>::run(A, u);
-                Dl[j] = Contract<IO>::run(Atc, dh);
-                const float v = shfl(W[j][3], (lane - 16) & 63);
-                wup[j] = grp == 0 ? 0.0f : v;
-            }
-
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t t = tr0 + r;
-                float vdx[CH], vdb[CH], vdc[CH];
-                float acc = 0.f, acc2 = 0.f;
-#pragma unroll
-                for (int j = 0; j < CH; ++j) {
-                    const float hv = W[j][r] + dk.G[r] * ein[j];           // jagged-window state
-                    const float dyv = dyr[r].get(j);
-                    vdc[j] = dyv * hv;
-                    const float du = Dl[j][r] + Rr[r] * eps[j];            // adjoint of u
-                    const float dblk = Dl[j][r] + Rr[r] * pr[j];           // ... from this block's rows
-                    vdx[j] = br[ps][r].get(j) * du;
-                    if (p.residual) vdx[j] += dyv;
-                    vdb[j] = xr[ps][r].get(j) * du;
-                    const float wprev = r == 0 ? wup[j] : W[j][r - 1];
-                    acc += wprev * du;
-                    acc2 += sin_[j] * du + (ein[j] - sin_[j]) * dblk;
-                }
-                da_acc[r] += acc + Gsh[r] * acc2;
-                const uint32_t o = in_range(t >= wk.t_begin && t < wk.t_end,
-                                            loff + (uint32_t)(r * rs + ps * PIECE * ES));
-                store_row<IO, CH>(rdx, o, vdx);
-                store_row<IO, CH>(rdb, o, vdb);
-                store_row<IO, CH>(rdc, o, vdc);
-            }
-        }
-        const __amdgpu_buffer_rsrc_t rda = rsrc(dab + r0 * das);
+                                     rdc = rsrc(dcb + r0 * rs), rda = rsrc(dab + r0 * das);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float tot = row_sum(da_acc[r]);
             const int64_t t = tr0 + r;
+            float vdx[CPL], vdb[CPL], vdc[CPL];
+            float acc = -Gsh[r] * Rr[r] * kd;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float dyv = dyr[r].get(m);
+                vdc[m] = dyv * W[m][r];
+                const float du = Dl[m][r] + Rr[r] * epsin[m];          // adjoint of u
+                vdx[m] = br[r].get(m) * du;
+                if (p.residual) vdx[m] += dyv;
+                vdb[m] = xr[r].get(m) * du;
+                acc += (r == 0 ? hup[m] : W[m][r - 1]) * du;
+            }
+            const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
+            store_row<IO, CPL>(rdx, o, vdx);
+            store_row<IO, CPL>(rdb, o, vdb);
+            store_row<IO, CPL>(rdc, o, vdc);
+            const float tot = row_sum(acc);
             __builtin_amdgcn_raw_buffer_store_b32(
                 __builtin_bit_cast(int, tot), rda,
-                (int)in_range(n == 0 && t >= wk.t_begin && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, 0);
+                (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, 0);
         }
     }
 }

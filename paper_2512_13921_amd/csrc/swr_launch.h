@@ -20,6 +20,8 @@ struct Params {
     float* da;
     void* db;
     void* dc;
+    float* carriers;    // [B][H][nblocks][D] float32 block carriers v_t (forward: optional output;
+                        // backward: input)
     int64_t B, T, H;
     int64_t sx_b, sx_t, sx_h;
     int64_t sa_b, sa_t, sa_h;
@@ -28,11 +30,14 @@ struct Params {
     int64_t run_len;    // tokens per workgroup run, a multiple of the step and of l
     int64_t nruns;      // runs per (batch, head) sequence
     int64_t nwork;      // B * H * nruns workgroups
+    int64_t nblocks;    // ceil(T / block): carriers per (batch, head)
 };
 
-// Waves per workgroup for a block length: a step (waves * 16 tokens) always
-// holds whole blocks and at least 64 tokens.
-inline int waves_for_block(int64_t block) { return block >= 128 ? 8 : 4; }
+// Waves per workgroup.  The backward's steps (waves * 16 tokens) must hold
+// whole blocks; the forward's need not, and it uses small workgroups so that
+// several run side by side on a compute unit.
+inline int bwd_waves_for_block(int64_t block) { return block >= 128 ? 8 : 4; }
+inline int fwd_waves_for_block(int64_t /*block*/) { return 4; }
 
 // Launches the forward or backward kernel for (dtype, D, waves) on `stream`.
 hipError_t launch(const Params& p, int dtype, int D, int nw, bool backward, void* stream);

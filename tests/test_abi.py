@@ -17,7 +17,7 @@ OK, E_NULL, E_SHAPE, E_DTYPE, E_BLOCK, E_ALIGN, E_ALIAS, E_UNSUP, E_HIP, E_VER =
 
 # Fake, well-aligned "device" addresses far apart: validation never dereferences them.
 GB = 1 << 30
-X, A, B_, C, Y, DY, DX, DA, DB, DC = (GB * (i + 1) for i in range(10))
+X, A, B_, C, Y, DY, DX, DA, DB, DC, V = (GB * (i + 1) for i in range(11))
 
 
 def problem(B=2, T=256, H=4, D=64, block=64, dtype=BF16, residual=False, run_len=0,
@@ -27,23 +27,28 @@ def problem(B=2, T=256, H=4, D=64, block=64, dtype=BF16, residual=False, run_len
     return swr.make_problem(B, T, H, D, block, dtype, xs, as_, residual, run_len)
 
 
-def fwd(p, x=X, a=A, b=B_, c=C, y=Y):
+def fwd(p, x=X, a=A, b=B_, c=C, y=Y, v_=0):
     v = ctypes.c_void_p
     return swr.load().swr_forward(ctypes.byref(p) if p is not None else None,
-                                  v(x), v(a), v(b), v(c), v(y), None)
+                                  v(x), v(a), v(b), v(c), v(y), v(v_), None)
 
 
-def bwd(p, x=X, a=A, b=B_, c=C, dy=DY, dx=DX, da=DA, db=DB, dc=DC):
+def bwd(p, x=X, a=A, b=B_, c=C, dy=DY, v_=V, dx=DX, da=DA, db=DB, dc=DC):
     v = ctypes.c_void_p
-    return swr.load().swr_backward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(dy), v(dx), v(da),
-                                   v(db), v(dc), None)
+    return swr.load().swr_backward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(dy), v(v_), v(dx),
+                                   v(da), v(db), v(dc), None)
+
+
+def car(p, x=X, a=A, b=B_, v_=V):
+    v = ctypes.c_void_p
+    return swr.load().swr_carriers(ctypes.byref(p), v(x), v(a), v(b), v(v_), None)
 
 
 def test_library_exports_every_declared_symbol():
     text = open(HEADER).read()
     names = set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(swr_\w+)\s*\(", text, re.M))
-    assert {"swr_forward", "swr_backward", "swr_error_string", "swr_abi_version",
-            "swr_launch_info"} <= names
+    assert {"swr_forward", "swr_backward", "swr_carriers", "swr_error_string", "swr_abi_version",
+            "swr_launch_info", "swr_carrier_elems"} <= names
     lib = swr.load()
     for name in names:
         assert hasattr(lib, name), name
@@ -86,7 +91,7 @@ def test_version_mismatch():
 ])
 def test_shape_validation(kw, code):
     p = problem(**kw)
-    assert fwd(p) == code and bwd(p) == code
+    assert fwd(p) == code and bwd(p) == code and car(p) == code
 
 
 def test_unknown_flags_and_reserved():
@@ -102,7 +107,8 @@ def test_empty_problems_are_noops_even_with_null_pointers():
     for kw in (dict(T=0), dict(B=0), dict(H=0)):
         p = problem(**kw)
         assert fwd(p, 0, 0, 0, 0, 0) == OK
-        assert bwd(p, 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
+        assert bwd(p, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
+        assert car(p, 0, 0, 0, 0) == OK
 
 
 @pytest.mark.parametrize("which", range(5))
@@ -112,11 +118,18 @@ def test_null_pointers_forward(which):
     assert fwd(problem(), *ptrs) == E_NULL
 
 
-@pytest.mark.parametrize("which", range(9))
+@pytest.mark.parametrize("which", range(10))
 def test_null_pointers_backward(which):
-    ptrs = [X, A, B_, C, DY, DX, DA, DB, DC]
+    ptrs = [X, A, B_, C, DY, V, DX, DA, DB, DC]      # the carriers are required too
     ptrs[which] = 0
     assert bwd(problem(), *ptrs) == E_NULL
+
+
+@pytest.mark.parametrize("which", range(4))
+def test_null_pointers_carriers(which):
+    ptrs = [X, A, B_, V]
+    ptrs[which] = 0
+    assert car(problem(), *ptrs) == E_NULL
 
 
 def test_alignment():
@@ -128,6 +141,9 @@ def test_alignment():
     assert fwd(problem(dtype=F32), a=A + 2) == E_ALIGN
     # row stride of 65 elements breaks the 8-byte vectors
     assert fwd(problem(H=1, x_strides=(256 * 65, 65, 65))) == E_ALIGN
+    assert fwd(problem(), v_=V + 8) == E_ALIGN          # carriers: 16-byte aligned
+    assert bwd(problem(), v_=V + 4) == E_ALIGN
+    assert car(problem(), v_=V + 8) == E_ALIGN
 
 
 def test_aliasing():
@@ -138,8 +154,24 @@ def test_aliasing():
     assert bwd(problem(), dc=DY) == E_ALIAS
     assert bwd(problem(), da=A) == E_ALIAS
     assert bwd(problem(), db=B_) == E_ALIAS
+    assert fwd(problem(), v_=X) == E_ALIAS              # carriers written by the forward
+    assert fwd(problem(), v_=Y) == E_ALIAS
+    assert car(problem(), v_=A) == E_ALIAS
+    assert bwd(problem(), dx=V) == E_ALIAS              # carriers read by the backward
     # (inputs may alias each other: exercised with real tensors in the GPU tests,
     # since a call that passes validation launches a kernel)
+
+
+def test_carrier_elems():
+    p = problem(B=2, T=250, H=3, D=64, block=64)
+    assert swr.swr_carrier_elems(p) == 2 * 3 * 4 * 64     # ceil(250 / 64) = 4 blocks
+    assert swr.load().swr_carrier_elems(ctypes.byref(problem(block=48))) == E_BLOCK
+
+
+def test_offsets_beyond_32_bits_rejected():
+    # a row stride whose 16-row span exceeds 2^31 bytes cannot be addressed
+    huge = (1 << 27)
+    assert fwd(problem(H=1, x_strides=(huge * 300, huge, huge))) == E_UNSUP
 
 
 def test_launch_info_defaults():

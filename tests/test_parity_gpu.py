@@ -43,8 +43,9 @@ def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd"):
         a = a.permute(0, 2, 1).contiguous().permute(0, 2, 1)
         if dy is not None:
             dy = dy.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
-    y = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len)
-    grads = swr.swr_backward(x, a, b, c, dy, cfg.block, residual=residual,
+    y, v = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len,
+                           save_carriers=True)
+    grads = swr.swr_backward(x, a, b, c, dy, v, cfg.block, residual=residual,
                              run_len=run_len) if backward else None
     torch.cuda.synchronize()
     return y, grads
@@ -144,8 +145,8 @@ def test_inputs_may_alias(swr):
     prob = W.random_problem(14, 1, 256, 2, 64, 64, "bf16")
     x = to_device(prob.x, "bf16")
     a = to_device(prob.a, "bf16")
-    y = swr.swr_forward(x, a, x, x, 64)
-    dx, da, db, dc = swr.swr_backward(x, a, x, x, x, 64)
+    y, v = swr.swr_forward(x, a, x, x, 64, save_carriers=True)
+    dx, da, db, dc = swr.swr_backward(x, a, x, x, x, v, 64)
     torch.cuda.synchronize()
     ref = oracle.forward(prob.x, prob.a, prob.x, prob.x, 64)
     assert_close(to_host(y), ref, "bf16", "aliased inputs")
@@ -157,9 +158,47 @@ def test_inputs_may_alias(swr):
 def test_empty_inputs(swr):
     x = torch.empty((2, 0, 3, 64), dtype=torch.bfloat16, device="cuda")
     a = torch.empty((2, 0, 3), dtype=torch.bfloat16, device="cuda")
-    y = swr.swr_forward(x, a, x, x, 64)
-    dx, da, db, dc = swr.swr_backward(x, a, x, x, x, 64)
-    assert y.shape == x.shape and da.shape == a.shape
+    y, v = swr.swr_forward(x, a, x, x, 64, save_carriers=True)
+    dx, da, db, dc = swr.swr_backward(x, a, x, x, x, v, 64)
+    assert y.shape == x.shape and da.shape == a.shape and v.shape == (2, 3, 0, 64)
+
+
+def _carriers_by_definition(prob):
+    """v_t: state at the end of block t of the recurrence restarted at the block's
+    start (float64 loop, the carrier definition of Alg. "Block Two-Pass")."""
+    cfg = prob.cfg
+    l, T = cfg.block, cfg.T
+    nb = -(-T // l)
+    u = prob.b.astype(np.float64) * prob.x.astype(np.float64)     # [B, T, H, D]
+    a = prob.a.astype(np.float64)
+    v = np.zeros((cfg.B, cfg.H, nb, cfg.D))
+    for t in range(nb):
+        s = np.zeros((cfg.B, cfg.H, cfg.D))
+        for m in range(t * l, min((t + 1) * l, T)):
+            s = a[:, m, :, None] * s + u[:, m]
+        v[:, :, t] = s
+    return v
+
+
+@pytest.mark.parametrize("dtype,D,block", [("bf16", 128, 128), ("f32", 64, 32), ("bf16", 16, 16)])
+def test_block_carriers(swr, dtype, D, block):
+    prob = W.random_problem(21, 2, 517, 3, D, block, dtype)
+    x, a, b, c = (to_device(getattr(prob, n), dtype) for n in "xabc")
+    _, v1 = swr.swr_forward(x, a, b, c, block, save_carriers=True, run_len=max(64, block))
+    v2 = swr.swr_carriers(x, a, b, block)
+    torch.cuda.synchronize()
+    assert torch.equal(v1, v2)          # the same kernel path, bit for bit
+    ref = _carriers_by_definition(prob)
+    scale = np.sqrt(np.mean(ref * ref))
+    err = np.abs(to_host(v1) - ref) / np.maximum(np.abs(ref), scale)
+    assert err.max() < 1e-4, err.max()
+
+
+def test_backward_needs_carriers(swr):
+    prob = W.random_problem(22, 1, 128, 1, 64, 64, "bf16")
+    x, a = to_device(prob.x, "bf16"), to_device(prob.a, "bf16")
+    with pytest.raises(ValueError):
+        swr.swr_backward(x, a, x, x, x, None, 64)
 
 
 def test_autograd_function(swr):
