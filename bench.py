@@ -200,7 +200,7 @@ def main():
     traffic = recorded_traffic(dom_kernel, cfg.name)
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
 
-    run_len, fwg, bwg = swr.swr_launch_info(swr.make_problem(
+    launch = swr.swr_launch_info(swr.make_problem(
         cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
         x.stride()[:3], a.stride(), False, args.run_len))
 
@@ -232,7 +232,7 @@ def main():
         "data": "synthetic (seeded host draws, rounded to the I/O dtype)",
         "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
                    "block": cfg.block, "global_batch": cfg.B, "seq_len": cfg.T,
-                   "parallelism": "single GPU", "run_len": run_len, "workgroups": fwg},
+                   "parallelism": "single GPU", "launch": launch},
         "roofline": {
             "bound": "hbm",
             "kernel": dom_kernel,

@@ -92,8 +92,9 @@ typedef struct swr_problem {
     int32_t reserved;      /* must be 0                                                    */
     int64_t sx_b, sx_t, sx_h;  /* element strides of the [B,T,H,D] tensors (channel = 1) */
     int64_t sa_b, sa_t, sa_h;  /* element strides of a and da                            */
-    int64_t run_len;       /* tokens per workgroup run: 0 = automatic, else a positive
-                              multiple of max(64, block); a tuning knob that does not
+    int64_t run_len;       /* tokens per workgroup run: 0 = automatic (chosen separately
+                              for the forward and the backward), else a positive multiple
+                              of max(64, block) used by both; a tuning knob that does not
                               change results beyond float32 rounding order              */
 } swr_problem_t;
 
@@ -129,11 +130,12 @@ const char* swr_error_string(int code);
 int swr_abi_version(void);
 
 /* Resolved launch shape for a problem (for reports and tests): the run length
- * in tokens that `run_len == 0` selects, and the number of workgroups the
- * forward and backward launch.  Returns an SWR_ERR_* code for a problem that
- * swr_forward would reject on shape grounds; pointers are not inspected. */
-int swr_launch_info(const swr_problem_t* problem, int64_t* run_len, int64_t* fwd_workgroups,
-                    int64_t* bwd_workgroups);
+ * in tokens and the number of workgroups of the forward and of the backward
+ * launch (any output pointer may be NULL).  Returns an SWR_ERR_* code for a
+ * problem that swr_forward would reject on shape grounds; pointers are not
+ * inspected. */
+int swr_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, int64_t* fwd_workgroups,
+                    int64_t* bwd_run_len, int64_t* bwd_workgroups);
 
 #ifdef __cplusplus
 }

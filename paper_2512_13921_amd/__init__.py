@@ -75,7 +75,7 @@ def load():
         lib.swr_error_string.restype = ctypes.c_char_p
         lib.swr_abi_version.restype = ctypes.c_int
         i64p = ctypes.POINTER(ctypes.c_int64)
-        lib.swr_launch_info.argtypes = [P, i64p, i64p, i64p]
+        lib.swr_launch_info.argtypes = [P, i64p, i64p, i64p, i64p]
         lib.swr_launch_info.restype = ctypes.c_int
         if lib.swr_abi_version() != SWR_ABI_VERSION:
             raise RuntimeError("libswr.so ABI version does not match the binding")
@@ -107,13 +107,13 @@ def make_problem(B, T, H, D, block, dtype_code, x_strides, a_strides, residual=F
 
 
 def swr_launch_info(problem: SwrProblem):
-    """(run_len, forward workgroups, backward workgroups) the library picks."""
-    r, f, b = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
-    rc = load().swr_launch_info(ctypes.byref(problem), ctypes.byref(r), ctypes.byref(f),
-                                ctypes.byref(b))
+    """{'fwd_run_len', 'fwd_workgroups', 'bwd_run_len', 'bwd_workgroups'} the library picks."""
+    v = [ctypes.c_int64() for _ in range(4)]
+    rc = load().swr_launch_info(ctypes.byref(problem), *(ctypes.byref(t) for t in v))
     if rc != 0:
         raise SwrError(rc, "swr_launch_info")
-    return r.value, f.value, b.value
+    return dict(zip(("fwd_run_len", "fwd_workgroups", "bwd_run_len", "bwd_workgroups"),
+                    (t.value for t in v)))
 
 
 def swr_carrier_elems(problem: SwrProblem) -> int:

@@ -12,10 +12,22 @@ namespace {
 
 constexpr int64_t kMaxWorkgroups = 0x7fffffffLL;
 constexpr int64_t kMaxExtent = (int64_t)1 << 62;
-// Default number of workgroups to aim for: a few per compute unit of the
-// MI355X (256 CUs), so that runs are long (few halo re-reads) while the grid
-// still fills the chip with some slack for uneven progress.
-constexpr int64_t kTargetWorkgroups = 1024;
+// Default grid sizes, measured on the MI355X (256 compute units): the forward
+// runs best with about two 4-wave workgroups per CU; the backward with one
+// workgroup per CU when a workgroup fills it (8 waves, or d = 128), and with
+// many shorter runs otherwise.  Longer runs mean fewer halo re-reads.
+constexpr int64_t kFwdWorkgroups = 512;
+constexpr int64_t kBwdWorkgroupsFull = 256;
+constexpr int64_t kBwdWorkgroupsLight = 2048;
+
+// Run length (tokens, a multiple of step) that splits each sequence into
+// enough runs to give about `target` workgroups.
+int64_t pick_run_len(int64_t T, int64_t seqs, int64_t step, int64_t target) {
+    const int64_t nsteps = (T + step - 1) / step;
+    const int64_t want = (target + seqs - 1) / seqs;
+    const int64_t runs = std::max<int64_t>(1, std::min(nsteps, want));
+    return ((nsteps + runs - 1) / runs) * step;
+}
 
 struct Dim {
     int64_t size, stride;
@@ -53,7 +65,8 @@ struct Resolved {
     int nw;             // waves per backward workgroup
     int nw_fwd;         // waves per forward workgroup
     int64_t step;       // tokens per workgroup step
-    int64_t run_len, nruns, nwork;
+    int64_t run_len, nruns, nwork;          // backward launch
+    int64_t run_len_f, nruns_f, nwork_f;    // forward launch
     int64_t xspan;      // bytes spanned by one [B,T,H,D] tensor
     int64_t aspan;      // elements spanned by a / da
     int64_t nblocks;    // blocks per sequence
@@ -88,19 +101,20 @@ int resolve(const swr_problem_t* p, Resolved* r) {
         r->aspan = ao + 1;
     }
     const int64_t seqs = p->B * p->H;
-    const int64_t nsteps = (p->T + r->step - 1) / r->step;
     if (p->run_len > 0) {
-        r->run_len = p->run_len;
+        r->run_len = r->run_len_f = p->run_len;
     } else if (r->empty) {
-        r->run_len = r->step;
+        r->run_len = r->run_len_f = r->step;
     } else {
-        const int64_t want = (kTargetWorkgroups + seqs - 1) / seqs;
-        const int64_t runs = std::max<int64_t>(1, std::min(nsteps, want));
-        r->run_len = ((nsteps + runs - 1) / runs) * r->step;
+        const bool full = r->nw == 8 || r->cpl == 8;
+        r->run_len = pick_run_len(p->T, seqs, r->step, full ? kBwdWorkgroupsFull : kBwdWorkgroupsLight);
+        r->run_len_f = pick_run_len(p->T, seqs, r->step, kFwdWorkgroups);
     }
     r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
-    if (!r->empty && r->nruns > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
+    r->nruns_f = r->empty ? 0 : (p->T + r->run_len_f - 1) / r->run_len_f;
+    if (!r->empty && std::max(r->nruns, r->nruns_f) > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
     r->nwork = seqs * r->nruns;
+    r->nwork_f = seqs * r->nruns_f;
     r->nblocks = (p->T + p->block - 1) / p->block;
     r->carriers = seqs * r->nblocks * p->D;
     if (!r->empty) {
@@ -133,16 +147,16 @@ Span span(const void* p, int64_t bytes) { return {(uintptr_t)p, (uintptr_t)p + (
 
 bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
 
-swr::Params make_params(const swr_problem_t* p, const Resolved& r) {
+swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward) {
     swr::Params k{};
     k.B = p->B; k.T = p->T; k.H = p->H;
     k.sx_b = p->sx_b; k.sx_t = p->sx_t; k.sx_h = p->sx_h;
     k.sa_b = p->sa_b; k.sa_t = p->sa_t; k.sa_h = p->sa_h;
     k.block = (int32_t)p->block;
     k.residual = (p->flags & SWR_FLAG_RESIDUAL) ? 1 : 0;
-    k.run_len = r.run_len;
-    k.nruns = r.nruns;
-    k.nwork = r.nwork;
+    k.run_len = backward ? r.run_len : r.run_len_f;
+    k.nruns = backward ? r.nruns : r.nruns_f;
+    k.nwork = backward ? r.nwork : r.nwork_f;
     k.nblocks = r.nblocks;
     return k;
 }
@@ -169,13 +183,14 @@ const char* swr_error_string(int code) {
     }
 }
 
-int swr_launch_info(const swr_problem_t* problem, int64_t* run_len, int64_t* fwd_workgroups,
-                    int64_t* bwd_workgroups) {
+int swr_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, int64_t* fwd_workgroups,
+                    int64_t* bwd_run_len, int64_t* bwd_workgroups) {
     Resolved r;
     const int rc = resolve(problem, &r);
     if (rc != SWR_OK) return rc;
-    if (run_len) *run_len = r.run_len;
-    if (fwd_workgroups) *fwd_workgroups = r.nwork;
+    if (fwd_run_len) *fwd_run_len = r.run_len_f;
+    if (fwd_workgroups) *fwd_workgroups = r.nwork_f;
+    if (bwd_run_len) *bwd_run_len = r.run_len;
     if (bwd_workgroups) *bwd_workgroups = r.nwork;
     return SWR_OK;
 }
@@ -208,7 +223,7 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
         if (overlap(sy, s) || overlap(sv, s)) return SWR_ERR_ALIAS;
     if (overlap(sy, sv)) return SWR_ERR_ALIAS;
 
-    swr::Params k = make_params(p, r);
+    swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
     return swr::launch(k, p->dtype, (int)p->D, r.nw_fwd, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
@@ -257,7 +272,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
             if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
     }
 
-    swr::Params k = make_params(p, r);
+    swr::Params k = make_params(p, r, true);
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);

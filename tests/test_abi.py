@@ -177,16 +177,19 @@ def test_offsets_beyond_32_bits_rejected():
 def test_launch_info_defaults():
     # headline workload: B=8, T=16384, H=16, D=128, block 128
     p = problem(B=8, T=16384, H=16, D=128, block=128)
-    run_len, fwd_wg, bwd_wg = swr.swr_launch_info(p)
-    assert run_len % 128 == 0 and fwd_wg == bwd_wg == 8 * 16 * (-(-16384 // run_len))
+    info = swr.swr_launch_info(p)
+    for k in ("fwd", "bwd"):
+        rl, wg = info[k + "_run_len"], info[k + "_workgroups"]
+        assert rl % 128 == 0 and wg == 8 * 16 * (-(-16384 // rl))
+    assert info["fwd_workgroups"] == 512 and info["bwd_workgroups"] == 256
     p = problem(B=1, T=1000, H=1, D=16, block=16, run_len=192)
-    run_len, wg, _ = swr.swr_launch_info(p)
-    assert run_len == 192 and wg == 6
+    info = swr.swr_launch_info(p)
+    assert info["fwd_run_len"] == info["bwd_run_len"] == 192
+    assert info["fwd_workgroups"] == info["bwd_workgroups"] == 6
 
 
 def test_non_contiguous_layouts_accepted():
     # [B, H, T, D] storage described through strides is valid
     B, T, H, D = 2, 256, 4, 64
     p = problem(B=B, T=T, H=H, D=D, x_strides=(H * T * D, D, T * D), a_strides=(H * T, 1, T))
-    rc = swr.swr_launch_info(p)
-    assert rc[0] > 0
+    assert swr.swr_launch_info(p)["fwd_run_len"] > 0
