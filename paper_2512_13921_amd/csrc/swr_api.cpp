@@ -12,13 +12,13 @@ namespace {
 
 constexpr int64_t kMaxWorkgroups = 0x7fffffffLL;
 constexpr int64_t kMaxExtent = (int64_t)1 << 62;
-// Default grid sizes, measured on the MI355X (256 compute units): the forward
-// runs best with about two 4-wave workgroups per CU; the backward with one
-// workgroup per CU when a workgroup fills it (8 waves, or d = 128), and with
-// many shorter runs otherwise.  Longer runs mean fewer halo re-reads.
+// Default grid sizes, measured on the MI355X (256 compute units) over the
+// benchmark workloads: the forward runs best with about two 4-wave
+// workgroups per CU; the backward with one 8-wave workgroup per CU, and with
+// more, shorter runs when its workgroups are 4 waves (the lighter they are,
+// the more).  Longer runs mean fewer halo re-reads.
 constexpr int64_t kFwdWorkgroups = 512;
-constexpr int64_t kBwdWorkgroupsFull = 256;
-constexpr int64_t kBwdWorkgroupsLight = 2048;
+int64_t bwd_workgroups(int nw, int cpl) { return nw == 8 ? 256 : (cpl == 8 ? 1024 : 4096); }
 
 // Run length (tokens, a multiple of step) that splits each sequence into
 // enough runs to give about `target` workgroups.
@@ -106,8 +106,7 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     } else if (r->empty) {
         r->run_len = r->run_len_f = r->step;
     } else {
-        const bool full = r->nw == 8 || r->cpl == 8;
-        r->run_len = pick_run_len(p->T, seqs, r->step, full ? kBwdWorkgroupsFull : kBwdWorkgroupsLight);
+        r->run_len = pick_run_len(p->T, seqs, r->step, bwd_workgroups(r->nw, r->cpl));
         r->run_len_f = pick_run_len(p->T, seqs, r->step, kFwdWorkgroups);
     }
     r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
@@ -153,6 +152,7 @@ swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward
     k.sx_b = p->sx_b; k.sx_t = p->sx_t; k.sx_h = p->sx_h;
     k.sa_b = p->sa_b; k.sa_t = p->sa_t; k.sa_h = p->sa_h;
     k.block = (int32_t)p->block;
+    k.lshift = p->block == 16 ? 4 : p->block == 32 ? 5 : p->block == 64 ? 6 : 7;
     k.residual = (p->flags & SWR_FLAG_RESIDUAL) ? 1 : 0;
     k.run_len = backward ? r.run_len : r.run_len_f;
     k.nruns = backward ? r.nruns : r.nruns_f;

@@ -165,6 +165,40 @@ __device__ inline void store_row(__amdgpu_buffer_rsrc_t r, uint32_t off, const f
     }
 }
 
+// Asynchronous copy of one row slice per lane from a buffer straight into
+// LDS (no registers are involved): lane i's BYTES land at
+// lds + chunk * 64 * CHUNK + i * CHUNK for each CHUNK-sized piece.  An
+// out-of-range offset is never relied on to write anything.
+template <int BYTES>
+struct LdsRow {
+    static constexpr int CHUNK = BYTES % 16 == 0 ? 16 : 4;
+    static constexpr int NCH = BYTES / CHUNK;
+    static constexpr int WORDS = BYTES / 4;          // uint32 per lane
+    static constexpr int SLOT_WORDS = WORDS * 64;    // uint32 per row slot of a wave
+
+    __device__ static void issue(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t* slot) {
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            auto* dst = (__attribute__((address_space(3))) void*)(slot + ch * 64 * (CHUNK / 4));
+            if constexpr (CHUNK == 16)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, off + ch * 16, 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 4, off + ch * 4, 0, 0, 0);
+        }
+    }
+    __device__ static void read(const uint32_t* slot, int lane, uint32_t (&w)[WORDS]) {
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            if constexpr (CHUNK == 16) {
+                const uint4 v = *(const uint4*)(slot + ch * 256 + lane * 4);
+                w[4 * ch + 0] = v.x; w[4 * ch + 1] = v.y; w[4 * ch + 2] = v.z; w[4 * ch + 3] = v.w;
+            } else {
+                w[ch] = slot[ch * 64 + lane];
+            }
+        }
+    }
+};
+
 template <class IO>
 __device__ inline float load_scalar(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     if constexpr (IO::ES == 2)
@@ -293,8 +327,8 @@ struct Contract {
 // Give every XCD a contiguous range of work items, so that the H heads of one
 // (batch, run) -- which share the cache lines of the [B, T, H] decay tensor --
 // and neighbouring runs land on the same L2.
-__device__ inline int64_t xcd_remap(int64_t id, int64_t n) {
-    const int64_t q = n / 8, rem = n % 8, x = id % 8, j = id / 8;
+__device__ inline uint32_t xcd_remap(uint32_t id, uint32_t n) {
+    const uint32_t q = n >> 3, rem = n & 7, x = id & 7, j = id >> 3;
     return x < rem ? x * (q + 1) + j : rem * (q + 1) + (x - rem) * q + j;
 }
 
@@ -303,12 +337,14 @@ struct Work {
 };
 
 __device__ inline Work decode_work(const Params& p) {
-    const int64_t wid = xcd_remap(blockIdx.x, p.nwork);
+    // nwork < 2^31 (checked on the host), so 32-bit arithmetic suffices.
+    const uint32_t wid = xcd_remap(blockIdx.x, (uint32_t)p.nwork);
+    const uint32_t H = (uint32_t)p.H, nruns = (uint32_t)p.nruns;
     Work wk;
-    wk.h = wid % p.H;
-    const int64_t rest = wid / p.H;
-    const int64_t run = rest % p.nruns;
-    wk.b = rest / p.nruns;
+    wk.h = wid % H;
+    const uint32_t rest = wid / H;
+    const int64_t run = rest % nruns;
+    wk.b = rest / nruns;
     wk.t_begin = run * p.run_len;
     wk.t_end = min(wk.t_begin + p.run_len, p.T);
     return wk;
@@ -368,19 +404,29 @@ __device__ inline Lanes lanes() {
 // Forward
 // ---------------------------------------------------------------------------
 
+// At least three waves per SIMD: with 4-wave workgroups that is three
+// workgroups per compute unit, whose memory and compute phases interleave.
 template <class IO, int CPL, int NW>
-__global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
+__global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
     constexpr int D = CPL * SB;
     constexpr int STEP = NW * SB;
     constexpr int ES = IO::ES;
     __shared__ float s_wl[2][NW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[2][NW];       // each sub-block's decay product
+    // The next step's x, b, c tiles are copied into a wave-private LDS slot
+    // while the current step computes (16-byte lane slices only; the slots of
+    // a workgroup stay small enough for three workgroups per compute unit).
+    using RW = Row<IO, CPL>;
+    using LR = LdsRow<RW::BYTES>;
+    constexpr bool PREFETCH = RW::BYTES % 16 == 0 && NW * 12 * LR::SLOT_WORDS * 4 <= 48 * 1024;
+    __shared__ __attribute__((aligned(16))) uint32_t s_tile[PREFETCH ? NW : 1][3][4][PREFETCH ? LR::SLOT_WORDS : 1];
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work(p);
     const int l = p.block;
-    const int S = l / SB;              // sub-blocks per block
+    const int S = l / SB;              // sub-blocks per block (a power of two)
+    const int smask = S - 1;
     const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);  // first token read
     const int64_t halo = wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
@@ -405,24 +451,57 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
     // Sweep to the end of the run's last block: when the sequence ends inside a
     // block, the step holding that block's last sub-block still computes its
     // carrier (its rows past the end are masked, so it moves no data).
-    const int64_t t_stop = ((wk.t_end + l - 1) / l) * l;
+    const int64_t t_stop = ((wk.t_end + l - 1) >> p.lshift) << p.lshift;
+    const int64_t t_first = wk.t_begin - halo * STEP;
+    // Which rows of which tensor a step reads: x and b from the halo block on,
+    // c only where y is written.
+    auto ok_xb = [&](int64_t t) { return t >= t_lo && t < wk.t_end; };
+    auto ok_c = [&](int64_t t) { return want_y && t >= wk.t_begin && t < wk.t_end; };
+    // Copies the x, b, c tiles of the step starting at token t0 into this wave's LDS slot.
+    auto prefetch = [&](int64_t t0) {
+        const int64_t r0 = t0 + wv * SB, tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs), rc = rsrc(cb + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = loff + (uint32_t)(r * rs);
+            LR::issue(rx, in_range(ok_xb(tr0 + r), o), s_tile[wv][0][r]);
+            LR::issue(rb, in_range(ok_xb(tr0 + r), o), s_tile[wv][1][r]);
+            LR::issue(rc, in_range(ok_c(tr0 + r), o), s_tile[wv][2][r]);
+        }
+    };
+    if constexpr (PREFETCH) {
+        if (t_first < t_stop) prefetch(t_first);
+    }
     int buf = 0;
-    for (int64_t t0 = wk.t_begin - halo * STEP; t0 < t_stop; t0 += STEP, buf ^= 1) {
+    for (int64_t t0 = t_first; t0 < t_stop; t0 += STEP, buf ^= 1) {
         const int64_t r0 = t0 + wv * SB;          // first token of this wave's sub-block (uniform)
         const int64_t tr0 = r0 + 4 * grp;         // first of this lane's four tokens
 
         // ---- loads -------------------------------------------------------
-        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                     rc = rsrc(cb + r0 * rs), ry = rsrc(yb + r0 * rs);
-        Row<IO, CPL> xr[4], br[4], cr[4];
+        const __amdgpu_buffer_rsrc_t ry = rsrc(yb + r0 * rs);
+        RW xr[4], br[4], cr[4];
+        if constexpr (PREFETCH) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t t = tr0 + r;
-            const uint32_t o = loff + (uint32_t)(r * rs);
-            const uint32_t ox = in_range(t >= t_lo && t < wk.t_end, o);
-            xr[r].load(rx, ox);
-            br[r].load(rb, ox);
-            cr[r].load(rc, in_range(want_y && t >= wk.t_begin && t < wk.t_end, o));
+            for (int r = 0; r < 4; ++r) {
+                LR::read(s_tile[wv][0][r], lane, xr[r].w);
+                LR::read(s_tile[wv][1][r], lane, br[r].w);
+                LR::read(s_tile[wv][2][r], lane, cr[r].w);
+                if (!ok_xb(tr0 + r)) { xr[r].zero(); br[r].zero(); }
+                if (!ok_c(tr0 + r)) cr[r].zero();
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the slot may be refilled
+            if (t0 + STEP < t_stop) prefetch(t0 + STEP);
+        } else {
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                         rc = rsrc(cb + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t t = tr0 + r;
+                const uint32_t o = loff + (uint32_t)(r * rs);
+                xr[r].load(rx, in_range(ok_xb(t), o));
+                br[r].load(rb, in_range(ok_xb(t), o));
+                cr[r].load(rc, in_range(ok_c(t), o));
+            }
         }
         const int64_t ta = r0 + n;
         // Past the end of the sequence the decay is 1 (and u = 0), so the
@@ -451,13 +530,13 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
         __syncthreads();
 
         // A step need not start at a block boundary: phase of its first sub-block.
-        const int ph = (int)((t0 / SB) % S);
+        const int ph = (int)(t0 >> 4) & smask;
         float ein[CPL], vout[CPL];
 #pragma unroll
         for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
 #pragma unroll 1
         for (int r = 0; r < NW; ++r) {
-            if ((ph + r) % S == 0) {   // a block starts: its carry-in is the previous block's v
+            if (((ph + r) & smask) == 0) {   // a block starts: its carry-in is the previous block's v
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -479,9 +558,9 @@ __global__ __launch_bounds__(NW * 64) void swr_fwd_kernel(Params p) {
         }
         // The wave holding a block's last sub-block saves that block's carrier
         // v_t (its block-restarted end state) for the backward.
-        if (vb && (ph + wv) % S == S - 1) {
-            const int64_t blk = r0 / l;
-            const int64_t t_blk = blk * l;   // first token of the block (it may end past T)
+        if (vb && ((ph + wv) & smask) == smask) {
+            const int64_t blk = r0 >> p.lshift;
+            const int64_t t_blk = blk << p.lshift;   // first token of the block (it may end past T)
             store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
                                                (uint32_t)(blk * D + n * CPL) * 4u), vout);
         }
@@ -541,7 +620,7 @@ __device__ inline void build_decay_transposed(float a_n, int grp, int n, float (
 // Only the run's end needs a halo: the first block after the run (c, dy, a)
 // gives the reverse carrier entering it.  Nothing is read twice.
 template <class IO, int CPL, int NW>
-__global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
+__global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
     constexpr int D = CPL * SB;
     constexpr int STEP = NW * SB;
     constexpr int ES = IO::ES;
@@ -554,7 +633,8 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work(p);
     const int l = p.block;
-    const int S = l / SB;
+    const int S = l / SB;              // sub-blocks per block (a power of two)
+    const int smask = S - 1;
     const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the halo block
 
     const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
@@ -615,7 +695,7 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
         __syncthreads();
 #pragma unroll 1
         for (int r = NW - 1; r >= 0; --r) {
-            if (r % S == S - 1) {
+            if ((r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
@@ -637,12 +717,15 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
         const int64_t tr0 = r0 + 4 * grp;
 
         // ---- loads ---------------------------------------------------------------
-        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                     rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
         R_ xr[4], br[4], dyr[4];
         float dh[4][CPL];
         {
+            // (Copying these tiles into LDS one step ahead, as the forward
+            // does, measured no faster here: the backward's eight waves keep
+            // enough loads in flight.)
             R_ cr[4];
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                         rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
@@ -661,7 +744,7 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
         float vprev[CPL];
         {
             Row<IoF32, CPL> vr;
-            const int64_t blk = t0 / l - 1;
+            const int64_t blk = (t0 >> p.lshift) - 1;
             vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
@@ -707,7 +790,7 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
 #pragma unroll 1
             for (int r = 0; r < wv; ++r) {
-                if (r % S == 0) {
+                if ((r & smask) == 0) {
 #pragma unroll
                     for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
@@ -719,7 +802,7 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
                     s[m] = c_ * s[m] + wl;
                 }
             }
-            if (wv % S == 0) {
+            if ((wv & smask) == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -731,7 +814,7 @@ __global__ __launch_bounds__(NW * 64) void swr_bwd_kernel(Params p) {
         float epsin[CPL], kd = 0.f;
 #pragma unroll 1
         for (int r = NW - 1; r >= 0; --r) {
-            if (r % S == S - 1) {
+            if ((r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }

@@ -25,7 +25,8 @@ struct Params {
     int64_t B, T, H;
     int64_t sx_b, sx_t, sx_h;
     int64_t sa_b, sa_t, sa_h;
-    int32_t block;      // l
+    int32_t block;      // l (16, 32, 64 or 128)
+    int32_t lshift;     // log2(l)
     int32_t residual;   // 0 or 1
     int64_t run_len;    // tokens per workgroup run, a multiple of the step and of l
     int64_t nruns;      // runs per (batch, head) sequence

@@ -181,7 +181,7 @@ def test_launch_info_defaults():
     for k in ("fwd", "bwd"):
         rl, wg = info[k + "_run_len"], info[k + "_workgroups"]
         assert rl % 128 == 0 and wg == 8 * 16 * (-(-16384 // rl))
-    assert info["fwd_workgroups"] == 512 and info["bwd_workgroups"] == 256
+    assert info["fwd_workgroups"] == 512 and info["bwd_workgroups"] == 256   # 8-wave backward groups
     p = problem(B=1, T=1000, H=1, D=16, block=16, run_len=192)
     info = swr.swr_launch_info(p)
     assert info["fwd_run_len"] == info["bwd_run_len"] == 192
