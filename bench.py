@@ -59,13 +59,18 @@ def contraction_flops(cfg, backward):
     return per * (3 if backward else 1)
 
 
+# The sources that decide what a launch does (kernels, grid policy): the
+# recorded traffic is stale once any of them changes.
+KERNEL_SOURCES = ("swr_kernels.hip", "swr_api.cpp", "swr_launch.h")
+
+
 def recorded_traffic(kernel, workload):
     """HBM bytes per launch measured with rocprofv3 counters for this kernel and
-    workload, as recorded in profiles/, or None when the kernel source has
-    changed since the counters were taken."""
+    workload, as recorded in profiles/, or None when a kernel or launch-policy
+    source has changed since the counters were taken."""
     import hashlib
     import re
-    src = os.path.join(ROOT, "paper_2512_13921_amd", "csrc", "swr_kernels.hip")
+    csrc = os.path.join(ROOT, "paper_2512_13921_amd", "csrc")
     prof = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(prof):
         return None
@@ -73,7 +78,10 @@ def recorded_traffic(kernel, workload):
     if not m:
         return None
     rec = json.loads(m.group(1))
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(open(os.path.join(csrc, name), "rb").read())
+    sha = h.hexdigest()
     return rec if rec.get("kernel_sha256") == sha else None
 
 
