@@ -17,7 +17,7 @@ constexpr int64_t kMaxExtent = (int64_t)1 << 62;
 // workgroups per CU; the backward with one 8-wave workgroup per CU, and with
 // more, shorter runs when its workgroups are 4 waves (the lighter they are,
 // the more).  Longer runs mean fewer halo re-reads.
-constexpr int64_t kFwdWorkgroups = 512;
+int64_t fwd_workgroups(const swr::Shape& s) { return s.tw * s.hw == 4 ? 512 : 256; }
 int64_t bwd_workgroups(int nw, int cpl) { return nw == 8 ? 256 : (cpl == 8 ? 1024 : 4096); }
 
 // Run length (tokens, a multiple of step) that splits each sequence into
@@ -62,9 +62,9 @@ struct Resolved {
     bool empty;
     int es;             // bytes per I/O element
     int cpl;            // channels per lane = D / 16
-    int nw;             // waves per backward workgroup
-    int nw_fwd;         // waves per forward workgroup
-    int64_t step;       // tokens per workgroup step
+    swr::Shape bwd;     // backward workgroup shape
+    swr::Shape fwd;     // forward workgroup shape
+    int64_t step;       // a multiple of both sweeps' steps
     int64_t run_len, nruns, nwork;          // backward launch
     int64_t run_len_f, nruns_f, nwork_f;    // forward launch
     int64_t xspan;      // bytes spanned by one [B,T,H,D] tensor
@@ -84,9 +84,9 @@ int resolve(const swr_problem_t* p, Resolved* r) {
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
     r->cpl = (int)(p->D / 16);
-    r->nw = swr::bwd_waves_for_block(p->block);
-    r->nw_fwd = swr::fwd_waves_for_block(p->block);
-    r->step = (int64_t)std::max(r->nw, r->nw_fwd) * 16;   // both sweeps' steps divide a run
+    r->bwd = swr::bwd_shape(p->block);
+    r->fwd = swr::fwd_shape(p->block, p->H);
+    r->step = (int64_t)std::max(r->bwd.tw, r->fwd.tw) * 16;   // both sweeps' steps divide a run
     if (p->run_len < 0 || (p->run_len > 0 && p->run_len % r->step != 0)) return SWR_ERR_UNSUPPORTED;
 
     r->empty = p->B == 0 || p->T == 0 || p->H == 0;
@@ -100,20 +100,21 @@ int resolve(const swr_problem_t* p, Resolved* r) {
         r->xspan = (xo + 1) * r->es;
         r->aspan = ao + 1;
     }
-    const int64_t seqs = p->B * p->H;
+    const int64_t seqs = p->B * p->H;              // (batch, head) sequences
+    const int64_t groups = seqs / r->fwd.hw;       // forward work items per run position
     if (p->run_len > 0) {
         r->run_len = r->run_len_f = p->run_len;
     } else if (r->empty) {
         r->run_len = r->run_len_f = r->step;
     } else {
-        r->run_len = pick_run_len(p->T, seqs, r->step, bwd_workgroups(r->nw, r->cpl));
-        r->run_len_f = pick_run_len(p->T, seqs, r->step, kFwdWorkgroups);
+        r->run_len = pick_run_len(p->T, seqs, r->step, bwd_workgroups(r->bwd.tw, r->cpl));
+        r->run_len_f = pick_run_len(p->T, groups, r->step, fwd_workgroups(r->fwd));
     }
     r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
     r->nruns_f = r->empty ? 0 : (p->T + r->run_len_f - 1) / r->run_len_f;
     if (!r->empty && std::max(r->nruns, r->nruns_f) > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
     r->nwork = seqs * r->nruns;
-    r->nwork_f = seqs * r->nruns_f;
+    r->nwork_f = groups * r->nruns_f;
     r->nblocks = (p->T + p->block - 1) / p->block;
     r->carriers = seqs * r->nblocks * p->D;
     if (!r->empty) {
@@ -225,7 +226,7 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
 
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, (int)p->D, r.nw_fwd, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, (int)p->D, r.fwd, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // namespace
@@ -276,7 +277,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, (int)p->D, r.nw, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, (int)p->D, r.bwd, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // extern "C"

@@ -53,6 +53,9 @@ namespace swr {
 namespace {
 
 constexpr int SB = 16;  // tokens per sub-block = MFMA tile edge
+// LDS a forward workgroup may spend on its next-step tiles (the copies pay
+// off only while several workgroups still fit on a compute unit).
+constexpr int kFwdPrefetchLds = 48 * 1024;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -336,13 +339,16 @@ struct Work {
     int64_t b, h, t_begin, t_end;
 };
 
-__device__ inline Work decode_work(const Params& p) {
+// A work item is (batch, group of HW consecutive heads, run); the host makes
+// HW divide H.  Returns the item of head hw of this workgroup's group.
+template <int HW>
+__device__ inline Work decode_work(const Params& p, int hw) {
     // nwork < 2^31 (checked on the host), so 32-bit arithmetic suffices.
     const uint32_t wid = xcd_remap(blockIdx.x, (uint32_t)p.nwork);
-    const uint32_t H = (uint32_t)p.H, nruns = (uint32_t)p.nruns;
+    const uint32_t G = (uint32_t)p.H / HW, nruns = (uint32_t)p.nruns;
     Work wk;
-    wk.h = wid % H;
-    const uint32_t rest = wid / H;
+    wk.h = (wid % G) * HW + hw;
+    const uint32_t rest = wid / G;
     const int64_t run = rest % nruns;
     wk.b = rest / nruns;
     wk.t_begin = run * p.run_len;
@@ -404,12 +410,17 @@ __device__ inline Lanes lanes() {
 // Forward
 // ---------------------------------------------------------------------------
 
-// At least three waves per SIMD: with 4-wave workgroups that is three
-// workgroups per compute unit, whose memory and compute phases interleave.
-template <class IO, int CPL, int NW>
-__global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
+// A workgroup holds HW heads of one batch entry and TW waves per head: wave
+// wv = hw * TW + tw owns sub-block tw of each TW * 16-token step of head hw.
+// Several heads per workgroup make each step read neighbouring heads' rows,
+// i.e. longer contiguous stretches of the [B, T, H, D] tensors, together.
+// At least three waves per SIMD, so that the memory and compute phases of
+// several workgroups interleave on a compute unit.
+template <class IO, int CPL, int TW, int HW>
+__global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
+    constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
-    constexpr int STEP = NW * SB;
+    constexpr int STEP = TW * SB;
     constexpr int ES = IO::ES;
     __shared__ float s_wl[2][NW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[2][NW];       // each sub-block's decay product
@@ -418,12 +429,13 @@ __global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
     // a workgroup stay small enough for three workgroups per compute unit).
     using RW = Row<IO, CPL>;
     using LR = LdsRow<RW::BYTES>;
-    constexpr bool PREFETCH = RW::BYTES % 16 == 0 && NW * 12 * LR::SLOT_WORDS * 4 <= 48 * 1024;
+    constexpr bool PREFETCH = RW::BYTES % 16 == 0 && NW * 12 * LR::SLOT_WORDS * 4 <= kFwdPrefetchLds;
     __shared__ __attribute__((aligned(16))) uint32_t s_tile[PREFETCH ? NW : 1][3][4][PREFETCH ? LR::SLOT_WORDS : 1];
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
-    const Work wk = decode_work(p);
+    const int hw = wv / TW, tw = wv % TW;    // head within the group, sub-block within the step
+    const Work wk = decode_work<HW>(p, hw);
     const int l = p.block;
     const int S = l / SB;              // sub-blocks per block (a power of two)
     const int smask = S - 1;
@@ -459,7 +471,7 @@ __global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
     auto ok_c = [&](int64_t t) { return want_y && t >= wk.t_begin && t < wk.t_end; };
     // Copies the x, b, c tiles of the step starting at token t0 into this wave's LDS slot.
     auto prefetch = [&](int64_t t0) {
-        const int64_t r0 = t0 + wv * SB, tr0 = r0 + 4 * grp;
+        const int64_t r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs), rc = rsrc(cb + r0 * rs);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -474,7 +486,7 @@ __global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
     }
     int buf = 0;
     for (int64_t t0 = t_first; t0 < t_stop; t0 += STEP, buf ^= 1) {
-        const int64_t r0 = t0 + wv * SB;          // first token of this wave's sub-block (uniform)
+        const int64_t r0 = t0 + tw * SB;          // first token of this wave's sub-block (uniform)
         const int64_t tr0 = r0 + 4 * grp;         // first of this lane's four tokens
 
         // ---- loads -------------------------------------------------------
@@ -535,30 +547,31 @@ __global__ __launch_bounds__(NW * 64, 3) void swr_fwd_kernel(Params p) {
 #pragma unroll
         for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
 #pragma unroll 1
-        for (int r = 0; r < NW; ++r) {
+        for (int r = 0; r < TW; ++r) {      // the sub-blocks of this wave's head, in order
             if (((ph + r) & smask) == 0) {   // a block starts: its carry-in is the previous block's v
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
-            if (r == wv) {
+            if (r == tw) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) ein[m] = e[m];
             }
-            const float cr_ = s_c[buf][r];
+            const int src = hw * TW + r;
+            const float cr_ = s_c[buf][src];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                const float wl = s_wl[buf][r][n * CPL + m];
+                const float wl = s_wl[buf][src][n * CPL + m];
                 e[m] = cr_ * e[m] + wl;
                 s[m] = cr_ * s[m] + wl;
             }
-            if (r == wv) {
+            if (r == tw) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) vout[m] = s[m];
             }
         }
         // The wave holding a block's last sub-block saves that block's carrier
         // v_t (its block-restarted end state) for the backward.
-        if (vb && ((ph + wv) & smask) == smask) {
+        if (vb && ((ph + tw) & smask) == smask) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;   // first token of the block (it may end past T)
             store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
@@ -631,7 +644,7 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
-    const Work wk = decode_work(p);
+    const Work wk = decode_work<1>(p, 0);
     const int l = p.block;
     const int S = l / SB;              // sub-blocks per block (a power of two)
     const int smask = S - 1;
@@ -889,38 +902,44 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <class IO, int CPL, int NW>
-static hipError_t launch_one(const Params& p, bool backward, hipStream_t stream) {
-    const dim3 grid((unsigned)p.nwork), block(NW * 64);
-    if (backward)
-        hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, NW>), grid, block, 0, stream, p);
-    else
-        hipLaunchKernelGGL((swr_fwd_kernel<IO, CPL, NW>), grid, block, 0, stream, p);
+template <class IO, int CPL>
+static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
+    const dim3 grid((unsigned)p.nwork);
+    if (backward) {
+        if (sh.tw == 4 && sh.hw == 1)
+            hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, 4>), grid, dim3(4 * 64), 0, stream, p);
+        else if (sh.tw == 8 && sh.hw == 1)
+            hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, 8>), grid, dim3(8 * 64), 0, stream, p);
+        else
+            return hipErrorInvalidValue;
+    } else {
+#define SWR_FWD(TW_, HW_)                                                                      \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
+        hipLaunchKernelGGL((swr_fwd_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+                           stream, p);
+        if (false) {}
+        SWR_FWD(4, 1) SWR_FWD(2, 2) SWR_FWD(1, 4) SWR_FWD(4, 2) SWR_FWD(2, 4)
+        else return hipErrorInvalidValue;
+#undef SWR_FWD
+    }
     return hipGetLastError();
 }
 
-template <class IO, int CPL>
-static hipError_t launch_nw(const Params& p, int nw, bool backward, hipStream_t stream) {
-    if (nw == 4) return launch_one<IO, CPL, 4>(p, backward, stream);
-    if (nw == 8) return launch_one<IO, CPL, 8>(p, backward, stream);
-    return hipErrorInvalidValue;
-}
-
 template <class IO>
-static hipError_t launch_cpl(const Params& p, int D, int nw, bool backward, hipStream_t stream) {
+static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, hipStream_t stream) {
     switch (D) {
-        case 16: return launch_nw<IO, 1>(p, nw, backward, stream);
-        case 32: return launch_nw<IO, 2>(p, nw, backward, stream);
-        case 64: return launch_nw<IO, 4>(p, nw, backward, stream);
-        case 128: return launch_nw<IO, 8>(p, nw, backward, stream);
+        case 16: return launch_shape<IO, 1>(p, sh, backward, stream);
+        case 32: return launch_shape<IO, 2>(p, sh, backward, stream);
+        case 64: return launch_shape<IO, 4>(p, sh, backward, stream);
+        case 128: return launch_shape<IO, 8>(p, sh, backward, stream);
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch(const Params& p, int dtype, int D, int nw, bool backward, void* stream) {
+hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == 1) return launch_cpl<IoBf16>(p, D, nw, backward, st);
-    return launch_cpl<IoF32>(p, D, nw, backward, st);
+    if (dtype == 1) return launch_cpl<IoBf16>(p, D, sh, backward, st);
+    return launch_cpl<IoF32>(p, D, sh, backward, st);
 }
 
 }  // namespace swr

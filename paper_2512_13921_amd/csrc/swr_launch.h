@@ -34,13 +34,21 @@ struct Params {
     int64_t nblocks;    // ceil(T / block): carriers per (batch, head)
 };
 
-// Waves per workgroup.  The backward's steps (waves * 16 tokens) must hold
-// whole blocks; the forward's need not, and it uses small workgroups so that
-// several run side by side on a compute unit.
-inline int bwd_waves_for_block(int64_t block) { return block >= 128 ? 8 : 4; }
-inline int fwd_waves_for_block(int64_t /*block*/) { return 4; }
+// Workgroup shape: tw waves per head along the tokens (a step is tw * 16
+// tokens) times hw heads of one batch entry.  The backward's steps must hold
+// whole blocks and it runs one head per workgroup.  The forward's steps need
+// not; several heads per workgroup make its loads of the [B, T, H, D] tensors
+// longer contiguous stretches (hw must divide H).
+struct Shape {
+    int tw, hw;
+};
+inline Shape bwd_shape(int64_t block) { return {block >= 128 ? 8 : 4, 1}; }
+inline Shape fwd_shape(int64_t /*block*/, int64_t H) {
+    if (H % 2 == 0) return {2, 2};
+    return {4, 1};
+}
 
-// Launches the forward or backward kernel for (dtype, D, waves) on `stream`.
-hipError_t launch(const Params& p, int dtype, int D, int nw, bool backward, void* stream);
+// Launches the forward or backward kernel for (dtype, D, shape) on `stream`.
+hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool backward, void* stream);
 
 }  // namespace swr

@@ -178,14 +178,20 @@ def test_launch_info_defaults():
     # headline workload: B=8, T=16384, H=16, D=128, block 128
     p = problem(B=8, T=16384, H=16, D=128, block=128)
     info = swr.swr_launch_info(p)
-    for k in ("fwd", "bwd"):
+    # the forward's workgroups hold 2 heads each, the backward's one
+    for k, heads in (("fwd", 2), ("bwd", 1)):
         rl, wg = info[k + "_run_len"], info[k + "_workgroups"]
-        assert rl % 128 == 0 and wg == 8 * 16 * (-(-16384 // rl))
+        assert rl % 128 == 0 and wg == 8 * (16 // heads) * (-(-16384 // rl))
     assert info["fwd_workgroups"] == 512 and info["bwd_workgroups"] == 256   # 8-wave backward groups
     p = problem(B=1, T=1000, H=1, D=16, block=16, run_len=192)
     info = swr.swr_launch_info(p)
     assert info["fwd_run_len"] == info["bwd_run_len"] == 192
-    assert info["fwd_workgroups"] == info["bwd_workgroups"] == 6
+    assert info["fwd_workgroups"] == info["bwd_workgroups"] == 6          # H = 1: one head per group
+    p = problem(B=3, T=1000, H=6, D=16, block=16, run_len=192)
+    info = swr.swr_launch_info(p)
+    assert info["fwd_workgroups"] == 3 * 3 * 6 and info["bwd_workgroups"] == 3 * 6 * 6
+    p = problem(B=2, T=1000, H=5, D=16, block=16, run_len=192)        # odd H: one head per group
+    assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * 5 * 6
 
 
 def test_non_contiguous_layouts_accepted():

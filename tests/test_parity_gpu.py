@@ -79,6 +79,8 @@ SMALL = [
     (1, 1, 1, 64, 64, "bf16"),      # a single token
     (1, 17, 1, 128, 128, "bf16"),   # shorter than one sub-block ... one block
     (1, 130, 1, 16, 128, "f32"),
+    (2, 700, 4, 64, 64, "bf16"),    # several head pairs per batch entry
+    (3, 300, 6, 128, 32, "f32"),
 ]
 
 
