@@ -13,12 +13,14 @@ namespace {
 constexpr int64_t kMaxWorkgroups = 0x7fffffffLL;
 constexpr int64_t kMaxExtent = (int64_t)1 << 62;
 // Default grid sizes, measured on the MI355X (256 compute units) over the
-// benchmark workloads: the forward runs best with about two 4-wave
-// workgroups per CU; the backward with one 8-wave workgroup per CU, and with
-// more, shorter runs when its workgroups are 4 waves (the lighter they are,
-// the more).  Longer runs mean fewer halo re-reads.
+// benchmark workloads: the forward runs best with two 4-wave workgroups per
+// CU; the backward with one 8-wave workgroup per CU, and with more, shorter
+// runs when its workgroups are 4 waves (the lighter they are, the more).
+// Longer runs mean fewer halo re-reads.
 int64_t fwd_workgroups(const swr::Shape& s) { return s.tw * s.hw == 4 ? 512 : 256; }
-int64_t bwd_workgroups(int nw, int cpl) { return nw == 8 ? 256 : (cpl == 8 ? 1024 : 4096); }
+int64_t bwd_workgroups(const swr::Shape& s, int cpl) {
+    return s.tw * s.hw == 8 ? 256 : (cpl == 8 ? 1024 : 4096);
+}
 
 // Run length (tokens, a multiple of step) that splits each sequence into
 // enough runs to give about `target` workgroups.
@@ -84,7 +86,7 @@ int resolve(const swr_problem_t* p, Resolved* r) {
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
     r->cpl = (int)(p->D / 16);
-    r->bwd = swr::bwd_shape(p->block);
+    r->bwd = swr::bwd_shape(p->block, p->H);
     r->fwd = swr::fwd_shape(p->block, p->H);
     r->step = (int64_t)std::max(r->bwd.tw, r->fwd.tw) * 16;   // both sweeps' steps divide a run
     if (p->run_len < 0 || (p->run_len > 0 && p->run_len % r->step != 0)) return SWR_ERR_UNSUPPORTED;
@@ -102,18 +104,19 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     }
     const int64_t seqs = p->B * p->H;              // (batch, head) sequences
     const int64_t groups = seqs / r->fwd.hw;       // forward work items per run position
+    const int64_t groups_b = seqs / r->bwd.hw;     // backward work items per run position
     if (p->run_len > 0) {
         r->run_len = r->run_len_f = p->run_len;
     } else if (r->empty) {
         r->run_len = r->run_len_f = r->step;
     } else {
-        r->run_len = pick_run_len(p->T, seqs, r->step, bwd_workgroups(r->bwd.tw, r->cpl));
+        r->run_len = pick_run_len(p->T, groups_b, r->step, bwd_workgroups(r->bwd, r->cpl));
         r->run_len_f = pick_run_len(p->T, groups, r->step, fwd_workgroups(r->fwd));
     }
     r->nruns = r->empty ? 0 : (p->T + r->run_len - 1) / r->run_len;
     r->nruns_f = r->empty ? 0 : (p->T + r->run_len_f - 1) / r->run_len_f;
     if (!r->empty && std::max(r->nruns, r->nruns_f) > kMaxWorkgroups / seqs) return SWR_ERR_UNSUPPORTED;
-    r->nwork = seqs * r->nruns;
+    r->nwork = groups_b * r->nruns;
     r->nwork_f = groups * r->nruns_f;
     r->nblocks = (p->T + p->block - 1) / p->block;
     r->carriers = seqs * r->nblocks * p->D;

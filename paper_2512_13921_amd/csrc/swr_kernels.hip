@@ -632,10 +632,11 @@ __device__ inline void build_decay_transposed(float a_n, int grp, int n, float (
 // saved by the forward pass (the paper's "checkpoint only the carrier").
 // Only the run's end needs a halo: the first block after the run (c, dy, a)
 // gives the reverse carrier entering it.  Nothing is read twice.
-template <class IO, int CPL, int NW>
-__global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
+template <class IO, int CPL, int TW, int HW>
+__global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
+    constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
-    constexpr int STEP = NW * SB;
+    constexpr int STEP = TW * SB;      // whole blocks
     constexpr int ES = IO::ES;
     using R_ = Row<IO, CPL>;
     __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve L u
@@ -644,7 +645,8 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
-    const Work wk = decode_work<1>(p, 0);
+    const int hw = wv / TW, tw = wv % TW;    // head within the group, sub-block within the step
+    const Work wk = decode_work<HW>(p, hw);
     const int l = p.block;
     const int S = l / SB;              // sub-blocks per block (a power of two)
     const int smask = S - 1;
@@ -680,7 +682,7 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
 
     // ---- halo: the first block after the run -----------------------------------
     if (wk.t_end < p.T) {
-        const int64_t r0 = wk.t_end + wv * SB;
+        const int64_t r0 = wk.t_end + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
         R_ cr[4], dyr[4];
@@ -707,15 +709,16 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
         if (lane == 0) s_c[buf][wv] = cq;
         __syncthreads();
 #pragma unroll 1
-        for (int r = NW - 1; r >= 0; --r) {
+        for (int r = TW - 1; r >= 0; --r) {
             if ((r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
-            const float c_ = s_c[buf][r];
+            const int src = hw * TW + r;
+            const float c_ = s_c[buf][src];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                const float df = s_df[buf][r][n * CPL + m];
+                const float df = s_df[buf][src][n * CPL + m];
                 eps[m] = c_ * eps[m] + df;
                 pr[m] = c_ * pr[m] + df;
             }
@@ -726,7 +729,7 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
     for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
         const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
-        const int64_t r0 = t0 + wv * SB;
+        const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
 
         // ---- loads ---------------------------------------------------------------
@@ -802,20 +805,21 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
 #pragma unroll 1
-            for (int r = 0; r < wv; ++r) {
+            for (int r = 0; r < tw; ++r) {
                 if ((r & smask) == 0) {
 #pragma unroll
                     for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
-                const float c_ = s_c[buf][r];
+                const int src = hw * TW + r;
+                const float c_ = s_c[buf][src];
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
-                    const float wl = s_wl[buf][r][n * CPL + m];
+                    const float wl = s_wl[buf][src][n * CPL + m];
                     e[m] = c_ * e[m] + wl;
                     s[m] = c_ * s[m] + wl;
                 }
             }
-            if ((wv & smask) == 0) {
+            if ((tw & smask) == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -826,22 +830,23 @@ __global__ __launch_bounds__(NW * 64, 2) void swr_bwd_kernel(Params p) {
         // ---- reverse carriers: capture at this sub-block, carry to the previous step ---
         float epsin[CPL], kd = 0.f;
 #pragma unroll 1
-        for (int r = NW - 1; r >= 0; --r) {
+        for (int r = TW - 1; r >= 0; --r) {
             if ((r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
-            if (r == wv) {
+            if (r == tw) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     epsin[m] = eps[m];
                     kd += (ein[m] - sin_[m]) * (eps[m] - pr[m]);
                 }
             }
-            const float c_ = s_c[buf][r];
+            const int src = hw * TW + r;
+            const float c_ = s_c[buf][src];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                const float df = s_df[buf][r][n * CPL + m];
+                const float df = s_df[buf][src][n * CPL + m];
                 eps[m] = c_ * eps[m] + df;
                 pr[m] = c_ * pr[m] + df;
             }
@@ -906,12 +911,14 @@ template <class IO, int CPL>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
     if (backward) {
-        if (sh.tw == 4 && sh.hw == 1)
-            hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, 4>), grid, dim3(4 * 64), 0, stream, p);
-        else if (sh.tw == 8 && sh.hw == 1)
-            hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, 8>), grid, dim3(8 * 64), 0, stream, p);
-        else
-            return hipErrorInvalidValue;
+#define SWR_BWD(TW_, HW_)                                                                      \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
+        hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+                           stream, p);
+        if (false) {}
+        SWR_BWD(8, 1) SWR_BWD(4, 1)
+        else return hipErrorInvalidValue;
+#undef SWR_BWD
     } else {
 #define SWR_FWD(TW_, HW_)                                                                      \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
