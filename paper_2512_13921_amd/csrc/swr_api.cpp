@@ -103,6 +103,13 @@ int resolve(const swr_problem_t* p, Resolved* r) {
         r->aspan = ao + 1;
     }
     const int64_t seqs = p->B * p->H;              // (batch, head) sequences
+    if (r->fwd.hw > 1 && p->run_len == 0 && !r->empty) {
+        // On a problem too small to fill the forward's grid, grouping heads
+        // would only halve it: keep one head per workgroup there.
+        const int64_t g = seqs / r->fwd.hw;
+        const int64_t rl = pick_run_len(p->T, g, r->step, fwd_workgroups(r->fwd));
+        if (g * ((p->T + rl - 1) / rl) < fwd_workgroups(r->fwd)) r->fwd = swr::fwd_shape_single();
+    }
     const int64_t groups = seqs / r->fwd.hw;       // forward work items per run position
     const int64_t groups_b = seqs / r->bwd.hw;     // backward work items per run position
     if (p->run_len > 0) {

@@ -47,9 +47,10 @@ struct Shape {
 inline Shape bwd_shape(int64_t block, int64_t /*H*/) {
     return {block >= 128 ? 8 : 4, 1};
 }
+inline Shape fwd_shape_single() { return {4, 1}; }
 inline Shape fwd_shape(int64_t /*block*/, int64_t H) {
     if (H % 2 == 0) return {2, 2};
-    return {4, 1};
+    return fwd_shape_single();
 }
 
 // Launches the forward or backward kernel for (dtype, D, shape) on `stream`.

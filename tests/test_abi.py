@@ -190,6 +190,9 @@ def test_launch_info_defaults():
     p = problem(B=3, T=1000, H=6, D=16, block=16, run_len=192)
     info = swr.swr_launch_info(p)
     assert info["fwd_workgroups"] == 3 * 3 * 6 and info["bwd_workgroups"] == 3 * 6 * 6
+    # a problem too small to fill the forward's grid keeps one head per group
+    p = problem(B=1, T=1024, H=4, D=64, block=64, dtype=F32)
+    assert swr.swr_launch_info(p)["fwd_workgroups"] == 4 * 16
     p = problem(B=2, T=1000, H=5, D=16, block=16, run_len=192)        # odd H: one head per group
     assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * 5 * 6
 
