@@ -34,8 +34,9 @@
  * dimension D contiguous (stride 1) and element strides sx_b, sx_t, sx_h for
  * the other three dimensions (shared by all eight tensors).  a is [B, T, H]
  * with strides sa_b, sa_t, sa_h; da uses the same strides as a but is always
- * float32.  Element type of x, a, b, c, y, dy, dx, db, dc is `dtype`;
- * accumulation is always float32.
+ * float32 (with SWR_FLAG_PER_CHANNEL_DECAY, a and da are [B, T, H, D] with the
+ * strides of x instead).  Element type of x, a, b, c, y, dy, dx, db, dc is
+ * `dtype`; accumulation is always float32.
  *
  * Ownership.  Every pointer is device memory owned by the caller.  The library
  * allocates no memory, needs no workspace and keeps no mutable global state;
@@ -83,6 +84,17 @@ typedef enum swr_dtype {
  * residual, Sec. 5). */
 #define SWR_FLAG_RESIDUAL 1u
 
+/* Per-channel decay: a holds one decay per token, head AND channel, i.e. the
+ * diagonal transition a_t (*) h_{t-1} of eq. (2.1) with a full diagonal
+ * instead of one scalar per head.  a is then [B, T, H, D] in the I/O dtype
+ * and da is [B, T, H, D] float32, both with the strides sx_* of x (sa_* are
+ * not read), with the alignment of x (da: of its float32 lane slices, i.e.
+ * min(16, 4 * min(D, 64) / 16) bytes).  The window truncation, carriers and
+ * every other convention are unchanged; the per-channel da is not summed
+ * over channels.  The intra-block solve is then a per-channel scan rather
+ * than a matrix product (the operator L_t differs from channel to channel). */
+#define SWR_FLAG_PER_CHANNEL_DECAY 2u
+
 typedef struct swr_problem {
     int32_t abi_version;   /* must be SWR_ABI_VERSION                                     */
     int32_t dtype;         /* swr_dtype_t of every tensor except da                       */
@@ -91,7 +103,8 @@ typedef struct swr_problem {
     uint32_t flags;        /* SWR_FLAG_* bits                                              */
     int32_t reserved;      /* must be 0                                                    */
     int64_t sx_b, sx_t, sx_h;  /* element strides of the [B,T,H,D] tensors (channel = 1) */
-    int64_t sa_b, sa_t, sa_h;  /* element strides of a and da                            */
+    int64_t sa_b, sa_t, sa_h;  /* element strides of a and da (ignored with
+                                  SWR_FLAG_PER_CHANNEL_DECAY: a, da then use sx_*)      */
     int64_t run_len;       /* tokens per workgroup run: 0 = automatic (chosen separately
                               for the forward and the backward), else a positive multiple
                               of max(64, block) used by both; a tuning knob that does not
@@ -110,7 +123,7 @@ int swr_forward(const swr_problem_t* problem, const void* x, const void* a, cons
 int swr_carriers(const swr_problem_t* problem, const void* x, const void* a, const void* b,
                  float* carriers, void* stream);
 
-/* Backward: given dy = dL/dy, writes dx, da (float32, [B,T,H] at a's strides),
+/* Backward: given dy = dL/dy, writes dx, da (float32 with a's shape and strides),
  * db and dc.  x, a, b, c are the forward's inputs and `carriers` the block
  * carriers of those same inputs (from swr_forward or swr_carriers; required).
  * Nothing else from the forward is needed: the kernel recomputes the local

@@ -8,7 +8,9 @@ GPU, the calls raise.
 
 Layouts: ``x, b, c, y, dy, dx, db, dc`` are ``[B, T, H, D]`` (channels
 contiguous, all with the same strides); ``a`` is ``[B, T, H]`` in the same
-dtype; ``da`` is float32 with ``a``'s shape.  Supported dtypes: float32 and
+dtype (one decay per head), or ``[B, T, H, D]`` with x's strides (one decay
+per channel, ``SWR_FLAG_PER_CHANNEL_DECAY``); ``da`` is float32 with ``a``'s
+shape.  Supported dtypes: float32 and
 bfloat16.  The block carriers that the forward saves for the backward are a
 float32 ``[B, H, ceil(T / block), D]`` tensor (``carrier_shape``).
 """
@@ -25,6 +27,7 @@ SWR_ABI_VERSION = 1
 SWR_DTYPE_F32 = 0
 SWR_DTYPE_BF16 = 1
 SWR_FLAG_RESIDUAL = 1
+SWR_FLAG_PER_CHANNEL_DECAY = 2
 
 
 class SwrProblem(ctypes.Structure):
@@ -91,14 +94,15 @@ def swr_abi_version() -> int:
     return int(load().swr_abi_version())
 
 
-def make_problem(B, T, H, D, block, dtype_code, x_strides, a_strides, residual=False, run_len=0):
+def make_problem(B, T, H, D, block, dtype_code, x_strides, a_strides, residual=False, run_len=0,
+                 per_channel=False):
     """A ``swr_problem_t`` from plain integers (strides in elements, [B, T, H] order)."""
     p = SwrProblem()
     p.abi_version = SWR_ABI_VERSION
     p.dtype = dtype_code
     p.B, p.T, p.H, p.D = int(B), int(T), int(H), int(D)
     p.block = int(block)
-    p.flags = SWR_FLAG_RESIDUAL if residual else 0
+    p.flags = (SWR_FLAG_RESIDUAL if residual else 0) | (SWR_FLAG_PER_CHANNEL_DECAY if per_channel else 0)
     p.reserved = 0
     p.sx_b, p.sx_t, p.sx_h = (int(s) for s in x_strides)
     p.sa_b, p.sa_t, p.sa_h = (int(s) for s in a_strides)
@@ -148,15 +152,22 @@ def _dtype_code(t):
 
 
 def _problem_from(x, a, block, residual, run_len):
-    if x.dim() != 4 or a.dim() != 3 or tuple(a.shape) != tuple(x.shape[:3]):
-        raise ValueError("x must be [B, T, H, D] and a must be [B, T, H]")
+    if x.dim() != 4:
+        raise ValueError("x must be [B, T, H, D]")
+    per_channel = a.dim() == 4
+    if per_channel:
+        if a.shape != x.shape or a.stride() != x.stride():
+            raise ValueError("a per-channel decay must have the shape and strides of x")
+    elif a.dim() != 3 or tuple(a.shape) != tuple(x.shape[:3]):
+        raise ValueError("a must be [B, T, H] (one decay per head) or [B, T, H, D] (per channel)")
     if x.stride(3) != 1 and x.shape[3] > 1:
         raise ValueError("the channel dimension of x must be contiguous")
     if a.dtype != x.dtype:
         raise TypeError("a must have the dtype of x")
     B, T, H, D = x.shape
-    return make_problem(B, T, H, D, block, _dtype_code(x), x.stride()[:3], a.stride(),
-                        residual, run_len)
+    return make_problem(B, T, H, D, block, _dtype_code(x), x.stride()[:3],
+                        x.stride()[:3] if per_channel else a.stride(), residual, run_len,
+                        per_channel)
 
 
 def _same_layout(ref, *others):

@@ -63,7 +63,12 @@ bool non_overlapping(Dim* d, int nd) {
 struct Resolved {
     bool empty;
     int es;             // bytes per I/O element
-    int cpl;            // channels per lane = D / 16
+    int cpl;            // channels per lane of the kernels = dk / 16
+    bool pc;            // per-channel decay: a and da have the [B, T, H, D] layout of x
+    int hshift;         // per-channel kernels: log2 of the virtual heads per head
+    int dk;             // channels a kernel's head covers (D, or D >> hshift)
+    int64_t hv;         // heads the kernels split the work over (H << hshift)
+    int64_t vbytes;     // bytes of one lane's slice of an x-like row (alignment unit)
     swr::Shape bwd;     // backward workgroup shape
     swr::Shape fwd;     // forward workgroup shape
     int64_t step;       // a multiple of both sweeps' steps
@@ -82,12 +87,18 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     if (p->B < 0 || p->T < 0 || p->H < 0 || p->D < 1) return SWR_ERR_SHAPE;
     if (p->block != 16 && p->block != 32 && p->block != 64 && p->block != 128) return SWR_ERR_BLOCK;
     if (p->D != 16 && p->D != 32 && p->D != 64 && p->D != 128) return SWR_ERR_UNSUPPORTED;
-    if ((p->flags & ~SWR_FLAG_RESIDUAL) != 0 || p->reserved != 0) return SWR_ERR_UNSUPPORTED;
+    if ((p->flags & ~(SWR_FLAG_RESIDUAL | SWR_FLAG_PER_CHANNEL_DECAY)) != 0 || p->reserved != 0)
+        return SWR_ERR_UNSUPPORTED;
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
-    r->cpl = (int)(p->D / 16);
-    r->bwd = swr::bwd_shape(p->block, p->H);
-    r->fwd = swr::fwd_shape(p->block, p->H);
+    r->pc = (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) != 0;
+    r->hshift = r->pc ? swr::pc_hshift(p->D) : 0;
+    r->dk = (int)(p->D >> r->hshift);
+    r->cpl = r->dk / 16;
+    r->hv = p->H << r->hshift;
+    r->vbytes = std::min<int64_t>(16, (int64_t)(r->dk / 16) * r->es);
+    r->bwd = swr::bwd_shape(p->block, r->hv);
+    r->fwd = swr::fwd_shape(p->block, r->hv);
     r->step = (int64_t)std::max(r->bwd.tw, r->fwd.tw) * 16;   // both sweeps' steps divide a run
     if (p->run_len < 0 || (p->run_len > 0 && p->run_len % r->step != 0)) return SWR_ERR_UNSUPPORTED;
 
@@ -95,14 +106,19 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     r->xspan = r->aspan = 0;
     if (!r->empty) {   // strides of an empty tensor are meaningless
         Dim xd[4] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}, {p->D, 1}};
-        Dim ad[3] = {{p->B, p->sa_b}, {p->T, p->sa_t}, {p->H, p->sa_h}};
-        const int64_t xo = max_offset(xd, 4), ao = max_offset(ad, 3);
-        if (xo < 0 || ao < 0) return SWR_ERR_SHAPE;
-        if (!non_overlapping(xd, 4) || !non_overlapping(ad, 3)) return SWR_ERR_SHAPE;
+        const int64_t xo = max_offset(xd, 4);
+        if (xo < 0 || !non_overlapping(xd, 4)) return SWR_ERR_SHAPE;
         r->xspan = (xo + 1) * r->es;
-        r->aspan = ao + 1;
+        if (r->pc) {       // a and da use the strides of x; sa_* are not read
+            r->aspan = xo + 1;
+        } else {
+            Dim ad[3] = {{p->B, p->sa_b}, {p->T, p->sa_t}, {p->H, p->sa_h}};
+            const int64_t ao = max_offset(ad, 3);
+            if (ao < 0 || !non_overlapping(ad, 3)) return SWR_ERR_SHAPE;
+            r->aspan = ao + 1;
+        }
     }
-    const int64_t seqs = p->B * p->H;              // (batch, head) sequences
+    const int64_t seqs = p->B * r->hv;             // (batch, head) sequences the kernels see
     if (r->fwd.hw > 1 && p->run_len == 0 && !r->empty) {
         // On a problem too small to fill the forward's grid, grouping heads
         // would only halve it: keep one head per workgroup there.
@@ -126,24 +142,28 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     r->nwork = groups_b * r->nruns;
     r->nwork_f = groups * r->nruns_f;
     r->nblocks = (p->T + p->block - 1) / p->block;
-    r->carriers = seqs * r->nblocks * p->D;
+    r->carriers = p->B * p->H * r->nblocks * p->D;
     if (!r->empty) {
         // The kernels address a lane's data with 32-bit byte offsets from a
         // per-step base: 16 rows of x-like tensors, 16 tokens of a / da, and a
         // (batch, head)'s carrier array must stay below 2^31 bytes.
         const int64_t lim = 0x7fffffffLL;
         if (p->sx_t > (lim - p->D * r->es) / (16 * r->es)) return SWR_ERR_UNSUPPORTED;
-        if (p->sa_t > lim / (16 * 4)) return SWR_ERR_UNSUPPORTED;
+        if (r->pc ? p->sx_t > (lim - p->D * 4) / (16 * 4) : p->sa_t > lim / (16 * 4))
+            return SWR_ERR_UNSUPPORTED;
         if (r->nblocks > lim / (p->D * 4)) return SWR_ERR_UNSUPPORTED;
     }
     return SWR_OK;
 }
 
 int check_strides_aligned(const swr_problem_t* p, const Resolved& r) {
-    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);   // bytes per lane row vector
+    const int64_t vda = std::min<int64_t>(16, (int64_t)(r.dk / 16) * 4);   // per-channel da slice
     const Dim xd[3] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}};
-    for (const Dim& d : xd)
-        if (d.size > 1 && (d.stride * r.es) % vb != 0) return SWR_ERR_ALIGN;
+    for (const Dim& d : xd) {
+        if (d.size > 1 && (d.stride * r.es) % r.vbytes != 0) return SWR_ERR_ALIGN;
+        if (r.pc && d.size > 1 && (d.stride * 4) % vda != 0) return SWR_ERR_ALIGN;
+    }
+    if (r.pc && (r.dk * r.es) % r.vbytes != 0) return SWR_ERR_ALIGN;   // a virtual head's offset
     return SWR_OK;
 }
 
@@ -160,6 +180,8 @@ bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; 
 swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward) {
     swr::Params k{};
     k.B = p->B; k.T = p->T; k.H = p->H;
+    k.Hv = r.hv;
+    k.hshift = r.hshift;
     k.sx_b = p->sx_b; k.sx_t = p->sx_t; k.sx_h = p->sx_h;
     k.sa_b = p->sa_b; k.sa_t = p->sa_t; k.sa_h = p->sa_h;
     k.block = (int32_t)p->block;
@@ -187,7 +209,7 @@ const char* swr_error_string(int code) {
         case SWR_ERR_BLOCK: return "block must be 16, 32, 64 or 128";
         case SWR_ERR_ALIGN: return "pointer or stride not aligned to the per-lane vector width";
         case SWR_ERR_ALIAS: return "an output overlaps an input or another output";
-        case SWR_ERR_UNSUPPORTED: return "unsupported: D must be 16, 32, 64 or 128; unknown flags; or bad run_len";
+        case SWR_ERR_UNSUPPORTED: return "unsupported: D must be 16, 32, 64 or 128; unknown flags; bad run_len; or offsets beyond 32 bits";
         case SWR_ERR_HIP: return "the HIP runtime rejected the kernel launch";
         case SWR_ERR_VERSION: return "ABI version mismatch";
         default: return "unknown status code";
@@ -222,10 +244,9 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
     if (!x || !a || !b || (y && !c)) return SWR_ERR_NULL;
-    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
     for (const void* q : {x, b, c, (const void*)y})
-        if (q && !aligned(q, vb)) return SWR_ERR_ALIGN;
-    if (!aligned(a, r.es) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
+        if (q && !aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.pc ? r.vbytes : r.es) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     const Span ins[4] = {span(x, r.xspan), span(b, r.xspan), span(c, c ? r.xspan : 0),
                          span(a, r.aspan * r.es)};
@@ -236,7 +257,7 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
 
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, (int)p->D, r.fwd, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // namespace
@@ -267,10 +288,11 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
     if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc) return SWR_ERR_NULL;
-    const int64_t vb = std::min<int64_t>(16, (int64_t)r.cpl * r.es);
     for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
-        if (!aligned(q, vb)) return SWR_ERR_ALIGN;
-    if (!aligned(a, r.es) || !aligned(da, 4) || !aligned(carriers, 16)) return SWR_ERR_ALIGN;
+        if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+    const int64_t va = r.pc ? r.vbytes : r.es;
+    const int64_t vda = r.pc ? std::min<int64_t>(16, (int64_t)(r.dk / 16) * 4) : 4;
+    if (!aligned(a, va) || !aligned(da, vda) || !aligned(carriers, 16)) return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     const Span outs[4] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan),
                           span(da, r.aspan * 4)};
@@ -287,7 +309,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, (int)p->D, r.bwd, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // extern "C"

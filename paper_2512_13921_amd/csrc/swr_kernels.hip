@@ -340,12 +340,13 @@ struct Work {
 };
 
 // A work item is (batch, group of HW consecutive heads, run); the host makes
-// HW divide H.  Returns the item of head hw of this workgroup's group.
+// HW divide the head count Hv (heads, or virtual heads of the per-channel
+// kernels).  Returns the item of head hw of this workgroup's group.
 template <int HW>
 __device__ inline Work decode_work(const Params& p, int hw) {
     // nwork < 2^31 (checked on the host), so 32-bit arithmetic suffices.
     const uint32_t wid = xcd_remap(blockIdx.x, (uint32_t)p.nwork);
-    const uint32_t G = (uint32_t)p.H / HW, nruns = (uint32_t)p.nruns;
+    const uint32_t G = (uint32_t)p.Hv / HW, nruns = (uint32_t)p.nruns;
     Work wk;
     wk.h = (wid % G) * HW + hw;
     const uint32_t rest = wid / G;
@@ -901,11 +902,510 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Per-channel decay
+// ---------------------------------------------------------------------------
+//
+// With a decay a_{k,mu} per token and channel, every channel is its own scalar
+// recurrence: the sub-block operator differs from channel to channel, so the
+// local solve is no longer one matrix product shared by the channels.  It is
+// a first-order linear scan instead, done per lane and channel: the lane's
+// four tokens in order, then a doubling scan over the four 16-lane rows
+// (tokens 0-3, 4-7, 8-11, 12-15) of the wave.  Everything else -- sub-blocks
+// composed through LDS, block carriers, runs, halos, the reverse sweep of the
+// backward -- is the scheme of the shared-decay kernels with each decay
+// product kept per channel.  Since no quantity couples channels any more, a
+// head of D = 128 channels is processed as two independent halves ("virtual
+// heads" of 64 channels), which keeps the per-channel products in registers.
+
+// Forward local solve of one sub-block, per channel:  w_k = a_k w_{k-1} + u_k
+// and G_k = a_k G_{k-1} (w_{-1} = 0, G_{-1} = 1) for this lane's tokens
+// k = 4*grp + r.  A state is carried through a stretch of tokens by
+// s -> G s + w, so stretches compose as (G1, w1) then (G2, w2) =
+// (G1 G2, G2 w1 + w2).
+template <int CPL>
+__device__ inline void chan_scan_fwd(const float (&a)[4][CPL], const float (&u)[4][CPL],
+                                     float (&w)[4][CPL], float (&G)[4][CPL], int grp, int lane) {
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) {
+        G[0][m] = a[0][m];
+        w[0][m] = u[0][m];
+#pragma unroll
+        for (int r = 1; r < 4; ++r) {
+            G[r][m] = a[r][m] * G[r - 1][m];
+            w[r][m] = a[r][m] * w[r - 1][m] + u[r][m];
+        }
+        // Inclusive scan of the row totals over rows 0..grp.
+        float tg = G[3][m], tw = w[3][m];
+        float pg = shfl(tg, (lane - 16) & 63), pw = shfl(tw, (lane - 16) & 63);
+        if (grp >= 1) { tw = tg * pw + tw; tg = pg * tg; }
+        pg = shfl(tg, (lane - 32) & 63); pw = shfl(tw, (lane - 32) & 63);
+        if (grp >= 2) { tw = tg * pw + tw; tg = pg * tg; }
+        // Exclusive: the stretch from the sub-block start to this row.
+        pg = shfl(tg, (lane - 16) & 63); pw = shfl(tw, (lane - 16) & 63);
+        const float gin = grp >= 1 ? pg : 1.0f, win = grp >= 1 ? pw : 0.0f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            w[r][m] += G[r][m] * win;
+            G[r][m] *= gin;
+        }
+    }
+}
+
+// Reverse local solve of one sub-block, per channel:  D_k = dh_k + a_{k+1} D_{k+1}
+// (D_16 = 0), i.e. D = L^T dh, and R_k = a_{k+1} ... a_15 (R_15 = 1).  It runs
+// on E_k = a_k D_k, the adjoint leaving token k towards k-1, so that each row
+// uses only its own decays: E_k = a_k (dh_k + E_{k+1}).  E is carried
+// backwards through a stretch by e -> Q e + E_loc with Q the stretch's decay
+// product.
+template <int CPL>
+__device__ inline void chan_scan_rev(const float (&a)[4][CPL], const float (&dh)[4][CPL],
+                                     float (&Dv)[4][CPL], float (&R)[4][CPL], int grp, int lane) {
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) {
+        // In-lane pass with nothing entering from the next row.
+        Dv[3][m] = dh[3][m];
+        R[3][m] = 1.0f;
+#pragma unroll
+        for (int r = 2; r >= 0; --r) {
+            Dv[r][m] = dh[r][m] + a[r + 1][m] * Dv[r + 1][m];
+            R[r][m] = a[r + 1][m] * R[r + 1][m];
+        }
+        // Row totals: Q = a_{4g} ... a_{4g+3}, E_loc = a_{4g} D_loc(4g).
+        float tq = a[0][m] * R[0][m], te = a[0][m] * Dv[0][m];
+        // Inclusive scan over rows grp..3.
+        float pq = shfl(tq, (lane + 16) & 63), pe = shfl(te, (lane + 16) & 63);
+        if (grp <= 2) { te = tq * pe + te; tq = tq * pq; }
+        pq = shfl(tq, (lane + 32) & 63); pe = shfl(te, (lane + 32) & 63);
+        if (grp <= 1) { te = tq * pe + te; tq = tq * pq; }
+        // Exclusive: E entering the row from the next one, and the decay
+        // product of the tokens after the row.
+        pq = shfl(tq, (lane + 16) & 63); pe = shfl(te, (lane + 16) & 63);
+        const float lam = grp <= 2 ? pe : 0.0f, qin = grp <= 2 ? pq : 1.0f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            Dv[r][m] += R[r][m] * lam;
+            R[r][m] *= qin;
+        }
+    }
+}
+
+// The decays of one row slice as floats; past the end of the sequence the
+// decay is 1 (and the input 0), so a partial last block's carrier is the
+// state at its last token.
+template <class IO, int CPL>
+__device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int64_t T, float (&av)[4][CPL]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) av[r][m] = tr0 + r >= T ? 1.0f : ar[r].get(m);
+}
+
+// Per-channel forward.  Same workgroup shape and sweep as swr_fwd_kernel;
+// wk.h is a virtual head: head wk.h >> hshift, channel half wk.h & (2^hshift - 1).
+template <class IO, int CPL, int TW, int HW>
+__global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
+    constexpr int NW = TW * HW;
+    constexpr int D = CPL * SB;        // channels of a virtual head
+    constexpr int STEP = TW * SB;
+    constexpr int ES = IO::ES;
+    using RW = Row<IO, CPL>;
+    __shared__ float s_wl[2][NW][D];   // last row of each sub-block's local solve
+    __shared__ float s_cc[2][NW][D];   // each sub-block's decay product, per channel
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
+    const int hw = wv / TW, tw = wv % TW;
+    const Work wk = decode_work<HW>(p, hw);
+    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
+    const int l = p.block;
+    const int smask = l / SB - 1;
+    const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);
+    const int64_t halo = wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
+
+    const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + half * D) * ES;
+    const char* xb = (const char*)p.x + xo;
+    const char* bb = (const char*)p.b + xo;
+    const char* cb = (const char*)p.c + xo;
+    const char* ab = (const char*)p.a + xo;
+    char* yb = (char*)p.y + xo;
+    const int64_t rs = p.sx_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const bool want_y = p.y != nullptr;
+    const int64_t dfull = (int64_t)D << p.hshift;   // channels of a real head: carrier row length
+    float* const vb = p.carriers ? p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D : nullptr;
+    const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
+
+    float e[CPL], s[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
+    const int64_t t_stop = ((wk.t_end + l - 1) >> p.lshift) << p.lshift;
+    const int64_t t_first = wk.t_begin - halo * STEP;
+    int buf = 0;
+    for (int64_t t0 = t_first; t0 < t_stop; t0 += STEP, buf ^= 1) {
+        const int64_t r0 = t0 + tw * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                     rc = rsrc(cb + r0 * rs), ra = rsrc(ab + r0 * rs);
+        RW xr[4], br[4], cr[4], ar[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t t = tr0 + r;
+            const uint32_t o = loff + (uint32_t)(r * rs);
+            const bool in_xb = t >= t_lo && t < wk.t_end;
+            xr[r].load(rx, in_range(in_xb, o));
+            br[r].load(rb, in_range(in_xb, o));
+            ar[r].load(ra, in_range(in_xb, o));
+            cr[r].load(rc, in_range(want_y && t >= wk.t_begin && t < wk.t_end, o));
+        }
+        float av[4][CPL], u[4][CPL], W[4][CPL], G[4][CPL];
+        decay_rows<IO, CPL>(ar, tr0, p.T, av);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * br[r].get(m);
+        chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
+
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_wl[buf][wv][n * CPL + m] = W[3][m];
+                s_cc[buf][wv][n * CPL + m] = G[3][m];
+            }
+        }
+        __syncthreads();
+
+        const int ph = (int)(t0 >> 4) & smask;
+        float ein[CPL], vout[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
+#pragma unroll 1
+        for (int r = 0; r < TW; ++r) {
+            if (((ph + r) & smask) == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+            }
+            if (r == tw) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) ein[m] = e[m];
+            }
+            const int src = hw * TW + r;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float c_ = s_cc[buf][src][n * CPL + m];
+                const float wl = s_wl[buf][src][n * CPL + m];
+                e[m] = c_ * e[m] + wl;
+                s[m] = c_ * s[m] + wl;
+            }
+            if (r == tw) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) vout[m] = s[m];
+            }
+        }
+        if (vb && ((ph + tw) & smask) == smask) {
+            const int64_t blk = r0 >> p.lshift;
+            const int64_t t_blk = blk << p.lshift;
+            store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
+                                               (uint32_t)(blk * dfull + n * CPL) * 4u), vout);
+        }
+        if (!want_y) continue;
+
+        const __amdgpu_buffer_rsrc_t ry = rsrc(yb + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t t = tr0 + r;
+            float yv[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                yv[m] = cr[r].get(m) * (W[r][m] + G[r][m] * ein[m]);
+                if (p.residual) yv[m] += xr[r].get(m);
+            }
+            store_row<IO, CPL>(ry, in_range(t >= wk.t_begin && t < wk.t_end, loff + (uint32_t)(r * rs)), yv);
+        }
+    }
+}
+
+// Per-channel backward: the reverse sweep of swr_bwd_kernel with per-channel
+// decay products.  The decay gradient keeps its closed form per channel,
+//     da_{k,mu} = H_{k-1,mu} du_{k,mu} - g_{k-1,mu} r_{k,mu} (e - s)_mu (eps - p)_mu,
+// and is stored per channel (no sum over the head's channels).
+template <class IO, int CPL, int TW, int HW>
+__global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
+    constexpr int NW = TW * HW;
+    constexpr int D = CPL * SB;
+    constexpr int STEP = TW * SB;      // whole blocks
+    constexpr int ES = IO::ES;
+    using R_ = Row<IO, CPL>;
+    __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve L u
+    __shared__ float s_df[2][NW][D];    // E_0 = a_0 D_0 of each sub-block's L^T dh
+    __shared__ float s_cc[2][NW][D];    // decay product of each sub-block, per channel
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
+    const int hw = wv / TW, tw = wv % TW;
+    const Work wk = decode_work<HW>(p, hw);
+    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
+    const int l = p.block;
+    const int smask = l / SB - 1;
+    const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);
+
+    const int64_t xe = wk.b * p.sx_b + head * p.sx_h + half * D;   // element offset
+    const int64_t xo = xe * ES;
+    const char* xb = (const char*)p.x + xo;
+    const char* bb = (const char*)p.b + xo;
+    const char* cb = (const char*)p.c + xo;
+    const char* dyb = (const char*)p.dy + xo;
+    const char* ab = (const char*)p.a + xo;
+    char* dxb = (char*)p.dx + xo;
+    char* dbb = (char*)p.db + xo;
+    char* dcb = (char*)p.dc + xo;
+    char* dab = (char*)(p.da + xe);
+    const int64_t dfull = (int64_t)D << p.hshift;
+    const float* vb = p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D;
+    const int64_t rs = p.sx_t * ES;
+    const int64_t das = p.sx_t * 4;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(n * CPL * 4);
+
+    float eps[CPL], pr[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; }
+    int buf = 0;
+
+    // ---- halo: the first block after the run -----------------------------------
+    if (wk.t_end < p.T) {
+        const int64_t r0 = wk.t_end + tw * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
+                                     ra = rsrc(ab + r0 * rs);
+        R_ cr[4], dyr[4], ar[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(tr0 + r < t_la, loff + (uint32_t)(r * rs));
+            cr[r].load(rc, o);
+            dyr[r].load(rdy, o);
+            ar[r].load(ra, o);
+        }
+        float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                av[r][m] = ar[r].get(m);
+                dh[r][m] = dyr[r].get(m) * cr[r].get(m);
+            }
+        chan_scan_rev<CPL>(av, dh, Dv, R, grp, lane);
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_df[buf][wv][n * CPL + m] = av[0][m] * Dv[0][m];
+                s_cc[buf][wv][n * CPL + m] = av[0][m] * R[0][m];   // a_0 ... a_15
+            }
+        }
+        __syncthreads();
+#pragma unroll 1
+        for (int r = TW - 1; r >= 0; --r) {
+            if ((r & smask) == smask) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
+            }
+            const int src = hw * TW + r;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float c_ = s_cc[buf][src][n * CPL + m];
+                const float df = s_df[buf][src][n * CPL + m];
+                eps[m] = c_ * eps[m] + df;
+                pr[m] = c_ * pr[m] + df;
+            }
+        }
+        buf ^= 1;
+    }
+
+    const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
+        const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
+        const int64_t r0 = t0 + tw * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+
+        R_ xr[4], br[4], dyr[4];
+        float av[4][CPL], dh[4][CPL];
+        {
+            R_ cr[4], ar[4];
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
+                                         rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
+                                         ra = rsrc(ab + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+                xr[r].load(rx, o);
+                br[r].load(rb, o);
+                cr[r].load(rc, o);
+                dyr[r].load(rdy, o);
+                ar[r].load(ra, o);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) {
+                    av[r][m] = ar[r].get(m);
+                    dh[r][m] = dyr[r].get(m) * cr[r].get(m);
+                }
+        }
+        float vprev[CPL];
+        {
+            Row<IoF32, CPL> vr;
+            const int64_t blk = (t0 >> p.lshift) - 1;
+            vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * dfull + n * CPL) * 4u));
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
+        }
+
+        // ---- local solves: W = L (b*x), G; Dv = L^T (c*dy), Rr -------------------------
+        float W[4][CPL], G[4][CPL], Dv[4][CPL], Rr[4][CPL];
+        {
+            float u[4][CPL];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * br[r].get(m);
+            chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
+        }
+        chan_scan_rev<CPL>(av, dh, Dv, Rr, grp, lane);
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_wl[buf][wv][n * CPL + m] = W[3][m];
+                s_cc[buf][wv][n * CPL + m] = G[3][m];
+            }
+        }
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_df[buf][wv][n * CPL + m] = av[0][m] * Dv[0][m];
+        }
+        __syncthreads();
+
+        // ---- forward carriers entering this wave's sub-block ---------------------------
+        float ein[CPL], sin_[CPL];
+        {
+            float e[CPL], s[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
+#pragma unroll 1
+            for (int r = 0; r < tw; ++r) {
+                if ((r & smask) == 0) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+                }
+                const int src = hw * TW + r;
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) {
+                    const float c_ = s_cc[buf][src][n * CPL + m];
+                    const float wl = s_wl[buf][src][n * CPL + m];
+                    e[m] = c_ * e[m] + wl;
+                    s[m] = c_ * s[m] + wl;
+                }
+            }
+            if ((tw & smask) == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+            }
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { ein[m] = e[m]; sin_[m] = s[m]; }
+        }
+
+        // ---- reverse carriers: capture at this sub-block, carry to the previous step ---
+        float epsin[CPL], kd[CPL];
+#pragma unroll 1
+        for (int r = TW - 1; r >= 0; --r) {
+            if ((r & smask) == smask) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
+            }
+            if (r == tw) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) {
+                    epsin[m] = eps[m];
+                    kd[m] = (ein[m] - sin_[m]) * (eps[m] - pr[m]);
+                }
+            }
+            const int src = hw * TW + r;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float c_ = s_cc[buf][src][n * CPL + m];
+                const float df = s_df[buf][src][n * CPL + m];
+                eps[m] = c_ * eps[m] + df;
+                pr[m] = c_ * pr[m] + df;
+            }
+        }
+
+        // ---- gradients -------------------------------------------------------------------
+        float Gsh[4][CPL], hup[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            const float gprev = shfl(G[3][m], (lane - 16) & 63);   // G_{4grp-1}; G_{-1} = 1
+            Gsh[0][m] = grp == 0 ? 1.0f : gprev;
+#pragma unroll
+            for (int r = 1; r < 4; ++r) Gsh[r][m] = G[r - 1][m];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) W[r][m] += G[r][m] * ein[m];   // H: the jagged-window state
+            const float hv = shfl(W[3][m], (lane - 16) & 63);
+            hup[m] = grp == 0 ? ein[m] : hv;
+        }
+        const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * rs),
+                                     rdc = rsrc(dcb + r0 * rs), rda = rsrc(dab + r0 * das);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t t = tr0 + r;
+            float vdx[CPL], vdb[CPL], vdc[CPL], vda[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float dyv = dyr[r].get(m);
+                vdc[m] = dyv * W[r][m];
+                const float du = Dv[r][m] + Rr[r][m] * epsin[m];
+                vdx[m] = br[r].get(m) * du;
+                if (p.residual) vdx[m] += dyv;
+                vdb[m] = xr[r].get(m) * du;
+                vda[m] = (r == 0 ? hup[m] : W[r - 1][m]) * du - Gsh[r][m] * Rr[r][m] * kd[m];
+            }
+            const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
+            store_row<IO, CPL>(rdx, o, vdx);
+            store_row<IO, CPL>(rdb, o, vdb);
+            store_row<IO, CPL>(rdc, o, vdc);
+            store_row<IoF32, CPL>(rda, in_range(t < wk.t_end, daoff + (uint32_t)(r * das)), vda);
+        }
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
+
+template <class IO, int CPL>
+static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
+    const dim3 grid((unsigned)p.nwork);
+    if (backward) {
+#define SWR_BWD(TW_, HW_)                                                                         \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
+        hipLaunchKernelGGL((swr_bwd_pc_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+                           stream, p);
+        if (false) {}
+        SWR_BWD(8, 1) SWR_BWD(4, 1)
+        else return hipErrorInvalidValue;
+#undef SWR_BWD
+    } else {
+#define SWR_FWD(TW_, HW_)                                                                         \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
+        hipLaunchKernelGGL((swr_fwd_pc_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+                           stream, p);
+        if (false) {}
+        SWR_FWD(4, 1) SWR_FWD(2, 2)
+        else return hipErrorInvalidValue;
+#undef SWR_FWD
+    }
+    return hipGetLastError();
+}
 
 template <class IO, int CPL>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
@@ -933,7 +1433,16 @@ static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, 
 }
 
 template <class IO>
-static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, hipStream_t stream) {
+static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
+                             hipStream_t stream) {
+    if (per_channel) {
+        switch (D) {   // channels of a virtual head (at most 64)
+            case 16: return launch_pc<IO, 1>(p, sh, backward, stream);
+            case 32: return launch_pc<IO, 2>(p, sh, backward, stream);
+            case 64: return launch_pc<IO, 4>(p, sh, backward, stream);
+            default: return hipErrorInvalidValue;
+        }
+    }
     switch (D) {
         case 16: return launch_shape<IO, 1>(p, sh, backward, stream);
         case 32: return launch_shape<IO, 2>(p, sh, backward, stream);
@@ -943,10 +1452,11 @@ static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backw
     }
 }
 
-hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, void* stream) {
+hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, bool per_channel,
+                  void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == 1) return launch_cpl<IoBf16>(p, D, sh, backward, st);
-    return launch_cpl<IoF32>(p, D, sh, backward, st);
+    if (dtype == 1) return launch_cpl<IoBf16>(p, D, sh, backward, per_channel, st);
+    return launch_cpl<IoF32>(p, D, sh, backward, per_channel, st);
 }
 
 }  // namespace swr

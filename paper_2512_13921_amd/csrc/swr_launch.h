@@ -23,11 +23,13 @@ struct Params {
     float* carriers;    // [B][H][nblocks][D] float32 block carriers v_t (forward: optional output;
                         // backward: input)
     int64_t B, T, H;
+    int64_t Hv;         // heads the work is split over: H, or H << hshift virtual heads
     int64_t sx_b, sx_t, sx_h;
     int64_t sa_b, sa_t, sa_h;
     int32_t block;      // l (16, 32, 64 or 128)
     int32_t lshift;     // log2(l)
     int32_t residual;   // 0 or 1
+    int32_t hshift;     // per-channel decay: log2 of the virtual heads per head (0 or 1)
     int64_t run_len;    // tokens per workgroup run, a multiple of the step and of l
     int64_t nruns;      // runs per (batch, head) sequence
     int64_t nwork;      // B * H * nruns workgroups
@@ -53,7 +55,13 @@ inline Shape fwd_shape(int64_t /*block*/, int64_t H) {
     return fwd_shape_single();
 }
 
-// Launches the forward or backward kernel for (dtype, D, shape) on `stream`.
-hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool backward, void* stream);
+// Per-channel decay: a head is processed as 2^hshift independent virtual
+// heads of at most 64 channels (nothing couples the channels there).
+inline int pc_hshift(int64_t D) { return D > 64 ? 1 : 0; }
+
+// Launches the forward or backward kernel for (dtype, D, shape) on `stream`;
+// for the per-channel kernels D is the channel count of a virtual head.
+hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool backward, bool per_channel,
+                  void* stream);
 
 }  // namespace swr

@@ -58,3 +58,40 @@ def assert_close(got, ref, dtype, what=""):
     else:
         assert st["max_e"] <= TOL_BF16_MAX and st["mean_e"] <= TOL_BF16_MEAN, f"{what}: {st}"
     return st
+
+
+def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd"):
+    """Forward (saving the block carriers) and backward through the library."""
+    import torch
+    cfg = prob.cfg
+    dt = cfg.dtype
+    x, b, c = (to_device(getattr(prob, n), dt) for n in ("x", "b", "c"))
+    a = to_device(prob.a, dt)            # [B, T, H], or [B, T, H, D] for a per-channel decay
+    dy = to_device(prob.dy, dt) if backward else None
+    if layout == "bhtd":   # store as [B, H, T, D] and hand the library a strided view
+        def bhtd(t):
+            if t.dim() == 4:
+                return t.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+            return t.permute(0, 2, 1).contiguous().permute(0, 2, 1)
+        x, b, c, a = (bhtd(t) for t in (x, b, c, a))
+        if dy is not None:
+            dy = bhtd(dy)
+    y, v = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len,
+                           save_carriers=True)
+    grads = swr.swr_backward(x, a, b, c, dy, v, cfg.block, residual=residual,
+                             run_len=run_len) if backward else None
+    torch.cuda.synchronize()
+    return y, grads
+
+
+def check_full(prob, y, grads, residual=False, what=""):
+    """Every output against the oracle on the same inputs; returns the error stats."""
+    import oracle
+    cfg = prob.cfg
+    ref_y = oracle.forward(prob.x, prob.a, prob.b, prob.c, cfg.block, residual)
+    stats = {"y": assert_close(to_host(y), ref_y, cfg.dtype, what + " y")}
+    if grads is not None:
+        ref = oracle.backward(prob.x, prob.a, prob.b, prob.c, prob.dy, cfg.block, residual)
+        for name, g, r in zip(("dx", "da", "db", "dc"), grads, ref):
+            stats[name] = assert_close(to_host(g), r, cfg.dtype, f"{what} {name}")
+    return stats

@@ -21,10 +21,10 @@ X, A, B_, C, Y, DY, DX, DA, DB, DC, V = (GB * (i + 1) for i in range(11))
 
 
 def problem(B=2, T=256, H=4, D=64, block=64, dtype=BF16, residual=False, run_len=0,
-            x_strides=None, a_strides=None):
+            x_strides=None, a_strides=None, per_channel=False):
     xs = x_strides or (T * H * D, H * D, D)
     as_ = a_strides or (T * H, H, 1)
-    return swr.make_problem(B, T, H, D, block, dtype, xs, as_, residual, run_len)
+    return swr.make_problem(B, T, H, D, block, dtype, xs, as_, residual, run_len, per_channel)
 
 
 def fwd(p, x=X, a=A, b=B_, c=C, y=Y, v_=0):
@@ -95,9 +95,10 @@ def test_shape_validation(kw, code):
 
 
 def test_unknown_flags_and_reserved():
-    p = problem()
-    p.flags = 2
-    assert fwd(p) == E_UNSUP
+    for bit in (4, 8, 1 << 31):
+        p = problem()
+        p.flags = bit
+        assert fwd(p) == E_UNSUP and bwd(p) == E_UNSUP and car(p) == E_UNSUP
     p = problem()
     p.reserved = 1
     assert bwd(p) == E_UNSUP
@@ -160,6 +161,39 @@ def test_aliasing():
     assert bwd(problem(), dx=V) == E_ALIAS              # carriers read by the backward
     # (inputs may alias each other: exercised with real tensors in the GPU tests,
     # since a call that passes validation launches a kernel)
+
+
+def test_per_channel_validation():
+    # a and da take the [B, T, H, D] layout of x; every call below fails before any launch
+    pc = dict(per_channel=True)
+    assert fwd(problem(D=48, **pc)) == E_UNSUP and bwd(problem(block=48, **pc)) == E_BLOCK
+    assert fwd(problem(**pc), a=A + 2) == E_ALIGN          # a needs x's 8-byte lane vectors
+    assert fwd(problem(dtype=F32, **pc), a=A + 8) == E_ALIGN
+    assert bwd(problem(**pc), da=DA + 8) == E_ALIGN        # 4 fp32 channels per lane: 16 bytes
+    assert bwd(problem(D=32, **pc), da=DA + 4) == E_ALIGN  # 2 fp32 channels per lane: 8 bytes
+    # D = 128 runs as two 64-channel halves: x needs only the 8-byte (bf16) lane vectors
+    assert fwd(problem(D=128, **pc), x=X + 4) == E_ALIGN
+    assert fwd(problem(D=128, **pc), y=Y + 8, x=X + 4) == E_ALIGN
+    # a's span is x's span: an output inside it aliases
+    span_x = 2 * 256 * 4 * 64 * 2
+    assert fwd(problem(**pc), y=A + span_x - 64) == E_ALIAS
+    assert bwd(problem(**pc), dx=A + span_x - 64) == E_ALIAS
+    assert bwd(problem(**pc), da=X + span_x - 64) == E_ALIAS
+    # sa_* are ignored with per-channel decay: even overlapping ones are accepted
+    # (checked through launch_info, which never launches)
+    p = problem(a_strides=(1, 1, 1), **pc)
+    assert swr.swr_launch_info(p)["fwd_workgroups"] > 0
+    p = problem(a_strides=(1, 1, 1))
+    assert swr.load().swr_launch_info(ctypes.byref(p), None, None, None, None) == E_SHAPE
+
+
+def test_per_channel_launch_shape():
+    # B=8, T=16384, H=16, D=128 with per-channel decay: 32 virtual heads of 64 channels
+    p = problem(B=8, T=16384, H=16, D=128, block=128, per_channel=True)
+    info = swr.swr_launch_info(p)
+    assert info["fwd_workgroups"] == 8 * 16 * (-(-16384 // info["fwd_run_len"]))
+    assert info["bwd_workgroups"] == 8 * 32 * (-(-16384 // info["bwd_run_len"]))
+    assert swr.swr_carrier_elems(p) == 8 * 16 * 128 * 128
 
 
 def test_carrier_elems():

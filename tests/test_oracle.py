@@ -256,3 +256,22 @@ def test_rejects_bad_arguments():
 def test_empty_sequence():
     x = np.zeros((2, 0, 3))
     assert oracle.forward_slices(x, np.zeros((2, 0)), x, x, block=4).shape == (2, 0, 3)
+
+
+@pytest.mark.parametrize("T,D,block", [(37, 3, 8), (100, 5, 16), (64, 2, 64)])
+def test_channel_constant_per_channel_decay_is_shared_decay(rng, T, D, block):
+    # The per-channel recurrence with the same decay on every channel is the
+    # shared-decay recurrence (eq. (2.1) with a scalar transition): identical
+    # outputs and input gradients, and the shared decay's gradient is the sum
+    # over channels of the per-channel one (chain rule through the broadcast).
+    x, a, b, c = _inputs(rng, T, D)
+    dy = rng.standard_normal((T, D))
+    ab = np.repeat(a[:, None], D, axis=1)
+    y1 = oracle.forward_slices(x[None], a[None], b[None], c[None], block)
+    y2 = oracle.forward_slices(x[None], ab[None], b[None], c[None], block)
+    np.testing.assert_allclose(y2, y1, rtol=1e-13, atol=1e-13)
+    g1 = oracle.backward_slices(x[None], a[None], b[None], c[None], dy[None], block)
+    g2 = oracle.backward_slices(x[None], ab[None], b[None], c[None], dy[None], block)
+    for i in (0, 2, 3):
+        np.testing.assert_allclose(g2[i], g1[i], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(g2[1].sum(axis=-1), g1[1], rtol=1e-12, atol=1e-12)

@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 import workloads as W
-from parity import assert_close, to_device, to_host
+from parity import assert_close, check_full, run_gpu, to_device, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -30,36 +30,6 @@ def swr():
     import paper_2512_13921_amd as lib
     lib.load()
     return lib
-
-
-def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd"):
-    cfg = prob.cfg
-    dt = cfg.dtype
-    x, b, c = (to_device(getattr(prob, n), dt) for n in ("x", "b", "c"))
-    a = to_device(prob.a, dt)
-    dy = to_device(prob.dy, dt) if backward else None
-    if layout == "bhtd":   # store as [B, H, T, D] and hand the library a strided view
-        x, b, c = (t.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3) for t in (x, b, c))
-        a = a.permute(0, 2, 1).contiguous().permute(0, 2, 1)
-        if dy is not None:
-            dy = dy.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
-    y, v = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len,
-                           save_carriers=True)
-    grads = swr.swr_backward(x, a, b, c, dy, v, cfg.block, residual=residual,
-                             run_len=run_len) if backward else None
-    torch.cuda.synchronize()
-    return y, grads
-
-
-def check_full(prob, y, grads, residual=False, what=""):
-    cfg = prob.cfg
-    ref_y = oracle.forward(prob.x, prob.a, prob.b, prob.c, cfg.block, residual)
-    stats = {"y": assert_close(to_host(y), ref_y, cfg.dtype, what + " y")}
-    if grads is not None:
-        ref = oracle.backward(prob.x, prob.a, prob.b, prob.c, prob.dy, cfg.block, residual)
-        for name, g, r in zip(("dx", "da", "db", "dc"), grads, ref):
-            stats[name] = assert_close(to_host(g), r, cfg.dtype, f"{what} {name}")
-    return stats
 
 
 # ----------------------------------------------------------------------------- small shapes

@@ -16,7 +16,9 @@ with the configuration's seed, in this fixed order):
 * ``a`` (shape ``[B, T, H]``: one decay per token and head, shared by the
   head's channels as in the paper's Phalanx layer, Sec. 5):
   ``sigmoid(N(mu, 1))`` or ``exp(-softplus(N(0, 1)) * Delta)`` with ``Delta``
-  uniform in ``[1e-3, 1e-1]``, drawn per (b, t, h).
+  uniform in ``[1e-3, 1e-1]``, drawn per (b, t, h).  Per-channel-decay
+  workloads draw ``a`` with the same recipe per (b, t, h, channel), shape
+  ``[B, T, H, D]``.
 * Every tensor is then rounded to the I/O dtype with round-to-nearest-even;
   the GPU library and the oracle both consume exactly these rounded values.
 """
@@ -85,6 +87,7 @@ class Config:
     seed: int = 0
     backward: bool = True
     width: Optional[int] = None   # model width of the projected-x recipe
+    per_channel: bool = False     # one decay per token, head and channel ([B, T, H, D])
 
     @property
     def tokens(self) -> int:
@@ -108,6 +111,14 @@ CONFIGS: Dict[int, Config] = {
 }
 
 HEADLINE = 3
+
+# The same shapes with one decay per token, head and channel (the diagonal
+# transition with a full diagonal): the tiny workload read with its decay
+# "per-token per-channel", and the headline shape.
+PER_CHANNEL: Dict[int, Config] = {
+    1: CONFIGS[1].with_(name=CONFIGS[1].name + "_perchannel", per_channel=True),
+    3: CONFIGS[3].with_(name=CONFIGS[3].name + "_perchannel", per_channel=True),
+}
 
 
 @dataclass
@@ -170,13 +181,15 @@ def generate(cfg: Config, with_dy: Optional[bool] = None) -> Problem:
     b = round_to(rng.standard_normal(shape, dtype=np.float32), cfg.dtype)
     c = round_to(rng.standard_normal(shape, dtype=np.float32), cfg.dtype)
     dy = round_to(rng.standard_normal(shape, dtype=np.float32), cfg.dtype) if with_dy else None
-    a = round_to(draw_decay(rng, shape[:3], cfg.a_kind, cfg.a_mu), cfg.dtype)
+    a_shape = shape if cfg.per_channel else shape[:3]
+    a = round_to(draw_decay(rng, a_shape, cfg.a_kind, cfg.a_mu), cfg.dtype)
     return Problem(cfg, x, a, b, c, dy)
 
 
 def random_problem(seed: int, B: int, T: int, H: int, D: int, block: int, dtype: str = "bf16",
-                   a_kind: str = "sigmoid", a_mu: float = 2.0, with_dy: bool = True) -> Problem:
+                   a_kind: str = "sigmoid", a_mu: float = 2.0, with_dy: bool = True,
+                   per_channel: bool = False) -> Problem:
     """A small ad-hoc workload with the same recipe (used by parity tests)."""
     cfg = Config(0, f"adhoc_B{B}_T{T}_H{H}_d{D}_l{block}_{dtype}", B, T, H, D, block, dtype,
-                 a_kind, a_mu, seed=seed, backward=with_dy)
+                 a_kind, a_mu, seed=seed, backward=with_dy, per_channel=per_channel)
     return generate(cfg, with_dy=with_dy)
