@@ -4,7 +4,10 @@
 One step = one forward (swr_forward) and one backward (swr_backward) pass over
 the whole workload, inputs already resident in HBM.  Prints ONE JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--decay head|channel]
+
+--decay channel times the per-channel-decay path (a and da of shape
+[B, T, H, D]) on the same workload shape instead of the shared decay.
 
 Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
 durations come from HIP events recorded on the stream the kernels run on.
@@ -46,15 +49,19 @@ def algorithmic_bytes(cfg, backward):
     e = 2 if cfg.dtype == "bf16" else 4
     th = cfg.B * cfg.T * cfg.H
     carriers = th * 4 * cfg.D // cfg.block
+    na = cfg.D if cfg.per_channel else 1     # decays per token-head
     if backward:   # x, b, c, dy, a, carriers in; dx, db, dc out; da out in fp32
-        return th * (e * (7 * cfg.D + 1) + 4) + carriers
-    return th * e * (4 * cfg.D + 1) + carriers   # x, b, c, a in; y, carriers out
+        return th * (e * (7 * cfg.D + na) + 4 * na) + carriers
+    return th * e * (4 * cfg.D + na) + carriers   # x, b, c, a in; y, carriers out
 
 
 def contraction_flops(cfg, backward):
     """Dense flops of the intra-block contractions (16x16 sub-block tiles):
     2 * 16 * D per token-head per contraction; the backward runs three
-    (forward recompute, reverse solve, look-ahead reverse solve)."""
+    (forward recompute, reverse solve, look-ahead reverse solve).  None for a
+    per-channel decay, whose local solves are scans on the vector ALUs."""
+    if cfg.per_channel:
+        return None
     per = 2 * 16 * cfg.D * cfg.B * cfg.T * cfg.H
     return per * (3 if backward else 1)
 
@@ -140,6 +147,8 @@ def main():
     ap.add_argument("--config", type=int, default=W.HEADLINE, choices=sorted(W.CONFIGS))
     ap.add_argument("--run-len", type=int, default=0, help="tokens per workgroup run (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decay", choices=("head", "channel"), default="head",
+                    help="one decay per token and head (default) or per token, head and channel")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -156,6 +165,8 @@ def main():
     swr.load()
 
     cfg = W.CONFIGS[args.config]
+    if args.decay == "channel":
+        cfg = W.PER_CHANNEL.get(args.config) or cfg.with_(name=cfg.name + "_perchannel", per_channel=True)
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -163,7 +174,7 @@ def main():
     x, a, b, c, dy = (to_device(getattr(prob, n), cfg.dtype) for n in ("x", "a", "b", "c", "dy"))
     y = torch.empty_like(x)
     dx, db, dc = (torch.empty_like(x) for _ in range(3))
-    da = torch.empty(a.shape, dtype=torch.float32, device=a.device)
+    da = torch.empty(a.shape, dtype=torch.float32, device=a.device)   # a's shape, contiguous
     carriers = torch.empty(swr.carrier_shape(x, cfg.block), dtype=torch.float32, device=x.device)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -204,13 +215,18 @@ def main():
     f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
     dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
     dom_gbs = b_gbs if dominant_bwd else f_gbs
-    dom_kernel = "swr_bwd_kernel" if dominant_bwd else "swr_fwd_kernel"
+    pc = "_pc" if cfg.per_channel else ""
+    dom_kernel = f"swr_bwd{pc}_kernel" if dominant_bwd else f"swr_fwd{pc}_kernel"
     traffic = recorded_traffic(dom_kernel, cfg.name)
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
 
+    def mfma_rate(backward, ms):
+        f = contraction_flops(cfg, backward)
+        return None if f is None else f / (ms * 1e-3) / 1e12
+
     launch = swr.swr_launch_info(swr.make_problem(
         cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
-        x.stride()[:3], a.stride(), False, args.run_len))
+        x.stride()[:3], a.stride()[:3], False, args.run_len, cfg.per_channel))
 
     # Reference: a plain device-to-device copy of one [B,T,H,D] tensor (read + write).
     cbuf = torch.empty_like(x)
@@ -239,7 +255,8 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic (seeded host draws, rounded to the I/O dtype)",
         "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
-                   "block": cfg.block, "global_batch": cfg.B, "seq_len": cfg.T,
+                   "block": cfg.block, "decay": "per channel" if cfg.per_channel else "per head",
+                   "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {
             "bound": "hbm",
@@ -256,11 +273,11 @@ def main():
         "kernels": {
             "forward": {"ms": float(fwd_ms.mean()), "ms_min": float(fwd_ms.min()),
                         "algorithmic_bytes": fb, "GB/s": f_gbs, "frac_hbm": f_gbs / HBM_PEAK_GBS,
-                        "mfma_tflops": contraction_flops(cfg, False) / (fwd_ms.mean() * 1e-3) / 1e12,
+                        "mfma_tflops": mfma_rate(False, fwd_ms.mean()),
                         "tokens_per_s": tokens / (fwd_ms.mean() * 1e-3)},
             "backward": {"ms": float(bwd_ms.mean()), "ms_min": float(bwd_ms.min()),
                          "algorithmic_bytes": bb, "GB/s": b_gbs, "frac_hbm": b_gbs / HBM_PEAK_GBS,
-                         "mfma_tflops": contraction_flops(cfg, True) / (bwd_ms.mean() * 1e-3) / 1e12,
+                         "mfma_tflops": mfma_rate(True, bwd_ms.mean()),
                          "tokens_per_s": tokens / (bwd_ms.mean() * 1e-3)},
             "mfma_peak_tflops": mfma_peak,
             "copy_GB/s": copy_gbs,
