@@ -95,6 +95,16 @@ typedef enum swr_dtype {
  * than a matrix product (the operator L_t differs from channel to channel). */
 #define SWR_FLAG_PER_CHANNEL_DECAY 2u
 
+/* Fused featurisation (Phalanx layer, Sec. 5, "Featurization": the decay and
+ * the key-like pre-gate are sigmoids of linear projections).  With
+ * SWR_FLAG_SIGMOID_DECAY, `a` holds logits z_a and the decay is sigmoid(z_a);
+ * with SWR_FLAG_SIGMOID_PREGATE, `b` holds logits z_b and the pre-gate is
+ * sigmoid(z_b).  The sigmoid is evaluated in float32 from the stored logits.
+ * swr_backward then returns da = dL/dz_a and db = dL/dz_b (the gradients
+ * with respect to the stored logits).  Either flag combines with the others. */
+#define SWR_FLAG_SIGMOID_DECAY 4u
+#define SWR_FLAG_SIGMOID_PREGATE 8u
+
 typedef struct swr_problem {
     int32_t abi_version;   /* must be SWR_ABI_VERSION                                     */
     int32_t dtype;         /* swr_dtype_t of every tensor except da                       */

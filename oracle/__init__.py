@@ -5,8 +5,13 @@ library is compared against.  Only ``tests/``, ``__graft_entry__.smoke()`` and
 the CPU-baseline leg of ``bench.py`` may import it.  It shares no code with the
 HIP library (``paper_2512_13921_amd``) and never imports it.
 
-The arithmetic lives in ``swr_oracle.c`` (see its header for the definition and
-the paper passages it follows); this module only marshals numpy arrays.
+The recurrence's arithmetic lives in ``swr_oracle.c`` (see its header for the
+definition and the paper passages it follows); this module marshals numpy
+arrays, and composes the Phalanx featurisation (Sec. 5, "Featurization": the
+decay and the key-like pre-gate are sigmoids of projections) around it in
+float64 when asked to: the forward evaluates the sigmoid of the given logits
+and runs the recurrence on the results; the backward multiplies the
+recurrence's da and db by the sigmoid's derivative (chain rule).
 
 Tensor layout at this level is the library's: ``x, b, c, y, dy, ...`` are
 ``[B, T, H, D]``; ``a`` is ``[B, T, H]`` (decay shared by a head's D channels,
@@ -102,17 +107,42 @@ def _from_slices(t, B, H):
     return np.moveaxis(t.reshape((B, H, T) + t.shape[2:]), 1, 2)
 
 
-def forward(x, a, b, c, block, residual=False):
-    """y = SWR(x, a, b, c) for [B, T, H, D] tensors (a: [B, T, H] or [B, T, H, D])."""
+def sigmoid(z):
+    """Logistic sigmoid 1 / (1 + exp(-z)) in float64, as exp(-log(1 + exp(-z)))
+    so that no intermediate overflows."""
+    z = np.asarray(z, np.float64)
+    return np.exp(-np.logaddexp(0.0, -z))
+
+
+def dsigmoid(z):
+    """Derivative of the sigmoid: sigmoid(z) * (1 - sigmoid(z)) = sigmoid(z) sigmoid(-z)."""
+    return sigmoid(z) * sigmoid(-np.asarray(z, np.float64))
+
+
+def forward(x, a, b, c, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """y = SWR(x, a, b, c) for [B, T, H, D] tensors (a: [B, T, H] or [B, T, H, D]).
+    With sigmoid_decay / sigmoid_pregate, a / b are logits and the recurrence
+    uses their sigmoids."""
     B, T, H, D = np.shape(x)
+    a = sigmoid(a) if sigmoid_decay else a
+    b = sigmoid(b) if sigmoid_pregate else b
     y = forward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c),
                        block, residual)
     return _from_slices(y, B, H)
 
 
-def backward(x, a, b, c, dy, block, residual=False):
-    """(dx, da, db, dc) for [B, T, H, D] tensors; da has the shape of a."""
+def backward(x, a, b, c, dy, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """(dx, da, db, dc) for [B, T, H, D] tensors; da has the shape of a.  With
+    sigmoid_decay / sigmoid_pregate, da / db are the gradients with respect to
+    the logits."""
     B, T, H, D = np.shape(x)
-    outs = backward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c),
+    av = sigmoid(a) if sigmoid_decay else a
+    bv = sigmoid(b) if sigmoid_pregate else b
+    outs = backward_slices(_to_slices(x), _to_slices(av), _to_slices(bv), _to_slices(c),
                            _to_slices(dy), block, residual)
-    return tuple(_from_slices(o, B, H) for o in outs)
+    dx, da, db, dc = (_from_slices(o, B, H) for o in outs)
+    if sigmoid_decay:
+        da = da * dsigmoid(a)
+    if sigmoid_pregate:
+        db = db * dsigmoid(b)
+    return dx, da, db, dc

@@ -10,7 +10,9 @@ Layouts: ``x, b, c, y, dy, dx, db, dc`` are ``[B, T, H, D]`` (channels
 contiguous, all with the same strides); ``a`` is ``[B, T, H]`` in the same
 dtype (one decay per head), or ``[B, T, H, D]`` with x's strides (one decay
 per channel, ``SWR_FLAG_PER_CHANNEL_DECAY``); ``da`` is float32 with ``a``'s
-shape.  Supported dtypes: float32 and
+shape.  ``sigmoid_decay`` / ``sigmoid_pregate`` make ``a`` / ``b`` logits whose
+sigmoids the kernels use (the Phalanx featurisation); the backward then
+returns gradients with respect to those logits.  Supported dtypes: float32 and
 bfloat16.  The block carriers that the forward saves for the backward are a
 float32 ``[B, H, ceil(T / block), D]`` tensor (``carrier_shape``).
 """
@@ -28,6 +30,8 @@ SWR_DTYPE_F32 = 0
 SWR_DTYPE_BF16 = 1
 SWR_FLAG_RESIDUAL = 1
 SWR_FLAG_PER_CHANNEL_DECAY = 2
+SWR_FLAG_SIGMOID_DECAY = 4
+SWR_FLAG_SIGMOID_PREGATE = 8
 
 
 class SwrProblem(ctypes.Structure):
@@ -95,14 +99,16 @@ def swr_abi_version() -> int:
 
 
 def make_problem(B, T, H, D, block, dtype_code, x_strides, a_strides, residual=False, run_len=0,
-                 per_channel=False):
+                 per_channel=False, sigmoid_decay=False, sigmoid_pregate=False):
     """A ``swr_problem_t`` from plain integers (strides in elements, [B, T, H] order)."""
     p = SwrProblem()
     p.abi_version = SWR_ABI_VERSION
     p.dtype = dtype_code
     p.B, p.T, p.H, p.D = int(B), int(T), int(H), int(D)
     p.block = int(block)
-    p.flags = (SWR_FLAG_RESIDUAL if residual else 0) | (SWR_FLAG_PER_CHANNEL_DECAY if per_channel else 0)
+    p.flags = ((SWR_FLAG_RESIDUAL if residual else 0) | (SWR_FLAG_PER_CHANNEL_DECAY if per_channel else 0)
+               | (SWR_FLAG_SIGMOID_DECAY if sigmoid_decay else 0)
+               | (SWR_FLAG_SIGMOID_PREGATE if sigmoid_pregate else 0))
     p.reserved = 0
     p.sx_b, p.sx_t, p.sx_h = (int(s) for s in x_strides)
     p.sa_b, p.sa_t, p.sa_h = (int(s) for s in a_strides)
@@ -151,7 +157,7 @@ def _dtype_code(t):
     raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
 
 
-def _problem_from(x, a, block, residual, run_len):
+def _problem_from(x, a, block, residual, run_len, sigmoid_decay=False, sigmoid_pregate=False):
     if x.dim() != 4:
         raise ValueError("x must be [B, T, H, D]")
     per_channel = a.dim() == 4
@@ -167,7 +173,7 @@ def _problem_from(x, a, block, residual, run_len):
     B, T, H, D = x.shape
     return make_problem(B, T, H, D, block, _dtype_code(x), x.stride()[:3],
                         x.stride()[:3] if per_channel else a.stride(), residual, run_len,
-                        per_channel)
+                        per_channel, sigmoid_decay, sigmoid_pregate)
 
 
 def _same_layout(ref, *others):
@@ -200,13 +206,13 @@ def _carrier_tensor(x, block, carriers):
 
 
 def swr_forward(x, a, b, c, block, residual=False, y=None, carriers=None, save_carriers=False,
-                run_len=0, stream=None):
+                run_len=0, stream=None, sigmoid_decay=False, sigmoid_pregate=False):
     """y = SWR(x, a, b, c) on the GPU (see ``include/swr.h``).
 
     Returns y, or (y, carriers) when ``save_carriers`` is true or a carrier
     tensor is passed in (it is filled)."""
     torch = _torch()
-    problem = _problem_from(x, a, block, residual, run_len)
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
     _same_layout(x, b, c)
     if y is None:
         y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
@@ -221,9 +227,10 @@ def swr_forward(x, a, b, c, block, residual=False, y=None, carriers=None, save_c
     return (y, v) if want_v else y
 
 
-def swr_carriers(x, a, b, block, carriers=None, run_len=0, stream=None):
+def swr_carriers(x, a, b, block, carriers=None, run_len=0, stream=None, sigmoid_decay=False,
+                 sigmoid_pregate=False):
     """The block carriers swr_forward would save, computed from x, a, b alone."""
-    problem = _problem_from(x, a, block, False, run_len)
+    problem = _problem_from(x, a, block, False, run_len, sigmoid_decay, sigmoid_pregate)
     _same_layout(x, b)
     v = _carrier_tensor(x, block, carriers)
     rc = load().swr_carriers(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(v),
@@ -234,11 +241,11 @@ def swr_carriers(x, a, b, block, carriers=None, run_len=0, stream=None):
 
 
 def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, run_len=0,
-                 stream=None):
+                 stream=None, sigmoid_decay=False, sigmoid_pregate=False):
     """(dx, da, db, dc) of the SWR forward given dy and the forward's block
     carriers (see ``include/swr.h``)."""
     torch = _torch()
-    problem = _problem_from(x, a, block, residual, run_len)
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
     _same_layout(x, b, c, dy)
     if carriers is None:
         raise ValueError("swr_backward needs the forward's block carriers: "
@@ -269,9 +276,10 @@ def _autograd_function():
         the backward recomputes what it needs from the saved inputs."""
 
         @staticmethod
-        def forward(ctx, x, a, b, c, block, residual=False):
+        def forward(ctx, x, a, b, c, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
             ctx.block, ctx.residual = block, residual
-            y, v = swr_forward(x, a, b, c, block, residual, save_carriers=True)
+            ctx.feat = dict(sigmoid_decay=sigmoid_decay, sigmoid_pregate=sigmoid_pregate)
+            y, v = swr_forward(x, a, b, c, block, residual, save_carriers=True, **ctx.feat)
             ctx.save_for_backward(x, a, b, c, v)     # the carriers are the only extra state
             return y
 
@@ -280,8 +288,8 @@ def _autograd_function():
             x, a, b, c, v = ctx.saved_tensors
             dy = dy if dy.stride() == x.stride() else torch.empty_strided(
                 x.shape, x.stride(), dtype=x.dtype, device=x.device).copy_(dy)
-            dx, da, db, dc = swr_backward(x, a, b, c, dy, v, ctx.block, ctx.residual)
-            return dx, da.to(a.dtype), db, dc, None, None
+            dx, da, db, dc = swr_backward(x, a, b, c, dy, v, ctx.block, ctx.residual, **ctx.feat)
+            return dx, da.to(a.dtype), db, dc, None, None, None, None
 
     return _SWRFunction
 

@@ -87,7 +87,9 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     if (p->B < 0 || p->T < 0 || p->H < 0 || p->D < 1) return SWR_ERR_SHAPE;
     if (p->block != 16 && p->block != 32 && p->block != 64 && p->block != 128) return SWR_ERR_BLOCK;
     if (p->D != 16 && p->D != 32 && p->D != 64 && p->D != 128) return SWR_ERR_UNSUPPORTED;
-    if ((p->flags & ~(SWR_FLAG_RESIDUAL | SWR_FLAG_PER_CHANNEL_DECAY)) != 0 || p->reserved != 0)
+    const uint32_t known = SWR_FLAG_RESIDUAL | SWR_FLAG_PER_CHANNEL_DECAY | SWR_FLAG_SIGMOID_DECAY |
+                           SWR_FLAG_SIGMOID_PREGATE;
+    if ((p->flags & ~known) != 0 || p->reserved != 0)
         return SWR_ERR_UNSUPPORTED;
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
@@ -187,6 +189,8 @@ swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward
     k.block = (int32_t)p->block;
     k.lshift = p->block == 16 ? 4 : p->block == 32 ? 5 : p->block == 64 ? 6 : 7;
     k.residual = (p->flags & SWR_FLAG_RESIDUAL) ? 1 : 0;
+    k.sig_a = (p->flags & SWR_FLAG_SIGMOID_DECAY) ? 1 : 0;
+    k.sig_b = (p->flags & SWR_FLAG_SIGMOID_PREGATE) ? 1 : 0;
     k.run_len = backward ? r.run_len : r.run_len_f;
     k.nruns = backward ? r.nruns : r.nruns_f;
     k.nwork = backward ? r.nwork : r.nwork_f;

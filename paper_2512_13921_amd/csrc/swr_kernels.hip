@@ -212,6 +212,28 @@ __device__ inline float load_scalar(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 
 
 // ---------------------------------------------------------------------------
+// Featurisation (Phalanx, Sec. 5: sigmoid-bounded decay and key-like pre-gate)
+// ---------------------------------------------------------------------------
+
+// Logistic sigmoid 1 / (1 + e^-z); e^-z overflows to +inf for very negative
+// z, whose reciprocal is the correct limit 0, so the result is finite for
+// every finite z.
+__device__ inline float sigmoid(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+
+// d sigmoid / dz = sigmoid(z) sigmoid(-z), without the cancellation of 1 - sigmoid(z).
+__device__ inline float dsigmoid(float z) { return sigmoid(z) * sigmoid(-z); }
+
+// The pre-gate value b of a loaded element (a logit when sig is set).
+__device__ inline float pregate(float z, int sig) { return sig ? sigmoid(z) : z; }
+
+// The same value, opaque to the compiler: a function of it computed again is
+// recomputed rather than kept alive in registers since its first use.
+__device__ inline float fresh(float v) {
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// ---------------------------------------------------------------------------
 // Cross-lane helpers (a DPP "row" is 16 lanes on CDNA)
 // ---------------------------------------------------------------------------
 
@@ -417,8 +439,9 @@ __device__ inline Lanes lanes() {
 // i.e. longer contiguous stretches of the [B, T, H, D] tensors, together.
 // At least three waves per SIMD, so that the memory and compute phases of
 // several workgroups interleave on a compute unit.
-template <class IO, int CPL, int TW, int HW>
+template <class IO, int CPL, int TW, int HW, bool FEAT>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
     constexpr int STEP = TW * SB;
@@ -517,10 +540,12 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             }
         }
         const int64_t ta = r0 + n;
+        const bool a_ok = ta >= t_lo && ta < wk.t_end;
+        float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(a_ok, aoff));
+        if (sig_a) a_n = a_ok ? sigmoid(a_n) : 0.0f;
         // Past the end of the sequence the decay is 1 (and u = 0), so the
         // carrier of a partial last block is the state at its last token.
-        const float a_n = ta >= p.T ? 1.0f
-                          : load_scalar<IO>(rsrc(ab + r0 * as), in_range(ta >= t_lo && ta < wk.t_end, aoff));
+        if (ta >= p.T) a_n = 1.0f;
 
         // ---- local solve W = L U on the matrix cores ---------------------
         const Decay dk = build_decay(a_n, grp, n);
@@ -530,7 +555,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
         for (int m = 0; m < CPL; ++m) {
             float u[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * br[q].get(m);   // pre-gate b*x
+            for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);   // pre-gate b*x
             W[m] = Contract<IO>::run(A, u);
         }
 
@@ -633,8 +658,9 @@ __device__ inline void build_decay_transposed(float a_n, int grp, int n, float (
 // saved by the forward pass (the paper's "checkpoint only the carrier").
 // Only the run's end needs a halo: the first block after the run (c, dy, a)
 // gives the reverse carrier entering it.  Nothing is read twice.
-template <class IO, int CPL, int TW, int HW>
+template <class IO, int CPL, int TW, int HW, bool FEAT>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
     constexpr int STEP = TW * SB;      // whole blocks
@@ -693,7 +719,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             cr[r].load(rc, o);
             dyr[r].load(rdy, o);
         }
-        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < t_la, aoff));
+        float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < t_la, aoff));
+        if (sig_a) a_n = r0 + n < t_la ? sigmoid(a_n) : 0.0f;
         float LT[4];
         build_decay_transposed(a_n, grp, n, LT);
         const typename Contract<IO>::A At = Contract<IO>::prep(LT);
@@ -756,7 +783,12 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);   // dh = dy * c
         }
-        const float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+        float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+        float ds_n = 1.0f;      // d a / d(input) of token n: 1, or sigma'(z) for a logit z
+        if (sig_a) {
+            ds_n = dsigmoid(a_n);
+            a_n = r0 + n < wk.t_end ? sigmoid(a_n) : 0.0f;
+        }
         // Carrier of the block before this step (zero before the sequence start).
         float vprev[CPL];
         {
@@ -780,7 +812,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 float u[4], d4[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    u[q] = xr[q].get(m) * br[q].get(m);
+                    u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
                     d4[q] = dh[q][m];
                 }
                 W[m] = Contract<IO>::run(A, u);
@@ -885,16 +917,18 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 const float dyv = dyr[r].get(m);
                 vdc[m] = dyv * W[m][r];
                 const float du = Dl[m][r] + Rr[r] * epsin[m];          // adjoint of u
-                vdx[m] = br[r].get(m) * du;
+                const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
+                vdx[m] = pregate(zb, sig_b) * du;
                 if (p.residual) vdx[m] += dyv;
                 vdb[m] = xr[r].get(m) * du;
+                if (sig_b) vdb[m] *= dsigmoid(zb);
                 acc += (r == 0 ? hup[m] : W[m][r - 1]) * du;
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL>(rdx, o, vdx);
             store_row<IO, CPL>(rdb, o, vdb);
             store_row<IO, CPL>(rdc, o, vdc);
-            const float tot = row_sum(acc);
+            const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
             __builtin_amdgcn_raw_buffer_store_b32(
                 __builtin_bit_cast(int, tot), rda,
                 (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, 0);
@@ -990,21 +1024,29 @@ __device__ inline void chan_scan_rev(const float (&a)[4][CPL], const float (&dh)
     }
 }
 
-// The decays of one row slice as floats; past the end of the sequence the
-// decay is 1 (and the input 0), so a partial last block's carrier is the
-// state at its last token.
+// The decays of one row slice as floats: the loaded values (through the
+// sigmoid when they are logits) for tokens in [t_lo, t_hi), 0 before or after
+// that range, and 1 past the end of the sequence, so that a partial last
+// block's carrier is the state at its last token.
 template <class IO, int CPL>
-__device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int64_t T, float (&av)[4][CPL]) {
+__device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int64_t t_lo, int64_t t_hi,
+                                  int64_t T, int sig, float (&av)[4][CPL]) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < 4; ++r) {
+        const int64_t t = tr0 + r;
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) av[r][m] = tr0 + r >= T ? 1.0f : ar[r].get(m);
+        for (int m = 0; m < CPL; ++m) {
+            const float z = ar[r].get(m);
+            av[r][m] = t >= T ? 1.0f : (t >= t_lo && t < t_hi) ? (sig ? sigmoid(z) : z) : 0.0f;
+        }
+    }
 }
 
 // Per-channel forward.  Same workgroup shape and sweep as swr_fwd_kernel;
 // wk.h is a virtual head: head wk.h >> hshift, channel half wk.h & (2^hshift - 1).
-template <class IO, int CPL, int TW, int HW>
+template <class IO, int CPL, int TW, int HW, bool FEAT>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;        // channels of a virtual head
     constexpr int STEP = TW * SB;
@@ -1059,11 +1101,11 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
             cr[r].load(rc, in_range(want_y && t >= wk.t_begin && t < wk.t_end, o));
         }
         float av[4][CPL], u[4][CPL], W[4][CPL], G[4][CPL];
-        decay_rows<IO, CPL>(ar, tr0, p.T, av);
+        decay_rows<IO, CPL>(ar, tr0, t_lo, wk.t_end, p.T, sig_a, av);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * br[r].get(m);
+            for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * pregate(br[r].get(m), sig_b);
         chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
 
         if (grp == 3) {
@@ -1129,8 +1171,9 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
 // decay products.  The decay gradient keeps its closed form per channel,
 //     da_{k,mu} = H_{k-1,mu} du_{k,mu} - g_{k-1,mu} r_{k,mu} (e - s)_mu (eps - p)_mu,
 // and is stored per channel (no sum over the head's channels).
-template <class IO, int CPL, int TW, int HW>
+template <class IO, int CPL, int TW, int HW, bool FEAT>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
     constexpr int STEP = TW * SB;      // whole blocks
@@ -1187,13 +1230,11 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             ar[r].load(ra, o);
         }
         float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
+        decay_rows<IO, CPL>(ar, tr0, wk.t_end, t_la, p.T, sig_a, av);   // (past T the 1s meet dh = 0)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) {
-                av[r][m] = ar[r].get(m);
-                dh[r][m] = dyr[r].get(m) * cr[r].get(m);
-            }
+            for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);
         chan_scan_rev<CPL>(av, dh, Dv, R, grp, lane);
         if (grp == 0) {
 #pragma unroll
@@ -1227,10 +1268,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
 
-        R_ xr[4], br[4], dyr[4];
+        R_ xr[4], br[4], dyr[4], ar[4];
         float av[4][CPL], dh[4][CPL];
         {
-            R_ cr[4], ar[4];
+            R_ cr[4];
             const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
                                          rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
                                          ra = rsrc(ab + r0 * rs);
@@ -1243,13 +1284,11 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 dyr[r].load(rdy, o);
                 ar[r].load(ra, o);
             }
+            decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) {
-                    av[r][m] = ar[r].get(m);
-                    dh[r][m] = dyr[r].get(m) * cr[r].get(m);
-                }
+                for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);
         }
         float vprev[CPL];
         {
@@ -1267,7 +1306,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * br[r].get(m);
+                for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * pregate(br[r].get(m), sig_b);
             chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
         }
         chan_scan_rev<CPL>(av, dh, Dv, Rr, grp, lane);
@@ -1362,10 +1401,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 const float dyv = dyr[r].get(m);
                 vdc[m] = dyv * W[r][m];
                 const float du = Dv[r][m] + Rr[r][m] * epsin[m];
-                vdx[m] = br[r].get(m) * du;
+                const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
+                vdx[m] = pregate(zb, sig_b) * du;
                 if (p.residual) vdx[m] += dyv;
                 vdb[m] = xr[r].get(m) * du;
+                if (sig_b) vdb[m] *= dsigmoid(zb);
                 vda[m] = (r == 0 ? hup[m] : W[r - 1][m]) * du - Gsh[r][m] * Rr[r][m] * kd[m];
+                if (sig_a) vda[m] *= dsigmoid(ar[r].get(m));
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL>(rdx, o, vdx);
@@ -1382,13 +1424,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <class IO, int CPL>
+template <class IO, int CPL, bool FEAT>
 static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
     if (backward) {
 #define SWR_BWD(TW_, HW_)                                                                         \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
-        hipLaunchKernelGGL((swr_bwd_pc_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+        hipLaunchKernelGGL((swr_bwd_pc_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
                            stream, p);
         if (false) {}
         SWR_BWD(8, 1) SWR_BWD(4, 1)
@@ -1397,7 +1439,7 @@ static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hip
     } else {
 #define SWR_FWD(TW_, HW_)                                                                         \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
-        hipLaunchKernelGGL((swr_fwd_pc_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+        hipLaunchKernelGGL((swr_fwd_pc_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
                            stream, p);
         if (false) {}
         SWR_FWD(4, 1) SWR_FWD(2, 2)
@@ -1407,13 +1449,13 @@ static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hip
     return hipGetLastError();
 }
 
-template <class IO, int CPL>
+template <class IO, int CPL, bool FEAT>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
     if (backward) {
 #define SWR_BWD(TW_, HW_)                                                                      \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
-        hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+        hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
                            stream, p);
         if (false) {}
         SWR_BWD(8, 1) SWR_BWD(4, 1)
@@ -1422,41 +1464,50 @@ static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, 
     } else {
 #define SWR_FWD(TW_, HW_)                                                                      \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
-        hipLaunchKernelGGL((swr_fwd_kernel<IO, CPL, TW_, HW_>), grid, dim3(TW_ * HW_ * 64), 0, \
+        hipLaunchKernelGGL((swr_fwd_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
                            stream, p);
         if (false) {}
-        SWR_FWD(4, 1) SWR_FWD(2, 2) SWR_FWD(1, 4) SWR_FWD(4, 2) SWR_FWD(2, 4)
+        SWR_FWD(4, 1) SWR_FWD(2, 2)
         else return hipErrorInvalidValue;
 #undef SWR_FWD
     }
     return hipGetLastError();
 }
 
-template <class IO>
+template <class IO, bool FEAT>
 static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
                              hipStream_t stream) {
     if (per_channel) {
         switch (D) {   // channels of a virtual head (at most 64)
-            case 16: return launch_pc<IO, 1>(p, sh, backward, stream);
-            case 32: return launch_pc<IO, 2>(p, sh, backward, stream);
-            case 64: return launch_pc<IO, 4>(p, sh, backward, stream);
+            case 16: return launch_pc<IO, 1, FEAT>(p, sh, backward, stream);
+            case 32: return launch_pc<IO, 2, FEAT>(p, sh, backward, stream);
+            case 64: return launch_pc<IO, 4, FEAT>(p, sh, backward, stream);
             default: return hipErrorInvalidValue;
         }
     }
     switch (D) {
-        case 16: return launch_shape<IO, 1>(p, sh, backward, stream);
-        case 32: return launch_shape<IO, 2>(p, sh, backward, stream);
-        case 64: return launch_shape<IO, 4>(p, sh, backward, stream);
-        case 128: return launch_shape<IO, 8>(p, sh, backward, stream);
+        case 16: return launch_shape<IO, 1, FEAT>(p, sh, backward, stream);
+        case 32: return launch_shape<IO, 2, FEAT>(p, sh, backward, stream);
+        case 64: return launch_shape<IO, 4, FEAT>(p, sh, backward, stream);
+        case 128: return launch_shape<IO, 8, FEAT>(p, sh, backward, stream);
         default: return hipErrorInvalidValue;
     }
+}
+
+// Kernels without the featurisation code are separate instantiations, so the
+// plain path carries none of its registers.
+template <class IO>
+static hipError_t launch_feat(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
+                              hipStream_t stream) {
+    if (p.sig_a || p.sig_b) return launch_cpl<IO, true>(p, D, sh, backward, per_channel, stream);
+    return launch_cpl<IO, false>(p, D, sh, backward, per_channel, stream);
 }
 
 hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, bool per_channel,
                   void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == 1) return launch_cpl<IoBf16>(p, D, sh, backward, per_channel, st);
-    return launch_cpl<IoF32>(p, D, sh, backward, per_channel, st);
+    if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, st);
+    return launch_feat<IoF32>(p, D, sh, backward, per_channel, st);
 }
 
 }  // namespace swr

@@ -29,6 +29,8 @@ struct Params {
     int32_t block;      // l (16, 32, 64 or 128)
     int32_t lshift;     // log2(l)
     int32_t residual;   // 0 or 1
+    int32_t sig_a;      // 1: a holds logits, the decay is sigmoid(a) (da is then d/d logit)
+    int32_t sig_b;      // 1: b holds logits, the pre-gate is sigmoid(b) (db is then d/d logit)
     int32_t hshift;     // per-channel decay: log2 of the virtual heads per head (0 or 1)
     int64_t run_len;    // tokens per workgroup run, a multiple of the step and of l
     int64_t nruns;      // runs per (batch, head) sequence

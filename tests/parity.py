@@ -60,7 +60,7 @@ def assert_close(got, ref, dtype, what=""):
     return st
 
 
-def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd"):
+def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd", **feat):
     """Forward (saving the block carriers) and backward through the library."""
     import torch
     cfg = prob.cfg
@@ -77,21 +77,21 @@ def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd"):
         if dy is not None:
             dy = bhtd(dy)
     y, v = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len,
-                           save_carriers=True)
+                           save_carriers=True, **feat)
     grads = swr.swr_backward(x, a, b, c, dy, v, cfg.block, residual=residual,
-                             run_len=run_len) if backward else None
+                             run_len=run_len, **feat) if backward else None
     torch.cuda.synchronize()
     return y, grads
 
 
-def check_full(prob, y, grads, residual=False, what=""):
+def check_full(prob, y, grads, residual=False, what="", **feat):
     """Every output against the oracle on the same inputs; returns the error stats."""
     import oracle
     cfg = prob.cfg
-    ref_y = oracle.forward(prob.x, prob.a, prob.b, prob.c, cfg.block, residual)
+    ref_y = oracle.forward(prob.x, prob.a, prob.b, prob.c, cfg.block, residual, **feat)
     stats = {"y": assert_close(to_host(y), ref_y, cfg.dtype, what + " y")}
     if grads is not None:
-        ref = oracle.backward(prob.x, prob.a, prob.b, prob.c, prob.dy, cfg.block, residual)
+        ref = oracle.backward(prob.x, prob.a, prob.b, prob.c, prob.dy, cfg.block, residual, **feat)
         for name, g, r in zip(("dx", "da", "db", "dc"), grads, ref):
             stats[name] = assert_close(to_host(g), r, cfg.dtype, f"{what} {name}")
     return stats

@@ -275,3 +275,59 @@ def test_channel_constant_per_channel_decay_is_shared_decay(rng, T, D, block):
     for i in (0, 2, 3):
         np.testing.assert_allclose(g2[i], g1[i], rtol=1e-13, atol=1e-13)
     np.testing.assert_allclose(g2[1].sum(axis=-1), g1[1], rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- featurisation
+
+
+def test_sigmoid_values():
+    # closed forms and the symmetry sigma(-z) = 1 - sigma(z), including the tails
+    z = np.array([-800.0, -40.0, -1.0, 0.0, 1.0, 40.0, 800.0])
+    s = oracle.sigmoid(z)
+    assert s[3] == 0.5 and s[0] == 0.0 and s[-1] == 1.0
+    np.testing.assert_allclose(s[4], 1.0 / (1.0 + np.exp(-1.0)), rtol=1e-15)
+    np.testing.assert_allclose(oracle.sigmoid(-z) + s, 1.0, rtol=0, atol=1e-15)
+    np.testing.assert_allclose(oracle.dsigmoid(0.0), 0.25, rtol=1e-15)
+    assert np.all(np.isfinite(oracle.dsigmoid(z)))
+
+
+@pytest.mark.parametrize("sig_a,sig_b", [(True, False), (False, True), (True, True)])
+@pytest.mark.parametrize("per_channel", [False, True])
+def test_featurised_gradients_by_finite_differences(rng, sig_a, sig_b, per_channel):
+    # d/dz of sum(dy * y(sigma(z_a), sigma(z_b))) by central differences on a few entries
+    B, T, H, D, block = 1, 23, 2, 3, 8
+    x, c, dy = (rng.standard_normal((B, T, H, D)) for _ in range(3))
+    za = rng.standard_normal((B, T, H, D) if per_channel else (B, T, H)) * 2.0
+    zb = rng.standard_normal((B, T, H, D)) * 2.0
+    kw = dict(sigmoid_decay=sig_a, sigmoid_pregate=sig_b)
+    dx, da, db, dc = oracle.backward(x, za, zb, c, dy, block, **kw)
+
+    def loss(za_, zb_):
+        return float(np.sum(dy * oracle.forward(x, za_, zb_, c, block, **kw)))
+
+    h = 1e-6
+    for idx in [(0, 0, 0), (0, 5, 1), (0, 22, 1)]:
+        full = idx + ((1,) if per_channel else ())
+        e = np.zeros_like(za); e[full] = h
+        fd = (loss(za + e, zb) - loss(za - e, zb)) / (2 * h)
+        np.testing.assert_allclose(da[full], fd, rtol=1e-6, atol=1e-8)
+        e = np.zeros_like(zb); e[idx + (2,)] = h
+        fd = (loss(za, zb + e) - loss(za, zb - e)) / (2 * h)
+        np.testing.assert_allclose(db[idx + (2,)], fd, rtol=1e-6, atol=1e-8)
+
+
+def test_featurised_equals_plain_on_sigmoid_values(rng):
+    # the featurised call on logits z is the plain call on sigma(z); gradients
+    # differ exactly by the factor sigma'(z)
+    B, T, H, D, block = 2, 40, 2, 4, 16
+    x, c, dy = (rng.standard_normal((B, T, H, D)) for _ in range(3))
+    za, zb = rng.standard_normal((B, T, H)), rng.standard_normal((B, T, H, D))
+    a, b = 1.0 / (1.0 + np.exp(-za)), 1.0 / (1.0 + np.exp(-zb))
+    y1 = oracle.forward(x, za, zb, c, block, sigmoid_decay=True, sigmoid_pregate=True)
+    np.testing.assert_allclose(y1, oracle.forward(x, a, b, c, block), rtol=1e-13, atol=1e-13)
+    g1 = oracle.backward(x, za, zb, c, dy, block, sigmoid_decay=True, sigmoid_pregate=True)
+    g0 = oracle.backward(x, a, b, c, dy, block)
+    np.testing.assert_allclose(g1[1], g0[1] * a * (1 - a), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(g1[2], g0[2] * b * (1 - b), rtol=1e-12, atol=1e-13)
+    for i in (0, 3):
+        np.testing.assert_allclose(g1[i], g0[i], rtol=1e-13, atol=1e-13)

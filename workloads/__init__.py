@@ -18,7 +18,8 @@ with the configuration's seed, in this fixed order):
   ``sigmoid(N(mu, 1))`` or ``exp(-softplus(N(0, 1)) * Delta)`` with ``Delta``
   uniform in ``[1e-3, 1e-1]``, drawn per (b, t, h).  Per-channel-decay
   workloads draw ``a`` with the same recipe per (b, t, h, channel), shape
-  ``[B, T, H, D]``.
+  ``[B, T, H, D]``.  Workloads fed through the fused sigmoid featurisation
+  (``logits``) store the normal ``N(mu, 1)`` itself, the decay's logit.
 * Every tensor is then rounded to the I/O dtype with round-to-nearest-even;
   the GPU library and the oracle both consume exactly these rounded values.
 """
@@ -88,6 +89,7 @@ class Config:
     backward: bool = True
     width: Optional[int] = None   # model width of the projected-x recipe
     per_channel: bool = False     # one decay per token, head and channel ([B, T, H, D])
+    logits: bool = False          # a holds the sigmoid's argument instead of the decay
 
     @property
     def tokens(self) -> int:
@@ -182,14 +184,21 @@ def generate(cfg: Config, with_dy: Optional[bool] = None) -> Problem:
     c = round_to(rng.standard_normal(shape, dtype=np.float32), cfg.dtype)
     dy = round_to(rng.standard_normal(shape, dtype=np.float32), cfg.dtype) if with_dy else None
     a_shape = shape if cfg.per_channel else shape[:3]
-    a = round_to(draw_decay(rng, a_shape, cfg.a_kind, cfg.a_mu), cfg.dtype)
+    if cfg.logits:     # the decay's logit z ~ N(mu, 1): the decay is sigmoid(z)
+        if cfg.a_kind != "sigmoid":
+            raise ValueError("logit inputs need the sigmoid decay recipe")
+        z = rng.standard_normal(a_shape, dtype=np.float32) + np.float32(cfg.a_mu)
+        a = round_to(z, cfg.dtype)
+    else:
+        a = round_to(draw_decay(rng, a_shape, cfg.a_kind, cfg.a_mu), cfg.dtype)
     return Problem(cfg, x, a, b, c, dy)
 
 
 def random_problem(seed: int, B: int, T: int, H: int, D: int, block: int, dtype: str = "bf16",
                    a_kind: str = "sigmoid", a_mu: float = 2.0, with_dy: bool = True,
-                   per_channel: bool = False) -> Problem:
+                   per_channel: bool = False, logits: bool = False) -> Problem:
     """A small ad-hoc workload with the same recipe (used by parity tests)."""
     cfg = Config(0, f"adhoc_B{B}_T{T}_H{H}_d{D}_l{block}_{dtype}", B, T, H, D, block, dtype,
-                 a_kind, a_mu, seed=seed, backward=with_dy, per_channel=per_channel)
+                 a_kind, a_mu, seed=seed, backward=with_dy, per_channel=per_channel,
+                 logits=logits)
     return generate(cfg, with_dy=with_dy)
