@@ -8,6 +8,8 @@ the whole workload, inputs already resident in HBM.  Prints ONE JSON line.
 
 --decay channel times the per-channel-decay path (a and da of shape
 [B, T, H, D]) on the same workload shape instead of the shared decay.
+--sigmoid feeds a and b as logits through the kernels' fused sigmoid (the
+Phalanx featurisation); a's logits are then drawn N(3, 1).
 
 Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
 durations come from HIP events recorded on the stream the kernels run on.
@@ -121,6 +123,8 @@ def cpu_baseline(cfg, prob, budget_s=10.0):
 
         xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
         t0 = time.perf_counter()
+        if cfg.logits:     # the featurisation is part of the timed work
+            as_, bs = oracle.sigmoid(as_), oracle.sigmoid(bs)
         oracle.forward_slices(xs, as_, bs, cs, cfg.block)
         oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
         elapsed += time.perf_counter() - t0
@@ -149,6 +153,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decay", choices=("head", "channel"), default="head",
                     help="one decay per token and head (default) or per token, head and channel")
+    ap.add_argument("--sigmoid", action="store_true",
+                    help="a and b are logits; the kernels apply the sigmoid (fused featurisation)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -167,6 +173,10 @@ def main():
     cfg = W.CONFIGS[args.config]
     if args.decay == "channel":
         cfg = W.PER_CHANNEL.get(args.config) or cfg.with_(name=cfg.name + "_perchannel", per_channel=True)
+    if args.sigmoid:
+        cfg = cfg.with_(name=cfg.name + "_sigmoid", logits=True, a_kind="sigmoid",
+                        a_mu=cfg.a_mu if cfg.a_kind == "sigmoid" else 3.0)
+    feat = dict(sigmoid_decay=args.sigmoid, sigmoid_pregate=args.sigmoid)
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -182,11 +192,11 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len)
+        swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
         if ev is not None:
             ev[1].record(stream)
         swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
-                         run_len=args.run_len)
+                         run_len=args.run_len, **feat)
         if ev is not None:
             ev[2].record(stream)
 
@@ -256,6 +266,7 @@ def main():
         "data": "synthetic (seeded host draws, rounded to the I/O dtype)",
         "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
                    "block": cfg.block, "decay": "per channel" if cfg.per_channel else "per head",
+                   "featurisation": "fused sigmoid of a and b" if args.sigmoid else "none",
                    "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {
