@@ -47,6 +47,11 @@ def _load():
             lead = [i64] if not name.endswith("_slice") else []
             fn.argtypes = lead + [i64, i64, i64, ci, ci] + [dp] * (nin + nout)
             fn.restype = ci
+        for name, lead in (("swr_oracle_exact_forward", [i64]), ("swr_oracle_exact_backward", [i64])):
+            fn = getattr(lib, name)
+            nptr = 6 if name.endswith("forward") else 12
+            fn.argtypes = lead + [i64, i64, ci, ci] + [dp] * nptr
+            fn.restype = ci
         lib.swr_oracle_max_threads.restype = ci
         _lib = lib
     return _lib
@@ -146,3 +151,85 @@ def backward(x, a, b, c, dy, block, residual=False, sigmoid_decay=False, sigmoid
     if sigmoid_pregate:
         db = db * dsigmoid(b)
     return dx, da, db, dc
+
+
+# ----------------------------------------------------------------------------
+# Exact (untruncated) recurrence with an initial state (Sec. 3, eq. (2.1); the
+# result of Alg. "Hierarchical Block Parallel Inference", Sec. 3.2)
+# ----------------------------------------------------------------------------
+
+def _opt_ptr(arr):
+    return None if arr is None else _ptr(arr)
+
+
+def exact_forward_slices(x, a, b, c, h0=None, residual=False):
+    """Exact recurrence on independent slices: x, b, c are [S, T, D]; a is
+    [S, T] or [S, T, D]; h0 is [S, D] or None (zero).  Returns (y, h_last)
+    with h_last = the state after the last token, [S, D]."""
+    lib = _load()
+    x, a, b, c = _c64(x), _c64(a), _c64(b), _c64(c)
+    S, T, D = x.shape
+    h0 = None if h0 is None else _c64(np.broadcast_to(h0, (S, D)))
+    y = np.empty((S, T, D), np.float64)
+    h_last = np.empty((S, D), np.float64)
+    rc = lib.swr_oracle_exact_forward(S, T, D, int(a.ndim == 3), RESIDUAL if residual else 0,
+                                      _ptr(x), _ptr(a), _ptr(b), _ptr(c), _opt_ptr(h0),
+                                      _ptr(y), _ptr(h_last))
+    if rc != 0:
+        raise ValueError("oracle exact forward rejected its arguments")
+    return y, h_last
+
+
+def exact_backward_slices(x, a, b, c, dy, h0=None, dh_last=None, residual=False):
+    """Gradients of sum(dy * y) + sum(dh_last * h_last) for the exact
+    recurrence on slices; returns (dx, da, db, dc, dh0) with da shaped like a
+    and dh0 = d/d h0, [S, D]."""
+    lib = _load()
+    x, a, b, c, dy = _c64(x), _c64(a), _c64(b), _c64(c), _c64(dy)
+    S, T, D = x.shape
+    h0 = None if h0 is None else _c64(np.broadcast_to(h0, (S, D)))
+    dh_last = None if dh_last is None else _c64(np.broadcast_to(dh_last, (S, D)))
+    dx, db, dc = (np.empty((S, T, D), np.float64) for _ in range(3))
+    da = np.empty(a.shape, np.float64)
+    dh0 = np.empty((S, D), np.float64)
+    rc = lib.swr_oracle_exact_backward(S, T, D, int(a.ndim == 3), RESIDUAL if residual else 0,
+                                       _ptr(x), _ptr(a), _ptr(b), _ptr(c), _opt_ptr(h0), _ptr(dy),
+                                       _opt_ptr(dh_last), _ptr(dx), _ptr(da), _ptr(db), _ptr(dc),
+                                       _ptr(dh0))
+    if rc != 0:
+        raise ValueError("oracle exact backward rejected its arguments")
+    return dx, da, db, dc, dh0
+
+
+def _state_to_slices(h, B, H):
+    # [B, H, D] -> [B*H, D]
+    return None if h is None else np.asarray(h, np.float64).reshape(B * H, -1)
+
+
+def exact_forward(x, a, b, c, h0=None, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """Exact recurrence for [B, T, H, D] tensors (a: [B, T, H] or [B, T, H, D]);
+    h0 is [B, H, D] or None.  Returns (y, h_last) with h_last [B, H, D]."""
+    B, T, H, D = np.shape(x)
+    a = sigmoid(a) if sigmoid_decay else a
+    b = sigmoid(b) if sigmoid_pregate else b
+    y, hl = exact_forward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c),
+                                 _state_to_slices(h0, B, H), residual)
+    return _from_slices(y, B, H), hl.reshape(B, H, D)
+
+
+def exact_backward(x, a, b, c, dy, h0=None, dh_last=None, residual=False,
+                   sigmoid_decay=False, sigmoid_pregate=False):
+    """(dx, da, db, dc, dh0) of the exact recurrence for [B, T, H, D] tensors;
+    dh_last and dh0 are [B, H, D]."""
+    B, T, H, D = np.shape(x)
+    av = sigmoid(a) if sigmoid_decay else a
+    bv = sigmoid(b) if sigmoid_pregate else b
+    outs = exact_backward_slices(_to_slices(x), _to_slices(av), _to_slices(bv), _to_slices(c),
+                                 _to_slices(dy), _state_to_slices(h0, B, H),
+                                 _state_to_slices(dh_last, B, H), residual)
+    dx, da, db, dc = (_from_slices(o, B, H) for o in outs[:4])
+    if sigmoid_decay:
+        da = da * dsigmoid(a)
+    if sigmoid_pregate:
+        db = db * dsigmoid(b)
+    return dx, da, db, dc, outs[4].reshape(B, H, D)

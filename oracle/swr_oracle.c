@@ -145,6 +145,113 @@ int swr_oracle_backward(int64_t S, int64_t T, int64_t D, int64_t block, int a_pe
     return err ? -1 : 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Exact (untruncated) recurrence, Sec. 3 eq. (2.1), with an initial state.  */
+/* ------------------------------------------------------------------------ */
+
+int swr_oracle_exact_forward_slice(int64_t T, int64_t D, int a_per_channel, int flags,
+                                   const double* x, const double* a, const double* b,
+                                   const double* c, const double* h0, double* y,
+                                   double* h_last) {
+    if (T < 0 || D < 1) return -1;
+    if (T > 0 && (!x || !a || !b || !c || !y)) return -1;
+    double* s = (double*)malloc((size_t)D * sizeof(double));
+    if (!s) return -1;
+    for (int64_t mu = 0; mu < D; ++mu) s[mu] = h0 ? h0[mu] : 0.0;
+    for (int64_t m = 0; m < T; ++m) {
+        for (int64_t mu = 0; mu < D; ++mu) {
+            const int64_t e = m * D + mu;
+            s[mu] = decay(a, a_per_channel, D, m, mu) * s[mu] + b[e] * x[e];
+            y[e] = c[e] * s[mu];
+            if (flags & SWR_ORACLE_RESIDUAL) y[e] += x[e];
+        }
+    }
+    if (h_last)
+        for (int64_t mu = 0; mu < D; ++mu) h_last[mu] = s[mu];
+    free(s);
+    return 0;
+}
+
+int swr_oracle_exact_backward_slice(int64_t T, int64_t D, int a_per_channel, int flags,
+                                    const double* x, const double* a, const double* b,
+                                    const double* c, const double* h0, const double* dy,
+                                    const double* dh_last, double* dx, double* da,
+                                    double* db, double* dc, double* dh0) {
+    if (T < 0 || D < 1) return -1;
+    if (T > 0 && (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc)) return -1;
+    /* Forward again, keeping the state entering every step (pre) and leaving it (post). */
+    double* pre = (double*)malloc((size_t)(T * D + D) * sizeof(double));
+    double* post = (double*)malloc((size_t)(T * D + D) * sizeof(double));
+    double* lam = (double*)malloc((size_t)D * sizeof(double));
+    if (!pre || !post || !lam) {
+        free(pre); free(post); free(lam);
+        return -1;
+    }
+    for (int64_t mu = 0; mu < D; ++mu) lam[mu] = h0 ? h0[mu] : 0.0; /* lam is the state here */
+    for (int64_t m = 0; m < T; ++m) {
+        for (int64_t mu = 0; mu < D; ++mu) {
+            const int64_t e = m * D + mu;
+            pre[e] = lam[mu];
+            lam[mu] = decay(a, a_per_channel, D, m, mu) * lam[mu] + b[e] * x[e];
+            post[e] = lam[mu];
+        }
+    }
+    if (T > 0) memset(da, 0, (size_t)(a_per_channel ? T * D : T) * sizeof(double));
+    /* Reverse sweep: lam = d(loss)/d(state after step m). */
+    for (int64_t mu = 0; mu < D; ++mu) lam[mu] = dh_last ? dh_last[mu] : 0.0;
+    for (int64_t m = T - 1; m >= 0; --m) {
+        for (int64_t mu = 0; mu < D; ++mu) {
+            const int64_t e = m * D + mu;
+            lam[mu] += c[e] * dy[e];          /* y_m = c_m * state_m            */
+            dc[e] = dy[e] * post[e];
+            const double du = lam[mu];        /* d state_m / d u_m = 1          */
+            dx[e] = b[e] * du;
+            if (flags & SWR_ORACLE_RESIDUAL) dx[e] += dy[e];
+            db[e] = x[e] * du;
+            if (a_per_channel)                /* d state_m / d a_m = state_{m-1} */
+                da[e] += lam[mu] * pre[e];
+            else
+                da[m] += lam[mu] * pre[e];
+            lam[mu] *= decay(a, a_per_channel, D, m, mu); /* d state_m / d state_{m-1} */
+        }
+    }
+    if (dh0)
+        for (int64_t mu = 0; mu < D; ++mu) dh0[mu] = lam[mu];
+    free(pre); free(post); free(lam);
+    return 0;
+}
+
+int swr_oracle_exact_forward(int64_t S, int64_t T, int64_t D, int a_per_channel, int flags,
+                             const double* x, const double* a, const double* b,
+                             const double* c, const double* h0, double* y, double* h_last) {
+    if (S < 0 || T < 0 || D < 1) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_exact_forward_slice(T, D, a_per_channel, flags, x + s * n, a + s * na,
+                                              b + s * n, c + s * n, h0 ? h0 + s * D : NULL,
+                                              y + s * n, h_last ? h_last + s * D : NULL) != 0;
+    return err ? -1 : 0;
+}
+
+int swr_oracle_exact_backward(int64_t S, int64_t T, int64_t D, int a_per_channel, int flags,
+                              const double* x, const double* a, const double* b,
+                              const double* c, const double* h0, const double* dy,
+                              const double* dh_last, double* dx, double* da, double* db,
+                              double* dc, double* dh0) {
+    if (S < 0 || T < 0 || D < 1) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_exact_backward_slice(
+                   T, D, a_per_channel, flags, x + s * n, a + s * na, b + s * n, c + s * n,
+                   h0 ? h0 + s * D : NULL, dy + s * n, dh_last ? dh_last + s * D : NULL,
+                   dx + s * n, da + s * na, db + s * n, dc + s * n, dh0 ? dh0 + s * D : NULL) != 0;
+    return err ? -1 : 0;
+}
+
 int swr_oracle_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

@@ -61,6 +61,43 @@ int swr_oracle_backward(int64_t S, int64_t T, int64_t D, int64_t block, int a_pe
                         const double* c, const double* dy, double* dx, double* da,
                         double* db, double* dc);
 
+/* The exact (untruncated) recurrence of Sec. 3, eq. (2.1), with an optional
+ * initial state: the state sequence that the hierarchical decomposition of
+ * Sec. 3.2 (Thm. "Hierarchical Decomposition", Alg. "Hierarchical Block
+ * Parallel Inference") computes exactly, and that the window truncation of
+ * Sec. 4.2 approximates.  For one slice and channel mu:
+ *
+ *     h_{-1} = h0 (zero when h0 is NULL),   h_m = a_m h_{m-1} + b_m x_m,
+ *     y_m    = c_m h_m   (+ x_m with the residual flag),
+ *
+ * and h_last = h_{T-1} (h0 itself when T = 0) when h_last is not NULL.
+ * h0 and h_last are [D].  Returns 0, or -1 on a bad argument. */
+int swr_oracle_exact_forward_slice(int64_t T, int64_t D, int a_per_channel, int flags,
+                                   const double* x, const double* a, const double* b,
+                                   const double* c, const double* h0, double* y,
+                                   double* h_last);
+
+/* Gradients of  L = sum(dy * y) + sum(dh_last * h_last)  for the exact forward
+ * above (dh_last NULL means zero): dx, da, db, dc as in the truncated
+ * backward, and dh0 = dL/dh0 ([D], skipped when NULL).  The exact
+ * reverse-mode adjoint of the forward loop. */
+int swr_oracle_exact_backward_slice(int64_t T, int64_t D, int a_per_channel, int flags,
+                                    const double* x, const double* a, const double* b,
+                                    const double* c, const double* h0, const double* dy,
+                                    const double* dh_last, double* dx, double* da,
+                                    double* db, double* dc, double* dh0);
+
+/* S slices back to back (as swr_oracle_forward); h0, h_last, dh_last, dh0 are
+ * [S][D] or NULL.  Slices run in parallel over OpenMP threads. */
+int swr_oracle_exact_forward(int64_t S, int64_t T, int64_t D, int a_per_channel, int flags,
+                             const double* x, const double* a, const double* b,
+                             const double* c, const double* h0, double* y, double* h_last);
+int swr_oracle_exact_backward(int64_t S, int64_t T, int64_t D, int a_per_channel, int flags,
+                              const double* x, const double* a, const double* b,
+                              const double* c, const double* h0, const double* dy,
+                              const double* dh_last, double* dx, double* da, double* db,
+                              double* dc, double* dh0);
+
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
 int swr_oracle_max_threads(void);
 

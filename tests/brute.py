@@ -14,6 +14,11 @@ either shows up as a disagreement:
                           obtained by a linear solve (Sec. 3.2, intra-block
                           operator), g_t the block's cumulative products and
                           r_t^T = e_l^T L_t (Sec. 3.2, carrier definitions).
+* ``dense_L_hierarchical`` -- the full operator from the exact hierarchical
+                          decomposition calL + G Z_b T R (Sec. 3.2, Thm.
+                          "Hierarchical Decomposition"), with the carrier
+                          transfer operator T = (I_b - C Z_b)^{-1} obtained by
+                          a linear solve.
 * ``window_sum``       -- the explicit sum of decay products over each token's
                           window.
 * ``torch_forward``    -- a differentiable float64 torch version of
@@ -143,3 +148,72 @@ def torch_grads(x, a, b, c, dy, block, residual=False, truncated=True):
     (y * torch.tensor(np.asarray(dy, np.float64))).sum().backward()
     # a leaf that no product touched (T = 1) gets no .grad: its gradient is 0
     return tuple(t.grad.numpy() if t.grad is not None else np.zeros(t.shape) for t in ts)
+
+
+def dense_L_hierarchical(a, block):
+    """Full transfer operator assembled as calL + G Z_b T R, T = (I - C Z_b)^{-1}
+    (the exact hierarchical decomposition; no truncation of T)."""
+    a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    nb = -(-n // block)
+    N = nb * block
+    ap = np.zeros(N)
+    ap[:n] = a
+    calL = np.zeros((N, N))
+    G = np.zeros((N, nb))
+    R = np.zeros((nb, N))
+    Cd = np.zeros(nb)
+    Zl = np.eye(block, k=-1)
+    for t in range(nb):
+        sl = slice(t * block, (t + 1) * block)
+        at = ap[sl]
+        Lt = np.linalg.solve(np.eye(block) - np.diag(at) @ Zl, np.eye(block))
+        calL[sl, sl] = Lt
+        G[sl, t] = np.cumprod(at)
+        R[t, sl] = Lt[block - 1, :]
+        Cd[t] = np.prod(at)                  # compound attenuation c_t = a_{t,l:1}
+    Zb = np.eye(nb, k=-1)
+    Tc = np.linalg.solve(np.eye(nb) - np.diag(Cd) @ Zb, np.eye(nb))
+    return (calL + G @ Zb @ Tc @ R)[:n, :n]
+
+
+def exact_states(a, u, h0=None):
+    """h_i = sum_{j<=i} a_{i:j+1} u_j + a_{i:0} h0 by explicit products, for u
+    [T, D] and a [T] or [T, D]."""
+    a = np.asarray(a, np.float64)
+    u = np.asarray(u, np.float64)
+    T, D = u.shape
+    h = np.zeros((T, D))
+    for mu in range(D):
+        aa = a if a.ndim == 1 else a[:, mu]
+        for i in range(T):
+            acc = 0.0
+            for j in range(i + 1):
+                acc += decay_product(aa, i, j) * u[j, mu]
+            if h0 is not None:
+                acc += decay_product(aa, i, -1) * h0[mu]
+            h[i, mu] = acc
+    return h
+
+
+def torch_exact(x, a, b, c, h0, residual=False):
+    """Differentiable float64 exact recurrence of one slice from explicit
+    products; returns (y, h_last)."""
+    import torch
+    T, D = x.shape
+    u = b * x
+    rows = []
+    for i in range(T):
+        acc = torch.zeros(D, dtype=torch.float64)
+        for j in range(-1, i + 1):
+            src = h0 if j < 0 else u[j]
+            if i > j:
+                w = torch.prod(a[j + 1:i + 1], dim=0) if a.dim() == 2 else torch.prod(a[j + 1:i + 1])
+            else:
+                w = torch.ones((), dtype=torch.float64)
+            acc = acc + w * src
+        rows.append(acc)
+    h = torch.stack(rows) if rows else torch.zeros((0, D), dtype=torch.float64)
+    y = c * h
+    h_last = h[-1] if T > 0 else h0
+    return (y + x if residual else y), h_last
