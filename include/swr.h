@@ -39,8 +39,9 @@
  * `dtype`; accumulation is always float32.
  *
  * Ownership.  Every pointer is device memory owned by the caller.  The library
- * allocates no memory, needs no workspace and keeps no mutable global state;
- * calls from several host threads are safe.  Outputs are fully overwritten.
+ * allocates no memory and keeps no mutable global state; calls from several
+ * host threads are safe.  Only the exact-recurrence calls need a workspace,
+ * which the caller provides.  Outputs are fully overwritten.
  *
  * Asynchrony.  Work is enqueued on `stream` (a hipStream_t passed as void*;
  * NULL = the default stream) and the call returns without waiting.  A fault
@@ -151,6 +152,59 @@ const char* swr_error_string(int code);
 
 /* SWR_ABI_VERSION of the built library. */
 int swr_abi_version(void);
+
+/* ------------------------------------------------------------------------
+ * Exact (untruncated) recurrence
+ *
+ * The state sequence of eq. (2.1) with no window truncation and an optional
+ * initial state h0:  h_{-1} = h0,  h_i = a_i h_{i-1} + b_i (*) x_i,
+ * y_i = c_i (*) h_i (+ x_i with SWR_FLAG_RESIDUAL).  It is the result of the
+ * hierarchical decomposition L = calL + G Z_b T R (Sec. 3.2, Thm.
+ * "Hierarchical Decomposition") evaluated by Alg. "Hierarchical Block Parallel
+ * Inference" in its three stages, at the granularity of a workgroup's run of
+ * blocks: (I) local solves of every run from zero, keeping each run's end
+ * state and decay product; (II) the carrier recurrence s_r = c_r s_{r-1} + v_r
+ * over a sequence's runs; (III) every run again from its exact entering
+ * state.  This is the recurrence that the jagged window approximates; with
+ * h0 and h_last it also chains a long sequence processed in pieces, and a
+ * single-token piece is the recurrent decoding step.  Stages I and III both
+ * read x, b and a, so the exact forward moves about 1.5x the bytes of
+ * swr_forward (the backward about 1.25x).
+ *
+ * Everything in swr_problem_t keeps its meaning except that `block` only sets
+ * the length of the exact block carriers; SWR_FLAG_PER_CHANNEL_DECAY is not
+ * supported here (SWR_ERR_UNSUPPORTED).  h0, h_last, dh_last and dh0 are
+ * float32 [B][H][D], contiguous, 16-byte aligned; NULL h0 / dh_last mean
+ * zero, NULL h_last / dh0 skip that output.
+ *
+ * Workspace: swr_exact_workspace_bytes(problem) bytes of device memory
+ * (16-byte aligned, owned by the caller, needing no initialisation; it may be
+ * NULL when that size is 0).  Its contents are scratch and are overwritten;
+ * two calls in flight at once need two workspaces.
+ * ------------------------------------------------------------------------ */
+
+/* Bytes of workspace swr_exact_forward / swr_exact_backward need for this
+ * problem, or a negative SWR_ERR_* code. */
+int64_t swr_exact_workspace_bytes(const swr_problem_t* problem);
+
+/* Exact forward.  y is required (unless the problem is empty).  carriers:
+ * NULL, or swr_carrier_elems(problem) float32 values that receive the exact
+ * state at the end of every block ([B][H][ceil(T/block)][D]; a partial last
+ * block's entry is the state at token T-1), which swr_exact_backward needs.
+ * h_last receives the state after token T-1 (h0 when T = 0). */
+int swr_exact_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                      const void* c, const float* h0, void* y, float* carriers, float* h_last,
+                      void* workspace, void* stream);
+
+/* Exact backward: gradients of  sum(dy * y) + sum(dh_last * h_last)  with
+ * respect to x, a (float32 with a's shape and strides), b, c and h0.  x, a, b,
+ * c and h0 are the forward's inputs and `carriers` its exact block carriers
+ * (required).  With the sigmoid flags, da and db are with respect to the
+ * logits, as in swr_backward. */
+int swr_exact_backward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                       const void* c, const void* dy, const float* h0, const float* carriers,
+                       const float* dh_last, void* dx, float* da, void* db, void* dc, float* dh0,
+                       void* workspace, void* stream);
 
 /* Resolved launch shape for a problem (for reports and tests): the run length
  * in tokens and the number of workgroups of the forward and of the backward

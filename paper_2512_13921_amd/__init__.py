@@ -23,6 +23,7 @@ from . import build as _build
 
 __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error_string",
            "swr_abi_version", "swr_launch_info", "swr_carrier_elems", "carrier_shape",
+           "swr_exact_forward", "swr_exact_backward", "swr_exact_workspace_bytes",
            "SWRFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
@@ -84,6 +85,12 @@ def load():
         i64p = ctypes.POINTER(ctypes.c_int64)
         lib.swr_launch_info.argtypes = [P, i64p, i64p, i64p, i64p]
         lib.swr_launch_info.restype = ctypes.c_int
+        lib.swr_exact_workspace_bytes.argtypes = [P]
+        lib.swr_exact_workspace_bytes.restype = ctypes.c_int64
+        lib.swr_exact_forward.argtypes = [P] + [vp] * 10
+        lib.swr_exact_forward.restype = ctypes.c_int
+        lib.swr_exact_backward.argtypes = [P] + [vp] * 15
+        lib.swr_exact_backward.restype = ctypes.c_int
         if lib.swr_abi_version() != SWR_ABI_VERSION:
             raise RuntimeError("libswr.so ABI version does not match the binding")
         _lib = lib
@@ -266,6 +273,104 @@ def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, 
     if rc != 0:
         raise SwrError(rc, "swr_backward")
     return dx, da, db, dc
+
+
+# ----------------------------------------------------------------------------- exact recurrence
+
+
+def swr_exact_workspace_bytes(problem: SwrProblem) -> int:
+    """Bytes of workspace the exact-recurrence calls need for a problem."""
+    n = int(load().swr_exact_workspace_bytes(ctypes.byref(problem)))
+    if n < 0:
+        raise SwrError(n, "swr_exact_workspace_bytes")
+    return n
+
+
+def _workspace(problem, device, workspace):
+    torch = _torch()
+    nbytes = swr_exact_workspace_bytes(problem)
+    if workspace is None:
+        return torch.empty(max(nbytes // 4, 1), dtype=torch.float32, device=device)
+    if workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes")
+    return workspace
+
+
+def _state(t, x, what):
+    """A [B, H, D] float32 state tensor (or None)."""
+    torch = _torch()
+    if t is None:
+        return None
+    B, T, H, D = x.shape
+    if (tuple(t.shape) != (B, H, D) or t.dtype != torch.float32 or not t.is_contiguous()
+            or t.device != x.device):
+        raise ValueError(f"{what} must be a contiguous float32 tensor of shape {(B, H, D)}")
+    return t
+
+
+def _opt(t):
+    return None if t is None else _ptr(t)
+
+
+def swr_exact_forward(x, a, b, c, block, h0=None, residual=False, y=None, carriers=None,
+                      save_carriers=False, want_h_last=False, workspace=None, run_len=0, stream=None,
+                      sigmoid_decay=False, sigmoid_pregate=False):
+    """The exact (untruncated) recurrence on the GPU (see ``include/swr.h``):
+    returns y, plus the exact block carriers (``save_carriers`` or a
+    ``carriers`` tensor) and the final state h_last ([B, H, D] float32,
+    ``want_h_last``), in that order.  ``h0`` is the initial state or None."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c)
+    h0 = _state(h0, x, "h0")
+    if y is None:
+        y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+    else:
+        _same_layout(x, y)
+    want_v = save_carriers or carriers is not None
+    v = _carrier_tensor(x, block, carriers) if want_v else None
+    B, T, H, D = x.shape
+    hl = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if want_h_last else None
+    ws = _workspace(problem, x.device, workspace)
+    rc = load().swr_exact_forward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _opt(h0),
+                                  _ptr(y), _opt(v), _opt(hl), _ptr(ws), _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_exact_forward")
+    out = (y,) + ((v,) if want_v else ()) + ((hl,) if want_h_last else ())
+    return out[0] if len(out) == 1 else out
+
+
+def swr_exact_backward(x, a, b, c, dy, carriers, block, h0=None, dh_last=None, residual=False,
+                       outputs=None, want_dh0=False, workspace=None, run_len=0, stream=None,
+                       sigmoid_decay=False, sigmoid_pregate=False):
+    """(dx, da, db, dc) of the exact recurrence, plus dh0 when ``want_dh0``;
+    ``carriers`` are the exact forward's block carriers, ``dh_last`` the
+    gradient flowing into its final state (or None)."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c, dy)
+    if carriers is None:
+        raise ValueError("swr_exact_backward needs the exact forward's block carriers")
+    carriers = _carrier_tensor(x, block, carriers)
+    h0, dh_last = _state(h0, x, "h0"), _state(dh_last, x, "dh_last")
+    if outputs is None:
+        dx, db, dc = (torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+                      for _ in range(3))
+        da = torch.empty_strided(a.shape, a.stride(), dtype=torch.float32, device=a.device)
+    else:
+        dx, da, db, dc = outputs
+        _same_layout(x, dx, db, dc)
+        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
+            raise ValueError("da must be float32 with the shape and strides of a")
+    B, T, H, D = x.shape
+    dh0 = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if want_dh0 else None
+    ws = _workspace(problem, x.device, workspace)
+    rc = load().swr_exact_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
+                                   _opt(h0), _ptr(carriers), _opt(dh_last), _ptr(dx), _ptr(da), _ptr(db),
+                                   _ptr(dc), _opt(dh0), _ptr(ws), _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_exact_backward")
+    return (dx, da, db, dc, dh0) if want_dh0 else (dx, da, db, dc)
 
 
 def _autograd_function():

@@ -261,7 +261,8 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
 
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kSwr, stream) == hipSuccess ? SWR_OK
+                                                                                        : SWR_ERR_HIP;
 }
 
 }  // namespace
@@ -313,7 +314,163 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kSwr, stream) == hipSuccess ? SWR_OK
+                                                                                       : SWR_ERR_HIP;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Exact (untruncated) recurrence
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Workspace of the exact recurrence, in float32 elements: per (batch, head)
+// and run, the run's aggregate end state (D), the value entering the run (D)
+// and the run's decay product (1), for the larger of the two launches' run
+// counts.
+struct ExactWs {
+    int64_t nr;       // runs per sequence the workspace is laid out for
+    int64_t floats;   // total float32 elements
+};
+
+ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
+    ExactWs w;
+    w.nr = std::max(r.nruns, r.nruns_f);
+    w.floats = p->B * p->H * w.nr * (2 * p->D + 1);
+    return w;
+}
+
+int resolve_exact(const swr_problem_t* p, Resolved* r) {
+    const int rc = resolve(p, r);
+    if (rc != SWR_OK) return rc;
+    if (r->pc) return SWR_ERR_UNSUPPORTED;   // per-channel decay: jagged window only
+    return SWR_OK;
+}
+
+// Pointers into the workspace for one launch.
+void exact_arrays(const swr_problem_t* p, const ExactWs& w, void* ws, float** v, float** carry, float** prod) {
+    float* f = (float*)ws;
+    const int64_t n = p->B * p->H * w.nr * p->D;
+    *v = f;
+    *carry = f + n;
+    *prod = f + 2 * n;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t swr_exact_workspace_bytes(const swr_problem_t* problem) {
+    Resolved r;
+    const int rc = resolve_exact(problem, &r);
+    if (rc != SWR_OK) return rc;
+    return exact_ws(problem, r).floats * 4;
+}
+
+int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                      const void* c, const float* h0, void* y, float* carriers, float* h_last,
+                      void* workspace, void* stream) {
+    Resolved r;
+    int rc = resolve_exact(p, &r);
+    if (rc != SWR_OK) return rc;
+    const ExactWs w = exact_ws(p, r);
+    const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
+    if (seqs == 0) return SWR_OK;
+    if (!r.empty && (!x || !a || !b || !c || !y)) return SWR_ERR_NULL;
+    if (w.floats > 0 && !workspace) return SWR_ERR_NULL;
+    for (const void* q : {(const void*)h0, (const void*)h_last, (const void*)carriers, (const void*)workspace})
+        if (q && !aligned(q, 16)) return SWR_ERR_ALIGN;
+    if (!r.empty) {
+        for (const void* q : {x, b, c, (const void*)y})
+            if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+        if (!aligned(a, r.es)) return SWR_ERR_ALIGN;
+        if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    }
+    const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es),
+                         span(h0, h0 ? sbytes : 0)};
+    const Span outs[4] = {span(y, r.xspan), span(carriers, carriers ? r.carriers * 4 : 0),
+                          span(h_last, h_last ? sbytes : 0), span(workspace, w.floats * 4)};
+    for (int i = 0; i < 4; ++i) {
+        for (const Span& s : ins)
+            if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
+    }
+
+    float *wv = nullptr, *wc = nullptr, *wp = nullptr;
+    if (w.floats > 0) exact_arrays(p, w, workspace, &wv, &wc, &wp);
+    swr::Params k = make_params(p, r, false);
+    k.x = x; k.a = a; k.b = b; k.c = c;
+    k.agg_v = wv; k.agg_p = wp; k.carry = wc;
+    // Stage I: local solves of every run, keeping each run's end state and decay product.
+    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, false, swr::kAggregate, stream) != hipSuccess)
+        return SWR_ERR_HIP;
+    // Stage II: the carrier recurrence over the runs, from h0; h_last is its final value.
+    swr::ScanParams q{};
+    q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = h0; q.fin = h_last;
+    q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 0;
+    if ((h_last || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
+    if (r.empty) return SWR_OK;
+    // Stage III: every run again from its exact entering state: outputs and exact block carriers.
+    k.y = y; k.carriers = carriers;
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, false, swr::kExact, stream) == hipSuccess ? SWR_OK
+                                                                                          : SWR_ERR_HIP;
+}
+
+int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                       const void* c, const void* dy, const float* h0, const float* carriers,
+                       const float* dh_last, void* dx, float* da, void* db, void* dc, float* dh0,
+                       void* workspace, void* stream) {
+    Resolved r;
+    int rc = resolve_exact(p, &r);
+    if (rc != SWR_OK) return rc;
+    const ExactWs w = exact_ws(p, r);
+    const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
+    if (seqs == 0) return SWR_OK;
+    if (!r.empty && (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc)) return SWR_ERR_NULL;
+    if (w.floats > 0 && !workspace) return SWR_ERR_NULL;
+    for (const void* q : {(const void*)h0, (const void*)dh_last, (const void*)dh0, (const void*)carriers,
+                          (const void*)workspace})
+        if (q && !aligned(q, 16)) return SWR_ERR_ALIGN;
+    if (!r.empty) {
+        for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
+            if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+        if (!aligned(a, r.es) || !aligned(da, 4)) return SWR_ERR_ALIGN;
+        if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    }
+    const Span ins[8] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
+                         span(a, r.aspan * r.es), span(carriers, carriers ? r.carriers * 4 : 0),
+                         span(h0, h0 ? sbytes : 0), span(dh_last, dh_last ? sbytes : 0)};
+    const Span outs[6] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan), span(da, r.aspan * 4),
+                          span(dh0, dh0 ? sbytes : 0), span(workspace, w.floats * 4)};
+    for (int i = 0; i < 6; ++i) {
+        for (const Span& s : ins)
+            if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
+        for (int j = i + 1; j < 6; ++j)
+            if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
+    }
+
+    float *wv = nullptr, *wc = nullptr, *wp = nullptr;
+    if (w.floats > 0) exact_arrays(p, w, workspace, &wv, &wc, &wp);
+    swr::Params k = make_params(p, r, true);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
+    k.agg_v = wv; k.agg_p = wp; k.carry = wc; k.h0 = h0;
+    // Stage I: reverse local solves of every run (from c, dy, a).
+    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.bwd, true, false, swr::kAggregate, stream) != hipSuccess)
+        return SWR_ERR_HIP;
+    // Stage II: the reverse carrier recurrence over the runs, from dh_last; dh0 is its final value.
+    swr::ScanParams q{};
+    q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = dh_last; q.fin = dh0;
+    q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 1;
+    if ((dh0 || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
+    if (r.empty) return SWR_OK;
+    // Stage III: the gradients, from the adjoint entering each run and the exact block carriers.
+    k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+    k.carriers = const_cast<float*>(carriers);
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, false, swr::kExact, stream) == hipSuccess ? SWR_OK
+                                                                                         : SWR_ERR_HIP;
 }
 
 }  // extern "C"

@@ -358,7 +358,7 @@ __device__ inline uint32_t xcd_remap(uint32_t id, uint32_t n) {
 }
 
 struct Work {
-    int64_t b, h, t_begin, t_end;
+    int64_t b, h, t_begin, t_end, run;
 };
 
 // A work item is (batch, group of HW consecutive heads, run); the host makes
@@ -374,6 +374,7 @@ __device__ inline Work decode_work(const Params& p, int hw) {
     const uint32_t rest = wid / G;
     const int64_t run = rest % nruns;
     wk.b = rest / nruns;
+    wk.run = run;
     wk.t_begin = run * p.run_len;
     wk.t_end = min(wk.t_begin + p.run_len, p.T);
     return wk;
@@ -439,8 +440,15 @@ __device__ inline Lanes lanes() {
 // i.e. longer contiguous stretches of the [B, T, H, D] tensors, together.
 // At least three waves per SIMD, so that the memory and compute phases of
 // several workgroups interleave on a compute unit.
-template <class IO, int CPL, int TW, int HW, bool FEAT>
+//
+// MODE selects what the sweep computes (swr_launch.h): the jagged window
+// (kSwr); or, for the exact recurrence, the runs' aggregates -- the end state
+// of each run started from zero and the run's decay product -- (kAggregate),
+// or the outputs from the exact state entering each run (kExact).  The exact
+// modes need no halo and never restart the carrier.
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
+    constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -463,8 +471,9 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     const int l = p.block;
     const int S = l / SB;              // sub-blocks per block (a power of two)
     const int smask = S - 1;
-    const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);  // first token read
-    const int64_t halo = wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
+    // First token read: the jagged window re-reads the block before the run.
+    const int64_t t_lo = SWR ? max(wk.t_begin - (int64_t)l, (int64_t)0) : wk.t_begin;
+    const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
     const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
     const char* xb = (const char*)p.x + xo;
@@ -476,13 +485,25 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     const int64_t as = p.sa_t * ES;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
-    const bool want_y = p.y != nullptr;            // false: only the block carriers are produced
-    float* const vb = p.carriers ? p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D : nullptr;
+    // false: only the block carriers (or the run aggregates) are produced
+    const bool want_y = MODE != kAggregate && p.y != nullptr;
+    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D
+                                                       : nullptr;
     const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
+    const int64_t slot = (wk.b * p.H + wk.h) * p.nruns + wk.run;   // this run's aggregate / carry
 
-    float e[CPL], s[CPL];   // carriers at the start of the step: full and block-restarted
+    // Carriers at the start of the step: e is the state the outputs use (the
+    // jagged-window state, or the exact state), s the block-restarted state.
+    float e[CPL], s[CPL];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
+    if constexpr (MODE == kExact) {   // the exact state entering the run (stage II's result)
+        Row<IoF32, CPL> ci;
+        ci.load(rsrc(p.carry + slot * D), (uint32_t)(n * CPL) * 4u);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) e[m] = ci.get(m);
+    }
+    float prod = 1.0f;   // kAggregate: decay product of the run so far
 
     // Sweep to the end of the run's last block: when the sequence ends inside a
     // block, the step holding that block's last sub-block still computes its
@@ -574,9 +595,11 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
         for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
 #pragma unroll 1
         for (int r = 0; r < TW; ++r) {      // the sub-blocks of this wave's head, in order
-            if (((ph + r) & smask) == 0) {   // a block starts: its carry-in is the previous block's v
+            if constexpr (SWR) {
+                if (((ph + r) & smask) == 0) {   // a block starts: its carry-in is the previous block's v
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+                    for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
+                }
             }
             if (r == tw) {
 #pragma unroll
@@ -584,19 +607,21 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             }
             const int src = hw * TW + r;
             const float cr_ = s_c[buf][src];
+            if constexpr (MODE == kAggregate) prod *= cr_;
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 const float wl = s_wl[buf][src][n * CPL + m];
                 e[m] = cr_ * e[m] + wl;
-                s[m] = cr_ * s[m] + wl;
+                if constexpr (SWR) s[m] = cr_ * s[m] + wl;
             }
             if (r == tw) {
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) vout[m] = s[m];
+                for (int m = 0; m < CPL; ++m) vout[m] = SWR ? s[m] : e[m];
             }
         }
         // The wave holding a block's last sub-block saves that block's carrier
-        // v_t (its block-restarted end state) for the backward.
+        // for the backward: v_t (the block-restarted end state) for the jagged
+        // window, the exact state at the block's end for the exact recurrence.
         if (vb && ((ph + tw) & smask) == smask) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;   // first token of the block (it may end past T)
@@ -618,6 +643,11 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             }
             store_row<IO, CPL>(ry, in_range(t >= wk.t_begin && t < wk.t_end, loff + (uint32_t)(r * rs)), yv);
         }
+    }
+    if constexpr (MODE == kAggregate) {   // the run's end state from zero, and its decay product
+        store_row<IoF32, CPL>(rsrc(p.agg_v + slot * D), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), e);
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, prod), rsrc(p.agg_p + slot),
+                                              (int)in_range(tw == 0 && lane == 0, 0u), 0, 0);
     }
 }
 
@@ -658,8 +688,14 @@ __device__ inline void build_decay_transposed(float a_n, int grp, int n, float (
 // saved by the forward pass (the paper's "checkpoint only the carrier").
 // Only the run's end needs a halo: the first block after the run (c, dy, a)
 // gives the reverse carrier entering it.  Nothing is read twice.
-template <class IO, int CPL, int TW, int HW, bool FEAT>
+//
+// MODE kExact gives the gradient of the exact recurrence instead: the adjoint
+// entering the run from its end is stage II's result (no halo), the state
+// entering each step is the previous block's exact carrier (or the initial
+// state), nothing restarts, and the decay gradient is sum_mu H_{k-1} du_k.
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
+    constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -705,10 +741,17 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     float eps[CPL], pr[CPL];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; }
+    const int64_t seq = wk.b * p.H + wk.h;
+    if constexpr (MODE == kExact) {   // the exact adjoint entering the run's end (stage II)
+        Row<IoF32, CPL> ci;
+        ci.load(rsrc(p.carry + (seq * p.nruns + wk.run) * D), (uint32_t)(n * CPL) * 4u);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) eps[m] = ci.get(m);
+    }
     int buf = 0;
 
     // ---- halo: the first block after the run -----------------------------------
-    if (wk.t_end < p.T) {
+    if (SWR && wk.t_end < p.T) {
         const int64_t r0 = wk.t_end + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
@@ -789,12 +832,19 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             ds_n = dsigmoid(a_n);
             a_n = r0 + n < wk.t_end ? sigmoid(a_n) : 0.0f;
         }
-        // Carrier of the block before this step (zero before the sequence start).
+        // Exact recurrence: past the end of the sequence the decay is 1, so
+        // the adjoint entering from the end reaches the last token intact.
+        if (MODE == kExact && r0 + n >= p.T) a_n = 1.0f;
+        // Carrier of the block before this step (zero before the sequence
+        // start, or the initial state for the exact recurrence).
         float vprev[CPL];
         {
             Row<IoF32, CPL> vr;
             const int64_t blk = (t0 >> p.lshift) - 1;
-            vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+            if (MODE == kExact && t0 == 0)
+                vr.load(rsrc(p.h0 + seq * D), in_range(p.h0 != nullptr, (uint32_t)(n * CPL) * 4u));
+            else
+                vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
         }
@@ -834,12 +884,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         // ---- forward carriers entering this wave's sub-block ---------------------------
         float ein[CPL], sin_[CPL];
         {
+            // Exact: e is the exact state (never restarted) and s is unused.
             float e[CPL], s[CPL];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
+            for (int m = 0; m < CPL; ++m) { e[m] = SWR ? 0.f : vprev[m]; s[m] = SWR ? vprev[m] : 0.f; }
 #pragma unroll 1
             for (int r = 0; r < tw; ++r) {
-                if ((r & smask) == 0) {
+                if (SWR && (r & smask) == 0) {
 #pragma unroll
                     for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
@@ -849,10 +900,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 for (int m = 0; m < CPL; ++m) {
                     const float wl = s_wl[buf][src][n * CPL + m];
                     e[m] = c_ * e[m] + wl;
-                    s[m] = c_ * s[m] + wl;
+                    if constexpr (SWR) s[m] = c_ * s[m] + wl;
                 }
             }
-            if ((tw & smask) == 0) {
+            if (SWR && (tw & smask) == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -864,7 +915,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         float epsin[CPL], kd = 0.f;
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
-            if ((r & smask) == smask) {
+            if (SWR && (r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
@@ -872,7 +923,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     epsin[m] = eps[m];
-                    kd += (ein[m] - sin_[m]) * (eps[m] - pr[m]);
+                    if constexpr (SWR) kd += (ein[m] - sin_[m]) * (eps[m] - pr[m]);
                 }
             }
             const int src = hw * TW + r;
@@ -881,7 +932,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float df = s_df[buf][src][n * CPL + m];
                 eps[m] = c_ * eps[m] + df;
-                pr[m] = c_ * pr[m] + df;
+                if constexpr (SWR) pr[m] = c_ * pr[m] + df;
             }
         }
 
@@ -911,7 +962,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         for (int r = 0; r < 4; ++r) {
             const int64_t t = tr0 + r;
             float vdx[CPL], vdb[CPL], vdc[CPL];
-            float acc = -Gsh[r] * Rr[r] * kd;
+            float acc = SWR ? -Gsh[r] * Rr[r] * kd : 0.0f;
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 const float dyv = dyr[r].get(m);
@@ -934,6 +985,117 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, 0);
         }
     }
+}
+
+// Stage I of the exact recurrence's backward: for every run, the adjoint that
+// leaves its first token towards the previous one when nothing enters from
+// the run's end (the reverse local solve D = L^T dh of the whole run, dh =
+// c * dy, scaled by the first token's decay), and the run's decay product.
+// Only c, dy and a are read.  Past the end of the sequence the decay is 1.
+template <class IO, int CPL, int TW, bool FEAT>
+__global__ __launch_bounds__(TW * 64, 2) void swr_bwd_agg_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0;
+    constexpr int D = CPL * SB;
+    constexpr int STEP = TW * SB;
+    constexpr int ES = IO::ES;
+    using R_ = Row<IO, CPL>;
+    __shared__ float s_df[2][TW][D];   // a_0 * first row of each sub-block's L^T dh
+    __shared__ float s_c[2][TW];       // decay product of each sub-block
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    const Work wk = decode_work<1>(p, 0);
+    const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    const char* cb = (const char*)p.c + xo;
+    const char* dyb = (const char*)p.dy + xo;
+    const char* ab = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * ES;
+    const int64_t rs = p.sx_t * ES;
+    const int64_t as = p.sa_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const int64_t slot = (wk.b * p.H + wk.h) * p.nruns + wk.run;
+
+    float eps[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) eps[m] = 0.f;
+    float prod = 1.0f;
+    int buf = 0;
+    const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
+        const int64_t r0 = wk.t_begin + k * STEP + tw * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+        R_ cr[4], dyr[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+            cr[r].load(rc, o);
+            dyr[r].load(rdy, o);
+        }
+        float a_n = load_scalar<IO>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+        if (sig_a) a_n = sigmoid(a_n);
+        if (r0 + n >= p.T) a_n = 1.0f;
+        float LT[4];
+        build_decay_transposed(a_n, grp, n, LT);
+        const typename Contract<IO>::A At = Contract<IO>::prep(LT);
+        const float a0 = shfl(a_n, 0);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            float dh[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) dh[q] = dyr[q].get(m) * cr[q].get(m);
+            const f32x4 Dn = Contract<IO>::run(At, dh);
+            if (grp == 0) s_df[buf][tw][n * CPL + m] = a0 * Dn[0];
+        }
+        const float cq = shfl(row_prefix_prod(a_n), 15);
+        if (lane == 0) s_c[buf][tw] = cq;
+        __syncthreads();
+#pragma unroll 1
+        for (int r = TW - 1; r >= 0; --r) {
+            const float c_ = s_c[buf][r];
+            prod *= c_;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) eps[m] = c_ * eps[m] + s_df[buf][r][n * CPL + m];
+        }
+    }
+    store_row<IoF32, CPL>(rsrc(p.agg_v + slot * D), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), eps);
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, prod), rsrc(p.agg_p + slot),
+                                          (int)in_range(tw == 0 && lane == 0, 0u), 0, 0);
+}
+
+// Stage II of the exact recurrence: the carrier recurrence over the runs of
+// one sequence (Alg. "Hierarchical Block Parallel Inference", global carrier
+// solve, here at run granularity), one thread per (sequence, channel).  The
+// runs' aggregates are loaded eight at a time ahead of the dependent chain.
+__global__ __launch_bounds__(256) void swr_scan_kernel(ScanParams q) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= q.seqs * q.D) return;
+    const int64_t seq = idx / q.D, ch = idx - seq * q.D;
+    const float* v = q.agg_v + seq * q.nruns * q.D + ch;
+    const float* pp = q.agg_p + seq * q.nruns;
+    float* cy = q.carry + seq * q.nruns * q.D + ch;
+    float S = q.init ? q.init[idx] : 0.0f;
+    constexpr int G = 8;
+    for (int64_t r0 = 0; r0 < q.nruns; r0 += G) {
+        float vv[G], pv[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int64_t j = r0 + g;
+            const int64_t r = q.reverse ? q.nruns - 1 - j : j;
+            vv[g] = j < q.nruns ? v[r * q.D] : 0.0f;
+            pv[g] = j < q.nruns ? pp[r] : 1.0f;
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int64_t j = r0 + g;
+            if (j < q.nruns) {
+                const int64_t r = q.reverse ? q.nruns - 1 - j : j;
+                cy[r * q.D] = S;
+                S = pv[g] * S + vv[g];
+            }
+        }
+    }
+    if (q.fin) q.fin[idx] = S;
 }
 
 // ---------------------------------------------------------------------------
@@ -1449,35 +1611,49 @@ static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hip
     return hipGetLastError();
 }
 
-template <class IO, int CPL, bool FEAT>
+template <class IO, int CPL, bool FEAT, int MODE>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
+#define SWR_LAUNCH(KERNEL, TW_, HW_)                                                                \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                          \
+        hipLaunchKernelGGL((KERNEL), grid, dim3(TW_ * HW_ * 64), 0, stream, p);
     if (backward) {
-#define SWR_BWD(TW_, HW_)                                                                      \
-    else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
-        hipLaunchKernelGGL((swr_bwd_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
-                           stream, p);
-        if (false) {}
-        SWR_BWD(8, 1) SWR_BWD(4, 1)
-        else return hipErrorInvalidValue;
-#undef SWR_BWD
+        if constexpr (MODE == kAggregate) {
+            if (false) {}
+            SWR_LAUNCH((swr_bwd_agg_kernel<IO, CPL, 8, FEAT>), 8, 1)
+            SWR_LAUNCH((swr_bwd_agg_kernel<IO, CPL, 4, FEAT>), 4, 1)
+            else return hipErrorInvalidValue;
+        } else {
+            if (false) {}
+            SWR_LAUNCH((swr_bwd_kernel<IO, CPL, 8, 1, FEAT, MODE>), 8, 1)
+            SWR_LAUNCH((swr_bwd_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
+            else return hipErrorInvalidValue;
+        }
     } else {
-#define SWR_FWD(TW_, HW_)                                                                      \
-    else if (sh.tw == TW_ && sh.hw == HW_)                                                     \
-        hipLaunchKernelGGL((swr_fwd_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
-                           stream, p);
         if (false) {}
-        SWR_FWD(4, 1) SWR_FWD(2, 2)
+        SWR_LAUNCH((swr_fwd_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
+        SWR_LAUNCH((swr_fwd_kernel<IO, CPL, 2, 2, FEAT, MODE>), 2, 2)
         else return hipErrorInvalidValue;
-#undef SWR_FWD
     }
+#undef SWR_LAUNCH
     return hipGetLastError();
+}
+
+template <class IO, int CPL, bool FEAT>
+static hipError_t launch_mode(const Params& p, const Shape& sh, bool backward, int mode, hipStream_t stream) {
+    switch (mode) {
+        case kSwr: return launch_shape<IO, CPL, FEAT, kSwr>(p, sh, backward, stream);
+        case kAggregate: return launch_shape<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
+        case kExact: return launch_shape<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <class IO, bool FEAT>
 static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
-                             hipStream_t stream) {
+                             int mode, hipStream_t stream) {
     if (per_channel) {
+        if (mode != kSwr) return hipErrorInvalidValue;
         switch (D) {   // channels of a virtual head (at most 64)
             case 16: return launch_pc<IO, 1, FEAT>(p, sh, backward, stream);
             case 32: return launch_pc<IO, 2, FEAT>(p, sh, backward, stream);
@@ -1486,10 +1662,10 @@ static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backw
         }
     }
     switch (D) {
-        case 16: return launch_shape<IO, 1, FEAT>(p, sh, backward, stream);
-        case 32: return launch_shape<IO, 2, FEAT>(p, sh, backward, stream);
-        case 64: return launch_shape<IO, 4, FEAT>(p, sh, backward, stream);
-        case 128: return launch_shape<IO, 8, FEAT>(p, sh, backward, stream);
+        case 16: return launch_mode<IO, 1, FEAT>(p, sh, backward, mode, stream);
+        case 32: return launch_mode<IO, 2, FEAT>(p, sh, backward, mode, stream);
+        case 64: return launch_mode<IO, 4, FEAT>(p, sh, backward, mode, stream);
+        case 128: return launch_mode<IO, 8, FEAT>(p, sh, backward, mode, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1498,16 +1674,23 @@ static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backw
 // plain path carries none of its registers.
 template <class IO>
 static hipError_t launch_feat(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
-                              hipStream_t stream) {
-    if (p.sig_a || p.sig_b) return launch_cpl<IO, true>(p, D, sh, backward, per_channel, stream);
-    return launch_cpl<IO, false>(p, D, sh, backward, per_channel, stream);
+                              int mode, hipStream_t stream) {
+    if (p.sig_a || p.sig_b) return launch_cpl<IO, true>(p, D, sh, backward, per_channel, mode, stream);
+    return launch_cpl<IO, false>(p, D, sh, backward, per_channel, mode, stream);
 }
 
 hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, bool per_channel,
-                  void* stream) {
+                  int mode, void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, st);
-    return launch_feat<IoF32>(p, D, sh, backward, per_channel, st);
+    if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, mode, st);
+    return launch_feat<IoF32>(p, D, sh, backward, per_channel, mode, st);
+}
+
+hipError_t launch_scan(const ScanParams& q, void* stream) {
+    const int64_t n = q.seqs * q.D;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(swr_scan_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream, q);
+    return hipGetLastError();
 }
 
 }  // namespace swr

@@ -36,6 +36,38 @@ struct Params {
     int64_t nruns;      // runs per (batch, head) sequence
     int64_t nwork;      // B * H * nruns workgroups
     int64_t nblocks;    // ceil(T / block): carriers per (batch, head)
+    // Exact (untruncated) recurrence, computed in three stages (local solves
+    // with run aggregates, a carrier scan over runs, reconstruction); the
+    // arrays live in the caller's workspace.
+    float* agg_v;       // [B*H][nruns][D]: each run's end state started from zero (stage I out)
+    float* agg_p;       // [B*H][nruns]: each run's decay product (stage I out)
+    const float* carry; // [B*H][nruns][D]: the state entering each run (stage III in); for the
+                        // backward, the adjoint entering each run from its end
+    const float* h0;    // [B][H][D] initial state (backward stage III), or NULL for zero
+};
+
+// What a forward or backward launch computes.
+enum Mode {
+    kSwr = 0,        // the jagged-window (truncated) recurrence
+    kAggregate = 1,  // exact, stage I: run aggregates only (no outputs)
+    kExact = 2,      // exact, stage III: outputs from the carry entering each run
+};
+
+// Stage II of the exact recurrence: for every (batch, head) and channel, the
+// carrier recurrence over a sequence's runs, S_r = P_r S_{r-1} + V_r forward
+// (reverse == 0) or S_r = P_r S_{r+1} + V_r backward, from `init` (or 0);
+// carry[r] receives the value entering run r and `fin` (if not NULL) the
+// value after the last run.
+struct ScanParams {
+    const float* agg_v;
+    const float* agg_p;
+    float* carry;
+    const float* init;  // [B*H][D] or NULL
+    float* fin;         // [B*H][D] or NULL
+    int64_t seqs;       // B * H
+    int64_t nruns;
+    int32_t D;
+    int32_t reverse;
 };
 
 // Workgroup shape: tw waves per head along the tokens (a step is tw * 16
@@ -64,6 +96,8 @@ inline int pc_hshift(int64_t D) { return D > 64 ? 1 : 0; }
 // Launches the forward or backward kernel for (dtype, D, shape) on `stream`;
 // for the per-channel kernels D is the channel count of a virtual head.
 hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool backward, bool per_channel,
-                  void* stream);
+                  int mode, void* stream);
+
+hipError_t launch_scan(const ScanParams& q, void* stream);
 
 }  // namespace swr

@@ -236,3 +236,62 @@ def test_non_contiguous_layouts_accepted():
     B, T, H, D = 2, 256, 4, 64
     p = problem(B=B, T=T, H=H, D=D, x_strides=(H * T * D, D, T * D), a_strides=(H * T, 1, T))
     assert swr.swr_launch_info(p)["fwd_run_len"] > 0
+
+
+# ----------------------------------------------------------------------------- exact recurrence
+
+H0, HL, WS, DH0, DHL = (GB * (i + 20) for i in range(5))
+
+
+def xfwd(p, x=X, a=A, b=B_, c=C, h0=H0, y=Y, v_=V, hl=HL, ws=WS):
+    v = ctypes.c_void_p
+    return swr.load().swr_exact_forward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(h0), v(y), v(v_),
+                                        v(hl), v(ws), None)
+
+
+def xbwd(p, x=X, a=A, b=B_, c=C, dy=DY, h0=H0, v_=V, dhl=DHL, dx=DX, da=DA, db=DB, dc=DC, dh0=DH0, ws=WS):
+    v = ctypes.c_void_p
+    return swr.load().swr_exact_backward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(dy), v(h0), v(v_),
+                                         v(dhl), v(dx), v(da), v(db), v(dc), v(dh0), v(ws), None)
+
+
+def test_exact_workspace_bytes():
+    p = problem(B=8, T=16384, H=16, D=128, block=128)
+    info = swr.swr_launch_info(p)
+    nr = max(-(-16384 // info["fwd_run_len"]), -(-16384 // info["bwd_run_len"]))
+    # per (batch, head) and run: aggregate end state, entering state (D each), decay product
+    assert swr.swr_exact_workspace_bytes(p) == 8 * 16 * nr * (2 * 128 + 1) * 4
+    assert swr.swr_exact_workspace_bytes(problem(T=0)) == 0
+    lib = swr.load()
+    assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(per_channel=True))) == E_UNSUP
+    assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(block=48))) == E_BLOCK
+
+
+def test_exact_validation():
+    p = problem()
+    assert xfwd(problem(per_channel=True)) == E_UNSUP and xbwd(problem(per_channel=True)) == E_UNSUP
+    assert xfwd(problem(D=48)) == E_UNSUP and xbwd(problem(block=48)) == E_BLOCK
+    for kw in ("x", "a", "b", "c", "y", "ws"):
+        assert xfwd(p, **{kw: 0}) == E_NULL, kw
+    for kw in ("x", "a", "b", "c", "dy", "v_", "dx", "da", "db", "dc", "ws"):
+        assert xbwd(p, **{kw: 0}) == E_NULL, kw
+    # states and workspace: 16-byte aligned
+    for kw in ("h0", "hl", "v_", "ws"):
+        assert xfwd(p, **{kw: GB * 40 + 8}) == E_ALIGN, kw
+    for kw in ("h0", "dhl", "dh0", "v_", "ws"):
+        assert xbwd(p, **{kw: GB * 40 + 8}) == E_ALIGN, kw
+    assert xfwd(p, x=X + 4) == E_ALIGN and xbwd(p, dx=DX + 2) == E_ALIGN
+    # outputs and the workspace must not overlap inputs or each other
+    assert xfwd(p, hl=H0) == E_ALIAS
+    assert xfwd(p, ws=X) == E_ALIAS
+    assert xfwd(p, ws=Y + 64) == E_ALIAS
+    assert xfwd(p, hl=V) == E_ALIAS
+    assert xbwd(p, dh0=H0) == E_ALIAS
+    assert xbwd(p, dh0=DHL) == E_ALIAS
+    assert xbwd(p, ws=V) == E_ALIAS
+    assert xbwd(p, ws=DA) == E_ALIAS
+    assert xbwd(p, dx=DH0) == E_ALIAS
+    # nothing to do for an empty batch or head set, even with NULL pointers
+    for kw in (dict(B=0), dict(H=0)):
+        assert xfwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
+        assert xbwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK

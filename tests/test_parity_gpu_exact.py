@@ -1,0 +1,224 @@
+"""GPU parity of the exact (untruncated) recurrence -- the three-stage
+hierarchical algorithm (Alg. "Hierarchical Block Parallel Inference") behind
+swr_exact_forward / swr_exact_backward -- against the oracle's exact loop on
+the same seeded, rounded inputs, with initial states and final-state
+gradients."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from parity import assert_close, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def swr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2512_13921_amd as lib
+    lib.load()
+    return lib
+
+
+def _state(rng, cfg, scale=1.0):
+    return (scale * rng.standard_normal((cfg.B, cfg.H, cfg.D))).astype(np.float32)
+
+
+def _exact_states(prob, h0, **feat):
+    """h at every token (float64 oracle run with c = 1), [B, T, H, D]."""
+    ones = np.ones_like(prob.c, dtype=np.float64)
+    h, _ = oracle.exact_forward(prob.x, prob.a, prob.b, ones, h0, **feat)
+    return h
+
+
+def _block_end_states(prob, h):
+    cfg = prob.cfg
+    nb = -(-cfg.T // cfg.block)
+    ends = [min((t + 1) * cfg.block, cfg.T) - 1 for t in range(nb)]
+    return np.transpose(h[:, ends], (0, 2, 1, 3))          # [B, H, nb, D]
+
+
+def run_exact(swr, prob, h0, dh_last, residual=False, run_len=0, backward=True, **feat):
+    cfg = prob.cfg
+    dt = cfg.dtype
+    x, a, b, c = (to_device(getattr(prob, n), dt) for n in "xabc")
+    h0_t = None if h0 is None else torch.from_numpy(h0).cuda()
+    dhl_t = None if dh_last is None else torch.from_numpy(dh_last).cuda()
+    y, v, hl = swr.swr_exact_forward(x, a, b, c, cfg.block, h0=h0_t, residual=residual, save_carriers=True,
+                                     want_h_last=True, run_len=run_len, **feat)
+    grads = None
+    if backward:
+        dy = to_device(prob.dy, dt)
+        grads = swr.swr_exact_backward(x, a, b, c, dy, v, cfg.block, h0=h0_t, dh_last=dhl_t,
+                                       residual=residual, want_dh0=True, run_len=run_len, **feat)
+    torch.cuda.synchronize()
+    return y, v, hl, grads
+
+
+def check_exact(prob, h0, dh_last, y, v, hl, grads, residual=False, what="", **feat):
+    cfg = prob.cfg
+    ref_y, ref_hl = oracle.exact_forward(prob.x, prob.a, prob.b, prob.c, h0, residual, **feat)
+    assert_close(to_host(y), ref_y, cfg.dtype, what + " y")
+    # The final state and the block carriers are float32 on every path.
+    assert_close(to_host(hl), ref_hl, "bf16" if cfg.dtype == "bf16" else "f32", what + " h_last")
+    ref_v = _block_end_states(prob, _exact_states(prob, h0, **feat))
+    assert_close(to_host(v), ref_v, cfg.dtype, what + " carriers")
+    if grads is not None:
+        ref = oracle.exact_backward(prob.x, prob.a, prob.b, prob.c, prob.dy, h0, dh_last, residual, **feat)
+        for name, g, r in zip(("dx", "da", "db", "dc", "dh0"), grads, ref):
+            assert_close(to_host(g), r, cfg.dtype, f"{what} {name}")
+
+
+SMALL = [
+    # (B, T, H, D, block, dtype)
+    (1, 64, 1, 16, 16, "f32"),
+    (2, 1000, 3, 64, 64, "f32"),
+    (1, 333, 2, 128, 128, "f32"),
+    (2, 517, 2, 32, 32, "f32"),
+    (2, 1000, 3, 64, 64, "bf16"),
+    (1, 777, 2, 128, 128, "bf16"),
+    (2, 300, 2, 16, 16, "bf16"),
+    (1, 1, 1, 64, 64, "bf16"),      # a single token: the recurrent decoding step
+    (1, 17, 1, 128, 128, "bf16"),
+    (2, 700, 4, 64, 64, "bf16"),
+    (3, 300, 6, 128, 32, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype", SMALL)
+@pytest.mark.parametrize("run_len", [0, "min"])
+def test_exact_small_against_oracle(swr, B, T, H, D, block, dtype, run_len):
+    rl = max(64, block) if run_len == "min" else 0    # "min": many runs, a long carrier chain
+    prob = W.random_problem(31 + T + D, B, T, H, D, block, dtype, "sigmoid", 2.0)
+    rng = np.random.default_rng(T)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    _say(f"[exact] B={B} T={T} H={H} D={D} l={block} {dtype} run_len={rl}")
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl, run_len=rl)
+    check_exact(prob, h0, dhl, y, v, hl, grads, what=f"exact {B}x{T}x{H}x{D} l{block} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_without_states(swr, dtype):
+    prob = W.random_problem(41, 2, 640, 2, 64, 64, dtype, "sigmoid", 3.0)
+    y, v, hl, grads = run_exact(swr, prob, None, None, run_len=64)
+    check_exact(prob, None, None, y, v, hl, grads, what="no h0")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_residual_and_featurisation(swr, dtype):
+    prob = W.random_problem(42, 2, 400, 2, 128, 64, dtype, "sigmoid", 3.0, logits=True)
+    rng = np.random.default_rng(1)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl, residual=True, run_len=64, **feat)
+    check_exact(prob, h0, dhl, y, v, hl, grads, residual=True, what="residual+sigmoid", **feat)
+
+
+@pytest.mark.parametrize("value", [0.0, 1.0])
+def test_exact_decay_closed_forms(swr, value):
+    # a == 0: y = c*b*x (h0 forgotten at once); a == 1: a running sum from h0.
+    prob = W.random_problem(43, 1, 300, 2, 64, 64, "f32")
+    prob.a[...] = value
+    rng = np.random.default_rng(2)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl, run_len=64)
+    check_exact(prob, h0, dhl, y, v, hl, grads, what=f"a={value}")
+
+
+def test_exact_equals_jagged_window_on_two_blocks(swr):
+    # T <= 2l: the window truncation drops nothing, so both paths agree.
+    prob = W.random_problem(44, 2, 256, 2, 128, 128, "f32")
+    x, a, b, c, dy = (to_device(getattr(prob, n), "f32") for n in ("x", "a", "b", "c", "dy"))
+    y_ex, v_ex = swr.swr_exact_forward(x, a, b, c, 128, save_carriers=True)
+    y_sw, v_sw = swr.swr_forward(x, a, b, c, 128, save_carriers=True)
+    g_ex = swr.swr_exact_backward(x, a, b, c, dy, v_ex, 128)
+    g_sw = swr.swr_backward(x, a, b, c, dy, v_sw, 128)
+    torch.cuda.synchronize()
+    assert_close(to_host(y_ex), to_host(y_sw).astype(np.float64), "f32", "exact vs window y")
+    for name, ge, gs in zip(("dx", "da", "db", "dc"), g_ex, g_sw):
+        assert_close(to_host(ge), to_host(gs), "f32", "exact vs window " + name)
+
+
+def test_exact_chunked_equals_one_pass(swr):
+    # Processing the sequence in pieces, passing h_last on as h0, is the same
+    # computation as one pass (recurrent prefill / decoding).
+    prob = W.random_problem(45, 2, 1000, 2, 64, 64, "f32", "sigmoid", 3.0)
+    x, a, b, c = (to_device(getattr(prob, n), "f32") for n in "xabc")
+    y_full = swr.swr_exact_forward(x, a, b, c, 64)
+    h = None
+    parts = []
+    for lo, hi in ((0, 333), (333, 334), (334, 640), (640, 1000)):
+        sl = slice(lo, hi)
+        yp, h = swr.swr_exact_forward(x[:, sl], a[:, sl], b[:, sl], c[:, sl], 64, h0=h, want_h_last=True)
+        parts.append(yp)
+    torch.cuda.synchronize()
+    assert_close(to_host(torch.cat(parts, dim=1)), to_host(y_full), "f32", "chunked")
+
+
+def test_exact_empty_sequence_passes_states(swr):
+    x = torch.empty((2, 0, 3, 64), dtype=torch.bfloat16, device="cuda")
+    a = torch.empty((2, 0, 3), dtype=torch.bfloat16, device="cuda")
+    h0 = torch.randn(2, 3, 64, device="cuda")
+    dhl = torch.randn(2, 3, 64, device="cuda")
+    y, v, hl = swr.swr_exact_forward(x, a, x, x, 64, h0=h0, save_carriers=True, want_h_last=True)
+    *_, dh0 = swr.swr_exact_backward(x, a, x, x, x, v, 64, h0=h0, dh_last=dhl, want_dh0=True)
+    torch.cuda.synchronize()
+    assert torch.equal(hl, h0) and torch.equal(dh0, dhl)
+    _, hz = swr.swr_exact_forward(x, a, x, x, 64, want_h_last=True)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(hz) == 0
+
+
+def test_exact_deterministic(swr):
+    prob = W.random_problem(46, 2, 2048, 4, 128, 128, "bf16")
+    rng = np.random.default_rng(3)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    r1 = run_exact(swr, prob, h0, dhl)
+    r2 = run_exact(swr, prob, h0, dhl)
+    for t1, t2 in zip(r1[:3] + tuple(r1[3]), r2[:3] + tuple(r2[3])):
+        assert torch.equal(t1, t2)
+
+
+@pytest.mark.parametrize("cid", [3, 4])
+def test_exact_full_size_sampled(swr, cid):
+    """Full-size exact forward and backward in the default launch
+    configuration; whole (batch, head) slices compared with the oracle."""
+    cfg = W.CONFIGS[cid]
+    _say(f"[exact config {cid}] {cfg.name}: generating inputs")
+    prob = W.generate(cfg)
+    rng = np.random.default_rng(cid)
+    h0, dhl = _state(rng, cfg), _state(rng, cfg)
+    _say(f"[exact config {cid}] running on the GPU")
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl)
+    picks = sorted({(0, 0), (cfg.B - 1, cfg.H - 1), (cfg.B // 2, cfg.H // 3)})
+    bi = np.array([p[0] for p in picks])
+    hi = np.array([p[1] for p in picks])
+
+    def take(t):
+        return np.ascontiguousarray(np.asarray(t)[bi, :, hi])
+
+    xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
+    h0s, dhls = h0[bi, hi], dhl[bi, hi]
+    _say(f"[exact config {cid}] oracle on {len(picks)} slices")
+    ref_y, ref_hl = oracle.exact_forward_slices(xs, as_, bs, cs, h0s)
+    ref = oracle.exact_backward_slices(xs, as_, bs, cs, dys, h0s, dhls)
+    assert_close(np.stack([to_host(y[b_, :, h_]) for b_, h_ in picks]), ref_y, cfg.dtype, "exact y")
+    assert_close(np.stack([to_host(hl[b_, h_]) for b_, h_ in picks]), ref_hl, cfg.dtype, "exact h_last")
+    for name, g, r in zip(("dx", "da", "db", "dc"), grads[:4], ref[:4]):
+        got = np.stack([to_host(g[b_, :, h_]) for b_, h_ in picks])
+        st = assert_close(got, r, cfg.dtype, f"exact config {cid} {name}")
+        _say(f"[exact config {cid}] {name}: {st}")
+    assert_close(np.stack([to_host(grads[4][b_, h_]) for b_, h_ in picks]), ref[4], cfg.dtype, "exact dh0")
+    for t in (y, v, hl) + tuple(grads):
+        assert torch.isfinite(t.float()).all()
