@@ -10,6 +10,9 @@ the whole workload, inputs already resident in HBM.  Prints ONE JSON line.
 [B, T, H, D]) on the same workload shape instead of the shared decay.
 --sigmoid feeds a and b as logits through the kernels' fused sigmoid (the
 Phalanx featurisation); a's logits are then drawn N(3, 1).
+--recurrence exact times the exact (untruncated) recurrence instead of the
+jagged window: swr_exact_forward / swr_exact_backward, three launches each
+(run aggregates, carrier scan, reconstruction), timed as a whole.
 
 Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
 durations come from HIP events recorded on the stream the kernels run on.
@@ -102,7 +105,7 @@ def to_device(arr, dtype):
     return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
 
 
-def cpu_baseline(cfg, prob, budget_s=10.0):
+def cpu_baseline(cfg, prob, budget_s=10.0, exact=False):
     """Oracle throughput on whole (batch, head) slices of the workload, in
     tokens/s of the full job (a token carries all H heads).  Slices are taken
     in a fixed shuffled order and revisited until about budget_s seconds of
@@ -125,8 +128,12 @@ def cpu_baseline(cfg, prob, budget_s=10.0):
         t0 = time.perf_counter()
         if cfg.logits:     # the featurisation is part of the timed work
             as_, bs = oracle.sigmoid(as_), oracle.sigmoid(bs)
-        oracle.forward_slices(xs, as_, bs, cs, cfg.block)
-        oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
+        if exact:
+            oracle.exact_forward_slices(xs, as_, bs, cs)
+            oracle.exact_backward_slices(xs, as_, bs, cs, dys)
+        else:
+            oracle.forward_slices(xs, as_, bs, cs, cfg.block)
+            oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
         elapsed += time.perf_counter() - t0
         done += len(idx)
         pos += len(idx)
@@ -155,6 +162,8 @@ def main():
                     help="one decay per token and head (default) or per token, head and channel")
     ap.add_argument("--sigmoid", action="store_true",
                     help="a and b are logits; the kernels apply the sigmoid (fused featurisation)")
+    ap.add_argument("--recurrence", choices=("window", "exact"), default="window",
+                    help="the jagged-window recurrence (default) or the exact, untruncated one")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -177,6 +186,12 @@ def main():
         cfg = cfg.with_(name=cfg.name + "_sigmoid", logits=True, a_kind="sigmoid",
                         a_mu=cfg.a_mu if cfg.a_kind == "sigmoid" else 3.0)
     feat = dict(sigmoid_decay=args.sigmoid, sigmoid_pregate=args.sigmoid)
+    exact = args.recurrence == "exact"
+    if exact:
+        if cfg.per_channel:
+            print("the exact recurrence is built for the per-head decay only", file=sys.stderr)
+            return 2
+        cfg = cfg.with_(name=cfg.name + "_exact")
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -187,16 +202,29 @@ def main():
     da = torch.empty(a.shape, dtype=torch.float32, device=a.device)   # a's shape, contiguous
     carriers = torch.empty(swr.carrier_shape(x, cfg.block), dtype=torch.float32, device=x.device)
     stream = torch.cuda.current_stream()
+    if exact:
+        wsp = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
+                               x.stride()[:3], a.stride()[:3], False, args.run_len)
+        workspace = torch.empty(max(swr.swr_exact_workspace_bytes(wsp) // 4, 1), dtype=torch.float32,
+                                device=x.device)
     torch.cuda.synchronize()
 
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
+        if exact:
+            swr.swr_exact_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, workspace=workspace,
+                                  run_len=args.run_len, **feat)
+        else:
+            swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
         if ev is not None:
             ev[1].record(stream)
-        swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
-                         run_len=args.run_len, **feat)
+        if exact:
+            swr.swr_exact_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
+                                   workspace=workspace, run_len=args.run_len, **feat)
+        else:
+            swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
+                             run_len=args.run_len, **feat)
         if ev is not None:
             ev[2].record(stream)
 
@@ -227,7 +255,13 @@ def main():
     dom_gbs = b_gbs if dominant_bwd else f_gbs
     pc = "_pc" if cfg.per_channel else ""
     dom_kernel = f"swr_bwd{pc}_kernel" if dominant_bwd else f"swr_fwd{pc}_kernel"
-    traffic = recorded_traffic(dom_kernel, cfg.name)
+    # The exact recurrence's passes are three launches each; their time is
+    # taken as a whole and no single kernel's counters stand for it.
+    traffic = None if exact else recorded_traffic(dom_kernel, cfg.name)
+    if exact:
+        dom_kernel = ("swr_exact_backward (swr_bwd_agg_kernel + swr_scan_kernel + swr_bwd_kernel)"
+                      if dominant_bwd else
+                      "swr_exact_forward (swr_fwd_kernel aggregate + swr_scan_kernel + swr_fwd_kernel)")
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
 
     def mfma_rate(backward, ms):
@@ -267,6 +301,7 @@ def main():
         "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
                    "block": cfg.block, "decay": "per channel" if cfg.per_channel else "per head",
                    "featurisation": "fused sigmoid of a and b" if args.sigmoid else "none",
+                   "recurrence": "exact (untruncated)" if exact else "jagged window",
                    "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {
@@ -298,7 +333,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(cfg, prob)
+        out["cpu_baseline"] = cpu_baseline(cfg, prob, exact=exact)
     print(json.dumps(out), flush=True)
     return 0
 
