@@ -52,6 +52,8 @@ def _load():
             nptr = 6 if name.endswith("forward") else 12
             fn.argtypes = lead + [i64, i64, ci, ci] + [dp] * nptr
             fn.restype = ci
+        lib.swr_oracle_step.argtypes = [i64, i64, i64, i64, i64, ci, ci] + [dp] * 6
+        lib.swr_oracle_step.restype = ci
         lib.swr_oracle_max_threads.restype = ci
         _lib = lib
     return _lib
@@ -233,3 +235,35 @@ def exact_backward(x, a, b, c, dy, h0=None, dh_last=None, residual=False,
     if sigmoid_pregate:
         db = db * dsigmoid(b)
     return dx, da, db, dc, outs[4].reshape(B, H, D)
+
+
+# ----------------------------------------------------------------------------
+# Recurrent form of the jagged window (decoding with a carried state)
+# ----------------------------------------------------------------------------
+
+def step_slices(x, a, b, c, state, t0, block, residual=False):
+    """K tokens at positions t0 .. t0+K-1 of independent slices: x, b, c are
+    [S, K, D]; a is [S, K] or [S, K, D]; state is [S, 2, D] (e, s after token
+    t0-1).  Returns (y, new_state)."""
+    lib = _load()
+    x, a, b, c = _c64(x), _c64(a), _c64(b), _c64(c)
+    S, K, D = x.shape
+    st = np.array(state, dtype=np.float64, copy=True).reshape(S, 2, D)
+    y = np.empty((S, K, D), np.float64)
+    rc = lib.swr_oracle_step(S, K, D, int(block), int(t0), int(a.ndim == 3), RESIDUAL if residual else 0,
+                             _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(st), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle step rejected its arguments")
+    return y, st
+
+
+def step(x, a, b, c, state, t0, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """Recurrent jagged-window step for [B, K, H, D] tensors (a: [B, K, H] or
+    [B, K, H, D]) with state [B, H, 2, D] (None: zeros, i.e. t0 = 0).
+    Returns (y, new_state)."""
+    B, K, H, D = np.shape(x)
+    a = sigmoid(a) if sigmoid_decay else a
+    b = sigmoid(b) if sigmoid_pregate else b
+    st = np.zeros((B * H, 2, D)) if state is None else np.asarray(state, np.float64).reshape(B * H, 2, D)
+    y, st = step_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c), st, t0, block, residual)
+    return _from_slices(y, B, H), st.reshape(B, H, 2, D)

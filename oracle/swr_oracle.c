@@ -252,6 +252,50 @@ int swr_oracle_exact_backward(int64_t S, int64_t T, int64_t D, int a_per_channel
     return err ? -1 : 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Recurrent form of the jagged window (two states per channel).            */
+/* ------------------------------------------------------------------------ */
+
+int swr_oracle_step_slice(int64_t K, int64_t D, int64_t block, int64_t t0, int a_per_channel,
+                          int flags, const double* x, const double* a, const double* b,
+                          const double* c, double* state, double* y) {
+    if (K < 0 || D < 1 || block < 1 || t0 < 0 || !state) return -1;
+    if (K > 0 && (!x || !a || !b || !c || !y)) return -1;
+    double* e = state;
+    double* s = state + D;
+    for (int64_t k = 0; k < K; ++k) {
+        const int64_t t = t0 + k;
+        for (int64_t mu = 0; mu < D; ++mu) {
+            const int64_t i = k * D + mu;
+            if (t % block == 0) { /* a block starts: the window now reaches back to the
+                                     start of the block that just ended */
+                e[mu] = s[mu];
+                s[mu] = 0.0;
+            }
+            const double am = decay(a, a_per_channel, D, k, mu);
+            const double u = b[i] * x[i];
+            e[mu] = am * e[mu] + u;
+            s[mu] = am * s[mu] + u;
+            y[i] = c[i] * e[mu];
+            if (flags & SWR_ORACLE_RESIDUAL) y[i] += x[i];
+        }
+    }
+    return 0;
+}
+
+int swr_oracle_step(int64_t S, int64_t K, int64_t D, int64_t block, int64_t t0,
+                    int a_per_channel, int flags, const double* x, const double* a,
+                    const double* b, const double* c, double* state, double* y) {
+    if (S < 0 || K < 0 || D < 1) return -1;
+    const int64_t n = K * D, na = a_per_channel ? K * D : K;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_step_slice(K, D, block, t0, a_per_channel, flags, x + s * n, a + s * na,
+                                     b + s * n, c + s * n, state + s * 2 * D, y + s * n) != 0;
+    return err ? -1 : 0;
+}
+
 int swr_oracle_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

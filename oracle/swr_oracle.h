@@ -98,6 +98,25 @@ int swr_oracle_exact_backward(int64_t S, int64_t T, int64_t D, int a_per_channel
                               const double* dh_last, double* dx, double* da, double* db,
                               double* dc, double* dh0);
 
+/* Recurrent (token-by-token) form of the jagged window, with its state: the
+ * same outputs as the restarted-window loop above, obtained by carrying two
+ * states per channel -- e, the jagged-window state (restarted at the start of
+ * the previous block), and s, the state restarted at the start of the current
+ * block -- and exchanging them at every block boundary (at a token t with
+ * t mod block == 0: e <- s, s <- 0), before the update
+ *     e <- a_t e + u_t,  s <- a_t s + u_t,  y_t = c_t e (+ x_t).
+ * The K tokens of one call sit at positions t0 .. t0+K-1 of their sequence;
+ * `state` ([2][D]: e then s, the state after token t0-1; zeros at t0 = 0) is
+ * read and overwritten with the state after the last token.  Returns 0 or -1. */
+int swr_oracle_step_slice(int64_t K, int64_t D, int64_t block, int64_t t0, int a_per_channel,
+                          int flags, const double* x, const double* a, const double* b,
+                          const double* c, double* state, double* y);
+
+/* S slices back to back (x: [S][K][D], a: [S][K] or [S][K][D], state: [S][2][D]). */
+int swr_oracle_step(int64_t S, int64_t K, int64_t D, int64_t block, int64_t t0,
+                    int a_per_channel, int flags, const double* x, const double* a,
+                    const double* b, const double* c, double* state, double* y);
+
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
 int swr_oracle_max_threads(void);
 
