@@ -206,6 +206,46 @@ int swr_exact_backward(const swr_problem_t* problem, const void* x, const void* 
                        const float* dh_last, void* dx, float* da, void* db, void* dc, float* dh0,
                        void* workspace, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Recurrent decoding
+ *
+ * The recurrence processed token by token with a carried state, for
+ * generating one (or a few) tokens at a time after a prompt, i.e. decoding
+ * the layer as a recurrence (Sec. 6, comparison of Phalanx variants).  problem->T is the
+ * number of tokens K in the call (usually 1); x, a, b, c, y hold those K
+ * tokens with the usual layouts and strides; every flag applies.  The
+ * alignment rules are those of swr_forward without the per-channel flag
+ * (a per-channel a then needs the alignment of x).  The state is float32,
+ * contiguous, 16-byte aligned, and is read and overwritten in place; K = 0
+ * leaves it unchanged.  A thread carries each (batch, head, 16th of the
+ * channels) through the K tokens in order: meant for short calls; long
+ * prompts go through swr_forward and swr_decode_state.
+ * ------------------------------------------------------------------------ */
+
+/* Jagged window.  state is [B][H][2][D]: per channel e, the state restarted
+ * at the start of the previous block (what the outputs read), then s, the
+ * state restarted at the start of the current block -- both after token t0-1
+ * (zeros before the first token).  When a token t with t mod block == 0
+ * starts a block, e takes s and s restarts from zero; then e and s both take
+ * the step h <- a_t h + b_t x_t and y_t = c_t e (+ x_t).  The outputs are
+ * exactly those of swr_forward over the whole sequence (Sec. 4.2's window). */
+int swr_step(const swr_problem_t* problem, int64_t t0, const void* x, const void* a, const void* b,
+             const void* c, void* y, float* state, void* stream);
+
+/* Exact recurrence: state is h, [B][H][D] (h0 / h_last of swr_exact_forward);
+ * h <- a_t h + b_t x_t, y_t = c_t h (+ x_t).  problem->block must be valid but
+ * is not used. */
+int swr_exact_step(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                   const void* c, void* y, float* state, void* stream);
+
+/* The jagged window's decoding state (swr_step's [B][H][2][D]) after a
+ * forward pass over tokens 0 .. T-1 of `problem`, from that pass's block
+ * carriers (swr_forward / swr_carriers) and a: s is the carrier of the last
+ * (possibly partial) block and e = s + (product of the last block's decays)
+ * times the carrier of the block before it. */
+int swr_decode_state(const swr_problem_t* problem, const void* a, const float* carriers, float* state,
+                     void* stream);
+
 /* Resolved launch shape for a problem (for reports and tests): the run length
  * in tokens and the number of workgroups of the forward and of the backward
  * launch (any output pointer may be NULL).  Returns an SWR_ERR_* code for a

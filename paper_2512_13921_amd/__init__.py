@@ -24,6 +24,7 @@ from . import build as _build
 __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error_string",
            "swr_abi_version", "swr_launch_info", "swr_carrier_elems", "carrier_shape",
            "swr_exact_forward", "swr_exact_backward", "swr_exact_workspace_bytes",
+           "swr_step", "swr_exact_step", "swr_decode_state",
            "SWRFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
@@ -91,6 +92,12 @@ def load():
         lib.swr_exact_forward.restype = ctypes.c_int
         lib.swr_exact_backward.argtypes = [P] + [vp] * 15
         lib.swr_exact_backward.restype = ctypes.c_int
+        lib.swr_step.argtypes = [P, ctypes.c_int64] + [vp] * 7
+        lib.swr_step.restype = ctypes.c_int
+        lib.swr_exact_step.argtypes = [P] + [vp] * 7
+        lib.swr_exact_step.restype = ctypes.c_int
+        lib.swr_decode_state.argtypes = [P] + [vp] * 4
+        lib.swr_decode_state.restype = ctypes.c_int
         if lib.swr_abi_version() != SWR_ABI_VERSION:
             raise RuntimeError("libswr.so ABI version does not match the binding")
         _lib = lib
@@ -371,6 +378,78 @@ def swr_exact_backward(x, a, b, c, dy, carriers, block, h0=None, dh_last=None, r
     if rc != 0:
         raise SwrError(rc, "swr_exact_backward")
     return (dx, da, db, dc, dh0) if want_dh0 else (dx, da, db, dc)
+
+
+# ----------------------------------------------------------------------------- recurrent decoding
+
+
+def _step_state(state, x, exact):
+    torch = _torch()
+    B, K, H, D = x.shape
+    shape = (B, H, D) if exact else (B, H, 2, D)
+    if state is None:
+        return torch.zeros(shape, dtype=torch.float32, device=x.device)
+    if (tuple(state.shape) != shape or state.dtype != torch.float32 or not state.is_contiguous()
+            or state.device != x.device):
+        raise ValueError(f"state must be a contiguous float32 tensor of shape {shape}")
+    return state
+
+
+def swr_step(x, a, b, c, block, t0, state=None, residual=False, y=None, stream=None,
+             sigmoid_decay=False, sigmoid_pregate=False):
+    """K = x.shape[1] tokens at sequence positions t0 .. t0+K-1 in recurrent
+    form (see ``include/swr.h``).  ``state`` ([B, H, 2, D] float32; None =
+    zeros, i.e. t0 = 0) is updated in place.  Returns (y, state)."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, residual, 0, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c)
+    state = _step_state(state, x, False)
+    if y is None:
+        y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+    else:
+        _same_layout(x, y)
+    rc = load().swr_step(ctypes.byref(problem), int(t0), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y),
+                         _ptr(state), _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_step")
+    return y, state
+
+
+def swr_exact_step(x, a, b, c, state=None, residual=False, y=None, stream=None,
+                   sigmoid_decay=False, sigmoid_pregate=False):
+    """K tokens of the exact recurrence from the state h ([B, H, D] float32,
+    updated in place; None = zeros).  Returns (y, state)."""
+    torch = _torch()
+    problem = _problem_from(x, a, 16, residual, 0, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c)
+    state = _step_state(state, x, True)
+    if y is None:
+        y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+    else:
+        _same_layout(x, y)
+    rc = load().swr_exact_step(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y),
+                               _ptr(state), _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_exact_step")
+    return y, state
+
+
+def swr_decode_state(x, a, carriers, block, state=None, stream=None, sigmoid_decay=False):
+    """swr_step's state after a jagged-window forward over all of x's tokens,
+    from that forward's block carriers (x gives the shape and strides only)."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, False, 0, sigmoid_decay, False)
+    carriers = _carrier_tensor(x, block, carriers)
+    B, T, H, D = x.shape
+    if state is None:
+        state = torch.empty((B, H, 2, D), dtype=torch.float32, device=x.device)
+    else:
+        state = _step_state(state, x, False)
+    rc = load().swr_decode_state(ctypes.byref(problem), _ptr(a), _ptr(carriers), _ptr(state),
+                                 _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_decode_state")
+    return state
 
 
 def _autograd_function():

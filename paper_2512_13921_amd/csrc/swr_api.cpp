@@ -474,3 +474,102 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Recurrent steps and the decoding state
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Bytes of one thread's slice of a row in the step and state kernels: D/16
+// channels (the whole head is one slice set even for a per-channel decay).
+int64_t step_vbytes(const swr_problem_t* p, const Resolved& r) {
+    return std::min<int64_t>(16, (p->D / 16) * r.es);
+}
+
+int check_step_strides(const swr_problem_t* p, const Resolved& r, int64_t vb) {
+    const Dim xd[3] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}};
+    for (const Dim& d : xd)
+        if (d.size > 1 && (d.stride * r.es) % vb != 0) return SWR_ERR_ALIGN;
+    return SWR_OK;
+}
+
+int step_impl(const swr_problem_t* p, int64_t t0, const void* x, const void* a, const void* b,
+              const void* c, void* y, float* state, bool exact, void* stream) {
+    Resolved r;
+    int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    if (t0 < 0) return SWR_ERR_SHAPE;
+    const int64_t seqs = p->B * p->H;
+    if (seqs == 0 || p->T == 0) return SWR_OK;   // no token: the state is unchanged
+    if (!x || !a || !b || !c || !y || !state) return SWR_ERR_NULL;
+    const int64_t vb = step_vbytes(p, r);
+    for (const void* q : {x, b, c, (const void*)y})
+        if (!aligned(q, vb)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.pc ? vb : r.es) || !aligned(state, 16)) return SWR_ERR_ALIGN;
+    if ((rc = check_step_strides(p, r, vb)) != SWR_OK) return rc;
+    const int64_t sbytes = seqs * p->D * 4 * (exact ? 1 : 2);
+    const Span ins[4] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es)};
+    const Span sy = span(y, r.xspan), ss = span(state, sbytes);
+    for (const Span& s : ins)
+        if (overlap(sy, s) || overlap(ss, s)) return SWR_ERR_ALIAS;
+    if (overlap(sy, ss)) return SWR_ERR_ALIAS;
+
+    swr::StepParams q{};
+    q.x = x; q.a = a; q.b = b; q.c = c; q.y = y; q.state = state;
+    q.B = p->B; q.K = p->T; q.H = p->H;
+    q.sx_b = p->sx_b; q.sx_t = p->sx_t; q.sx_h = p->sx_h;
+    q.sa_b = p->sa_b; q.sa_t = p->sa_t; q.sa_h = p->sa_h;
+    q.t0 = t0;
+    q.block = (int32_t)p->block;
+    q.residual = (p->flags & SWR_FLAG_RESIDUAL) ? 1 : 0;
+    q.sig_a = (p->flags & SWR_FLAG_SIGMOID_DECAY) ? 1 : 0;
+    q.sig_b = (p->flags & SWR_FLAG_SIGMOID_PREGATE) ? 1 : 0;
+    return swr::launch_step(q, p->dtype, (int)p->D, exact, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int swr_step(const swr_problem_t* problem, int64_t t0, const void* x, const void* a, const void* b,
+             const void* c, void* y, float* state, void* stream) {
+    return step_impl(problem, t0, x, a, b, c, y, state, false, stream);
+}
+
+int swr_exact_step(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                   const void* c, void* y, float* state, void* stream) {
+    return step_impl(problem, 0, x, a, b, c, y, state, true, stream);
+}
+
+int swr_decode_state(const swr_problem_t* p, const void* a, const float* carriers, float* state,
+                     void* stream) {
+    Resolved r;
+    const int rc = resolve(p, &r);
+    if (rc != SWR_OK) return rc;
+    const int64_t seqs = p->B * p->H;
+    if (seqs == 0) return SWR_OK;
+    if (!state || (p->T > 0 && (!a || !carriers))) return SWR_ERR_NULL;
+    const int64_t vb = step_vbytes(p, r);
+    if (!aligned(state, 16) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
+    if (p->T > 0) {
+        if (!aligned(a, r.pc ? vb : r.es)) return SWR_ERR_ALIGN;
+        if (r.pc && check_step_strides(p, r, vb) != SWR_OK) return SWR_ERR_ALIGN;
+    }
+    const Span ss = span(state, seqs * 2 * p->D * 4);
+    if (overlap(ss, span(a, r.aspan * r.es)) || overlap(ss, span(carriers, r.carriers * 4)))
+        return SWR_ERR_ALIAS;
+
+    swr::StateParams q{};
+    q.a = a; q.carriers = carriers; q.state = state;
+    q.B = p->B; q.T = p->T; q.H = p->H;
+    q.sa_b = r.pc ? p->sx_b : p->sa_b;
+    q.sa_t = r.pc ? p->sx_t : p->sa_t;
+    q.sa_h = r.pc ? p->sx_h : p->sa_h;
+    q.nblocks = r.nblocks;
+    q.lshift = p->block == 16 ? 4 : p->block == 32 ? 5 : p->block == 64 ? 6 : 7;
+    q.sig_a = (p->flags & SWR_FLAG_SIGMOID_DECAY) ? 1 : 0;
+    return swr::launch_state(q, p->dtype, (int)p->D, r.pc, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1099,6 +1099,131 @@ __global__ __launch_bounds__(256) void swr_scan_kernel(ScanParams q) {
 }
 
 // ---------------------------------------------------------------------------
+// Recurrent steps (decoding)
+// ---------------------------------------------------------------------------
+//
+// One thread per (batch, head) and 16th of the channels (the lane slice of the
+// block kernels, so the same alignment rules hold); the tokens of a call are
+// taken in order.  The jagged window is carried as two states per channel
+// (Sec. 4.2's window as a recurrence): e, restarted at the start of the
+// previous block, which the outputs read, and s, restarted at the start of
+// the current block; when a block starts, e takes s and s restarts from zero.
+// The exact recurrence carries h alone.  Work per token is a few flops per
+// channel: a launch of a handful of tokens is bound by latency, not by HBM.
+template <class IO, int CPL, bool EXACT, bool PC, bool FEAT>
+__global__ __launch_bounds__(256) void swr_step_kernel(StepParams q) {
+    constexpr int D = CPL * SB;
+    constexpr int ES = IO::ES;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= q.B * q.H * 16) return;   // no barriers below: idle threads may leave
+    const int sig_a = FEAT ? q.sig_a : 0, sig_b = FEAT ? q.sig_b : 0;
+    const int64_t seq = idx >> 4;
+    const int n = (int)(idx & 15);
+    const int64_t bb = seq / q.H, hh = seq - bb * q.H;
+    const int64_t xo = (bb * q.sx_b + hh * q.sx_h) * ES + n * CPL * ES;   // this thread's slice, token 0
+    const int64_t ao = PC ? xo : (bb * q.sa_b + hh * q.sa_h) * ES;
+    const int64_t rs = q.sx_t * ES, as = PC ? rs : q.sa_t * ES;
+    float* st = q.state + seq * (EXACT ? D : 2 * D) + n * CPL;
+
+    float e[CPL], s[CPL];
+    {
+        Row<IoF32, CPL> re, rs_;
+        re.load(rsrc(st), 0u);
+        if constexpr (!EXACT) rs_.load(rsrc(st + D), 0u);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            e[m] = re.get(m);
+            s[m] = EXACT ? 0.f : rs_.get(m);
+        }
+    }
+    for (int64_t k = 0; k < q.K; ++k) {
+        const int64_t t = q.t0 + k;
+        Row<IO, CPL> xr, br, cr, ar;
+        xr.load(rsrc((const char*)q.x + xo + k * rs), 0u);
+        br.load(rsrc((const char*)q.b + xo + k * rs), 0u);
+        cr.load(rsrc((const char*)q.c + xo + k * rs), 0u);
+        float av[CPL];
+        if constexpr (PC) {
+            ar.load(rsrc((const char*)q.a + ao + k * as), 0u);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) av[m] = ar.get(m);
+        } else {
+            const float a1 = load_scalar<IO>(rsrc((const char*)q.a + ao + k * as), 0u);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) av[m] = a1;
+        }
+        const bool restart = !EXACT && (t & (q.block - 1)) == 0;   // a block starts at t
+        float yv[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            const float a_ = sig_a ? sigmoid(av[m]) : av[m];
+            const float u = xr.get(m) * pregate(br.get(m), sig_b);
+            if (restart) { e[m] = s[m]; s[m] = 0.f; }
+            e[m] = a_ * e[m] + u;
+            if constexpr (!EXACT) s[m] = a_ * s[m] + u;
+            yv[m] = cr.get(m) * e[m];
+            if (q.residual) yv[m] += xr.get(m);
+        }
+        store_row<IO, CPL>(rsrc((char*)q.y + xo + k * rs), 0u, yv);
+    }
+    store_row<IoF32, CPL>(rsrc(st), 0u, e);
+    if constexpr (!EXACT) store_row<IoF32, CPL>(rsrc(st + D), 0u, s);
+}
+
+// The jagged window's state after tokens 0 .. T-1, from the forward's block
+// carriers: s is the carrier of the last (possibly partial) block tau, whose
+// window restarts at that block's start; e restarts one block earlier, so it
+// adds the previous block's carrier carried through the last block's decays,
+// e = s + (a_{tau l} ... a_{T-1}) v_{tau-1}.
+template <class IO, int CPL, bool PC, bool FEAT>
+__global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
+    constexpr int D = CPL * SB;
+    constexpr int ES = IO::ES;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= q.B * q.H * 16) return;
+    const int sig_a = FEAT ? q.sig_a : 0;
+    const int64_t seq = idx >> 4;
+    const int n = (int)(idx & 15);
+    const int64_t bb = seq / q.H, hh = seq - bb * q.H;
+    float e[CPL], s[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
+    if (q.T > 0) {
+        const int64_t tau = (q.T - 1) >> q.lshift, t_blk = tau << q.lshift;
+        const float* vb = q.carriers + seq * q.nblocks * D + n * CPL;
+        Row<IoF32, CPL> rv, rp;
+        rv.load(rsrc(vb + tau * D), 0u);
+        rp.load(rsrc(vb + (tau - 1) * D), in_range(tau > 0, 0u));
+        const int64_t ao = (bb * q.sa_b + hh * q.sa_h) * ES + (PC ? n * CPL * ES : 0);
+        const int64_t as = q.sa_t * ES;
+        float G[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) G[m] = 1.f;
+        for (int64_t t = t_blk; t < q.T; ++t) {
+            if constexpr (PC) {
+                Row<IO, CPL> ar;
+                ar.load(rsrc((const char*)q.a + ao + t * as), 0u);
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) G[m] *= sig_a ? sigmoid(ar.get(m)) : ar.get(m);
+            } else {
+                const float a1 = load_scalar<IO>(rsrc((const char*)q.a + ao + t * as), 0u);
+                const float a_ = sig_a ? sigmoid(a1) : a1;
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) G[m] *= a_;
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            s[m] = rv.get(m);
+            e[m] = s[m] + G[m] * rp.get(m);
+        }
+    }
+    float* st = q.state + seq * 2 * D + n * CPL;
+    store_row<IoF32, CPL>(rsrc(st), 0u, e);
+    store_row<IoF32, CPL>(rsrc(st + D), 0u, s);
+}
+
+// ---------------------------------------------------------------------------
 // Per-channel decay
 // ---------------------------------------------------------------------------
 //
@@ -1684,6 +1809,75 @@ hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backw
     hipStream_t st = (hipStream_t)stream;
     if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, mode, st);
     return launch_feat<IoF32>(p, D, sh, backward, per_channel, mode, st);
+}
+
+template <class IO, int CPL>
+static hipError_t launch_step_cpl(const StepParams& q, bool exact, bool pc, bool feat, hipStream_t st) {
+    const int64_t n = q.B * q.H * 16;
+    const dim3 grid((unsigned)((n + 255) / 256)), blk(256);
+    const int sel = (exact ? 4 : 0) | (pc ? 2 : 0) | (feat ? 1 : 0);
+    switch (sel) {
+        case 0: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, false, false, false>), grid, blk, 0, st, q); break;
+        case 1: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, false, false, true>), grid, blk, 0, st, q); break;
+        case 2: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, false, true, false>), grid, blk, 0, st, q); break;
+        case 3: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, false, true, true>), grid, blk, 0, st, q); break;
+        case 4: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, true, false, false>), grid, blk, 0, st, q); break;
+        case 5: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, true, false, true>), grid, blk, 0, st, q); break;
+        case 6: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, true, true, false>), grid, blk, 0, st, q); break;
+        default: hipLaunchKernelGGL((swr_step_kernel<IO, CPL, true, true, true>), grid, blk, 0, st, q); break;
+    }
+    return hipGetLastError();
+}
+
+template <class IO>
+static hipError_t launch_step_io(const StepParams& q, int D, bool exact, bool pc, hipStream_t st) {
+    const bool feat = q.sig_a || q.sig_b;
+    switch (D) {
+        case 16: return launch_step_cpl<IO, 1>(q, exact, pc, feat, st);
+        case 32: return launch_step_cpl<IO, 2>(q, exact, pc, feat, st);
+        case 64: return launch_step_cpl<IO, 4>(q, exact, pc, feat, st);
+        case 128: return launch_step_cpl<IO, 8>(q, exact, pc, feat, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_step(const StepParams& q, int dtype, int D, bool exact, bool per_channel, void* stream) {
+    if (q.B * q.H == 0) return hipSuccess;
+    hipStream_t st = (hipStream_t)stream;
+    if (dtype == 1) return launch_step_io<IoBf16>(q, D, exact, per_channel, st);
+    return launch_step_io<IoF32>(q, D, exact, per_channel, st);
+}
+
+template <class IO, int CPL>
+static hipError_t launch_state_cpl(const StateParams& q, bool pc, hipStream_t st) {
+    const int64_t n = q.B * q.H * 16;
+    const dim3 grid((unsigned)((n + 255) / 256)), blk(256);
+    const int sel = (pc ? 2 : 0) | (q.sig_a ? 1 : 0);
+    switch (sel) {
+        case 0: hipLaunchKernelGGL((swr_state_kernel<IO, CPL, false, false>), grid, blk, 0, st, q); break;
+        case 1: hipLaunchKernelGGL((swr_state_kernel<IO, CPL, false, true>), grid, blk, 0, st, q); break;
+        case 2: hipLaunchKernelGGL((swr_state_kernel<IO, CPL, true, false>), grid, blk, 0, st, q); break;
+        default: hipLaunchKernelGGL((swr_state_kernel<IO, CPL, true, true>), grid, blk, 0, st, q); break;
+    }
+    return hipGetLastError();
+}
+
+template <class IO>
+static hipError_t launch_state_io(const StateParams& q, int D, bool pc, hipStream_t st) {
+    switch (D) {
+        case 16: return launch_state_cpl<IO, 1>(q, pc, st);
+        case 32: return launch_state_cpl<IO, 2>(q, pc, st);
+        case 64: return launch_state_cpl<IO, 4>(q, pc, st);
+        case 128: return launch_state_cpl<IO, 8>(q, pc, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_state(const StateParams& q, int dtype, int D, bool per_channel, void* stream) {
+    if (q.B * q.H == 0) return hipSuccess;
+    hipStream_t st = (hipStream_t)stream;
+    if (dtype == 1) return launch_state_io<IoBf16>(q, D, per_channel, st);
+    return launch_state_io<IoF32>(q, D, per_channel, st);
 }
 
 hipError_t launch_scan(const ScanParams& q, void* stream) {

@@ -70,6 +70,38 @@ struct ScanParams {
     int32_t reverse;
 };
 
+// Recurrent (token-by-token) steps: K tokens at positions t0 .. t0+K-1 of
+// every (batch, head) sequence, carrying the state across calls.  The jagged
+// window's state is (e, s) per channel, [B*H][2][D]; the exact recurrence's
+// is h, [B*H][D]; both are read and overwritten in place.
+struct StepParams {
+    const void* x;
+    const void* a;
+    const void* b;
+    const void* c;
+    void* y;
+    float* state;
+    int64_t B, K, H;
+    int64_t sx_b, sx_t, sx_h;   // element strides of x, b, c, y (and of a for a per-channel decay)
+    int64_t sa_b, sa_t, sa_h;   // element strides of a (one decay per head)
+    int64_t t0;                 // sequence position of the first token
+    int32_t block;              // l (the jagged window's block length)
+    int32_t residual, sig_a, sig_b;
+};
+
+// The jagged window's recurrent state after a forward pass over tokens
+// 0 .. T-1, from that pass's block carriers and the decays of its last block.
+struct StateParams {
+    const void* a;
+    const float* carriers;      // [B][H][nblocks][D]
+    float* state;               // [B*H][2][D]
+    int64_t B, T, H;
+    int64_t sa_b, sa_t, sa_h;   // strides of a (those of x for a per-channel decay)
+    int64_t nblocks;
+    int32_t lshift;             // log2(l)
+    int32_t sig_a;
+};
+
 // Workgroup shape: tw waves per head along the tokens (a step is tw * 16
 // tokens) times hw heads of one batch entry (hw must divide H).  The
 // backward's steps must hold whole blocks.  Two heads per forward workgroup
@@ -99,5 +131,9 @@ hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool ba
                   int mode, void* stream);
 
 hipError_t launch_scan(const ScanParams& q, void* stream);
+
+hipError_t launch_step(const StepParams& q, int dtype, int D, bool exact, bool per_channel, void* stream);
+
+hipError_t launch_state(const StateParams& q, int dtype, int D, bool per_channel, void* stream);
 
 }  // namespace swr

@@ -295,3 +295,50 @@ def test_exact_validation():
     for kw in (dict(B=0), dict(H=0)):
         assert xfwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
         assert xbwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
+
+
+# ----------------------------------------------------------------------------- recurrent decoding
+
+ST = GB * 30
+
+
+def stp(p, t0=0, x=X, a=A, b=B_, c=C, y=Y, st=ST):
+    v = ctypes.c_void_p
+    return swr.load().swr_step(ctypes.byref(p), t0, v(x), v(a), v(b), v(c), v(y), v(st), None)
+
+
+def xstp(p, x=X, a=A, b=B_, c=C, y=Y, st=ST):
+    v = ctypes.c_void_p
+    return swr.load().swr_exact_step(ctypes.byref(p), v(x), v(a), v(b), v(c), v(y), v(st), None)
+
+
+def dstate(p, a=A, v_=V, st=ST):
+    v = ctypes.c_void_p
+    return swr.load().swr_decode_state(ctypes.byref(p), v(a), v(v_), v(st), None)
+
+
+def test_step_validation():
+    p = problem(T=1)
+    assert stp(p, t0=-1) == E_SHAPE
+    for kw in ("x", "a", "b", "c", "y", "st"):
+        assert stp(p, **{kw: 0}) == E_NULL, kw
+        assert xstp(p, **{kw: 0}) == E_NULL, kw
+    assert stp(p, st=ST + 8) == E_ALIGN and xstp(p, st=ST + 4) == E_ALIGN
+    assert stp(p, x=X + 2) == E_ALIGN
+    # a per-channel decay needs the whole head's lane slices aligned (D = 128 bf16: 16 bytes)
+    assert stp(problem(T=1, D=128, per_channel=True), a=A + 8) == E_ALIGN
+    assert stp(p, y=X) == E_ALIAS and stp(p, st=A) == E_ALIAS and stp(p, st=Y) == E_ALIAS
+    assert xstp(p, st=C) == E_ALIAS
+    assert stp(problem(T=1, block=48)) == E_BLOCK
+    # no token or no sequence: nothing to do, even with NULL pointers
+    assert stp(problem(T=0), 5, 0, 0, 0, 0, 0, 0) == OK
+    assert xstp(problem(B=0, T=1), 0, 0, 0, 0, 0, 0) == OK
+
+
+def test_decode_state_validation():
+    p = problem()
+    assert dstate(p, st=0) == E_NULL and dstate(p, a=0) == E_NULL and dstate(p, v_=0) == E_NULL
+    assert dstate(p, st=ST + 4) == E_ALIGN and dstate(p, v_=V + 4) == E_ALIGN
+    assert dstate(problem(D=128, per_channel=True), a=A + 8) == E_ALIGN
+    assert dstate(p, st=V) == E_ALIAS and dstate(p, st=A) == E_ALIAS
+    assert dstate(problem(B=0)) == OK
