@@ -150,6 +150,65 @@ def cpu_baseline(cfg, prob, budget_s=10.0, exact=False):
     }
 
 
+def decode_bench(args, cfg, swr, torch):
+    """Recurrent decoding: K=1 token for each of the B sequences per call, at
+    sequence positions following a prompt of the workload's length T.  A
+    step is one call; its time is launch-bound (B*H*D channels of a few flops
+    each), so the line reports tokens/s and microseconds per step, and the
+    bytes a step must move (inputs, outputs, the state read and written)."""
+    exact = args.recurrence == "exact"
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    B, H, D = cfg.B, cfg.H, cfg.D
+    g = torch.Generator(device="cuda").manual_seed(cfg.seed)
+    n = args.steps
+    x, b, c = (torch.randn(B, n, H, D, device="cuda", generator=g).to(dt) for _ in range(3))
+    a = torch.sigmoid(torch.randn(B, n, H, device="cuda", generator=g) + 3.0).to(dt)
+    y = torch.empty_like(x)
+    state = torch.zeros((B, H, D) if exact else (B, H, 2, D), dtype=torch.float32, device="cuda")
+    t0 = cfg.T
+
+    def step(i, out):
+        s = slice(i, i + 1)
+        if exact:
+            swr.swr_exact_step(x[:, s], a[:, s], b[:, s], c[:, s], state, y=out[:, s])
+        else:
+            swr.swr_step(x[:, s], a[:, s], b[:, s], c[:, s], cfg.block, t0 + i, state, y=out[:, s])
+
+    for i in range(min(args.warmup, n)):
+        step(i, y)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n):
+        step(i, y)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    e = 2 if cfg.dtype == "bf16" else 4
+    nbytes = B * H * (e * (4 * D + 1) + 4 * D * (2 if exact else 4))
+    out = {
+        "metric": "SWR recurrent decoding step (one token per sequence)",
+        "value": B / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": n, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded device draws)",
+        "config": {"workload": cfg.name + ("_exact" if exact else "") + "_decode", "B": B, "H": H, "d": D,
+                   "block": cfg.block, "prompt_len": cfg.T,
+                   "recurrence": "exact (untruncated)" if exact else "jagged window"},
+        "bytes_per_step": nbytes,
+        "us_per_step": ms * 1e3,
+        "GB/s": nbytes / (ms * 1e-3) / 1e9,
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -164,6 +223,9 @@ def main():
                     help="a and b are logits; the kernels apply the sigmoid (fused featurisation)")
     ap.add_argument("--recurrence", choices=("window", "exact"), default="window",
                     help="the jagged-window recurrence (default) or the exact, untruncated one")
+    ap.add_argument("--decode", action="store_true",
+                    help="time recurrent decoding instead: one token per sequence per call "
+                         "(swr_step / swr_exact_step) after a prompt of the workload's length")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -180,6 +242,8 @@ def main():
     swr.load()
 
     cfg = W.CONFIGS[args.config]
+    if args.decode:
+        return decode_bench(args, cfg, swr, torch)
     if args.decay == "channel":
         cfg = W.PER_CHANNEL.get(args.config) or cfg.with_(name=cfg.name + "_perchannel", per_channel=True)
     if args.sigmoid:

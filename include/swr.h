@@ -172,8 +172,9 @@ int swr_abi_version(void);
  * swr_forward (the backward about 1.25x).
  *
  * Everything in swr_problem_t keeps its meaning except that `block` only sets
- * the length of the exact block carriers; SWR_FLAG_PER_CHANNEL_DECAY is not
- * supported here (SWR_ERR_UNSUPPORTED).  h0, h_last, dh_last and dh0 are
+ * the length of the exact block carriers; every flag applies (with
+ * SWR_FLAG_PER_CHANNEL_DECAY the layouts and alignment of a and da are those
+ * of swr_forward / swr_backward with that flag).  h0, h_last, dh_last and dh0 are
  * float32 [B][H][D], contiguous, 16-byte aligned; NULL h0 / dh_last mean
  * zero, NULL h_last / dh0 skip that output.
  *

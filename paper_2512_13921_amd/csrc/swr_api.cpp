@@ -338,16 +338,12 @@ struct ExactWs {
 ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
     ExactWs w;
     w.nr = std::max(r.nruns, r.nruns_f);
-    w.floats = p->B * p->H * w.nr * (2 * p->D + 1);
+    // a per-channel decay has one run decay product per channel
+    w.floats = p->B * p->H * w.nr * (2 * p->D + (r.pc ? p->D : 1));
     return w;
 }
 
-int resolve_exact(const swr_problem_t* p, Resolved* r) {
-    const int rc = resolve(p, r);
-    if (rc != SWR_OK) return rc;
-    if (r->pc) return SWR_ERR_UNSUPPORTED;   // per-channel decay: jagged window only
-    return SWR_OK;
-}
+int resolve_exact(const swr_problem_t* p, Resolved* r) { return resolve(p, r); }
 
 // Pointers into the workspace for one launch.
 void exact_arrays(const swr_problem_t* p, const ExactWs& w, void* ws, float** v, float** carry, float** prod) {
@@ -385,7 +381,7 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     if (!r.empty) {
         for (const void* q : {x, b, c, (const void*)y})
             if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
-        if (!aligned(a, r.es)) return SWR_ERR_ALIGN;
+        if (!aligned(a, r.pc ? r.vbytes : r.es)) return SWR_ERR_ALIGN;
         if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     }
     const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es),
@@ -405,17 +401,18 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     k.x = x; k.a = a; k.b = b; k.c = c;
     k.agg_v = wv; k.agg_p = wp; k.carry = wc;
     // Stage I: local solves of every run, keeping each run's end state and decay product.
-    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, false, swr::kAggregate, stream) != hipSuccess)
+    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kAggregate, stream) != hipSuccess)
         return SWR_ERR_HIP;
     // Stage II: the carrier recurrence over the runs, from h0; h_last is its final value.
     swr::ScanParams q{};
     q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = h0; q.fin = h_last;
     q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 0;
+    q.p_per_channel = r.pc ? 1 : 0;
     if ((h_last || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
     if (r.empty) return SWR_OK;
     // Stage III: every run again from its exact entering state: outputs and exact block carriers.
     k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, r.dk, r.fwd, false, false, swr::kExact, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kExact, stream) == hipSuccess ? SWR_OK
                                                                                           : SWR_ERR_HIP;
 }
 
@@ -437,7 +434,8 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     if (!r.empty) {
         for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
             if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
-        if (!aligned(a, r.es) || !aligned(da, 4)) return SWR_ERR_ALIGN;
+        const int64_t vda = r.pc ? std::min<int64_t>(16, (int64_t)(r.dk / 16) * 4) : 4;
+        if (!aligned(a, r.pc ? r.vbytes : r.es) || !aligned(da, vda)) return SWR_ERR_ALIGN;
         if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     }
     const Span ins[8] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
@@ -458,18 +456,19 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.agg_v = wv; k.agg_p = wp; k.carry = wc; k.h0 = h0;
     // Stage I: reverse local solves of every run (from c, dy, a).
-    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.bwd, true, false, swr::kAggregate, stream) != hipSuccess)
+    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kAggregate, stream) != hipSuccess)
         return SWR_ERR_HIP;
     // Stage II: the reverse carrier recurrence over the runs, from dh_last; dh0 is its final value.
     swr::ScanParams q{};
     q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = dh_last; q.fin = dh0;
     q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 1;
+    q.p_per_channel = r.pc ? 1 : 0;
     if ((dh0 || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
     if (r.empty) return SWR_OK;
     // Stage III: the gradients, from the adjoint entering each run and the exact block carriers.
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, false, swr::kExact, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kExact, stream) == hipSuccess ? SWR_OK
                                                                                          : SWR_ERR_HIP;
 }
 

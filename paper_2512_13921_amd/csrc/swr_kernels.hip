@@ -1105,7 +1105,8 @@ __global__ __launch_bounds__(256) void swr_scan_kernel(ScanParams q) {
     if (idx >= q.seqs * q.D) return;
     const int64_t seq = idx / q.D, ch = idx - seq * q.D;
     const float* v = q.agg_v + seq * q.nruns * q.D + ch;
-    const float* pp = q.agg_p + seq * q.nruns;
+    const float* pp = q.p_per_channel ? q.agg_p + seq * q.nruns * q.D + ch : q.agg_p + seq * q.nruns;
+    const int64_t pstride = q.p_per_channel ? q.D : 1;
     float* cy = q.carry + seq * q.nruns * q.D + ch;
     float S = q.init ? q.init[idx] : 0.0f;
     constexpr int G = 8;
@@ -1116,7 +1117,7 @@ __global__ __launch_bounds__(256) void swr_scan_kernel(ScanParams q) {
             const int64_t j = r0 + g;
             const int64_t r = q.reverse ? q.nruns - 1 - j : j;
             vv[g] = j < q.nruns ? v[r * q.D] : 0.0f;
-            pv[g] = j < q.nruns ? pp[r] : 1.0f;
+            pv[g] = j < q.nruns ? pp[r * pstride] : 1.0f;
         }
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -1364,8 +1365,11 @@ __device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int6
 
 // Per-channel forward.  Same workgroup shape and sweep as swr_fwd_kernel;
 // wk.h is a virtual head: head wk.h >> hshift, channel half wk.h & (2^hshift - 1).
-template <class IO, int CPL, int TW, int HW, bool FEAT>
+// MODE as for swr_fwd_kernel; the exact modes keep a decay product per
+// channel for each run.
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
+    constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;        // channels of a virtual head
@@ -1382,8 +1386,8 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
     const int l = p.block;
     const int smask = l / SB - 1;
-    const int64_t t_lo = max(wk.t_begin - (int64_t)l, (int64_t)0);
-    const int64_t halo = wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
+    const int64_t t_lo = SWR ? max(wk.t_begin - (int64_t)l, (int64_t)0) : wk.t_begin;
+    const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
     const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + half * D) * ES;
     const char* xb = (const char*)p.x + xo;
@@ -1393,14 +1397,23 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     char* yb = (char*)p.y + xo;
     const int64_t rs = p.sx_t * ES;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
-    const bool want_y = p.y != nullptr;
+    const bool want_y = MODE != kAggregate && p.y != nullptr;
     const int64_t dfull = (int64_t)D << p.hshift;   // channels of a real head: carrier row length
-    float* const vb = p.carriers ? p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D : nullptr;
+    float* const vb = MODE != kAggregate && p.carriers
+                          ? p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D : nullptr;
     const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
+    // This run's aggregate / carry slot (channel offset of this virtual head included).
+    const int64_t slot = ((wk.b * p.H + head) * p.nruns + wk.run) * dfull + half * D;
 
-    float e[CPL], s[CPL];
+    float e[CPL], s[CPL], prod[CPL];
 #pragma unroll
-    for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
+    for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; prod[m] = 1.f; }
+    if constexpr (MODE == kExact) {
+        Row<IoF32, CPL> ci;
+        ci.load(rsrc(p.carry + slot), (uint32_t)(n * CPL) * 4u);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) e[m] = ci.get(m);
+    }
     const int64_t t_stop = ((wk.t_end + l - 1) >> p.lshift) << p.lshift;
     const int64_t t_first = wk.t_begin - halo * STEP;
     int buf = 0;
@@ -1443,7 +1456,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
         for (int m = 0; m < CPL; ++m) { ein[m] = 0.f; vout[m] = 0.f; }
 #pragma unroll 1
         for (int r = 0; r < TW; ++r) {
-            if (((ph + r) & smask) == 0) {
+            if (SWR && ((ph + r) & smask) == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -1457,11 +1470,12 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
                 const float c_ = s_cc[buf][src][n * CPL + m];
                 const float wl = s_wl[buf][src][n * CPL + m];
                 e[m] = c_ * e[m] + wl;
-                s[m] = c_ * s[m] + wl;
+                if constexpr (SWR) s[m] = c_ * s[m] + wl;
+                if constexpr (MODE == kAggregate) prod[m] *= c_;
             }
             if (r == tw) {
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) vout[m] = s[m];
+                for (int m = 0; m < CPL; ++m) vout[m] = SWR ? s[m] : e[m];
             }
         }
         if (vb && ((ph + tw) & smask) == smask) {
@@ -1485,14 +1499,20 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
             store_row<IO, CPL, kFwdStore>(ry, in_range(t >= wk.t_begin && t < wk.t_end, loff + (uint32_t)(r * rs)), yv);
         }
     }
+    if constexpr (MODE == kAggregate) {   // the run's end state from zero and decay products
+        store_row<IoF32, CPL>(rsrc(p.agg_v + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), e);
+        store_row<IoF32, CPL>(rsrc(p.agg_p + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), prod);
+    }
 }
 
 // Per-channel backward: the reverse sweep of swr_bwd_kernel with per-channel
 // decay products.  The decay gradient keeps its closed form per channel,
 //     da_{k,mu} = H_{k-1,mu} du_{k,mu} - g_{k-1,mu} r_{k,mu} (e - s)_mu (eps - p)_mu,
 // and is stored per channel (no sum over the head's channels).
-template <class IO, int CPL, int TW, int HW, bool FEAT>
+// MODE kExact: the gradient of the exact recurrence, as in swr_bwd_kernel.
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
+    constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -1533,10 +1553,17 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     float eps[CPL], pr[CPL];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; }
+    const int64_t seq = wk.b * p.H + head;
+    if constexpr (MODE == kExact) {   // the exact adjoint entering the run's end (stage II)
+        Row<IoF32, CPL> ci;
+        ci.load(rsrc(p.carry + (seq * p.nruns + wk.run) * dfull + half * D), (uint32_t)(n * CPL) * 4u);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) eps[m] = ci.get(m);
+    }
     int buf = 0;
 
     // ---- halo: the first block after the run -----------------------------------
-    if (wk.t_end < p.T) {
+    if (SWR && wk.t_end < p.T) {
         const int64_t r0 = wk.t_end + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
@@ -1614,7 +1641,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         {
             Row<IoF32, CPL> vr;
             const int64_t blk = (t0 >> p.lshift) - 1;
-            vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * dfull + n * CPL) * 4u));
+            if (MODE == kExact && t0 == 0)
+                vr.load(rsrc(p.h0 + seq * dfull + half * D), in_range(p.h0 != nullptr, (uint32_t)(n * CPL) * 4u));
+            else
+                vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * dfull + n * CPL) * 4u));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
         }
@@ -1648,10 +1678,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         {
             float e[CPL], s[CPL];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = vprev[m]; }
+            for (int m = 0; m < CPL; ++m) { e[m] = SWR ? 0.f : vprev[m]; s[m] = SWR ? vprev[m] : 0.f; }
 #pragma unroll 1
             for (int r = 0; r < tw; ++r) {
-                if ((r & smask) == 0) {
+                if (SWR && (r & smask) == 0) {
 #pragma unroll
                     for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
                 }
@@ -1661,10 +1691,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                     const float c_ = s_cc[buf][src][n * CPL + m];
                     const float wl = s_wl[buf][src][n * CPL + m];
                     e[m] = c_ * e[m] + wl;
-                    s[m] = c_ * s[m] + wl;
+                    if constexpr (SWR) s[m] = c_ * s[m] + wl;
                 }
             }
-            if ((tw & smask) == 0) {
+            if (SWR && (tw & smask) == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { e[m] = s[m]; s[m] = 0.f; }
             }
@@ -1676,7 +1706,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         float epsin[CPL], kd[CPL];
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
-            if ((r & smask) == smask) {
+            if (SWR && (r & smask) == smask) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) { eps[m] = pr[m]; pr[m] = 0.f; }
             }
@@ -1684,7 +1714,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     epsin[m] = eps[m];
-                    kd[m] = (ein[m] - sin_[m]) * (eps[m] - pr[m]);
+                    kd[m] = SWR ? (ein[m] - sin_[m]) * (eps[m] - pr[m]) : 0.f;
                 }
             }
             const int src = hw * TW + r;
@@ -1693,7 +1723,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 const float c_ = s_cc[buf][src][n * CPL + m];
                 const float df = s_df[buf][src][n * CPL + m];
                 eps[m] = c_ * eps[m] + df;
-                pr[m] = c_ * pr[m] + df;
+                if constexpr (SWR) pr[m] = c_ * pr[m] + df;
             }
         }
 
@@ -1738,35 +1768,119 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     }
 }
 
+// Stage I of the exact backward with a per-channel decay: per run, the
+// adjoint leaving its first token and the run's decay product, per channel.
+template <class IO, int CPL, int TW, bool FEAT>
+__global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
+    const int sig_a = FEAT ? p.sig_a : 0;
+    constexpr int D = CPL * SB;
+    constexpr int STEP = TW * SB;
+    constexpr int ES = IO::ES;
+    using R_ = Row<IO, CPL>;
+    __shared__ float s_df[2][TW][D];
+    __shared__ float s_cc[2][TW][D];
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    const Work wk = decode_work<1>(p, 0);
+    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
+    const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + half * D) * ES;
+    const char* cb = (const char*)p.c + xo;
+    const char* dyb = (const char*)p.dy + xo;
+    const char* ab = (const char*)p.a + xo;
+    const int64_t rs = p.sx_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const int64_t dfull = (int64_t)D << p.hshift;
+    const int64_t slot = ((wk.b * p.H + head) * p.nruns + wk.run) * dfull + half * D;
+
+    float eps[CPL], prod[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; prod[m] = 1.f; }
+    int buf = 0;
+    const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
+        const int64_t r0 = wk.t_begin + k * STEP + tw * SB;
+        const int64_t tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs), ra = rsrc(ab + r0 * rs);
+        R_ cr[4], dyr[4], ar[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+            cr[r].template load<kBwdLoad>(rc, o);
+            dyr[r].template load<kBwdLoad>(rdy, o);
+            ar[r].template load<kBwdLoad>(ra, o);
+        }
+        float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
+        decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);   // 1 past the end
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);
+        chan_scan_rev<CPL>(av, dh, Dv, R, grp, lane);
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_df[buf][tw][n * CPL + m] = av[0][m] * Dv[0][m];
+                s_cc[buf][tw][n * CPL + m] = av[0][m] * R[0][m];
+            }
+        }
+        __syncthreads();
+#pragma unroll 1
+        for (int r = TW - 1; r >= 0; --r) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float c_ = s_cc[buf][r][n * CPL + m];
+                prod[m] *= c_;
+                eps[m] = c_ * eps[m] + s_df[buf][r][n * CPL + m];
+            }
+        }
+    }
+    store_row<IoF32, CPL>(rsrc(p.agg_v + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), eps);
+    store_row<IoF32, CPL>(rsrc(p.agg_p + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), prod);
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <class IO, int CPL, bool FEAT>
+template <class IO, int CPL, bool FEAT, int MODE>
 static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
+#define SWR_LAUNCH(KERNEL, TW_, HW_)                                                                \
+    else if (sh.tw == TW_ && sh.hw == HW_)                                                          \
+        hipLaunchKernelGGL((KERNEL), grid, dim3(TW_ * HW_ * 64), 0, stream, p);
     if (backward) {
-#define SWR_BWD(TW_, HW_)                                                                         \
-    else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
-        hipLaunchKernelGGL((swr_bwd_pc_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
-                           stream, p);
-        if (false) {}
-        SWR_BWD(8, 1) SWR_BWD(4, 1)
-        else return hipErrorInvalidValue;
-#undef SWR_BWD
+        if constexpr (MODE == kAggregate) {
+            if (false) {}
+            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 8, FEAT>), 8, 1)
+            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 4, FEAT>), 4, 1)
+            else return hipErrorInvalidValue;
+        } else {
+            if (false) {}
+            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 8, 1, FEAT, MODE>), 8, 1)
+            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
+            else return hipErrorInvalidValue;
+        }
     } else {
-#define SWR_FWD(TW_, HW_)                                                                         \
-    else if (sh.tw == TW_ && sh.hw == HW_)                                                        \
-        hipLaunchKernelGGL((swr_fwd_pc_kernel<IO, CPL, TW_, HW_, FEAT>), grid, dim3(TW_ * HW_ * 64), 0, \
-                           stream, p);
         if (false) {}
-        SWR_FWD(4, 1) SWR_FWD(2, 2)
+        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
+        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 2, 2, FEAT, MODE>), 2, 2)
         else return hipErrorInvalidValue;
-#undef SWR_FWD
     }
+#undef SWR_LAUNCH
     return hipGetLastError();
+}
+
+template <class IO, int CPL, bool FEAT>
+static hipError_t launch_pc_mode(const Params& p, const Shape& sh, bool backward, int mode, hipStream_t stream) {
+    switch (mode) {
+        case kSwr: return launch_pc<IO, CPL, FEAT, kSwr>(p, sh, backward, stream);
+        case kAggregate: return launch_pc<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
+        case kExact: return launch_pc<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <class IO, int CPL, bool FEAT, int MODE>
@@ -1811,11 +1925,10 @@ template <class IO, bool FEAT>
 static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
                              int mode, hipStream_t stream) {
     if (per_channel) {
-        if (mode != kSwr) return hipErrorInvalidValue;
         switch (D) {   // channels of a virtual head (at most 64)
-            case 16: return launch_pc<IO, 1, FEAT>(p, sh, backward, stream);
-            case 32: return launch_pc<IO, 2, FEAT>(p, sh, backward, stream);
-            case 64: return launch_pc<IO, 4, FEAT>(p, sh, backward, stream);
+            case 16: return launch_pc_mode<IO, 1, FEAT>(p, sh, backward, mode, stream);
+            case 32: return launch_pc_mode<IO, 2, FEAT>(p, sh, backward, mode, stream);
+            case 64: return launch_pc_mode<IO, 4, FEAT>(p, sh, backward, mode, stream);
             default: return hipErrorInvalidValue;
         }
     }

@@ -40,7 +40,8 @@ struct Params {
     // with run aggregates, a carrier scan over runs, reconstruction); the
     // arrays live in the caller's workspace.
     float* agg_v;       // [B*H][nruns][D]: each run's end state started from zero (stage I out)
-    float* agg_p;       // [B*H][nruns]: each run's decay product (stage I out)
+    float* agg_p;       // [B*H][nruns]: each run's decay product (stage I out); per channel,
+                        // [B*H][nruns][D], with a per-channel decay
     const float* carry; // [B*H][nruns][D]: the state entering each run (stage III in); for the
                         // backward, the adjoint entering each run from its end
     const float* h0;    // [B][H][D] initial state (backward stage III), or NULL for zero
@@ -68,6 +69,7 @@ struct ScanParams {
     int64_t nruns;
     int32_t D;
     int32_t reverse;
+    int32_t p_per_channel;   // agg_p holds one product per channel ([B*H][nruns][D])
 };
 
 // Recurrent (token-by-token) steps: K tokens at positions t0 .. t0+K-1 of

@@ -263,13 +263,19 @@ def test_exact_workspace_bytes():
     assert swr.swr_exact_workspace_bytes(p) == 8 * 16 * nr * (2 * 128 + 1) * 4
     assert swr.swr_exact_workspace_bytes(problem(T=0)) == 0
     lib = swr.load()
-    assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(per_channel=True))) == E_UNSUP
+    # a per-channel decay keeps one run decay product per channel
+    pc = problem(B=2, T=256, H=4, D=64, block=64, per_channel=True)
+    info = swr.swr_launch_info(pc)
+    nr = max(-(-256 // info["fwd_run_len"]), -(-256 // info["bwd_run_len"]))
+    assert swr.swr_exact_workspace_bytes(pc) == 2 * 4 * nr * (3 * 64) * 4
     assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(block=48))) == E_BLOCK
 
 
 def test_exact_validation():
     p = problem()
-    assert xfwd(problem(per_channel=True)) == E_UNSUP and xbwd(problem(per_channel=True)) == E_UNSUP
+    # a per-channel decay takes x's layout and lane-vector alignment (bf16, D = 64: 8 bytes)
+    assert xfwd(problem(per_channel=True), a=A + 2) == E_ALIGN
+    assert xbwd(problem(per_channel=True), da=DA + 8) == E_ALIGN
     assert xfwd(problem(D=48)) == E_UNSUP and xbwd(problem(block=48)) == E_BLOCK
     for kw in ("x", "a", "b", "c", "y", "ws"):
         assert xfwd(p, **{kw: 0}) == E_NULL, kw

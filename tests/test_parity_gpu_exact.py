@@ -108,6 +108,53 @@ def test_exact_small_against_oracle(swr, B, T, H, D, block, dtype, run_len):
     check_exact(prob, h0, dhl, y, v, hl, grads, what=f"exact {B}x{T}x{H}x{D} l{block} {dtype}")
 
 
+PC = [
+    # (B, T, H, D, block, dtype): per-channel decay; D = 128 runs as two 64-channel halves
+    (1, 64, 1, 16, 16, "f32"),
+    (2, 1000, 3, 64, 64, "f32"),
+    (1, 777, 2, 128, 128, "bf16"),
+    (2, 300, 2, 32, 32, "bf16"),
+    (1, 1, 1, 64, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype", PC)
+@pytest.mark.parametrize("run_len", [0, "min"])
+def test_exact_per_channel_against_oracle(swr, B, T, H, D, block, dtype, run_len):
+    rl = max(64, block) if run_len == "min" else 0
+    prob = W.random_problem(71 + T + D, B, T, H, D, block, dtype, "sigmoid", 2.0, per_channel=True)
+    rng = np.random.default_rng(T + 1)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl, run_len=rl)
+    check_exact(prob, h0, dhl, y, v, hl, grads, what=f"exact pc {B}x{T}x{H}x{D} l{block} {dtype}")
+
+
+def test_exact_per_channel_featurised_residual(swr):
+    prob = W.random_problem(72, 2, 300, 2, 128, 64, "bf16", "sigmoid", 3.0, per_channel=True, logits=True)
+    rng = np.random.default_rng(9)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl, residual=True, run_len=128, **feat)
+    check_exact(prob, h0, dhl, y, v, hl, grads, residual=True, what="pc residual+sigmoid", **feat)
+
+
+def test_exact_per_channel_constant_equals_shared(swr):
+    # a decay constant across channels: the per-channel path gives the shared
+    # path's outputs, and its da summed over channels is the shared da.
+    prob = W.random_problem(73, 1, 500, 2, 64, 64, "f32", "sigmoid", 2.0)
+    x, a, b, c, dy = (to_device(getattr(prob, n), "f32") for n in ("x", "a", "b", "c", "dy"))
+    apc = a[..., None].expand(-1, -1, -1, 64).contiguous()
+    y1, v1 = swr.swr_exact_forward(x, a, b, c, 64, save_carriers=True)
+    y2, v2 = swr.swr_exact_forward(x, apc, b, c, 64, save_carriers=True)
+    g1 = swr.swr_exact_backward(x, a, b, c, dy, v1, 64)
+    g2 = swr.swr_exact_backward(x, apc, b, c, dy, v2, 64)
+    torch.cuda.synchronize()
+    assert_close(to_host(y2), to_host(y1), "f32", "pc vs shared y")
+    for name, u, w in zip(("dx", "db", "dc"), (g2[0], g2[2], g2[3]), (g1[0], g1[2], g1[3])):
+        assert_close(to_host(u), to_host(w), "f32", "pc vs shared " + name)
+    assert_close(to_host(g2[1]).sum(-1), to_host(g1[1]), "f32", "pc vs shared da")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_exact_without_states(swr, dtype):
     prob = W.random_problem(41, 2, 640, 2, 64, 64, dtype, "sigmoid", 3.0)
