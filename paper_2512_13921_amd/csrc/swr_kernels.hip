@@ -253,11 +253,20 @@ __device__ inline float load_scalar(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 // every finite z.
 __device__ inline float sigmoid(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
-// d sigmoid / dz = sigmoid(z) sigmoid(-z), without the cancellation of 1 - sigmoid(z).
-__device__ inline float dsigmoid(float z) { return sigmoid(z) * sigmoid(-z); }
-
 // The pre-gate value b of a loaded element (a logit when sig is set).
 __device__ inline float pregate(float z, int sig) { return sig ? sigmoid(z) : z; }
+
+// sigmoid(z) and its slope from one exponential and one reciprocal:
+// with E = e^-z and s = 1 / (1 + E), sigmoid(-z) = E s, so the slope
+// sigmoid(z) sigmoid(-z) is E s^2 (0 where E overflows, its limit).
+struct SigSlope {
+    float s, ds;
+};
+__device__ inline SigSlope sigmoid_slope(float z) {
+    const float E = __expf(-z);
+    const float s = __builtin_amdgcn_rcpf(1.0f + E);
+    return {s, __builtin_isinf(E) ? 0.0f : (E * s) * s};
+}
 
 // The same value, opaque to the compiler: a function of it computed again is
 // recomputed rather than kept alive in registers since its first use.
@@ -862,8 +871,9 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
         float ds_n = 1.0f;      // d a / d(input) of token n: 1, or sigma'(z) for a logit z
         if (sig_a) {
-            ds_n = dsigmoid(a_n);
-            a_n = r0 + n < wk.t_end ? sigmoid(a_n) : 0.0f;
+            const SigSlope g = sigmoid_slope(a_n);
+            ds_n = g.ds;
+            a_n = r0 + n < wk.t_end ? g.s : 0.0f;
         }
         // Exact recurrence: past the end of the sequence the decay is 1, so
         // the adjoint entering from the end reaches the last token intact.
@@ -1002,10 +1012,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 vdc[m] = dyv * W[m][r];
                 const float du = Dl[m][r] + Rr[r] * epsin[m];          // adjoint of u
                 const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
-                vdx[m] = pregate(zb, sig_b) * du;
+                const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
+                vdx[m] = g.s * du;
                 if (p.residual) vdx[m] += dyv;
-                vdb[m] = xr[r].get(m) * du;
-                if (sig_b) vdb[m] *= dsigmoid(zb);
+                vdb[m] = xr[r].get(m) * du * g.ds;
                 acc += (r == 0 ? hup[m] : W[m][r - 1]) * du;
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
@@ -1752,12 +1762,12 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 vdc[m] = dyv * W[r][m];
                 const float du = Dv[r][m] + Rr[r][m] * epsin[m];
                 const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
-                vdx[m] = pregate(zb, sig_b) * du;
+                const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
+                vdx[m] = g.s * du;
                 if (p.residual) vdx[m] += dyv;
-                vdb[m] = xr[r].get(m) * du;
-                if (sig_b) vdb[m] *= dsigmoid(zb);
+                vdb[m] = xr[r].get(m) * du * g.ds;
                 vda[m] = (r == 0 ? hup[m] : W[r - 1][m]) * du - Gsh[r][m] * Rr[r][m] * kd[m];
-                if (sig_a) vda[m] *= dsigmoid(ar[r].get(m));
+                if (sig_a) vda[m] *= sigmoid_slope(ar[r].get(m)).ds;
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
