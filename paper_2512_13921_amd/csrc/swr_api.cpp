@@ -326,10 +326,22 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
 
 namespace {
 
+// The backward's stage I reads only c, dy and a and has no block structure:
+// it runs 4-wave groups over runs finer than the backward's own (halving
+// them while fewer than ~2048 groups would result), so that it streams at
+// the rate of a read-only pass.  Returns the aggregate run length (a
+// divisor of the backward's run length, a multiple of 64 tokens).
+int64_t bwd_agg_len(const swr_problem_t* p, const Resolved& r) {
+    const int64_t seqs = p->B * r.hv;
+    int64_t len = r.run_len;
+    while (len % 128 == 0 && seqs * ((p->T + len - 1) / len) < 2048) len /= 2;
+    return len;
+}
+
 // Workspace of the exact recurrence, in float32 elements: per (batch, head)
-// and run, the run's aggregate end state (D), the value entering the run (D)
-// and the run's decay product (1), for the larger of the two launches' run
-// counts.
+// and aggregate run, the run's aggregate end state (D), the value entering
+// the run (D) and the run's decay product (1, or D for a per-channel decay),
+// for the largest of the launches' run counts.
 struct ExactWs {
     int64_t nr;       // runs per sequence the workspace is laid out for
     int64_t floats;   // total float32 elements
@@ -337,7 +349,8 @@ struct ExactWs {
 
 ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
     ExactWs w;
-    w.nr = std::max(r.nruns, r.nruns_f);
+    const int64_t na = r.empty ? 0 : (p->T + bwd_agg_len(p, r) - 1) / bwd_agg_len(p, r);
+    w.nr = std::max(std::max(r.nruns, r.nruns_f), na);
     // a per-channel decay has one run decay product per channel
     w.floats = p->B * p->H * w.nr * (2 * p->D + (r.pc ? p->D : 1));
     return w;
@@ -400,6 +413,7 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c;
     k.agg_v = wv; k.agg_p = wp; k.carry = wc;
+    k.agg_len = k.run_len; k.agg_nruns = k.nruns;
     // Stage I: local solves of every run, keeping each run's end state and decay product.
     if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kAggregate, stream) != hipSuccess)
         return SWR_ERR_HIP;
@@ -455,13 +469,22 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     swr::Params k = make_params(p, r, true);
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.agg_v = wv; k.agg_p = wp; k.carry = wc; k.h0 = h0;
-    // Stage I: reverse local solves of every run (from c, dy, a).
-    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kAggregate, stream) != hipSuccess)
-        return SWR_ERR_HIP;
-    // Stage II: the reverse carrier recurrence over the runs, from dh_last; dh0 is its final value.
+    k.agg_len = r.empty ? 1 : bwd_agg_len(p, r);
+    k.agg_nruns = r.empty ? 0 : (p->T + k.agg_len - 1) / k.agg_len;
+    // Stage I: reverse local solves of every aggregate run (from c, dy, a), 4-wave groups.
+    if (!r.empty) {
+        swr::Params ka = k;
+        ka.run_len = k.agg_len;
+        ka.nruns = k.agg_nruns;
+        ka.nwork = p->B * r.hv * k.agg_nruns;
+        if (swr::launch(ka, p->dtype, r.dk, swr::Shape{4, 1}, true, r.pc, swr::kAggregate, stream) != hipSuccess)
+            return SWR_ERR_HIP;
+    }
+    // Stage II: the reverse carrier recurrence over the aggregate runs, from dh_last; dh0 is
+    // its final value.
     swr::ScanParams q{};
     q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = dh_last; q.fin = dh0;
-    q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 1;
+    q.seqs = seqs; q.nruns = k.agg_nruns; q.D = (int32_t)p->D; q.reverse = 1;
     q.p_per_channel = r.pc ? 1 : 0;
     if ((dh0 || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
     if (r.empty) return SWR_OK;

@@ -541,7 +541,8 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; }
     if constexpr (MODE == kExact) {   // the exact state entering the run (stage II's result)
         Row<IoF32, CPL> ci;
-        ci.load(rsrc(p.carry + slot * D), (uint32_t)(n * CPL) * 4u);
+        const int64_t j = (wk.b * p.H + wk.h) * p.agg_nruns + wk.t_begin / p.agg_len;
+        ci.load(rsrc(p.carry + j * D), (uint32_t)(n * CPL) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) e[m] = ci.get(m);
     }
@@ -786,7 +787,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     const int64_t seq = wk.b * p.H + wk.h;
     if constexpr (MODE == kExact) {   // the exact adjoint entering the run's end (stage II)
         Row<IoF32, CPL> ci;
-        ci.load(rsrc(p.carry + (seq * p.nruns + wk.run) * D), (uint32_t)(n * CPL) * 4u);
+        const int64_t j = seq * p.agg_nruns + (wk.t_end - 1) / p.agg_len;   // the run's last aggregate
+        ci.load(rsrc(p.carry + j * D), (uint32_t)(n * CPL) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) eps[m] = ci.get(m);
     }
@@ -1420,7 +1422,8 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; prod[m] = 1.f; }
     if constexpr (MODE == kExact) {
         Row<IoF32, CPL> ci;
-        ci.load(rsrc(p.carry + slot), (uint32_t)(n * CPL) * 4u);
+        const int64_t j = (wk.b * p.H + head) * p.agg_nruns + wk.t_begin / p.agg_len;
+        ci.load(rsrc(p.carry + j * dfull + half * D), (uint32_t)(n * CPL) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) e[m] = ci.get(m);
     }
@@ -1566,7 +1569,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     const int64_t seq = wk.b * p.H + head;
     if constexpr (MODE == kExact) {   // the exact adjoint entering the run's end (stage II)
         Row<IoF32, CPL> ci;
-        ci.load(rsrc(p.carry + (seq * p.nruns + wk.run) * dfull + half * D), (uint32_t)(n * CPL) * 4u);
+        const int64_t j = seq * p.agg_nruns + (wk.t_end - 1) / p.agg_len;   // the run's last aggregate
+        ci.load(rsrc(p.carry + j * dfull + half * D), (uint32_t)(n * CPL) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) eps[m] = ci.get(m);
     }

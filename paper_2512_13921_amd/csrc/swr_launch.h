@@ -45,6 +45,9 @@ struct Params {
     const float* carry; // [B*H][nruns][D]: the state entering each run (stage III in); for the
                         // backward, the adjoint entering each run from its end
     const float* h0;    // [B][H][D] initial state (backward stage III), or NULL for zero
+    int64_t agg_len;    // stage III: tokens per aggregate run of stage I (this launch's run
+                        // length divides by it), and their number per sequence
+    int64_t agg_nruns;
 };
 
 // What a forward or backward launch computes.

@@ -255,10 +255,21 @@ def xbwd(p, x=X, a=A, b=B_, c=C, dy=DY, h0=H0, v_=V, dhl=DHL, dx=DX, da=DA, db=D
                                          v(dhl), v(dx), v(da), v(db), v(dc), v(dh0), v(ws), None)
 
 
+def _agg_runs(T, seqs, bwd_run_len):
+    # the exact backward's stage I halves the backward's runs while fewer
+    # than 2048 groups would result (keeping a multiple of 64 tokens)
+    agg = bwd_run_len
+    while agg % 128 == 0 and seqs * (-(-T // agg)) < 2048:
+        agg //= 2
+    return -(-T // agg)
+
+
 def test_exact_workspace_bytes():
     p = problem(B=8, T=16384, H=16, D=128, block=128)
     info = swr.swr_launch_info(p)
-    nr = max(-(-16384 // info["fwd_run_len"]), -(-16384 // info["bwd_run_len"]))
+    nr = max(-(-16384 // info["fwd_run_len"]), -(-16384 // info["bwd_run_len"]),
+             _agg_runs(16384, 8 * 16, info["bwd_run_len"]))
+    assert nr == 16           # 1024-token aggregate runs: 2048 stage-I groups
     # per (batch, head) and run: aggregate end state, entering state (D each), decay product
     assert swr.swr_exact_workspace_bytes(p) == 8 * 16 * nr * (2 * 128 + 1) * 4
     assert swr.swr_exact_workspace_bytes(problem(T=0)) == 0
@@ -266,7 +277,8 @@ def test_exact_workspace_bytes():
     # a per-channel decay keeps one run decay product per channel
     pc = problem(B=2, T=256, H=4, D=64, block=64, per_channel=True)
     info = swr.swr_launch_info(pc)
-    nr = max(-(-256 // info["fwd_run_len"]), -(-256 // info["bwd_run_len"]))
+    nr = max(-(-256 // info["fwd_run_len"]), -(-256 // info["bwd_run_len"]),
+             _agg_runs(256, 2 * 4, info["bwd_run_len"]))
     assert swr.swr_exact_workspace_bytes(pc) == 2 * 4 * nr * (3 * 64) * 4
     assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(block=48))) == E_BLOCK
 
