@@ -95,6 +95,7 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // B=8, T=16384, H=16, D=128: the hint on the forward's loads and stores
 // takes it from 413 to 372 us; on any of the backward's loads or stores it
 // makes the backward slower (783 us -> 803-870 us), so it keeps the default.
+// The exact backward's stage I (reads only) takes the hint: 1014 -> 978 us.
 #ifndef SWR_FWD_LOAD_POLICY
 #define SWR_FWD_LOAD_POLICY 2
 #endif
@@ -113,6 +114,10 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 #ifndef SWR_BWD_DECAY_POLICY
 #define SWR_BWD_DECAY_POLICY SWR_BWD_LOAD_POLICY
 #endif
+#ifndef SWR_AGG_LOAD_POLICY
+#define SWR_AGG_LOAD_POLICY 2
+#endif
+constexpr int kAggLoad = SWR_AGG_LOAD_POLICY;     // the exact backward's stage I
 constexpr int kFwdDecay = SWR_FWD_DECAY_POLICY;   // loads of a
 constexpr int kBwdDecay = SWR_BWD_DECAY_POLICY;
 constexpr int kFwdLoad = SWR_FWD_LOAD_POLICY;
@@ -1074,10 +1079,10 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_agg_kernel(Params p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
-            cr[r].template load<kBwdLoad>(rc, o);
-            dyr[r].template load<kBwdLoad>(rdy, o);
+            cr[r].template load<kAggLoad>(rc, o);
+            dyr[r].template load<kAggLoad>(rdy, o);
         }
-        float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+        float a_n = load_scalar<IO, kAggLoad>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
         if (sig_a) a_n = sigmoid(a_n);
         if (r0 + n >= p.T) a_n = 1.0f;
         float LT[4];
@@ -1820,9 +1825,9 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
-            cr[r].template load<kBwdLoad>(rc, o);
-            dyr[r].template load<kBwdLoad>(rdy, o);
-            ar[r].template load<kBwdLoad>(ra, o);
+            cr[r].template load<kAggLoad>(rc, o);
+            dyr[r].template load<kAggLoad>(rdy, o);
+            ar[r].template load<kAggLoad>(ra, o);
         }
         float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
         decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);   // 1 past the end
