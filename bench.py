@@ -177,10 +177,28 @@ def decode_bench(args, cfg, swr, torch):
     for i in range(min(args.warmup, n)):
         step(i, y)
     torch.cuda.synchronize()
+    # Eager calls: what a Python caller sees (host launch overhead included).
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(n):
         step(i, y)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_eager = e0.elapsed_time(e1) / n
+    # The same n steps captured once in a HIP graph and replayed: the device
+    # time per step, as a decoder that captures its step would see it.
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(n):
+                step(i, y)
+    torch.cuda.current_stream().wait_stream(s)
+    g.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    g.replay()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / n
@@ -202,6 +220,8 @@ def decode_bench(args, cfg, swr, torch):
                    "recurrence": "exact (untruncated)" if exact else "jagged window"},
         "bytes_per_step": nbytes,
         "us_per_step": ms * 1e3,
+        "us_per_step_eager": ms_eager * 1e3,
+        "timing": "HIP graph of the timed steps, replayed once (us_per_step_eager: Python calls)",
         "GB/s": nbytes / (ms * 1e-3) / 1e9,
         "cpu_baseline": None,
     }
@@ -252,9 +272,6 @@ def main():
     feat = dict(sigmoid_decay=args.sigmoid, sigmoid_pregate=args.sigmoid)
     exact = args.recurrence == "exact"
     if exact:
-        if cfg.per_channel:
-            print("the exact recurrence is built for the per-head decay only", file=sys.stderr)
-            return 2
         cfg = cfg.with_(name=cfg.name + "_exact")
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
@@ -268,7 +285,7 @@ def main():
     stream = torch.cuda.current_stream()
     if exact:
         wsp = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
-                               x.stride()[:3], a.stride()[:3], False, args.run_len)
+                               x.stride()[:3], a.stride()[:3], False, args.run_len, cfg.per_channel)
         workspace = torch.empty(max(swr.swr_exact_workspace_bytes(wsp) // 4, 1), dtype=torch.float32,
                                 device=x.device)
     torch.cuda.synchronize()

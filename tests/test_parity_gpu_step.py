@@ -144,3 +144,39 @@ def test_step_empty_calls_keep_state(swr):
     z = swr.swr_decode_state(x, a, torch.empty((2, 3, 0, 64), device="cuda"), 64)
     torch.cuda.synchronize()
     assert torch.equal(st, keep) and torch.equal(h, hk) and torch.count_nonzero(z) == 0
+
+
+def test_step_in_a_captured_graph(swr):
+    # Decoding steps captured once in a HIP graph and replayed: every replay
+    # (from the same starting state) reproduces the eager calls bit for bit.
+    prob = W.random_problem(65, 2, 24, 2, 128, 16, "bf16", "sigmoid", 2.0, with_dy=False)
+    x, a, b, c = _dev(prob)
+    st0 = torch.randn(2, 2, 2, 128, device="cuda")
+    st = st0.clone()
+    y_eager = torch.empty_like(x)
+    for t in range(24):
+        s = slice(t, t + 1)
+        swr.swr_step(x[:, s], a[:, s], b[:, s], c[:, s], 16, 40 + t, st, y=y_eager[:, s])
+    torch.cuda.synchronize()
+    st_eager = st.clone()
+
+    st.copy_(st0)
+    y = torch.zeros_like(x)
+    g = torch.cuda.CUDAGraph()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(g, stream=stream):
+            for t in range(24):
+                s = slice(t, t + 1)
+                swr.swr_step(x[:, s], a[:, s], b[:, s], c[:, s], 16, 40 + t, st, y=y[:, s])
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        st.copy_(st0)
+        y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), rep
+        assert torch.equal(st, st_eager), rep
