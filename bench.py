@@ -162,7 +162,9 @@ def decode_bench(args, cfg, swr, torch):
     g = torch.Generator(device="cuda").manual_seed(cfg.seed)
     n = args.steps
     x, b, c = (torch.randn(B, n, H, D, device="cuda", generator=g).to(dt) for _ in range(3))
-    a = torch.sigmoid(torch.randn(B, n, H, device="cuda", generator=g) + 3.0).to(dt)
+    per_channel = args.decay == "channel"
+    a = torch.sigmoid(torch.randn((B, n, H, D) if per_channel else (B, n, H), device="cuda",
+                                  generator=g) + 3.0).to(dt)
     y = torch.empty_like(x)
     state = torch.zeros((B, H, D) if exact else (B, H, 2, D), dtype=torch.float32, device="cuda")
     t0 = cfg.T
@@ -203,7 +205,7 @@ def decode_bench(args, cfg, swr, torch):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / n
     e = 2 if cfg.dtype == "bf16" else 4
-    nbytes = B * H * (e * (4 * D + 1) + 4 * D * (2 if exact else 4))
+    nbytes = B * H * (e * (3 * D + (D if per_channel else 1)) + e * D + 4 * D * (2 if exact else 4))
     out = {
         "metric": "SWR recurrent decoding step (one token per sequence)",
         "value": B / (ms * 1e-3),
@@ -215,8 +217,9 @@ def decode_bench(args, cfg, swr, torch):
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded device draws)",
-        "config": {"workload": cfg.name + ("_exact" if exact else "") + "_decode", "B": B, "H": H, "d": D,
-                   "block": cfg.block, "prompt_len": cfg.T,
+        "config": {"workload": cfg.name + ("_perchannel" if per_channel else "") + ("_exact" if exact else "")
+                   + "_decode", "B": B, "H": H, "d": D, "block": cfg.block, "prompt_len": cfg.T,
+                   "decay": "per channel" if per_channel else "per head",
                    "recurrence": "exact (untruncated)" if exact else "jagged window"},
         "bytes_per_step": nbytes,
         "us_per_step": ms * 1e3,

@@ -1150,6 +1150,70 @@ __global__ __launch_bounds__(256) void swr_scan_kernel(ScanParams q) {
 }
 
 // ---------------------------------------------------------------------------
+// Plain global accesses (per-lane 64-bit addresses)
+// ---------------------------------------------------------------------------
+//
+// The buffer accesses above take their base address from a wave-uniform
+// resource; where every lane addresses a different (batch, head), as in the
+// decoding kernels below, a per-lane base would make the compiler loop over
+// the lanes' distinct resources.  These load and store a lane's row slice
+// through an ordinary pointer instead.
+
+template <class IO, int CPL>
+__device__ inline void gload(Row<IO, CPL>& r, const void* p) {
+    constexpr int BYTES = Row<IO, CPL>::BYTES;
+    if constexpr (BYTES == 2) {
+        r.w[0] = *(const uint16_t*)p;
+    } else if constexpr (BYTES == 4) {
+        r.w[0] = *(const uint32_t*)p;
+    } else if constexpr (BYTES == 8) {
+        const uint2 v = *(const uint2*)p;
+        r.w[0] = v.x; r.w[1] = v.y;
+    } else {
+#pragma unroll
+        for (int i = 0; i < BYTES / 16; ++i) {
+            const uint4 v = ((const uint4*)p)[i];
+            r.w[4 * i + 0] = v.x; r.w[4 * i + 1] = v.y; r.w[4 * i + 2] = v.z; r.w[4 * i + 3] = v.w;
+        }
+    }
+}
+
+template <class IO, int CPL>
+__device__ inline void gstore(void* p, const float (&v)[CPL]) {
+    constexpr int BYTES = CPL * IO::ES;
+    uint32_t w[BYTES >= 4 ? BYTES / 4 : 1];
+    if constexpr (IO::ES == 2) {
+        if constexpr (CPL == 1) {
+            *(uint16_t*)p = (uint16_t)IoBf16::from_f32(v[0]);
+            return;
+        } else {
+#pragma unroll
+            for (int i = 0; i < CPL / 2; ++i)
+                w[i] = IoBf16::from_f32(v[2 * i]) | (IoBf16::from_f32(v[2 * i + 1]) << 16);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) w[i] = __builtin_bit_cast(uint32_t, v[i]);
+    }
+    if constexpr (BYTES == 4) {
+        *(uint32_t*)p = w[0];
+    } else if constexpr (BYTES == 8) {
+        *(uint2*)p = uint2{w[0], w[1]};
+    } else if constexpr (BYTES >= 16) {
+#pragma unroll
+        for (int i = 0; i < BYTES / 16; ++i) ((uint4*)p)[i] = uint4{w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
+    }
+}
+
+template <class IO>
+__device__ inline float gload_scalar(const void* p) {
+    if constexpr (IO::ES == 2)
+        return IoBf16::to_f32(*(const uint16_t*)p);
+    else
+        return *(const float*)p;
+}
+
+// ---------------------------------------------------------------------------
 // Recurrent steps (decoding)
 // ---------------------------------------------------------------------------
 //
@@ -1179,8 +1243,8 @@ __global__ __launch_bounds__(256) void swr_step_kernel(StepParams q) {
     float e[CPL], s[CPL];
     {
         Row<IoF32, CPL> re, rs_;
-        re.load(rsrc(st), 0u);
-        if constexpr (!EXACT) rs_.load(rsrc(st + D), 0u);
+        gload(re, st);
+        if constexpr (!EXACT) gload(rs_, st + D);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) {
             e[m] = re.get(m);
@@ -1190,16 +1254,16 @@ __global__ __launch_bounds__(256) void swr_step_kernel(StepParams q) {
     for (int64_t k = 0; k < q.K; ++k) {
         const int64_t t = q.t0 + k;
         Row<IO, CPL> xr, br, cr, ar;
-        xr.load(rsrc((const char*)q.x + xo + k * rs), 0u);
-        br.load(rsrc((const char*)q.b + xo + k * rs), 0u);
-        cr.load(rsrc((const char*)q.c + xo + k * rs), 0u);
+        gload(xr, (const char*)q.x + xo + k * rs);
+        gload(br, (const char*)q.b + xo + k * rs);
+        gload(cr, (const char*)q.c + xo + k * rs);
         float av[CPL];
         if constexpr (PC) {
-            ar.load(rsrc((const char*)q.a + ao + k * as), 0u);
+            gload(ar, (const char*)q.a + ao + k * as);
 #pragma unroll
             for (int m = 0; m < CPL; ++m) av[m] = ar.get(m);
         } else {
-            const float a1 = load_scalar<IO>(rsrc((const char*)q.a + ao + k * as), 0u);
+            const float a1 = gload_scalar<IO>((const char*)q.a + ao + k * as);
 #pragma unroll
             for (int m = 0; m < CPL; ++m) av[m] = a1;
         }
@@ -1215,10 +1279,10 @@ __global__ __launch_bounds__(256) void swr_step_kernel(StepParams q) {
             yv[m] = cr.get(m) * e[m];
             if (q.residual) yv[m] += xr.get(m);
         }
-        store_row<IO, CPL>(rsrc((char*)q.y + xo + k * rs), 0u, yv);
+        gstore<IO, CPL>((char*)q.y + xo + k * rs, yv);
     }
-    store_row<IoF32, CPL>(rsrc(st), 0u, e);
-    if constexpr (!EXACT) store_row<IoF32, CPL>(rsrc(st + D), 0u, s);
+    gstore<IoF32, CPL>(st, e);
+    if constexpr (!EXACT) gstore<IoF32, CPL>(st + D, s);
 }
 
 // The jagged window's state after tokens 0 .. T-1, from the forward's block
@@ -1243,9 +1307,12 @@ __global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
         const int64_t tau = (q.T - 1) >> q.lshift, t_blk = tau << q.lshift;
         const float* vb = q.carriers + seq * q.nblocks * D + n * CPL;
         Row<IoF32, CPL> rv, rp;
-        rv.load(rsrc(vb + tau * D), 0u);
-        rp.load(rsrc(vb + (tau - 1) * D), in_range(tau > 0, 0u));
-        const int64_t ao = (bb * q.sa_b + hh * q.sa_h) * ES + (PC ? n * CPL * ES : 0);
+        gload(rv, vb + tau * D);
+        if (tau > 0)
+            gload(rp, vb + (tau - 1) * D);
+        else
+            rp.zero();
+        const char* ab = (const char*)q.a + (bb * q.sa_b + hh * q.sa_h) * ES + (PC ? n * CPL * ES : 0);
         const int64_t as = q.sa_t * ES;
         float G[CPL];
 #pragma unroll
@@ -1253,11 +1320,11 @@ __global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
         for (int64_t t = t_blk; t < q.T; ++t) {
             if constexpr (PC) {
                 Row<IO, CPL> ar;
-                ar.load(rsrc((const char*)q.a + ao + t * as), 0u);
+                gload(ar, ab + t * as);
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) G[m] *= sig_a ? sigmoid(ar.get(m)) : ar.get(m);
             } else {
-                const float a1 = load_scalar<IO>(rsrc((const char*)q.a + ao + t * as), 0u);
+                const float a1 = gload_scalar<IO>(ab + t * as);
                 const float a_ = sig_a ? sigmoid(a1) : a1;
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) G[m] *= a_;
@@ -1270,8 +1337,8 @@ __global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
         }
     }
     float* st = q.state + seq * 2 * D + n * CPL;
-    store_row<IoF32, CPL>(rsrc(st), 0u, e);
-    store_row<IoF32, CPL>(rsrc(st + D), 0u, s);
+    gstore<IoF32, CPL>(st, e);
+    gstore<IoF32, CPL>(st + D, s);
 }
 
 // ---------------------------------------------------------------------------
