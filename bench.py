@@ -150,6 +150,49 @@ def cpu_baseline(cfg, prob, budget_s=10.0, exact=False):
     }
 
 
+# The paper's forward times of its B2P kernel at this shape (Sec. 6, the
+# mixer forward-time figure; H100, batch not stated), in ms.
+PAPER_B2P_FWD_MS = {1024: 0.04324, 2048: 0.07401, 4096: 0.115, 8192: 0.201, 16384: 0.362,
+                    32768: 0.682, 65536: 1.31, 131072: 2.568, 262144: 5.055, 524288: 10.033}
+
+
+def paper_shape_bench(args, swr, torch):
+    """Forward-only sweep at the shape the paper times its own kernel on
+    (model width 2048 as 128 heads of 16 channels, block 16), B = 1, bf16,
+    synthetic inputs drawn on the device.  The paper's numbers come from
+    another GPU and are context, not a target."""
+    H, D, l = 128, 16, 16
+    rows = []
+    g = torch.Generator(device="cuda").manual_seed(0)
+    for T in sorted(PAPER_B2P_FWD_MS):
+        x, b, c = (torch.randn(1, T, H, D, device="cuda", generator=g).to(torch.bfloat16) for _ in range(3))
+        a = torch.sigmoid(torch.randn(1, T, H, device="cuda", generator=g) + 3.0).to(torch.bfloat16)
+        y = torch.empty_like(x)
+        for _ in range(args.warmup):
+            swr.swr_forward(x, a, b, c, l, y=y)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            swr.swr_forward(x, a, b, c, l, y=y)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        nbytes = T * H * 2 * (4 * D + 1)
+        rows.append({"T": T, "ms": ms, "GB/s": nbytes / (ms * 1e-3) / 1e9, "tokens_per_s": T / (ms * 1e-3),
+                     "paper_ms": PAPER_B2P_FWD_MS[T]})
+        log(f"[paper shape] T={T}: {ms * 1e3:.1f} us ({rows[-1]['GB/s']:.0f} GB/s), paper {PAPER_B2P_FWD_MS[T] * 1e3:.1f} us")
+        del x, b, c, a, y
+    out = {"metric": "SWR forward time at the paper's mixer shape (B=1, D=2048 = 128 heads x 16, block 16)",
+           "value": rows[-1]["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": rows[-1]["ms"], "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded device draws)",
+           "config": {"workload": "paper_shape_B1_H128_d16_l16_forward", "sweep": rows},
+           "cpu_baseline": None}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def decode_bench(args, cfg, swr, torch):
     """Recurrent decoding: K=1 token for each of the B sequences per call, at
     sequence positions following a prompt of the workload's length T.  A
@@ -246,6 +289,9 @@ def main():
                     help="a and b are logits; the kernels apply the sigmoid (fused featurisation)")
     ap.add_argument("--recurrence", choices=("window", "exact"), default="window",
                     help="the jagged-window recurrence (default) or the exact, untruncated one")
+    ap.add_argument("--paper-shape", action="store_true",
+                    help="forward-only sweep at the paper's own mixer-timing shape (B=1, D=2048 as "
+                         "H=128 heads of d=16, block 16, bf16) over T = 1K .. 512K")
     ap.add_argument("--decode", action="store_true",
                     help="time recurrent decoding instead: one token per sequence per call "
                          "(swr_step / swr_exact_step) after a prompt of the workload's length")
@@ -267,6 +313,8 @@ def main():
     cfg = W.CONFIGS[args.config]
     if args.decode:
         return decode_bench(args, cfg, swr, torch)
+    if args.paper_shape:
+        return paper_shape_bench(args, swr, torch)
     if args.decay == "channel":
         cfg = W.PER_CHANNEL.get(args.config) or cfg.with_(name=cfg.name + "_perchannel", per_channel=True)
     if args.sigmoid:

@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <initializer_list>
 
 #include "../../include/swr.h"
 #include "swr_launch.h"
@@ -66,6 +67,7 @@ struct Resolved {
     int cpl;            // channels per lane of the kernels = dk / 16
     bool pc;            // per-channel decay: a and da have the [B, T, H, D] layout of x
     int hshift;         // per-channel kernels: log2 of the virtual heads per head
+    int pack;           // > 1: heads of 64 / pack channels packed into 64-channel virtual heads
     int dk;             // channels a kernel's head covers (D, or D >> hshift)
     int64_t hv;         // heads the kernels split the work over (H << hshift)
     int64_t vbytes;     // bytes of one lane's slice of an x-like row (alignment unit)
@@ -80,7 +82,7 @@ struct Resolved {
     int64_t carriers;   // float32 carriers of the whole problem
 };
 
-int resolve(const swr_problem_t* p, Resolved* r) {
+int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true) {
     if (!p) return SWR_ERR_NULL;
     if (p->abi_version != SWR_ABI_VERSION) return SWR_ERR_VERSION;
     if (p->dtype != SWR_DTYPE_F32 && p->dtype != SWR_DTYPE_BF16) return SWR_ERR_DTYPE;
@@ -96,8 +98,17 @@ int resolve(const swr_problem_t* p, Resolved* r) {
     r->pc = (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) != 0;
     r->hshift = r->pc ? swr::pc_hshift(p->D) : 0;
     r->dk = (int)(p->D >> r->hshift);
+    r->pack = 1;
+    // Heads of 16 or 32 channels stored next to each other run as packed
+    // 64-channel virtual heads on the per-channel kernels (a lane slice of one
+    // such head would be 2-4 bytes); the caller's pointers may still veto it
+    // (alignment), see resolve_for.
+    if (allow_pack && !r->pc && (p->D == 16 || p->D == 32) && p->H % (64 / p->D) == 0 && p->sx_h == p->D) {
+        r->pack = (int)(64 / p->D);
+        r->dk = 64;
+    }
     r->cpl = r->dk / 16;
-    r->hv = p->H << r->hshift;
+    r->hv = r->pack > 1 ? p->H / r->pack : p->H << r->hshift;
     r->vbytes = std::min<int64_t>(16, (int64_t)(r->dk / 16) * r->es);
     r->bwd = swr::bwd_shape(p->block, r->hv);
     r->fwd = swr::fwd_shape(p->block, r->hv);
@@ -170,6 +181,18 @@ int check_strides_aligned(const swr_problem_t* p, const Resolved& r) {
 }
 
 bool aligned(const void* ptr, int64_t bytes) { return ((uintptr_t)ptr % (uintptr_t)bytes) == 0; }
+
+// resolve() for a call with these [B,T,H,D] tensors: packed small heads need
+// each lane's 64-channel row slice aligned (8 or 16 bytes); otherwise the
+// heads run one by one.
+int resolve_for(const swr_problem_t* p, Resolved* r, std::initializer_list<const void*> xs) {
+    int rc = resolve(p, r, true);
+    if (rc != SWR_OK || r->pack == 1 || r->empty) return rc;
+    bool ok = check_strides_aligned(p, *r) == SWR_OK;
+    for (const void* q : xs)
+        if (q && !aligned(q, r->vbytes)) ok = false;
+    return ok ? SWR_OK : resolve(p, r, false);
+}
 
 struct Span {
     uintptr_t lo, hi;   // [lo, hi)
@@ -244,7 +267,7 @@ namespace {
 int forward_impl(const swr_problem_t* p, const void* x, const void* a, const void* b,
                  const void* c, void* y, float* carriers, void* stream) {
     Resolved r;
-    int rc = resolve(p, &r);
+    int rc = resolve_for(p, &r, {x, b, c, (const void*)y});
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
     if (!x || !a || !b || (y && !c)) return SWR_ERR_NULL;
@@ -261,7 +284,7 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
 
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kSwr, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, swr::kSwr, stream) == hipSuccess ? SWR_OK
                                                                                         : SWR_ERR_HIP;
 }
 
@@ -289,7 +312,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
                  const void* c, const void* dy, const float* carriers, void* dx, float* da,
                  void* db, void* dc, void* stream) {
     Resolved r;
-    int rc = resolve(p, &r);
+    int rc = resolve_for(p, &r, {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc});
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
     if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc) return SWR_ERR_NULL;
@@ -314,7 +337,7 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kSwr, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, swr::kSwr, stream) == hipSuccess ? SWR_OK
                                                                                        : SWR_ERR_HIP;
 }
 
@@ -352,11 +375,11 @@ ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
     const int64_t na = r.empty ? 0 : (p->T + bwd_agg_len(p, r) - 1) / bwd_agg_len(p, r);
     w.nr = std::max(std::max(r.nruns, r.nruns_f), na);
     // a per-channel decay has one run decay product per channel
-    w.floats = p->B * p->H * w.nr * (2 * p->D + (r.pc ? p->D : 1));
+    w.floats = p->B * p->H * w.nr * (2 * p->D + (r.pc || r.pack > 1 ? p->D : 1));
     return w;
 }
 
-int resolve_exact(const swr_problem_t* p, Resolved* r) { return resolve(p, r); }
+
 
 // Pointers into the workspace for one launch.
 void exact_arrays(const swr_problem_t* p, const ExactWs& w, void* ws, float** v, float** carry, float** prod) {
@@ -372,17 +395,20 @@ void exact_arrays(const swr_problem_t* p, const ExactWs& w, void* ws, float** v,
 extern "C" {
 
 int64_t swr_exact_workspace_bytes(const swr_problem_t* problem) {
-    Resolved r;
-    const int rc = resolve_exact(problem, &r);
+    // enough for either launch plan (packed small heads or not), since the
+    // pointers of the later call decide between them
+    Resolved r, u;
+    int rc = resolve(problem, &r, true);
     if (rc != SWR_OK) return rc;
-    return exact_ws(problem, r).floats * 4;
+    if ((rc = resolve(problem, &u, false)) != SWR_OK) return rc;
+    return std::max(exact_ws(problem, r).floats, exact_ws(problem, u).floats) * 4;
 }
 
 int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
                       const void* c, const float* h0, void* y, float* carriers, float* h_last,
                       void* workspace, void* stream) {
     Resolved r;
-    int rc = resolve_exact(p, &r);
+    int rc = resolve_for(p, &r, {x, b, c, (const void*)y});
     if (rc != SWR_OK) return rc;
     const ExactWs w = exact_ws(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
@@ -415,18 +441,18 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     k.agg_v = wv; k.agg_p = wp; k.carry = wc;
     k.agg_len = k.run_len; k.agg_nruns = k.nruns;
     // Stage I: local solves of every run, keeping each run's end state and decay product.
-    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kAggregate, stream) != hipSuccess)
+    if (!r.empty && swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, swr::kAggregate, stream) != hipSuccess)
         return SWR_ERR_HIP;
     // Stage II: the carrier recurrence over the runs, from h0; h_last is its final value.
     swr::ScanParams q{};
     q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = h0; q.fin = h_last;
     q.seqs = seqs; q.nruns = r.empty ? 0 : k.nruns; q.D = (int32_t)p->D; q.reverse = 0;
-    q.p_per_channel = r.pc ? 1 : 0;
+    q.p_per_channel = r.pc || r.pack > 1 ? 1 : 0;
     if ((h_last || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
     if (r.empty) return SWR_OK;
     // Stage III: every run again from its exact entering state: outputs and exact block carriers.
     k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, swr::kExact, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, swr::kExact, stream) == hipSuccess ? SWR_OK
                                                                                           : SWR_ERR_HIP;
 }
 
@@ -435,7 +461,7 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
                        const float* dh_last, void* dx, float* da, void* db, void* dc, float* dh0,
                        void* workspace, void* stream) {
     Resolved r;
-    int rc = resolve_exact(p, &r);
+    int rc = resolve_for(p, &r, {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc});
     if (rc != SWR_OK) return rc;
     const ExactWs w = exact_ws(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
@@ -477,7 +503,8 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
         ka.run_len = k.agg_len;
         ka.nruns = k.agg_nruns;
         ka.nwork = p->B * r.hv * k.agg_nruns;
-        if (swr::launch(ka, p->dtype, r.dk, swr::Shape{4, 1}, true, r.pc, swr::kAggregate, stream) != hipSuccess)
+        if (swr::launch(ka, p->dtype, r.dk, swr::Shape{4, 1}, true, r.pc, r.pack, swr::kAggregate, stream) !=
+            hipSuccess)
             return SWR_ERR_HIP;
     }
     // Stage II: the reverse carrier recurrence over the aggregate runs, from dh_last; dh0 is
@@ -485,13 +512,13 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     swr::ScanParams q{};
     q.agg_v = wv; q.agg_p = wp; q.carry = wc; q.init = dh_last; q.fin = dh0;
     q.seqs = seqs; q.nruns = k.agg_nruns; q.D = (int32_t)p->D; q.reverse = 1;
-    q.p_per_channel = r.pc ? 1 : 0;
+    q.p_per_channel = r.pc || r.pack > 1 ? 1 : 0;
     if ((dh0 || !r.empty) && swr::launch_scan(q, stream) != hipSuccess) return SWR_ERR_HIP;
     if (r.empty) return SWR_OK;
     // Stage III: the gradients, from the adjoint entering each run and the exact block carriers.
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, swr::kExact, stream) == hipSuccess ? SWR_OK
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, swr::kExact, stream) == hipSuccess ? SWR_OK
                                                                                          : SWR_ERR_HIP;
 }
 

@@ -1447,11 +1447,60 @@ __device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int6
     }
 }
 
+// Where a lane's channels live in the per-channel kernels.  A kernel "head"
+// (virtual head) is D = CPL * 16 channels.  With a per-channel decay it is
+// one real head or one half of it (2^hshift halves).  With packed heads
+// (PK > 1: a decay per token and head, heads of 64 / PK channels stored next
+// to each other) it is PK adjacent real heads; lane n then holds channels
+// (n % (16/PK)) * CPL ... of real head n / (16/PK).  Small heads are
+// processed this way because a lane slice of one such head is only 2 or 4
+// bytes, while a lane slice of the packed row is 8 or 16.
+template <int PK, int CPL>
+struct Geo {
+    static constexpr int LPH = 16 / PK;   // lanes per real head when packed
+    int64_t head;   // first real head of the virtual head
+    int64_t half;   // channel half of a split real head, else 0
+    int64_t Dr;     // channels of a real head (the row length of carriers and states)
+    int lh;         // real head of this lane within the virtual head
+    int lch;        // first channel of this lane within its real head
+    __device__ Geo(int64_t vh, int hshift, int n) {
+        constexpr int D = CPL * SB;
+        if constexpr (PK > 1) {
+            head = vh * PK; half = 0; Dr = D / PK; lh = n / LPH; lch = (n % LPH) * CPL;
+        } else {
+            head = vh >> hshift; half = vh & ((1 << hshift) - 1); Dr = (int64_t)D << hshift;
+            lh = 0; lch = (int)half * D + n * CPL;
+        }
+    }
+    // Offset (in float32 elements) of this lane's slice of row `row` of a
+    // per-head array [B*H][rows][Dr], from the start of the virtual head's first head.
+    __device__ uint32_t off(int64_t rows, int64_t row) const {
+        return (uint32_t)((lh * rows + row) * Dr + lch);
+    }
+};
+
+// Decays of one row slice for packed heads: one scalar per lane (its real
+// head's decay), with the conventions of decay_rows.
+template <class IO, int CPL, int POL>
+__device__ inline void decay_rows_packed(__amdgpu_buffer_rsrc_t ra, uint32_t aoff, uint32_t astep, int64_t tr0,
+                                         int64_t t_lo, int64_t t_hi, int64_t T, int sig, float (&az)[4],
+                                         float (&av)[4][CPL]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int64_t t = tr0 + r;
+        const bool ok = t >= t_lo && t < t_hi;
+        az[r] = load_scalar<IO, POL>(ra, in_range(ok, aoff + (uint32_t)r * astep));
+        const float v = t >= T ? 1.0f : ok ? (sig ? sigmoid(az[r]) : az[r]) : 0.0f;
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) av[r][m] = v;
+    }
+}
+
 // Per-channel forward.  Same workgroup shape and sweep as swr_fwd_kernel;
 // wk.h is a virtual head: head wk.h >> hshift, channel half wk.h & (2^hshift - 1).
 // MODE as for swr_fwd_kernel; the exact modes keep a decay product per
 // channel for each run.
-template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE, int PK>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
@@ -1467,35 +1516,34 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const int hw = wv / TW, tw = wv % TW;
     const Work wk = decode_work<HW>(p, hw);
-    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
+    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
     const int l = p.block;
     const int smask = l / SB - 1;
     const int64_t t_lo = SWR ? max(wk.t_begin - (int64_t)l, (int64_t)0) : wk.t_begin;
     const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
-    const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + half * D) * ES;
+    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D) * ES;
     const char* xb = (const char*)p.x + xo;
     const char* bb = (const char*)p.b + xo;
     const char* cb = (const char*)p.c + xo;
-    const char* ab = (const char*)p.a + xo;
+    // per-channel decay: rows like x; packed heads: one decay per token and real head
+    const char* ab = PK > 1 ? (const char*)p.a + (wk.b * p.sa_b + geo.head * p.sa_h) * ES : (const char*)p.a + xo;
     char* yb = (char*)p.y + xo;
     const int64_t rs = p.sx_t * ES;
+    const int64_t as = PK > 1 ? p.sa_t * ES : rs;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
     const bool want_y = MODE != kAggregate && p.y != nullptr;
-    const int64_t dfull = (int64_t)D << p.hshift;   // channels of a real head: carrier row length
-    float* const vb = MODE != kAggregate && p.carriers
-                          ? p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D : nullptr;
+    const int64_t hb = wk.b * p.H + geo.head;   // first real (batch, head) of the virtual head
+    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + hb * p.nblocks * geo.Dr : nullptr;
     const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
-    // This run's aggregate / carry slot (channel offset of this virtual head included).
-    const int64_t slot = ((wk.b * p.H + head) * p.nruns + wk.run) * dfull + half * D;
 
     float e[CPL], s[CPL], prod[CPL];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { e[m] = 0.f; s[m] = 0.f; prod[m] = 1.f; }
     if constexpr (MODE == kExact) {
         Row<IoF32, CPL> ci;
-        const int64_t j = (wk.b * p.H + head) * p.agg_nruns + wk.t_begin / p.agg_len;
-        ci.load(rsrc(p.carry + j * dfull + half * D), (uint32_t)(n * CPL) * 4u);
+        ci.load(rsrc(p.carry + hb * p.agg_nruns * geo.Dr), geo.off(p.agg_nruns, wk.t_begin / p.agg_len) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) e[m] = ci.get(m);
     }
@@ -1506,7 +1554,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
         const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                     rc = rsrc(cb + r0 * rs), ra = rsrc(ab + r0 * rs);
+                                     rc = rsrc(cb + r0 * rs), ra = rsrc(ab + r0 * as);
         RW xr[4], br[4], cr[4], ar[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1515,11 +1563,16 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
             const bool in_xb = t >= t_lo && t < wk.t_end;
             xr[r].template load<kFwdLoad>(rx, in_range(in_xb, o));
             br[r].template load<kFwdLoad>(rb, in_range(in_xb, o));
-            ar[r].template load<kFwdLoad>(ra, in_range(in_xb, o));
+            if constexpr (PK == 1) ar[r].template load<kFwdLoad>(ra, in_range(in_xb, o));
             cr[r].template load<kFwdLoad>(rc, in_range(want_y && t >= wk.t_begin && t < wk.t_end, o));
         }
         float av[4][CPL], u[4][CPL], W[4][CPL], G[4][CPL];
-        decay_rows<IO, CPL>(ar, tr0, t_lo, wk.t_end, p.T, sig_a, av);
+        if constexpr (PK > 1) {
+            float az[4];
+            decay_rows_packed<IO, CPL, kFwdDecay>(ra, aoffp, (uint32_t)as, tr0, t_lo, wk.t_end, p.T, sig_a, az, av);
+        } else {
+            decay_rows<IO, CPL>(ar, tr0, t_lo, wk.t_end, p.T, sig_a, av);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -1567,7 +1620,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;
             store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
-                                               (uint32_t)(blk * dfull + n * CPL) * 4u), vout);
+                                               geo.off(p.nblocks, blk) * 4u), vout);
         }
         if (!want_y) continue;
 
@@ -1585,8 +1638,9 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
         }
     }
     if constexpr (MODE == kAggregate) {   // the run's end state from zero and decay products
-        store_row<IoF32, CPL>(rsrc(p.agg_v + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), e);
-        store_row<IoF32, CPL>(rsrc(p.agg_p + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), prod);
+        const uint32_t o = in_range(tw == 0 && grp == 0, geo.off(p.nruns, wk.run) * 4u);
+        store_row<IoF32, CPL>(rsrc(p.agg_v + hb * p.nruns * geo.Dr), o, e);
+        store_row<IoF32, CPL>(rsrc(p.agg_p + hb * p.nruns * geo.Dr), o, prod);
     }
 }
 
@@ -1595,7 +1649,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
 //     da_{k,mu} = H_{k-1,mu} du_{k,mu} - g_{k-1,mu} r_{k,mu} (e - s)_mu (eps - p)_mu,
 // and is stored per channel (no sum over the head's channels).
 // MODE kExact: the gradient of the exact recurrence, as in swr_bwd_kernel.
-template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
+template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE, int PK>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     constexpr bool SWR = MODE == kSwr;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
@@ -1612,37 +1666,42 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const int hw = wv / TW, tw = wv % TW;
     const Work wk = decode_work<HW>(p, hw);
-    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
+    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
     const int l = p.block;
     const int smask = l / SB - 1;
     const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);
 
-    const int64_t xe = wk.b * p.sx_b + head * p.sx_h + half * D;   // element offset
+    const int64_t xe = wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D;   // element offset
     const int64_t xo = xe * ES;
     const char* xb = (const char*)p.x + xo;
     const char* bb = (const char*)p.b + xo;
     const char* cb = (const char*)p.c + xo;
     const char* dyb = (const char*)p.dy + xo;
-    const char* ab = (const char*)p.a + xo;
     char* dxb = (char*)p.dx + xo;
     char* dbb = (char*)p.db + xo;
     char* dcb = (char*)p.dc + xo;
-    char* dab = (char*)(p.da + xe);
-    const int64_t dfull = (int64_t)D << p.hshift;
-    const float* vb = p.carriers + (wk.b * p.H + head) * p.nblocks * dfull + half * D;
+    // per-channel decay: a and da are rows like x; packed heads: one decay per
+    // token and real head (da float32 with a's strides)
+    const int64_t ae = PK > 1 ? wk.b * p.sa_b + geo.head * p.sa_h : xe;
+    const char* ab = (const char*)p.a + ae * ES;
+    char* dab = (char*)(p.da + ae);
+    const int64_t hb = wk.b * p.H + geo.head;   // first real (batch, head) of the virtual head
+    const float* vb = p.carriers + hb * p.nblocks * geo.Dr;
     const int64_t rs = p.sx_t * ES;
-    const int64_t das = p.sx_t * 4;
+    const int64_t as = PK > 1 ? p.sa_t * ES : rs;
+    const int64_t das = PK > 1 ? p.sa_t * 4 : p.sx_t * 4;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
-    const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(n * CPL * 4);
+    const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
+    const uint32_t daoff = PK > 1 ? (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(geo.lh * p.sa_h * 4)
+                                  : (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(n * CPL * 4);
 
     float eps[CPL], pr[CPL];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) { eps[m] = 0.f; pr[m] = 0.f; }
-    const int64_t seq = wk.b * p.H + head;
     if constexpr (MODE == kExact) {   // the exact adjoint entering the run's end (stage II)
         Row<IoF32, CPL> ci;
-        const int64_t j = seq * p.agg_nruns + (wk.t_end - 1) / p.agg_len;   // the run's last aggregate
-        ci.load(rsrc(p.carry + j * dfull + half * D), (uint32_t)(n * CPL) * 4u);
+        // the run's last aggregate
+        ci.load(rsrc(p.carry + hb * p.agg_nruns * geo.Dr), geo.off(p.agg_nruns, (wk.t_end - 1) / p.agg_len) * 4u);
 #pragma unroll
         for (int m = 0; m < CPL; ++m) eps[m] = ci.get(m);
     }
@@ -1653,17 +1712,22 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         const int64_t r0 = wk.t_end + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
         const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
-                                     ra = rsrc(ab + r0 * rs);
+                                     ra = rsrc(ab + r0 * as);
         R_ cr[4], dyr[4], ar[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t o = in_range(tr0 + r < t_la, loff + (uint32_t)(r * rs));
             cr[r].template load<kBwdLoad>(rc, o);
             dyr[r].template load<kBwdLoad>(rdy, o);
-            ar[r].template load<kBwdLoad>(ra, o);
+            if constexpr (PK == 1) ar[r].template load<kBwdLoad>(ra, o);
         }
         float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
-        decay_rows<IO, CPL>(ar, tr0, wk.t_end, t_la, p.T, sig_a, av);   // (past T the 1s meet dh = 0)
+        if constexpr (PK > 1) {   // (past T the 1s meet dh = 0)
+            float az[4];
+            decay_rows_packed<IO, CPL, kBwdDecay>(ra, aoffp, (uint32_t)as, tr0, wk.t_end, t_la, p.T, sig_a, az, av);
+        } else {
+            decay_rows<IO, CPL>(ar, tr0, wk.t_end, t_la, p.T, sig_a, av);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -1702,12 +1766,12 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         const int64_t tr0 = r0 + 4 * grp;
 
         R_ xr[4], br[4], dyr[4], ar[4];
-        float av[4][CPL], dh[4][CPL];
+        float av[4][CPL], dh[4][CPL], az[4];
         {
             R_ cr[4];
             const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
                                          rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
-                                         ra = rsrc(ab + r0 * rs);
+                                         ra = rsrc(ab + r0 * as);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
@@ -1715,9 +1779,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 br[r].template load<kBwdLoad>(rb, o);
                 cr[r].template load<kBwdLoad>(rc, o);
                 dyr[r].template load<kBwdLoad>(rdy, o);
-                ar[r].template load<kBwdLoad>(ra, o);
+                if constexpr (PK == 1) ar[r].template load<kBwdLoad>(ra, o);
             }
-            decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
+            if constexpr (PK > 1)
+                decay_rows_packed<IO, CPL, kBwdDecay>(ra, aoffp, (uint32_t)as, tr0, wk.t_begin, wk.t_end, p.T, sig_a,
+                                                      az, av);
+            else
+                decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -1728,9 +1796,9 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             Row<IoF32, CPL> vr;
             const int64_t blk = (t0 >> p.lshift) - 1;
             if (MODE == kExact && t0 == 0)
-                vr.load(rsrc(p.h0 + seq * dfull + half * D), in_range(p.h0 != nullptr, (uint32_t)(n * CPL) * 4u));
+                vr.load(rsrc(p.h0 + hb * geo.Dr), in_range(p.h0 != nullptr, geo.off(1, 0) * 4u));
             else
-                vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * dfull + n * CPL) * 4u));
+                vr.load(rsrc(vb), in_range(t0 > 0, geo.off(p.nblocks, blk) * 4u));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
         }
@@ -1843,20 +1911,34 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 if (p.residual) vdx[m] += dyv;
                 vdb[m] = xr[r].get(m) * du * g.ds;
                 vda[m] = (r == 0 ? hup[m] : W[r - 1][m]) * du - Gsh[r][m] * Rr[r][m] * kd[m];
-                if (sig_a) vda[m] *= sigmoid_slope(ar[r].get(m)).ds;
+                if (PK == 1 && sig_a) vda[m] *= sigmoid_slope(ar[r].get(m)).ds;
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
             store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
             store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
-            store_row<IoF32, CPL, kBwdStore>(rda, in_range(t < wk.t_end, daoff + (uint32_t)(r * das)), vda);
+            if constexpr (PK > 1) {
+                // one decay per real head: sum over the head's channels (this
+                // lane's and those of the head's other lanes of the row)
+                float tot = 0.f;
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) tot += vda[m];
+#pragma unroll
+                for (int w = 1; w < Geo<PK, CPL>::LPH; w <<= 1) tot += __shfl_xor(tot, w, 64);
+                if (sig_a) tot *= sigmoid_slope(az[r]).ds;
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    __builtin_bit_cast(int, tot), rda,
+                    (int)in_range(t < wk.t_end && geo.lch == 0, daoff + (uint32_t)(r * das)), 0, kBwdStore);
+            } else {
+                store_row<IoF32, CPL, kBwdStore>(rda, in_range(t < wk.t_end, daoff + (uint32_t)(r * das)), vda);
+            }
         }
     }
 }
 
 // Stage I of the exact backward with a per-channel decay: per run, the
 // adjoint leaving its first token and the run's decay product, per channel.
-template <class IO, int CPL, int TW, bool FEAT>
+template <class IO, int CPL, int TW, bool FEAT, int PK>
 __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
     const int sig_a = FEAT ? p.sig_a : 0;
     constexpr int D = CPL * SB;
@@ -1869,15 +1951,16 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
     const Lanes ln = lanes();
     const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work<1>(p, 0);
-    const int64_t head = wk.h >> p.hshift, half = wk.h & ((1 << p.hshift) - 1);
-    const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + half * D) * ES;
+    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
+    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D) * ES;
     const char* cb = (const char*)p.c + xo;
     const char* dyb = (const char*)p.dy + xo;
-    const char* ab = (const char*)p.a + xo;
+    const char* ab = PK > 1 ? (const char*)p.a + (wk.b * p.sa_b + geo.head * p.sa_h) * ES : (const char*)p.a + xo;
     const int64_t rs = p.sx_t * ES;
+    const int64_t as = PK > 1 ? p.sa_t * ES : rs;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
-    const int64_t dfull = (int64_t)D << p.hshift;
-    const int64_t slot = ((wk.b * p.H + head) * p.nruns + wk.run) * dfull + half * D;
+    const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
+    const int64_t hb = wk.b * p.H + geo.head;
 
     float eps[CPL], prod[CPL];
 #pragma unroll
@@ -1887,17 +1970,22 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
     for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
         const int64_t r0 = wk.t_begin + k * STEP + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
-        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs), ra = rsrc(ab + r0 * rs);
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs), ra = rsrc(ab + r0 * as);
         R_ cr[4], dyr[4], ar[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
             cr[r].template load<kAggLoad>(rc, o);
             dyr[r].template load<kAggLoad>(rdy, o);
-            ar[r].template load<kAggLoad>(ra, o);
+            if constexpr (PK == 1) ar[r].template load<kAggLoad>(ra, o);
         }
         float av[4][CPL], dh[4][CPL], Dv[4][CPL], R[4][CPL];
-        decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);   // 1 past the end
+        if constexpr (PK > 1) {   // 1 past the end
+            float az[4];
+            decay_rows_packed<IO, CPL, kAggLoad>(ra, aoffp, (uint32_t)as, tr0, wk.t_begin, wk.t_end, p.T, sig_a, az, av);
+        } else {
+            decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -1921,8 +2009,9 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
             }
         }
     }
-    store_row<IoF32, CPL>(rsrc(p.agg_v + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), eps);
-    store_row<IoF32, CPL>(rsrc(p.agg_p + slot), in_range(tw == 0 && grp == 0, (uint32_t)(n * CPL) * 4u), prod);
+    const uint32_t o = in_range(tw == 0 && grp == 0, geo.off(p.nruns, wk.run) * 4u);
+    store_row<IoF32, CPL>(rsrc(p.agg_v + hb * p.nruns * geo.Dr), o, eps);
+    store_row<IoF32, CPL>(rsrc(p.agg_p + hb * p.nruns * geo.Dr), o, prod);
 }
 
 }  // namespace
@@ -1931,7 +2020,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <class IO, int CPL, bool FEAT, int MODE>
+template <class IO, int CPL, bool FEAT, int MODE, int PK>
 static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     const dim3 grid((unsigned)p.nwork);
 #define SWR_LAUNCH(KERNEL, TW_, HW_)                                                                \
@@ -1940,31 +2029,31 @@ static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hip
     if (backward) {
         if constexpr (MODE == kAggregate) {
             if (false) {}
-            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 8, FEAT>), 8, 1)
-            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 4, FEAT>), 4, 1)
+            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 8, FEAT, PK>), 8, 1)
+            SWR_LAUNCH((swr_bwd_pc_agg_kernel<IO, CPL, 4, FEAT, PK>), 4, 1)
             else return hipErrorInvalidValue;
         } else {
             if (false) {}
-            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 8, 1, FEAT, MODE>), 8, 1)
-            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
+            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 8, 1, FEAT, MODE, PK>), 8, 1)
+            SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE, PK>), 4, 1)
             else return hipErrorInvalidValue;
         }
     } else {
         if (false) {}
-        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
-        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 2, 2, FEAT, MODE>), 2, 2)
+        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE, PK>), 4, 1)
+        SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 2, 2, FEAT, MODE, PK>), 2, 2)
         else return hipErrorInvalidValue;
     }
 #undef SWR_LAUNCH
     return hipGetLastError();
 }
 
-template <class IO, int CPL, bool FEAT>
+template <class IO, int CPL, bool FEAT, int PK>
 static hipError_t launch_pc_mode(const Params& p, const Shape& sh, bool backward, int mode, hipStream_t stream) {
     switch (mode) {
-        case kSwr: return launch_pc<IO, CPL, FEAT, kSwr>(p, sh, backward, stream);
-        case kAggregate: return launch_pc<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
-        case kExact: return launch_pc<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
+        case kSwr: return launch_pc<IO, CPL, FEAT, kSwr, PK>(p, sh, backward, stream);
+        case kAggregate: return launch_pc<IO, CPL, FEAT, kAggregate, PK>(p, sh, backward, stream);
+        case kExact: return launch_pc<IO, CPL, FEAT, kExact, PK>(p, sh, backward, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -2009,12 +2098,17 @@ static hipError_t launch_mode(const Params& p, const Shape& sh, bool backward, i
 
 template <class IO, bool FEAT>
 static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
-                             int mode, hipStream_t stream) {
+                             int pack, int mode, hipStream_t stream) {
+    if (pack > 1) {   // packed small heads: 64-channel virtual heads of 4 or 2 real heads
+        if (D != 64) return hipErrorInvalidValue;
+        return pack == 4 ? launch_pc_mode<IO, 4, FEAT, 4>(p, sh, backward, mode, stream)
+                         : launch_pc_mode<IO, 4, FEAT, 2>(p, sh, backward, mode, stream);
+    }
     if (per_channel) {
         switch (D) {   // channels of a virtual head (at most 64)
-            case 16: return launch_pc_mode<IO, 1, FEAT>(p, sh, backward, mode, stream);
-            case 32: return launch_pc_mode<IO, 2, FEAT>(p, sh, backward, mode, stream);
-            case 64: return launch_pc_mode<IO, 4, FEAT>(p, sh, backward, mode, stream);
+            case 16: return launch_pc_mode<IO, 1, FEAT, 1>(p, sh, backward, mode, stream);
+            case 32: return launch_pc_mode<IO, 2, FEAT, 1>(p, sh, backward, mode, stream);
+            case 64: return launch_pc_mode<IO, 4, FEAT, 1>(p, sh, backward, mode, stream);
             default: return hipErrorInvalidValue;
         }
     }
@@ -2031,16 +2125,16 @@ static hipError_t launch_cpl(const Params& p, int D, const Shape& sh, bool backw
 // plain path carries none of its registers.
 template <class IO>
 static hipError_t launch_feat(const Params& p, int D, const Shape& sh, bool backward, bool per_channel,
-                              int mode, hipStream_t stream) {
-    if (p.sig_a || p.sig_b) return launch_cpl<IO, true>(p, D, sh, backward, per_channel, mode, stream);
-    return launch_cpl<IO, false>(p, D, sh, backward, per_channel, mode, stream);
+                              int pack, int mode, hipStream_t stream) {
+    if (p.sig_a || p.sig_b) return launch_cpl<IO, true>(p, D, sh, backward, per_channel, pack, mode, stream);
+    return launch_cpl<IO, false>(p, D, sh, backward, per_channel, pack, mode, stream);
 }
 
 hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, bool per_channel,
-                  int mode, void* stream) {
+                  int pack, int mode, void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, mode, st);
-    return launch_feat<IoF32>(p, D, sh, backward, per_channel, mode, st);
+    if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, pack, mode, st);
+    return launch_feat<IoF32>(p, D, sh, backward, per_channel, pack, mode, st);
 }
 
 template <class IO, int CPL>

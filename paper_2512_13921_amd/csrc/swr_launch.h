@@ -132,8 +132,10 @@ inline int pc_hshift(int64_t D) { return D > 64 ? 1 : 0; }
 
 // Launches the forward or backward kernel for (dtype, D, shape) on `stream`;
 // for the per-channel kernels D is the channel count of a virtual head.
+// pack > 1: a per-head decay with heads of 64 / pack channels, run on the
+// per-channel kernels with `pack` adjacent heads per 64-channel virtual head.
 hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool backward, bool per_channel,
-                  int mode, void* stream);
+                  int pack, int mode, void* stream);
 
 hipError_t launch_scan(const ScanParams& q, void* stream);
 
