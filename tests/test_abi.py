@@ -360,3 +360,23 @@ def test_decode_state_validation():
     assert dstate(problem(D=128, per_channel=True), a=A + 8) == E_ALIGN
     assert dstate(p, st=V) == E_ALIAS and dstate(p, st=A) == E_ALIAS
     assert dstate(problem(B=0)) == OK
+
+
+def test_small_heads_are_packed_when_adjacent():
+    # heads of 16 (32) channels stored next to each other run four (two) to a
+    # 64-channel virtual head: the launch covers H / 4 (H / 2) heads
+    p = problem(B=1, T=4096, H=8, D=16, block=16, run_len=256)
+    info = swr.swr_launch_info(p)
+    assert info["fwd_workgroups"] == (8 // 4 // 2) * (4096 // 256)   # 2 virtual heads, 2 per group
+    assert info["bwd_workgroups"] == (8 // 4) * (4096 // 256)
+    p = problem(B=1, T=4096, H=8, D=32, block=32, run_len=256)
+    assert swr.swr_launch_info(p)["bwd_workgroups"] == (8 // 2) * (4096 // 256)
+    # not adjacent ([B, H, T, D] storage) or a head count that does not divide: one at a time
+    B, T, H, D = 1, 4096, 8, 16
+    p = problem(B=B, T=T, H=H, D=D, block=16, run_len=256, x_strides=(H * T * D, D, T * D), a_strides=(H * T, 1, T))
+    assert swr.swr_launch_info(p)["bwd_workgroups"] == 8 * (4096 // 256)
+    p = problem(B=1, T=4096, H=6, D=16, block=16, run_len=256)
+    assert swr.swr_launch_info(p)["bwd_workgroups"] == 6 * (4096 // 256)
+    # the exact workspace covers either plan
+    p = problem(B=2, T=1000, H=8, D=16, block=16)
+    assert swr.swr_exact_workspace_bytes(p) > 0
