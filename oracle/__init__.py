@@ -52,6 +52,10 @@ def _load():
             nptr = 6 if name.endswith("forward") else 12
             fn.argtypes = lead + [i64, i64, ci, ci] + [dp] * nptr
             fn.restype = ci
+        for name, nptr in (("swr_oracle_uniform_forward", 5), ("swr_oracle_uniform_backward", 9)):
+            fn = getattr(lib, name)
+            fn.argtypes = [i64, i64, i64, i64, ci, ci] + [dp] * nptr
+            fn.restype = ci
         lib.swr_oracle_step.argtypes = [i64, i64, i64, i64, i64, ci, ci] + [dp] * 6
         lib.swr_oracle_step.restype = ci
         lib.swr_oracle_max_threads.restype = ci
@@ -267,3 +271,61 @@ def step(x, a, b, c, state, t0, block, residual=False, sigmoid_decay=False, sigm
     st = np.zeros((B * H, 2, D)) if state is None else np.asarray(state, np.float64).reshape(B * H, 2, D)
     y, st = step_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c), st, t0, block, residual)
     return _from_slices(y, B, H), st.reshape(B, H, 2, D)
+
+
+# ----------------------------------------------------------------------------
+# Uniform window (Sec. 4.1): the banded operator I + AZ + ... + (AZ)^{k-1}
+# ----------------------------------------------------------------------------
+
+def uniform_forward_slices(x, a, b, c, k, residual=False):
+    """Uniform-window forward on independent slices (every token sees the k
+    most recent tokens): x, b, c are [S, T, D]; a is [S, T] or [S, T, D]."""
+    lib = _load()
+    x, a, b, c = _c64(x), _c64(a), _c64(b), _c64(c)
+    S, T, D = x.shape
+    y = np.empty((S, T, D), np.float64)
+    rc = lib.swr_oracle_uniform_forward(S, T, D, int(k), int(a.ndim == 3), RESIDUAL if residual else 0,
+                                        _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle uniform forward rejected its arguments")
+    return y
+
+
+def uniform_backward_slices(x, a, b, c, dy, k, residual=False):
+    """Uniform-window backward on slices; returns (dx, da, db, dc)."""
+    lib = _load()
+    x, a, b, c, dy = _c64(x), _c64(a), _c64(b), _c64(c), _c64(dy)
+    S, T, D = x.shape
+    dx, db, dc = (np.empty((S, T, D), np.float64) for _ in range(3))
+    da = np.empty(a.shape, np.float64)
+    rc = lib.swr_oracle_uniform_backward(S, T, D, int(k), int(a.ndim == 3), RESIDUAL if residual else 0,
+                                         _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
+                                         _ptr(dx), _ptr(da), _ptr(db), _ptr(dc))
+    if rc != 0:
+        raise ValueError("oracle uniform backward rejected its arguments")
+    return dx, da, db, dc
+
+
+def uniform_forward(x, a, b, c, k, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """Uniform-window y for [B, T, H, D] tensors (a: [B, T, H] or [B, T, H, D])."""
+    B, T, H, D = np.shape(x)
+    a = sigmoid(a) if sigmoid_decay else a
+    b = sigmoid(b) if sigmoid_pregate else b
+    y = uniform_forward_slices(_to_slices(x), _to_slices(a), _to_slices(b), _to_slices(c), k, residual)
+    return _from_slices(y, B, H)
+
+
+def uniform_backward(x, a, b, c, dy, k, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """(dx, da, db, dc) of the uniform window for [B, T, H, D] tensors; with the
+    sigmoid flags da / db are with respect to the logits."""
+    B, T, H, D = np.shape(x)
+    av = sigmoid(a) if sigmoid_decay else a
+    bv = sigmoid(b) if sigmoid_pregate else b
+    outs = uniform_backward_slices(_to_slices(x), _to_slices(av), _to_slices(bv), _to_slices(c),
+                                   _to_slices(dy), k, residual)
+    dx, da, db, dc = (_from_slices(o, B, H) for o in outs)
+    if sigmoid_decay:
+        da = da * dsigmoid(a)
+    if sigmoid_pregate:
+        db = db * dsigmoid(b)
+    return dx, da, db, dc

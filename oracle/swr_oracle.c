@@ -296,6 +296,118 @@ int swr_oracle_step(int64_t S, int64_t K, int64_t D, int64_t block, int64_t t0,
     return err ? -1 : 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Uniform window: the banded operator of Sec. 4.1 (lags 0 .. k-1).          */
+/* ------------------------------------------------------------------------ */
+
+int swr_oracle_uniform_forward_slice(int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                     int flags, const double* x, const double* a,
+                                     const double* b, const double* c, double* y) {
+    if (bad_args(T, D, k)) return -1;
+    if (T == 0) return 0;
+    if (!x || !a || !b || !c || !y) return -1;
+    double* s = (double*)malloc((size_t)D * sizeof(double));
+    if (!s) return -1;
+    for (int64_t i = 0; i < T; ++i) {
+        /* Token i's window: the k most recent tokens, i-k+1 .. i (clipped at 0). */
+        const int64_t start = i - k + 1 > 0 ? i - k + 1 : 0;
+        for (int64_t mu = 0; mu < D; ++mu) s[mu] = 0.0;
+        for (int64_t m = start; m <= i; ++m)
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu;
+                s[mu] = decay(a, a_per_channel, D, m, mu) * s[mu] + b[e] * x[e];
+            }
+        for (int64_t mu = 0; mu < D; ++mu) {
+            const int64_t e = i * D + mu;
+            y[e] = c[e] * s[mu];
+            if (flags & SWR_ORACLE_RESIDUAL) y[e] += x[e];
+        }
+    }
+    free(s);
+    return 0;
+}
+
+int swr_oracle_uniform_backward_slice(int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                      int flags, const double* x, const double* a,
+                                      const double* b, const double* c, const double* dy,
+                                      double* dx, double* da, double* db, double* dc) {
+    if (bad_args(T, D, k)) return -1;
+    if (T == 0) return 0;
+    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return -1;
+    const int64_t win = k < T ? k : T; /* longest window */
+    double* du = (double*)calloc((size_t)(T * D), sizeof(double));
+    double* pre = (double*)malloc((size_t)(win * D) * sizeof(double));
+    double* lam = (double*)malloc((size_t)D * sizeof(double));
+    if (!du || !pre || !lam) {
+        free(du); free(pre); free(lam);
+        return -1;
+    }
+    memset(da, 0, (size_t)(a_per_channel ? T * D : T) * sizeof(double));
+    for (int64_t i = 0; i < T; ++i) {
+        const int64_t start = i - k + 1 > 0 ? i - k + 1 : 0;
+        /* Re-run token i's window, keeping the state entering every step. */
+        for (int64_t mu = 0; mu < D; ++mu) lam[mu] = 0.0; /* lam is the state here */
+        for (int64_t m = start; m <= i; ++m)
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu;
+                pre[(m - start) * D + mu] = lam[mu];
+                lam[mu] = decay(a, a_per_channel, D, m, mu) * lam[mu] + b[e] * x[e];
+            }
+        for (int64_t mu = 0; mu < D; ++mu) {   /* y_i = c_i * state_i */
+            const int64_t e = i * D + mu;
+            dc[e] = dy[e] * lam[mu];
+            lam[mu] = c[e] * dy[e];            /* now d(loss)/d(state after step i) */
+        }
+        for (int64_t m = i; m >= start; --m)
+            for (int64_t mu = 0; mu < D; ++mu) {
+                const int64_t e = m * D + mu;
+                du[e] += lam[mu];              /* d state_m / d u_m = 1          */
+                const double g = lam[mu] * pre[(m - start) * D + mu];
+                if (a_per_channel)             /* d state_m / d a_m = state_{m-1} */
+                    da[e] += g;
+                else
+                    da[m] += g;
+                lam[mu] *= decay(a, a_per_channel, D, m, mu);
+            }
+    }
+    for (int64_t e = 0; e < T * D; ++e) {
+        dx[e] = b[e] * du[e];
+        if (flags & SWR_ORACLE_RESIDUAL) dx[e] += dy[e];
+        db[e] = x[e] * du[e];
+    }
+    free(du); free(pre); free(lam);
+    return 0;
+}
+
+int swr_oracle_uniform_forward(int64_t S, int64_t T, int64_t D, int64_t k, int a_per_channel,
+                               int flags, const double* x, const double* a, const double* b,
+                               const double* c, double* y) {
+    if (S < 0 || bad_args(T, D, k)) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_uniform_forward_slice(T, D, k, a_per_channel, flags, x + s * n,
+                                                a + s * na, b + s * n, c + s * n, y + s * n) != 0;
+    return err ? -1 : 0;
+}
+
+int swr_oracle_uniform_backward(int64_t S, int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                int flags, const double* x, const double* a, const double* b,
+                                const double* c, const double* dy, double* dx, double* da,
+                                double* db, double* dc) {
+    if (S < 0 || bad_args(T, D, k)) return -1;
+    const int64_t n = T * D, na = a_per_channel ? T * D : T;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t s = 0; s < S; ++s)
+        err |= swr_oracle_uniform_backward_slice(T, D, k, a_per_channel, flags, x + s * n,
+                                                 a + s * na, b + s * n, c + s * n, dy + s * n,
+                                                 dx + s * n, da + s * na, db + s * n,
+                                                 dc + s * n) != 0;
+    return err ? -1 : 0;
+}
+
 int swr_oracle_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

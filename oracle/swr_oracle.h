@@ -117,6 +117,33 @@ int swr_oracle_step(int64_t S, int64_t K, int64_t D, int64_t block, int64_t t0,
                     int a_per_channel, int flags, const double* x, const double* a,
                     const double* b, const double* c, double* state, double* y);
 
+/* Uniform window (Sec. 4.1, "Uniform Window Recurrences"): the Kogge-Stone
+ * factorisation of Sec. 3.1 (eq. (2.4)) stopped after log2 k stages keeps the banded
+ * operator  L~ = I + AZ + (AZ)^2 + ... + (AZ)^{k-1},  i.e. every token sees
+ * exactly the k most recent tokens (lags 0 .. k-1):
+ *
+ *     h~_i = sum_{j = max(0, i-k+1)}^{i} ( prod_{m=j+1}^{i} a_m ) * u_j ,
+ *     y_i  = c_i (*) h~_i   (+ x_i with the residual flag).
+ *
+ * The forward runs the recurrence restarted from zero at i-k+1 once for every
+ * token i (O(T k D)); the backward is the exact reverse-mode adjoint of that
+ * loop.  Any k >= 1 is accepted (the kernels take powers of two, the stage
+ * counts of the scan).  Layouts and return codes as for the jagged window. */
+int swr_oracle_uniform_forward_slice(int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                     int flags, const double* x, const double* a,
+                                     const double* b, const double* c, double* y);
+int swr_oracle_uniform_backward_slice(int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                      int flags, const double* x, const double* a,
+                                      const double* b, const double* c, const double* dy,
+                                      double* dx, double* da, double* db, double* dc);
+int swr_oracle_uniform_forward(int64_t S, int64_t T, int64_t D, int64_t k, int a_per_channel,
+                               int flags, const double* x, const double* a, const double* b,
+                               const double* c, double* y);
+int swr_oracle_uniform_backward(int64_t S, int64_t T, int64_t D, int64_t k, int a_per_channel,
+                                int flags, const double* x, const double* a, const double* b,
+                                const double* c, const double* dy, double* dx, double* da,
+                                double* db, double* dc);
+
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
 int swr_oracle_max_threads(void);
 

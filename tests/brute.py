@@ -24,6 +24,16 @@ either shows up as a disagreement:
 * ``torch_forward``    -- a differentiable float64 torch version of
                           ``window_sum`` whose autograd gradients pin the
                           oracle's backward.
+* ``kogge_stone``      -- the Kogge-Stone scan in the paper's matrix form
+                          (Sec. 3.1, Alg. "Kogge-Stone Parallel Algorithm":
+                          v <- v + F v with F = diag(f) Z^s, then F <- F^2),
+                          optionally stopped after a number of stages, which
+                          is how Sec. 4.1 defines the uniform window.
+* ``dense_L_banded``   -- the uniform window's banded operator
+                          I + AZ + ... + (AZ)^{k-1} (Sec. 4.1) by matrix powers.
+* ``uniform_window_sum`` / ``torch_uniform`` -- explicit sums over each
+                          token's k most recent tokens, and a differentiable
+                          torch version of them.
 Everything is float64.  Sizes must be tiny (the dense builders are O(T^2)).
 """
 import numpy as np
@@ -217,3 +227,72 @@ def torch_exact(x, a, b, c, h0, residual=False):
     y = c * h
     h_last = h[-1] if T > 0 else h0
     return (y + x if residual else y), h_last
+
+
+def kogge_stone(a, u, stages=None):
+    """Kogge-Stone scan of x_i = a_i x_{i-1} + u_i in the matrix form of
+    Sec. 3.1: the work vector v starts as u and f as a; stage t applies
+    v <- v + diag(f) Z^s v and squares F = diag(f) Z^s (f_i <- f_i f_{i-s}),
+    s = 2^t.  ``stages`` stops the loop early (all stages when None).
+    u is [T, D]; a is [T] or [T, D]."""
+    u = np.asarray(u, np.float64)
+    T = u.shape[0]
+    a = np.asarray(a, np.float64)
+    f = (a[:, None] * np.ones_like(u)) if a.ndim == 1 else a.copy()
+    v = u.copy()
+    s, t = 1, 0
+    while s <= T - 1 and (stages is None or t < stages):
+        v_new = v.copy()
+        v_new[s:] = v[s:] + f[s:] * v[:-s]
+        f_new = f.copy()
+        f_new[s:] = f[s:] * f[:-s]   # rows i <= s of F are zero: their f is never used
+        v, f = v_new, f_new
+        s, t = 2 * s, t + 1
+    return v
+
+
+def dense_L_banded(a, k):
+    """Uniform-window operator I + AZ + ... + (AZ)^{k-1} (shared decay a [T])."""
+    a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    AZ = np.diag(a) @ np.eye(n, k=-1)
+    L = np.zeros((n, n))
+    P = np.eye(n)
+    for _ in range(k):
+        L += P
+        P = P @ AZ
+    return L
+
+
+def uniform_window_sum(a, u, k):
+    """h_i = sum_{j=max(0,i-k+1)}^{i} a_{i:j+1} u_j (u [T, D]; a [T] or [T, D])."""
+    a = np.asarray(a, np.float64)
+    u = np.asarray(u, np.float64)
+    T, D = u.shape
+    h = np.zeros((T, D))
+    for i in range(T):
+        for j in range(max(0, i - k + 1), i + 1):
+            for mu in range(D):
+                aa = a if a.ndim == 1 else a[:, mu]
+                h[i, mu] += decay_product(aa, i, j) * u[j, mu]
+    return h
+
+
+def torch_uniform(x, a, b, c, k, residual=False):
+    """Differentiable float64 uniform-window forward of one slice (explicit products)."""
+    import torch
+    T, D = x.shape
+    u = b * x
+    rows = []
+    for i in range(T):
+        acc = torch.zeros(D, dtype=torch.float64)
+        for j in range(max(0, i - k + 1), i + 1):
+            if a.dim() == 1:
+                w = torch.prod(a[j + 1:i + 1]) if i > j else torch.ones((), dtype=torch.float64)
+            else:
+                w = torch.prod(a[j + 1:i + 1], dim=0) if i > j else torch.ones(D, dtype=torch.float64)
+            acc = acc + w * u[j]
+        rows.append(acc)
+    h = torch.stack(rows)
+    y = c * h
+    return y + x if residual else y
