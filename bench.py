@@ -73,7 +73,7 @@ def contraction_flops(cfg, backward):
 
 # The sources that decide what a launch does (kernels, grid policy): the
 # recorded traffic is stale once any of them changes.
-KERNEL_SOURCES = ("swr_kernels.hip", "swr_api.cpp", "swr_launch.h")
+KERNEL_SOURCES = ("swr_kernels.hip", "swr_device.h", "swr_api.cpp", "swr_launch.h")
 
 
 def recorded_traffic(kernel, workload):

@@ -247,6 +247,46 @@ int swr_exact_step(const swr_problem_t* problem, const void* x, const void* a, c
 int swr_decode_state(const swr_problem_t* problem, const void* a, const float* carriers, float* state,
                      void* stream);
 
+/* ------------------------------------------------------------------------
+ * Uniform window
+ *
+ * The other truncation of Sec. 4 (Sec. 4.1, "Uniform Window Recurrences"):
+ * the Kogge-Stone factorisation of Sec. 3.1, eq. (2.4), stopped after log2 k
+ * stages, i.e. the banded operator  L~ = I + AZ + (AZ)^2 + ... + (AZ)^{k-1}.
+ * Every token sees exactly its k most recent tokens:
+ *
+ *     h~_i = sum_{j = max(0, i-k+1)}^{i} ( prod_{m=j+1}^{i} a_m ) b_j (*) x_j
+ *     y_i  = c_i (*) h~_i   (+ x_i if SWR_FLAG_RESIDUAL)
+ *
+ * The window length k is problem->block (16, 32, 64 or 128; the stage counts
+ * 4 .. 7 of the scan).  With the jagged window of the same block, a token
+ * sees at least these lags (all of them on a block's first token) and at most
+ * those of the uniform window of 2k.  The kernels evaluate it block by block
+ * (a local solve plus, for every row, the tail of the previous block that its
+ * window still holds), not as the paper's truncated flat scan; nothing is
+ * saved between the forward and the backward, which recomputes what it needs
+ * from the previous block's x, b and a.  Everything in swr_problem_t keeps its
+ * meaning; SWR_FLAG_PER_CHANNEL_DECAY is not supported (SWR_ERR_UNSUPPORTED).
+ * Alignment: x, b, c, y, dy, dx, db, dc and every sx_* in multiples of
+ * min(16 bytes, min(D, 64)/16 elements); a of one element; da of 4 bytes.
+ * ------------------------------------------------------------------------ */
+
+/* Forward: y = the uniform-window recurrence of x, a, b, c. */
+int swr_uniform_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                        const void* c, void* y, void* stream);
+
+/* Backward: given dy, the exact gradients dx, da (float32, a's shape and
+ * strides), db and dc of swr_uniform_forward (with the sigmoid flags, da and
+ * db with respect to the logits). */
+int swr_uniform_backward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
+                         const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
+                         void* stream);
+
+/* Launch shape the uniform-window calls pick (run length and workgroups of
+ * the forward and of the backward); as swr_launch_info. */
+int swr_uniform_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, int64_t* fwd_workgroups,
+                            int64_t* bwd_run_len, int64_t* bwd_workgroups);
+
 /* Resolved launch shape for a problem (for reports and tests): the run length
  * in tokens and the number of workgroups of the forward and of the backward
  * launch (any output pointer may be NULL).  Returns an SWR_ERR_* code for a

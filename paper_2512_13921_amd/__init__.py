@@ -25,6 +25,7 @@ __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error
            "swr_abi_version", "swr_launch_info", "swr_carrier_elems", "carrier_shape",
            "swr_exact_forward", "swr_exact_backward", "swr_exact_workspace_bytes",
            "swr_step", "swr_exact_step", "swr_decode_state",
+           "swr_uniform_forward", "swr_uniform_backward", "swr_uniform_launch_info",
            "SWRFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
@@ -98,6 +99,12 @@ def load():
         lib.swr_exact_step.restype = ctypes.c_int
         lib.swr_decode_state.argtypes = [P] + [vp] * 4
         lib.swr_decode_state.restype = ctypes.c_int
+        lib.swr_uniform_forward.argtypes = [P] + [vp] * 6
+        lib.swr_uniform_forward.restype = ctypes.c_int
+        lib.swr_uniform_backward.argtypes = [P] + [vp] * 10
+        lib.swr_uniform_backward.restype = ctypes.c_int
+        lib.swr_uniform_launch_info.argtypes = [P, i64p, i64p, i64p, i64p]
+        lib.swr_uniform_launch_info.restype = ctypes.c_int
         if lib.swr_abi_version() != SWR_ABI_VERSION:
             raise RuntimeError("libswr.so ABI version does not match the binding")
         _lib = lib
@@ -450,6 +457,59 @@ def swr_decode_state(x, a, carriers, block, state=None, stream=None, sigmoid_dec
     if rc != 0:
         raise SwrError(rc, "swr_decode_state")
     return state
+
+
+# ----------------------------------------------------------------------------- uniform window
+
+
+def swr_uniform_launch_info(problem: SwrProblem):
+    """Launch shape of the uniform-window calls, as ``swr_launch_info``."""
+    v = [ctypes.c_int64() for _ in range(4)]
+    rc = load().swr_uniform_launch_info(ctypes.byref(problem), *(ctypes.byref(t) for t in v))
+    if rc != 0:
+        raise SwrError(rc, "swr_uniform_launch_info")
+    return dict(zip(("fwd_run_len", "fwd_workgroups", "bwd_run_len", "bwd_workgroups"),
+                    (t.value for t in v)))
+
+
+def swr_uniform_forward(x, a, b, c, window, residual=False, y=None, run_len=0, stream=None,
+                        sigmoid_decay=False, sigmoid_pregate=False):
+    """y of the uniform-window recurrence (every token sees its ``window``
+    most recent tokens; see ``include/swr.h``)."""
+    torch = _torch()
+    problem = _problem_from(x, a, window, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c)
+    if y is None:
+        y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+    else:
+        _same_layout(x, y)
+    rc = load().swr_uniform_forward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(y),
+                                    _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_uniform_forward")
+    return y
+
+
+def swr_uniform_backward(x, a, b, c, dy, window, residual=False, outputs=None, run_len=0, stream=None,
+                         sigmoid_decay=False, sigmoid_pregate=False):
+    """(dx, da, db, dc) of the uniform-window forward given dy."""
+    torch = _torch()
+    problem = _problem_from(x, a, window, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _same_layout(x, b, c, dy)
+    if outputs is None:
+        dx, db, dc = (torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+                      for _ in range(3))
+        da = torch.empty_strided(a.shape, a.stride(), dtype=torch.float32, device=a.device)
+    else:
+        dx, da, db, dc = outputs
+        _same_layout(x, dx, db, dc)
+        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
+            raise ValueError("da must be float32 with the shape and strides of a")
+    rc = load().swr_uniform_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
+                                     _ptr(dx), _ptr(da), _ptr(db), _ptr(dc), _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_uniform_backward")
+    return dx, da, db, dc
 
 
 def _autograd_function():

@@ -7,12 +7,13 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libswr.so")
-SOURCES = [os.path.join(CSRC, "swr_api.cpp"), os.path.join(CSRC, "swr_kernels.hip")]
-HEADERS = [os.path.join(CSRC, "swr_launch.h"),
+SOURCES = [os.path.join(CSRC, n) for n in ("swr_api.cpp", "swr_kernels.hip", "swr_uniform.hip")]
+HEADERS = [os.path.join(CSRC, "swr_launch.h"), os.path.join(CSRC, "swr_device.h"),
            os.path.join(os.path.dirname(HERE), "include", "swr.h")]
 ARCH = "gfx950"
 
@@ -24,27 +25,55 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (set HIPCC or install ROCm)")
 
 
-def command(out: str, extra=()) -> list:
-    return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-            # no packed-fp32 instructions in device code (host pass ignores the feature)
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-Wall", "-Wno-unused-function", *extra, *SOURCES, "-o", out]
+FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+         # no packed-fp32 instructions in device code (host pass ignores the feature)
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wall", "-Wno-unused-function"]
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    cmd = command(LIB + ".tmp", extra)
-    if verbose:
-        print(" ".join(cmd))
-    res = subprocess.run(cmd, capture_output=True, text=True)
+def compile_command(src: str, obj: str, extra=()) -> list:
+    return [hipcc(), *FLAGS, *extra, "-c", src, "-o", obj]
+
+
+def link_command(objs, out: str) -> list:
+    return [hipcc(), f"--offload-arch={ARCH}", "-shared", *objs, "-o", out]
+
+
+def _messages(res) -> list:
     # hipcc's host pass warns that it does not know the packed-fp32 feature
     noise = "is not a recognized feature for this target"
-    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln]
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
-    if verbose and msgs:
-        print("\n".join(msgs))
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    return [ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln]
+
+
+def build(verbose: bool = False, extra=(), out: str = LIB) -> str:
+    """Compiles every source to an object (in parallel), then links ``out``."""
+    with tempfile.TemporaryDirectory() as tmp:
+        objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in SOURCES]
+        procs = []
+        for src, obj in zip(SOURCES, objs):
+            cmd = compile_command(src, obj, extra)
+            if verbose:
+                print(" ".join(cmd))
+            procs.append(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True))
+        failed = []
+        for proc in procs:
+            stdout, stderr = proc.communicate()
+            res = subprocess.CompletedProcess(proc.args, proc.returncode, stdout, stderr)
+            msgs = _messages(res)
+            if res.returncode != 0:
+                failed.append("\n".join(msgs))
+            elif verbose and msgs:
+                print("\n".join(msgs))
+        if failed:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
+        cmd = link_command(objs, out + ".tmp")
+        if verbose:
+            print(" ".join(cmd))
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError("hipcc link failed:\n" + "\n".join(_messages(res)))
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def is_stale() -> bool:

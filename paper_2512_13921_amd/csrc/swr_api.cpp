@@ -622,3 +622,125 @@ int swr_decode_state(const swr_problem_t* p, const void* a, const float* carrier
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Uniform window
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Launch plan of the uniform-window kernels: heads of more than 64 channels
+// run as 64-channel virtual heads; a workgroup holds 8 waves, one per
+// sub-block of a block, times 128 / block virtual heads.
+struct UniPlan {
+    Resolved r;         // shape, stride and size validation shared with the jagged window
+    int hshift, dk, cpl;
+    int64_t hv, vbytes, run_len, nruns, nwork;
+};
+
+int uni_resolve(const swr_problem_t* p, UniPlan* u, bool backward) {
+    int rc = resolve(p, &u->r, false);
+    if (rc != SWR_OK) return rc;
+    if (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) return SWR_ERR_UNSUPPORTED;
+    u->hshift = p->D > 64 ? 1 : 0;
+    u->dk = (int)(p->D >> u->hshift);
+    u->cpl = u->dk / 16;
+    u->hv = p->H << u->hshift;
+    u->vbytes = std::min<int64_t>(16, (int64_t)u->cpl * u->r.es);
+    const int64_t hw = 128 / p->block;                   // virtual heads per workgroup
+    const int64_t groups = p->B * ((u->hv + hw - 1) / hw);
+    if (u->r.empty) {
+        u->run_len = p->block;
+        u->nruns = u->nwork = 0;
+        return SWR_OK;
+    }
+    // one 8-wave workgroup per compute unit for the backward, two for the forward
+    u->run_len = p->run_len > 0 ? p->run_len : pick_run_len(p->T, groups, p->block, backward ? 256 : 512);
+    u->nruns = (p->T + u->run_len - 1) / u->run_len;
+    if (u->nruns > kMaxWorkgroups / groups) return SWR_ERR_UNSUPPORTED;
+    u->nwork = groups * u->nruns;
+    return SWR_OK;
+}
+
+int uni_check_strides(const swr_problem_t* p, const UniPlan& u) {
+    const Dim xd[3] = {{p->B, p->sx_b}, {p->T, p->sx_t}, {p->H, p->sx_h}};
+    for (const Dim& d : xd)
+        if (d.size > 1 && (d.stride * u.r.es) % u.vbytes != 0) return SWR_ERR_ALIGN;
+    return SWR_OK;
+}
+
+swr::Params uni_params(const swr_problem_t* p, const UniPlan& u) {
+    swr::Params k = make_params(p, u.r, false);
+    k.Hv = u.hv;
+    k.hshift = u.hshift;
+    k.run_len = u.run_len;
+    k.nruns = u.nruns;
+    k.nwork = u.nwork;
+    return k;
+}
+
+}  // namespace
+
+extern "C" {
+
+int swr_uniform_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                        const void* c, void* y, void* stream) {
+    UniPlan u;
+    int rc = uni_resolve(p, &u, false);
+    if (rc != SWR_OK) return rc;
+    if (u.r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !y) return SWR_ERR_NULL;
+    for (const void* q : {x, b, c, (const void*)y})
+        if (!aligned(q, u.vbytes)) return SWR_ERR_ALIGN;
+    if (!aligned(a, u.r.es)) return SWR_ERR_ALIGN;
+    if ((rc = uni_check_strides(p, u)) != SWR_OK) return rc;
+    const Span sy = span(y, u.r.xspan);
+    for (const Span& s : {span(x, u.r.xspan), span(b, u.r.xspan), span(c, u.r.xspan), span(a, u.r.aspan * u.r.es)})
+        if (overlap(sy, s)) return SWR_ERR_ALIAS;
+    swr::Params k = uni_params(p, u);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.y = y;
+    return swr::launch_uniform(k, p->dtype, u.cpl, false, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+int swr_uniform_backward(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                         const void* c, const void* dy, void* dx, float* da, void* db, void* dc,
+                         void* stream) {
+    UniPlan u;
+    int rc = uni_resolve(p, &u, true);
+    if (rc != SWR_OK) return rc;
+    if (u.r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return SWR_ERR_NULL;
+    for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
+        if (!aligned(q, u.vbytes)) return SWR_ERR_ALIGN;
+    if (!aligned(a, u.r.es) || !aligned(da, 4)) return SWR_ERR_ALIGN;
+    if ((rc = uni_check_strides(p, u)) != SWR_OK) return rc;
+    const Span outs[4] = {span(dx, u.r.xspan), span(db, u.r.xspan), span(dc, u.r.xspan),
+                          span(da, u.r.aspan * 4)};
+    const Span ins[5] = {span(x, u.r.xspan), span(b, u.r.xspan), span(c, u.r.xspan), span(dy, u.r.xspan),
+                         span(a, u.r.aspan * u.r.es)};
+    for (int i = 0; i < 4; ++i) {
+        for (const Span& s : ins)
+            if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
+    }
+    swr::Params k = uni_params(p, u);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
+    k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+    return swr::launch_uniform(k, p->dtype, u.cpl, true, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+int swr_uniform_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, int64_t* fwd_workgroups,
+                            int64_t* bwd_run_len, int64_t* bwd_workgroups) {
+    UniPlan f, b;
+    int rc = uni_resolve(problem, &f, false);
+    if (rc != SWR_OK) return rc;
+    if ((rc = uni_resolve(problem, &b, true)) != SWR_OK) return rc;
+    if (fwd_run_len) *fwd_run_len = f.run_len;
+    if (fwd_workgroups) *fwd_workgroups = f.nwork;
+    if (bwd_run_len) *bwd_run_len = b.run_len;
+    if (bwd_workgroups) *bwd_workgroups = b.nwork;
+    return SWR_OK;
+}
+
+}  // extern "C"

@@ -139,6 +139,12 @@ hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool ba
 
 hipError_t launch_scan(const ScanParams& q, void* stream);
 
+// Uniform window of block tokens (the window length): forward or backward
+// over 2^hshift virtual heads of 16 * cpl channels per head; the workgroups
+// hold 8 waves, 128 / block virtual heads each, and p.nwork is B times the
+// number of such head groups (the last one padded) times the runs.
+hipError_t launch_uniform(const Params& p, int dtype, int cpl, bool backward, void* stream);
+
 hipError_t launch_step(const StepParams& q, int dtype, int D, bool exact, bool per_channel, void* stream);
 
 hipError_t launch_state(const StateParams& q, int dtype, int D, bool per_channel, void* stream);

@@ -380,3 +380,44 @@ def test_small_heads_are_packed_when_adjacent():
     # the exact workspace covers either plan
     p = problem(B=2, T=1000, H=8, D=16, block=16)
     assert swr.swr_exact_workspace_bytes(p) > 0
+
+
+# ---------------------------------------------------------------------------- uniform window
+
+
+def ufwd(p, x=X, a=A, b=B_, c=C, y=Y):
+    v = ctypes.c_void_p
+    return swr.load().swr_uniform_forward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(y), None)
+
+
+def ubwd(p, x=X, a=A, b=B_, c=C, dy=DY, dx=DX, da=DA, db=DB, dc=DC):
+    v = ctypes.c_void_p
+    return swr.load().swr_uniform_backward(ctypes.byref(p), v(x), v(a), v(b), v(c), v(dy), v(dx),
+                                           v(da), v(db), v(dc), None)
+
+
+def test_uniform_validation():
+    p = problem()
+    assert ufwd(p, y=0) == E_NULL and ubwd(p, da=0) == E_NULL
+    assert ufwd(problem(block=48)) == E_BLOCK and ubwd(problem(D=48)) == E_UNSUP
+    assert ufwd(problem(per_channel=True)) == E_UNSUP and ubwd(problem(per_channel=True)) == E_UNSUP
+    assert ufwd(p, y=X) == E_ALIAS and ubwd(p, db=DX) == E_ALIAS and ubwd(p, da=A) == E_ALIAS
+    assert ufwd(p, c=C + 2) == E_ALIGN and ubwd(p, da=DA + 2) == E_ALIGN
+    assert ufwd(problem(run_len=96)) == E_UNSUP
+    # a 128-channel head runs as two 64-channel halves: 8-byte lane slices in bf16
+    p128 = problem(D=128)
+    assert ufwd(p128, x=X + 8) != E_ALIGN and ufwd(p128, x=X + 4) == E_ALIGN
+    assert ufwd(problem(B=0)) == OK and ubwd(problem(T=0), x=0, dx=0) == OK
+
+
+@pytest.mark.parametrize("block", [16, 32, 64, 128])
+@pytest.mark.parametrize("H,D", [(3, 64), (4, 128), (16, 16)])
+def test_uniform_launch_plan(block, H, D):
+    B, T = 2, 4096
+    info = swr.swr_uniform_launch_info(problem(B=B, T=T, H=H, D=D, block=block, run_len=512))
+    hv = H * (2 if D > 64 else 1)
+    groups = B * -(-hv // (128 // block))
+    assert info["fwd_run_len"] == info["bwd_run_len"] == 512
+    assert info["fwd_workgroups"] == info["bwd_workgroups"] == groups * (T // 512)
+    auto = swr.swr_uniform_launch_info(problem(B=B, T=T, H=H, D=D, block=block))
+    assert auto["fwd_run_len"] % block == 0 and auto["bwd_run_len"] % block == 0
