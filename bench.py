@@ -13,6 +13,8 @@ Phalanx featurisation); a's logits are then drawn N(3, 1).
 --recurrence exact times the exact (untruncated) recurrence instead of the
 jagged window: swr_exact_forward / swr_exact_backward, three launches each
 (run aggregates, carrier scan, reconstruction), timed as a whole.
+--recurrence uniform times the uniform window of the same length (every token
+sees its `block` most recent tokens): swr_uniform_forward / swr_uniform_backward.
 
 Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
 durations come from HIP events recorded on the stream the kernels run on.
@@ -46,34 +48,39 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(cfg, backward):
+def algorithmic_bytes(cfg, backward, with_carriers=True):
     """HBM bytes one launch must move: inputs read once, outputs written once.
     The block carriers (4*D bytes per block per (batch, head), written by the
     forward and read by the backward: 4*D/block bytes per token-head) are part
-    of the algorithm's state and are counted."""
+    of the algorithm's state and are counted (the uniform window has none)."""
     e = 2 if cfg.dtype == "bf16" else 4
     th = cfg.B * cfg.T * cfg.H
-    carriers = th * 4 * cfg.D // cfg.block
+    carriers = th * 4 * cfg.D // cfg.block if with_carriers else 0
     na = cfg.D if cfg.per_channel else 1     # decays per token-head
     if backward:   # x, b, c, dy, a, carriers in; dx, db, dc out; da out in fp32
         return th * (e * (7 * cfg.D + na) + 4 * na) + carriers
     return th * e * (4 * cfg.D + na) + carriers   # x, b, c, a in; y, carriers out
 
 
-def contraction_flops(cfg, backward):
+def contraction_flops(cfg, backward, uniform=False):
     """Dense flops of the intra-block contractions (16x16 sub-block tiles):
-    2 * 16 * D per token-head per contraction; the backward runs three
-    (forward recompute, reverse solve, look-ahead reverse solve).  None for a
-    per-channel decay, whose local solves are scans on the vector ALUs."""
+    2 * 16 * D per token-head per contraction; the jagged backward runs three
+    (forward recompute, reverse solve, look-ahead reverse solve); the uniform
+    window's forward two (local and strict-suffix solves) and its backward six
+    (local, reverse, prefix and previous block's suffix solves, and the two
+    solves of its decay gradient).  None for a per-channel decay, whose local
+    solves are scans on the vector ALUs."""
     if cfg.per_channel:
         return None
     per = 2 * 16 * cfg.D * cfg.B * cfg.T * cfg.H
+    if uniform:
+        return per * (6 if backward else 2)
     return per * (3 if backward else 1)
 
 
 # The sources that decide what a launch does (kernels, grid policy): the
 # recorded traffic is stale once any of them changes.
-KERNEL_SOURCES = ("swr_kernels.hip", "swr_device.h", "swr_api.cpp", "swr_launch.h")
+KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_device.h", "swr_api.cpp", "swr_launch.h")
 
 
 def recorded_traffic(kernel, workload):
@@ -105,7 +112,7 @@ def to_device(arr, dtype):
     return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
 
 
-def cpu_baseline(cfg, prob, budget_s=10.0, exact=False):
+def cpu_baseline(cfg, prob, budget_s=10.0, exact=False, uniform=False):
     """Oracle throughput on whole (batch, head) slices of the workload, in
     tokens/s of the full job (a token carries all H heads).  Slices are taken
     in a fixed shuffled order and revisited until about budget_s seconds of
@@ -131,6 +138,9 @@ def cpu_baseline(cfg, prob, budget_s=10.0, exact=False):
         if exact:
             oracle.exact_forward_slices(xs, as_, bs, cs)
             oracle.exact_backward_slices(xs, as_, bs, cs, dys)
+        elif uniform:
+            oracle.uniform_forward_slices(xs, as_, bs, cs, cfg.block)
+            oracle.uniform_backward_slices(xs, as_, bs, cs, dys, cfg.block)
         else:
             oracle.forward_slices(xs, as_, bs, cs, cfg.block)
             oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
@@ -287,8 +297,9 @@ def main():
                     help="one decay per token and head (default) or per token, head and channel")
     ap.add_argument("--sigmoid", action="store_true",
                     help="a and b are logits; the kernels apply the sigmoid (fused featurisation)")
-    ap.add_argument("--recurrence", choices=("window", "exact"), default="window",
-                    help="the jagged-window recurrence (default) or the exact, untruncated one")
+    ap.add_argument("--recurrence", choices=("window", "exact", "uniform"), default="window",
+                    help="the jagged-window recurrence (default), the exact, untruncated one, or "
+                         "the uniform window of the same length")
     ap.add_argument("--paper-shape", action="store_true",
                     help="forward-only sweep at the paper's own mixer-timing shape (B=1, D=2048 as "
                          "H=128 heads of d=16, block 16, bf16) over T = 1K .. 512K")
@@ -311,6 +322,9 @@ def main():
     swr.load()
 
     cfg = W.CONFIGS[args.config]
+    if args.recurrence == "uniform" and (args.decode or args.paper_shape):
+        print("--recurrence uniform times the forward and backward passes only", file=sys.stderr)
+        return 2
     if args.decode:
         return decode_bench(args, cfg, swr, torch)
     if args.paper_shape:
@@ -322,8 +336,14 @@ def main():
                         a_mu=cfg.a_mu if cfg.a_kind == "sigmoid" else 3.0)
     feat = dict(sigmoid_decay=args.sigmoid, sigmoid_pregate=args.sigmoid)
     exact = args.recurrence == "exact"
+    uniform = args.recurrence == "uniform"
     if exact:
         cfg = cfg.with_(name=cfg.name + "_exact")
+    if uniform:
+        if cfg.per_channel:
+            print("the uniform window supports one decay per head only", file=sys.stderr)
+            return 2
+        cfg = cfg.with_(name=cfg.name + "_uniform")
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -347,6 +367,8 @@ def main():
         if exact:
             swr.swr_exact_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, workspace=workspace,
                                   run_len=args.run_len, **feat)
+        elif uniform:
+            swr.swr_uniform_forward(x, a, b, c, cfg.block, y=y, run_len=args.run_len, **feat)
         else:
             swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
         if ev is not None:
@@ -354,6 +376,9 @@ def main():
         if exact:
             swr.swr_exact_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
                                    workspace=workspace, run_len=args.run_len, **feat)
+        elif uniform:
+            swr.swr_uniform_backward(x, a, b, c, dy, cfg.block, outputs=(dx, da, db, dc),
+                                     run_len=args.run_len, **feat)
         else:
             swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
                              run_len=args.run_len, **feat)
@@ -381,12 +406,14 @@ def main():
     tokens = cfg.B * cfg.T
     value = tokens / (ms_per_step * 1e-3)
 
-    fb, bb = algorithmic_bytes(cfg, False), algorithmic_bytes(cfg, True)
+    fb, bb = algorithmic_bytes(cfg, False, not uniform), algorithmic_bytes(cfg, True, not uniform)
     f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
     dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
     dom_gbs = b_gbs if dominant_bwd else f_gbs
     pc = "_pc" if cfg.per_channel else ""
     dom_kernel = f"swr_bwd{pc}_kernel" if dominant_bwd else f"swr_fwd{pc}_kernel"
+    if uniform:
+        dom_kernel = "swr_uni_bwd_kernel" if dominant_bwd else "swr_uni_fwd_kernel"
     # The exact recurrence's passes are three launches each; their time is
     # taken as a whole and no single kernel's counters stand for it.
     traffic = None if exact else recorded_traffic(dom_kernel, cfg.name)
@@ -397,10 +424,10 @@ def main():
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_MFMA_PEAK_TFLOPS
 
     def mfma_rate(backward, ms):
-        f = contraction_flops(cfg, backward)
+        f = contraction_flops(cfg, backward, uniform)
         return None if f is None else f / (ms * 1e-3) / 1e12
 
-    launch = swr.swr_launch_info(swr.make_problem(
+    launch = (swr.swr_uniform_launch_info if uniform else swr.swr_launch_info)(swr.make_problem(
         cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
         x.stride()[:3], a.stride()[:3], False, args.run_len, cfg.per_channel))
 
@@ -433,7 +460,8 @@ def main():
         "config": {"workload": cfg.name, "B": cfg.B, "T": cfg.T, "H": cfg.H, "d": cfg.D,
                    "block": cfg.block, "decay": "per channel" if cfg.per_channel else "per head",
                    "featurisation": "fused sigmoid of a and b" if args.sigmoid else "none",
-                   "recurrence": "exact (untruncated)" if exact else "jagged window",
+                   "recurrence": ("exact (untruncated)" if exact else
+                                  "uniform window" if uniform else "jagged window"),
                    "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {
@@ -465,7 +493,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(cfg, prob, exact=exact)
+        out["cpu_baseline"] = cpu_baseline(cfg, prob, exact=exact, uniform=uniform)
     print(json.dumps(out), flush=True)
     return 0
 
