@@ -329,3 +329,34 @@ def uniform_backward(x, a, b, c, dy, k, residual=False, sigmoid_decay=False, sig
     if sigmoid_pregate:
         db = db * dsigmoid(b)
     return dx, da, db, dc
+
+
+# ----------------------------------------------------------------------------
+# Gates shared by groups of heads (Sec. 5, "Gate sharing across heads")
+# ----------------------------------------------------------------------------
+
+def _expand_heads(g, group):
+    # [B, T, G, D] -> [B, T, G * group, D]: head h reads group h // group
+    return np.repeat(np.asarray(g, np.float64), group, axis=2)
+
+
+def grouped_forward(x, a, b, c, block, group, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+    """Jagged-window forward where heads g*group .. g*group+group-1 share the
+    pre-gate b[:, :, g] and the post-gate c[:, :, g] ([B, T, H/group, D]):
+    the plain recurrence on gates repeated over each group's heads."""
+    return forward(x, a, _expand_heads(b, group), _expand_heads(c, group), block, residual,
+                   sigmoid_decay, sigmoid_pregate)
+
+
+def grouped_backward(x, a, b, c, dy, block, group, residual=False, sigmoid_decay=False,
+                     sigmoid_pregate=False):
+    """(dx, da, db, dc) for shared gates: db and dc ([B, T, H/group, D]) are
+    the per-head gradients of the repeated gates summed over each group."""
+    dx, da, db, dc = backward(x, a, _expand_heads(b, group), _expand_heads(c, group), dy, block,
+                              residual, sigmoid_decay, sigmoid_pregate)
+    B, T, H, D = db.shape
+
+    def fold(t):
+        return t.reshape(B, T, H // group, group, D).sum(axis=3)
+
+    return dx, da, fold(db), fold(dc)
