@@ -40,8 +40,9 @@
  *
  * Ownership.  Every pointer is device memory owned by the caller.  The library
  * allocates no memory and keeps no mutable global state; calls from several
- * host threads are safe.  Only the exact-recurrence calls need a workspace,
- * which the caller provides.  Outputs are fully overwritten.
+ * host threads are safe.  Only the exact-recurrence calls and the backward
+ * with shared gates need a workspace, which the caller provides.  Outputs are
+ * fully overwritten.
  *
  * Asynchrony.  Work is enqueued on `stream` (a hipStream_t passed as void*;
  * NULL = the default stream) and the call returns without waiting.  A fault
@@ -246,6 +247,43 @@ int swr_exact_step(const swr_problem_t* problem, const void* x, const void* a, c
  * times the carrier of the block before it. */
 int swr_decode_state(const swr_problem_t* problem, const void* a, const float* carriers, float* state,
                      void* stream);
+
+/* ------------------------------------------------------------------------
+ * Gates shared by groups of heads
+ *
+ * The Phalanx layer may share the key-like pre-gate and the query-like
+ * post-gate across groups of heads, as grouped-query attention shares keys
+ * and values (Sec. 5, "Gate sharing across heads"): heads g*group ..
+ * g*group + group - 1 all use b[:, :, g] and c[:, :, g].  b and c (and db,
+ * dc) are then [B, T, H / group, D] with element strides gate_strides[0..2]
+ * (batch, token, group; the channel stride is 1), alignment as for x.  The
+ * recurrence is the jagged window of swr_forward / swr_backward, with the
+ * same carriers; db and dc are the gradients with respect to the shared
+ * gates (sums over each group's heads, added in head order, so results are
+ * reproducible).  The backward writes every head's share of db and dc in
+ * float32 to a caller-provided workspace and sums the groups in a second
+ * launch.  One decay per head only (SWR_FLAG_PER_CHANNEL_DECAY is rejected);
+ * heads of 16 and 32 channels are not packed.  group = 1 is the ordinary
+ * layout with b, c at their own strides.
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes swr_backward_shared_gates needs: 2 * B * T * H * D float32
+ * (the heads' shares of db and dc), or a negative SWR_ERR_* code. */
+int64_t swr_shared_gates_workspace_bytes(const swr_problem_t* problem, int64_t group);
+
+/* Forward with shared gates: y = SWR(x, a, b, c) where head h reads
+ * b[:, :, h / group] and c[:, :, h / group].  carriers as for swr_forward. */
+int swr_forward_shared_gates(const swr_problem_t* problem, int64_t group, const int64_t* gate_strides,
+                             const void* x, const void* a, const void* b, const void* c, void* y,
+                             float* carriers, void* stream);
+
+/* Backward with shared gates: dx, da as for swr_backward; db and dc in the
+ * gates' layout.  workspace: swr_shared_gates_workspace_bytes bytes of device
+ * memory (16-byte aligned, no initialisation needed, overwritten). */
+int swr_backward_shared_gates(const swr_problem_t* problem, int64_t group, const int64_t* gate_strides,
+                              const void* x, const void* a, const void* b, const void* c, const void* dy,
+                              const float* carriers, void* dx, float* da, void* db, void* dc,
+                              void* workspace, void* stream);
 
 /* ------------------------------------------------------------------------
  * Uniform window

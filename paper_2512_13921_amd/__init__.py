@@ -26,6 +26,7 @@ __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error
            "swr_exact_forward", "swr_exact_backward", "swr_exact_workspace_bytes",
            "swr_step", "swr_exact_step", "swr_decode_state",
            "swr_uniform_forward", "swr_uniform_backward", "swr_uniform_launch_info",
+           "swr_forward_shared_gates", "swr_backward_shared_gates", "swr_shared_gates_workspace_bytes",
            "SWRFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
@@ -105,6 +106,13 @@ def load():
         lib.swr_uniform_backward.restype = ctypes.c_int
         lib.swr_uniform_launch_info.argtypes = [P, i64p, i64p, i64p, i64p]
         lib.swr_uniform_launch_info.restype = ctypes.c_int
+        i64 = ctypes.c_int64
+        lib.swr_shared_gates_workspace_bytes.argtypes = [P, i64]
+        lib.swr_shared_gates_workspace_bytes.restype = i64
+        lib.swr_forward_shared_gates.argtypes = [P, i64, vp] + [vp] * 7
+        lib.swr_forward_shared_gates.restype = ctypes.c_int
+        lib.swr_backward_shared_gates.argtypes = [P, i64, vp] + [vp] * 12
+        lib.swr_backward_shared_gates.restype = ctypes.c_int
         if lib.swr_abi_version() != SWR_ABI_VERSION:
             raise RuntimeError("libswr.so ABI version does not match the binding")
         _lib = lib
@@ -457,6 +465,89 @@ def swr_decode_state(x, a, carriers, block, state=None, stream=None, sigmoid_dec
     if rc != 0:
         raise SwrError(rc, "swr_decode_state")
     return state
+
+
+# ----------------------------------------------------------------------------- shared gates
+
+
+def _gates_check(x, b, group):
+    B, T, H, D = x.shape
+    if group < 1 or H % group != 0:
+        raise ValueError("group must divide the number of heads")
+    if tuple(b.shape) != (B, T, H // group, D):
+        raise ValueError(f"shared gates must be [B, T, H / group, D] = {(B, T, H // group, D)}")
+    if b.dtype != x.dtype or b.device != x.device or (b.stride(3) != 1 and D > 1):
+        raise ValueError("shared gates need x's dtype and device and contiguous channels")
+
+
+def _i64x3(strides):
+    return (ctypes.c_int64 * 3)(*(int(s) for s in strides[:3]))
+
+
+def swr_shared_gates_workspace_bytes(problem: SwrProblem, group: int) -> int:
+    """Bytes of workspace swr_backward_shared_gates needs."""
+    n = int(load().swr_shared_gates_workspace_bytes(ctypes.byref(problem), int(group)))
+    if n < 0:
+        raise SwrError(n, "swr_shared_gates_workspace_bytes")
+    return n
+
+
+def swr_forward_shared_gates(x, a, b, c, block, group, residual=False, y=None, carriers=None,
+                             save_carriers=False, run_len=0, stream=None, sigmoid_decay=False,
+                             sigmoid_pregate=False):
+    """Jagged-window forward where heads g*group .. g*group+group-1 share the
+    gates b[:, :, g] and c[:, :, g] (b, c: [B, T, H / group, D]).  Returns y,
+    or (y, carriers) as swr_forward."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _gates_check(x, b, group)
+    _same_layout(b, c)
+    if y is None:
+        y = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+    else:
+        _same_layout(x, y)
+    want_v = save_carriers or carriers is not None
+    v = _carrier_tensor(x, block, carriers) if want_v else None
+    rc = load().swr_forward_shared_gates(ctypes.byref(problem), int(group), _i64x3(b.stride()), _ptr(x),
+                                         _ptr(a), _ptr(b), _ptr(c), _ptr(y), _ptr(v) if want_v else None,
+                                         _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_forward_shared_gates")
+    return (y, v) if want_v else y
+
+
+def swr_backward_shared_gates(x, a, b, c, dy, carriers, block, group, residual=False, outputs=None,
+                              workspace=None, run_len=0, stream=None, sigmoid_decay=False,
+                              sigmoid_pregate=False):
+    """(dx, da, db, dc) of swr_forward_shared_gates; db and dc have b's layout."""
+    torch = _torch()
+    problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
+    _gates_check(x, b, group)
+    _same_layout(b, c)
+    _same_layout(x, dy)
+    carriers = _carrier_tensor(x, block, carriers)
+    if outputs is None:
+        dx = torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
+        db, dc = (torch.empty_strided(b.shape, b.stride(), dtype=b.dtype, device=b.device) for _ in range(2))
+        da = torch.empty_strided(a.shape, a.stride(), dtype=torch.float32, device=a.device)
+    else:
+        dx, da, db, dc = outputs
+        _same_layout(x, dx)
+        _same_layout(b, db, dc)
+        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
+            raise ValueError("da must be float32 with the shape and strides of a")
+    nbytes = swr_shared_gates_workspace_bytes(problem, group)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes // 4, 1), dtype=torch.float32, device=x.device)
+    elif workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes")
+    rc = load().swr_backward_shared_gates(ctypes.byref(problem), int(group), _i64x3(b.stride()), _ptr(x),
+                                          _ptr(a), _ptr(b), _ptr(c), _ptr(dy), _ptr(carriers), _ptr(dx),
+                                          _ptr(da), _ptr(db), _ptr(dc), _ptr(workspace),
+                                          _stream(stream, x.device))
+    if rc != 0:
+        raise SwrError(rc, "swr_backward_shared_gates")
+    return dx, da, db, dc
 
 
 # ----------------------------------------------------------------------------- uniform window

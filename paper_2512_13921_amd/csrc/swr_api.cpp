@@ -744,3 +744,113 @@ int swr_uniform_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Gates shared by groups of heads
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Validation common to both shared-gate calls: the problem as for the jagged
+// window (no per-channel decay, no packing), then the group and the gate
+// tensors' strides.  gspan receives the bytes spanned by one gate tensor.
+int gates_resolve(const swr_problem_t* p, int64_t group, const int64_t* gst, Resolved* r, int64_t* gspan) {
+    int rc = resolve(p, r, false);
+    if (rc != SWR_OK) return rc;
+    if (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) return SWR_ERR_UNSUPPORTED;
+    if (group < 1 || (p->H > 0 && p->H % group != 0)) return SWR_ERR_SHAPE;
+    *gspan = 0;
+    if (r->empty) return SWR_OK;
+    if (!gst) return SWR_ERR_NULL;
+    Dim gd[4] = {{p->B, gst[0]}, {p->T, gst[1]}, {p->H / group, gst[2]}, {p->D, 1}};
+    for (int i = 0; i < 3; ++i)
+        if (gd[i].size > 1 && (gd[i].stride * r->es) % r->vbytes != 0) return SWR_ERR_ALIGN;
+    const int64_t go = max_offset(gd, 4);
+    if (go < 0 || !non_overlapping(gd, 4)) return SWR_ERR_SHAPE;   // (sorts gd)
+    *gspan = (go + 1) * r->es;
+    const int64_t lim = 0x7fffffffLL;   // 32-bit lane offsets over 16 rows
+    if (gst[1] > (lim - p->D * r->es) / (16 * r->es)) return SWR_ERR_UNSUPPORTED;
+    if (p->H * p->D > (lim - p->D * 4) / (16 * 4)) return SWR_ERR_UNSUPPORTED;
+    return SWR_OK;
+}
+
+void set_gates(swr::Params* k, int64_t group, const int64_t* gst) {
+    k->group = group;
+    k->sg_b = gst[0]; k->sg_t = gst[1]; k->sg_h = gst[2];
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t swr_shared_gates_workspace_bytes(const swr_problem_t* p, int64_t group) {
+    Resolved r;
+    const int rc = resolve(p, &r, false);
+    if (rc != SWR_OK) return rc;
+    if (group < 1 || (p->H > 0 && p->H % group != 0)) return SWR_ERR_SHAPE;
+    return 2 * p->B * p->T * p->H * p->D * 4;
+}
+
+int swr_forward_shared_gates(const swr_problem_t* p, int64_t group, const int64_t* gate_strides,
+                             const void* x, const void* a, const void* b, const void* c, void* y,
+                             float* carriers, void* stream) {
+    Resolved r;
+    int64_t gspan;
+    int rc = gates_resolve(p, group, gate_strides, &r, &gspan);
+    if (rc != SWR_OK) return rc;
+    if (r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !y) return SWR_ERR_NULL;
+    for (const void* q : {x, b, c, (const void*)y})
+        if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
+    if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    const Span ins[4] = {span(x, r.xspan), span(b, gspan), span(c, gspan), span(a, r.aspan * r.es)};
+    const Span sy = span(y, r.xspan), sv = span(carriers, carriers ? r.carriers * 4 : 0);
+    for (const Span& s : ins)
+        if (overlap(sy, s) || overlap(sv, s)) return SWR_ERR_ALIAS;
+    if (overlap(sy, sv)) return SWR_ERR_ALIAS;
+    swr::Params k = make_params(p, r, false);
+    set_gates(&k, group, gate_strides);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, false, 1, swr::kGrouped, stream) == hipSuccess
+               ? SWR_OK : SWR_ERR_HIP;
+}
+
+int swr_backward_shared_gates(const swr_problem_t* p, int64_t group, const int64_t* gate_strides,
+                              const void* x, const void* a, const void* b, const void* c, const void* dy,
+                              const float* carriers, void* dx, float* da, void* db, void* dc,
+                              void* workspace, void* stream) {
+    Resolved r;
+    int64_t gspan;
+    int rc = gates_resolve(p, group, gate_strides, &r, &gspan);
+    if (rc != SWR_OK) return rc;
+    if (r.empty) return SWR_OK;
+    if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc || !workspace) return SWR_ERR_NULL;
+    for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
+        if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
+    if (!aligned(a, r.es) || !aligned(da, 4) || !aligned(carriers, 16) || !aligned(workspace, 16))
+        return SWR_ERR_ALIGN;
+    if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
+    const int64_t wbytes = 2 * p->B * p->T * p->H * p->D * 4;
+    const Span outs[5] = {span(dx, r.xspan), span(db, gspan), span(dc, gspan), span(da, r.aspan * 4),
+                          span(workspace, wbytes)};
+    const Span ins[6] = {span(x, r.xspan), span(b, gspan), span(c, gspan), span(dy, r.xspan),
+                         span(a, r.aspan * r.es), span(carriers, r.carriers * 4)};
+    for (int i = 0; i < 5; ++i) {
+        for (const Span& s : ins)
+            if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
+        for (int j = i + 1; j < 5; ++j)
+            if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
+    }
+    swr::Params k = make_params(p, r, true);
+    set_gates(&k, group, gate_strides);
+    k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
+    k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+    k.carriers = const_cast<float*>(carriers);
+    k.gws = (float*)workspace;
+    if (swr::launch(k, p->dtype, r.dk, r.bwd, true, false, 1, swr::kGrouped, stream) != hipSuccess)
+        return SWR_ERR_HIP;
+    return swr::launch_gate_reduce(k, p->dtype, (int)p->D, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+}
+
+}  // extern "C"

@@ -68,10 +68,12 @@ namespace {
 // (kSwr); or, for the exact recurrence, the runs' aggregates -- the end state
 // of each run started from zero and the run's decay product -- (kAggregate),
 // or the outputs from the exact state entering each run (kExact).  The exact
-// modes need no halo and never restart the carrier.
+// modes need no halo and never restart the carrier.  kGrouped is the jagged
+// window with b and c shared by groups of p.group heads (their own strides).
 template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
-    constexpr bool SWR = MODE == kSwr;
+    constexpr bool GG = MODE == kGrouped;
+    constexpr bool SWR = MODE == kSwr || GG;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -99,14 +101,18 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
     const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    // b and c: this head's rows, or its group's with shared gates
+    const int64_t go = GG ? (wk.b * p.sg_b + (wk.h / p.group) * p.sg_h) * ES : xo;
     const char* xb = (const char*)p.x + xo;
-    const char* bb = (const char*)p.b + xo;
-    const char* cb = (const char*)p.c + xo;
+    const char* bb = (const char*)p.b + go;
+    const char* cb = (const char*)p.c + go;
     char* yb = (char*)p.y + xo;
     const char* ab = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * ES;
     const int64_t rs = p.sx_t * ES;    // row stride in bytes
+    const int64_t gs = GG ? p.sg_t * ES : rs;   // of b and c
     const int64_t as = p.sa_t * ES;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t goff = GG ? (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES) : loff;
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     // false: only the block carriers (or the run aggregates) are produced
     const bool want_y = MODE != kAggregate && p.y != nullptr;
@@ -141,13 +147,13 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     // Copies the x, b, c tiles of the step starting at token t0 into this wave's LDS slot.
     auto prefetch = [&](int64_t t0) {
         const int64_t r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
-        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs), rc = rsrc(cb + r0 * rs);
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs), rc = rsrc(cb + r0 * gs);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const uint32_t o = loff + (uint32_t)(r * rs);
+            const uint32_t o = loff + (uint32_t)(r * rs), og = goff + (uint32_t)(r * gs);
             LR::template issue<kFwdLoad>(rx, in_range(ok_xb(tr0 + r), o), s_tile[wv][0][r]);
-            LR::template issue<kFwdLoad>(rb, in_range(ok_xb(tr0 + r), o), s_tile[wv][1][r]);
-            LR::template issue<kFwdLoad>(rc, in_range(ok_c(tr0 + r), o), s_tile[wv][2][r]);
+            LR::template issue<kFwdLoad>(rb, in_range(ok_xb(tr0 + r), og), s_tile[wv][1][r]);
+            LR::template issue<kFwdLoad>(rc, in_range(ok_c(tr0 + r), og), s_tile[wv][2][r]);
         }
     };
     if constexpr (PREFETCH) {
@@ -173,15 +179,15 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the slot may be refilled
             if (t0 + STEP < t_stop) prefetch(t0 + STEP);
         } else {
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                         rc = rsrc(cb + r0 * rs);
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs),
+                                         rc = rsrc(cb + r0 * gs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int64_t t = tr0 + r;
-                const uint32_t o = loff + (uint32_t)(r * rs);
+                const uint32_t o = loff + (uint32_t)(r * rs), og = goff + (uint32_t)(r * gs);
                 xr[r].template load<kFwdLoad>(rx, in_range(ok_xb(t), o));
-                br[r].template load<kFwdLoad>(rb, in_range(ok_xb(t), o));
-                cr[r].template load<kFwdLoad>(rc, in_range(ok_c(t), o));
+                br[r].template load<kFwdLoad>(rb, in_range(ok_xb(t), og));
+                cr[r].template load<kFwdLoad>(rc, in_range(ok_c(t), og));
             }
         }
         const int64_t ta = r0 + n;
@@ -305,9 +311,14 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
 // entering the run from its end is stage II's result (no halo), the state
 // entering each step is the previous block's exact carrier (or the initial
 // state), nothing restarts, and the decay gradient is sum_mu H_{k-1} du_k.
+//
+// MODE kGrouped: the jagged window with b and c shared by groups of heads;
+// this head's shares of db and dc go to the float32 workspace p.gws, summed
+// over each group afterwards (swr_gate_reduce_kernel).
 template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
-    constexpr bool SWR = MODE == kSwr;
+    constexpr bool GG = MODE == kGrouped;
+    constexpr bool SWR = MODE == kSwr || GG;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -328,21 +339,29 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the halo block
 
     const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    // b and c: this head's rows, or its group's with shared gates
+    const int64_t go = GG ? (wk.b * p.sg_b + (wk.h / p.group) * p.sg_h) * ES : xo;
     const char* xb = (const char*)p.x + xo;
-    const char* bb = (const char*)p.b + xo;
-    const char* cb = (const char*)p.c + xo;
+    const char* bb = (const char*)p.b + go;
+    const char* cb = (const char*)p.c + go;
     const char* dyb = (const char*)p.dy + xo;
     char* dxb = (char*)p.dx + xo;
-    char* dbb = (char*)p.db + xo;
-    char* dcb = (char*)p.dc + xo;
+    // db and dc: this head's float32 shares in the workspace with shared gates
+    const int64_t wso = ((wk.b * p.T) * p.H + wk.h) * D;
+    char* dbb = GG ? (char*)(p.gws + wso) : (char*)p.db + xo;
+    char* dcb = GG ? (char*)(p.gws + p.B * p.T * p.H * D + wso) : (char*)p.dc + xo;
     const int64_t ao = wk.b * p.sa_b + wk.h * p.sa_h;
     const char* ab = (const char*)p.a + ao * ES;
     char* dab = (char*)(p.da + ao);
     const float* vb = p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D;
     const int64_t rs = p.sx_t * ES;
+    const int64_t gs = GG ? p.sg_t * ES : rs;        // row stride of b and c
+    const int64_t ws = GG ? p.H * D * 4 : rs;         // row stride of db and dc
     const int64_t as = p.sa_t * ES;
     const int64_t das = p.sa_t * 4;
     const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t goff = GG ? (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES) : loff;
+    const uint32_t woff = GG ? (uint32_t)(4 * grp) * (uint32_t)ws + (uint32_t)(n * CPL * 4) : loff;
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das;
     const int base = lane & 48;   // first lane of this 16-lane row
@@ -367,13 +386,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     if (SWR && wk.t_end < p.T) {
         const int64_t r0 = wk.t_end + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
-        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+        const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * gs), rdy = rsrc(dyb + r0 * rs);
         R_ cr[4], dyr[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const uint32_t o = in_range(tr0 + r < t_la, loff + (uint32_t)(r * rs));
-            cr[r].template load<kBwdLoad>(rc, o);
-            dyr[r].template load<kBwdLoad>(rdy, o);
+            const bool ok = tr0 + r < t_la;
+            cr[r].template load<kBwdLoad>(rc, in_range(ok, goff + (uint32_t)(r * gs)));
+            dyr[r].template load<kBwdLoad>(rdy, in_range(ok, loff + (uint32_t)(r * rs)));
         }
         float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(r0 + n < t_la, aoff));
         if (sig_a) a_n = r0 + n < t_la ? sigmoid(a_n) : 0.0f;
@@ -424,14 +443,16 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             // does, measured no faster here: the backward's eight waves keep
             // enough loads in flight.)
             R_ cr[4];
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                         rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs),
+                                         rc = rsrc(cb + r0 * gs), rdy = rsrc(dyb + r0 * rs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+                const bool ok = tr0 + r < wk.t_end;
+                const uint32_t o = in_range(ok, loff + (uint32_t)(r * rs));
+                const uint32_t og = GG ? in_range(ok, goff + (uint32_t)(r * gs)) : o;
                 xr[r].template load<kBwdLoad>(rx, o);
-                br[r].template load<kBwdLoad>(rb, o);
-                cr[r].template load<kBwdLoad>(rc, o);
+                br[r].template load<kBwdLoad>(rb, og);
+                cr[r].template load<kBwdLoad>(rc, og);
                 dyr[r].template load<kBwdLoad>(rdy, o);
             }
 #pragma unroll
@@ -570,8 +591,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             Gsh[0] = grp == 0 ? 1.0f : gprev;
             Gsh[1] = dk.G[0]; Gsh[2] = dk.G[1]; Gsh[3] = dk.G[2];
         }
-        const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * rs),
-                                     rdc = rsrc(dcb + r0 * rs), rda = rsrc(dab + r0 * das);
+        const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * ws),
+                                     rdc = rsrc(dcb + r0 * ws), rda = rsrc(dab + r0 * das);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t t = tr0 + r;
@@ -591,8 +612,14 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
-            store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
-            store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
+            if constexpr (GG) {   // this head's float32 shares, summed over the group later
+                const uint32_t ow = in_range(t < wk.t_end, woff + (uint32_t)(r * ws));
+                store_row<IoF32, CPL>(rdb, ow, vdb);
+                store_row<IoF32, CPL>(rdc, ow, vdc);
+            } else {
+                store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
+                store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
+            }
             const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
             __builtin_amdgcn_raw_buffer_store_b32(
                 __builtin_bit_cast(int, tot), rda,
@@ -789,6 +816,37 @@ __device__ inline float gload_scalar(const void* p) {
 // the current block; when a block starts, e takes s and s restarts from zero.
 // The exact recurrence carries h alone.  Work per token is a few flops per
 // channel: a launch of a handful of tokens is bound by latency, not by HBM.
+// Gates shared by groups of heads: sums each group's float32 shares of db and
+// dc, which the kGrouped backward left in p.gws ([2][B][T][H][D]), over the
+// group's heads in head order (so the result does not depend on scheduling)
+// and stores db and dc ([B, T, H / group, D], strides sg_*) in the I/O dtype.
+// One thread per (batch, token, group, 16th of the channels).
+template <class IO, int CPL>
+__global__ __launch_bounds__(256) void swr_gate_reduce_kernel(Params p) {
+    constexpr int D = CPL * SB;
+    const int64_t G = p.H / p.group;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= p.B * p.T * G * 16) return;
+    const int n = (int)(i & 15);
+    const int64_t rest = i >> 4;
+    const int64_t g = rest % G, t = (rest / G) % p.T, b = rest / (G * p.T);
+    const float* src = p.gws + ((b * p.T + t) * p.H + g * p.group) * D + n * CPL;
+    const int64_t half = p.B * p.T * p.H * D;
+    float vb[CPL], vc[CPL];
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) { vb[m] = 0.f; vc[m] = 0.f; }
+    for (int64_t j = 0; j < p.group; ++j) {
+        Row<IoF32, CPL> rb, rc;
+        gload<IoF32, CPL>(rb, src + j * D);
+        gload<IoF32, CPL>(rc, src + half + j * D);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) { vb[m] += rb.get(m); vc[m] += rc.get(m); }
+    }
+    const int64_t o = (b * p.sg_b + t * p.sg_t + g * p.sg_h + n * CPL) * IO::ES;
+    gstore<IO, CPL>((char*)p.db + o, vb);
+    gstore<IO, CPL>((char*)p.dc + o, vc);
+}
+
 template <class IO, int CPL, bool EXACT, bool PC, bool FEAT>
 __global__ __launch_bounds__(256) void swr_step_kernel(StepParams q) {
     constexpr int D = CPL * SB;
@@ -1656,6 +1714,7 @@ static hipError_t launch_mode(const Params& p, const Shape& sh, bool backward, i
         case kSwr: return launch_shape<IO, CPL, FEAT, kSwr>(p, sh, backward, stream);
         case kAggregate: return launch_shape<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
         case kExact: return launch_shape<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
+        case kGrouped: return launch_shape<IO, CPL, FEAT, kGrouped>(p, sh, backward, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1768,6 +1827,26 @@ hipError_t launch_state(const StateParams& q, int dtype, int D, bool per_channel
     hipStream_t st = (hipStream_t)stream;
     if (dtype == 1) return launch_state_io<IoBf16>(q, D, per_channel, st);
     return launch_state_io<IoF32>(q, D, per_channel, st);
+}
+
+template <class IO>
+static hipError_t launch_gate_reduce_io(const Params& p, int D, hipStream_t st) {
+    const int64_t n = p.B * p.T * (p.H / p.group) * 16;
+    const dim3 grid((unsigned)((n + 255) / 256)), blk(256);
+    switch (D) {
+        case 16: hipLaunchKernelGGL((swr_gate_reduce_kernel<IO, 1>), grid, blk, 0, st, p); break;
+        case 32: hipLaunchKernelGGL((swr_gate_reduce_kernel<IO, 2>), grid, blk, 0, st, p); break;
+        case 64: hipLaunchKernelGGL((swr_gate_reduce_kernel<IO, 4>), grid, blk, 0, st, p); break;
+        case 128: hipLaunchKernelGGL((swr_gate_reduce_kernel<IO, 8>), grid, blk, 0, st, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gate_reduce(const Params& p, int dtype, int D, void* stream) {
+    if (p.B * p.T * p.H == 0) return hipSuccess;
+    hipStream_t st = (hipStream_t)stream;
+    return dtype == 1 ? launch_gate_reduce_io<IoBf16>(p, D, st) : launch_gate_reduce_io<IoF32>(p, D, st);
 }
 
 hipError_t launch_scan(const ScanParams& q, void* stream) {

@@ -48,6 +48,13 @@ struct Params {
     int64_t agg_len;    // stage III: tokens per aggregate run of stage I (this launch's run
                         // length divides by it), and their number per sequence
     int64_t agg_nruns;
+    // Gates shared by groups of heads (mode kGrouped): b and c are
+    // [B, T, H / group, D] with element strides sg_*; the backward writes
+    // every head's share of db and dc, in float32, to gws ([2][B][T][H][D],
+    // contiguous), which swr_gate_reduce_kernel then sums over each group.
+    int64_t group;
+    int64_t sg_b, sg_t, sg_h;
+    float* gws;
 };
 
 // What a forward or backward launch computes.
@@ -55,7 +62,13 @@ enum Mode {
     kSwr = 0,        // the jagged-window (truncated) recurrence
     kAggregate = 1,  // exact, stage I: run aggregates only (no outputs)
     kExact = 2,      // exact, stage III: outputs from the carry entering each run
+    kGrouped = 3,    // the jagged window with b and c shared by groups of heads
 };
+
+// Sums the per-head float32 shares of db and dc that a kGrouped backward left
+// in p.gws over each group of p.group heads, in head order, and writes db and
+// dc ([B, T, H / group, D], strides sg_*) in the I/O dtype.
+hipError_t launch_gate_reduce(const Params& p, int dtype, int D, void* stream);
 
 // Stage II of the exact recurrence: for every (batch, head) and channel, the
 // carrier recurrence over a sequence's runs, S_r = P_r S_{r-1} + V_r forward

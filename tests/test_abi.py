@@ -421,3 +421,39 @@ def test_uniform_launch_plan(block, H, D):
     assert info["fwd_workgroups"] == info["bwd_workgroups"] == groups * (T // 512)
     auto = swr.swr_uniform_launch_info(problem(B=B, T=T, H=H, D=D, block=block))
     assert auto["fwd_run_len"] % block == 0 and auto["bwd_run_len"] % block == 0
+
+
+# ---------------------------------------------------------------------------- shared gates
+
+
+def gfwd(p, group, gst, x=X, a=A, b=B_, c=C, y=Y):
+    v = ctypes.c_void_p
+    g = None if gst is None else (ctypes.c_int64 * 3)(*gst)
+    return swr.load().swr_forward_shared_gates(ctypes.byref(p), group, g, v(x), v(a), v(b), v(c), v(y),
+                                               None, None)
+
+
+def gbwd(p, group, gst, x=X, a=A, b=B_, c=C, dy=DY, v_=V, dx=DX, da=DA, db=DB, dc=DC, ws=GB * 20):
+    v = ctypes.c_void_p
+    g = None if gst is None else (ctypes.c_int64 * 3)(*gst)
+    return swr.load().swr_backward_shared_gates(ctypes.byref(p), group, g, v(x), v(a), v(b), v(c), v(dy),
+                                                v(v_), v(dx), v(da), v(db), v(dc), v(ws), None)
+
+
+def test_shared_gates_validation():
+    B, T, H, D = 2, 256, 4, 64
+    p = problem(B=B, T=T, H=H, D=D)
+    gst = (T * 2 * D, 2 * D, D)          # [B, T, 2 groups, D]
+    assert gfwd(p, 3, gst) == E_SHAPE and gfwd(p, 0, gst) == E_SHAPE
+    assert gfwd(p, 2, None) == E_NULL and gbwd(p, 2, gst, ws=0) == E_NULL
+    assert gfwd(problem(B=B, T=T, H=H, D=D, per_channel=True), 2, gst) == E_UNSUP
+    assert gfwd(p, 2, (T * 2 * D, 2 * D, D - 4)) in (E_SHAPE, E_ALIGN)
+    assert gfwd(p, 2, (T * 2 * D, 2 * D + 2, D)) == E_ALIGN       # 4-byte rows, 8-byte lane slices
+    assert gfwd(p, 2, gst, b=B_ + 4) == E_ALIGN
+    assert gfwd(p, 2, gst, y=B_) == E_ALIAS
+    assert gbwd(p, 2, gst, db=GB * 20) == E_ALIAS          # db inside the workspace
+    assert gbwd(p, 2, gst, dc=C) == E_ALIAS
+    assert gfwd(problem(B=0), 2, gst) == OK and gbwd(problem(T=0), 2, None) == OK
+    assert swr.swr_shared_gates_workspace_bytes(p, 2) == 2 * B * T * H * D * 4
+    with pytest.raises(swr.SwrError):
+        swr.swr_shared_gates_workspace_bytes(p, 3)
