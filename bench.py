@@ -15,6 +15,9 @@ jagged window: swr_exact_forward / swr_exact_backward, three launches each
 (run aggregates, carrier scan, reconstruction), timed as a whole.
 --recurrence uniform times the uniform window of the same length (every token
 sees its `block` most recent tokens): swr_uniform_forward / swr_uniform_backward.
+--gate-groups G shares b and c across groups of H/G heads (the Phalanx gate
+sharing): swr_forward_shared_gates / swr_backward_shared_gates, the backward
+timed with its group reduction.
 
 Throughput is tokens/s = B*T / (time of one forward + one backward).  Kernel
 durations come from HIP events recorded on the stream the kernels run on.
@@ -48,7 +51,7 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(cfg, backward, with_carriers=True):
+def algorithmic_bytes(cfg, backward, with_carriers=True, gate_groups=0):
     """HBM bytes one launch must move: inputs read once, outputs written once.
     The block carriers (4*D bytes per block per (batch, head), written by the
     forward and read by the backward: 4*D/block bytes per token-head) are part
@@ -57,6 +60,11 @@ def algorithmic_bytes(cfg, backward, with_carriers=True):
     th = cfg.B * cfg.T * cfg.H
     carriers = th * 4 * cfg.D // cfg.block if with_carriers else 0
     na = cfg.D if cfg.per_channel else 1     # decays per token-head
+    if gate_groups:   # b, c (and db, dc) once per group of heads
+        tg = cfg.B * cfg.T * gate_groups
+        if backward:
+            return th * (e * (3 * cfg.D + na) + 4 * na) + tg * e * 4 * cfg.D + carriers
+        return th * e * (2 * cfg.D + na) + tg * e * 2 * cfg.D + carriers
     if backward:   # x, b, c, dy, a, carriers in; dx, db, dc out; da out in fp32
         return th * (e * (7 * cfg.D + na) + 4 * na) + carriers
     return th * e * (4 * cfg.D + na) + carriers   # x, b, c, a in; y, carriers out
@@ -300,6 +308,8 @@ def main():
     ap.add_argument("--recurrence", choices=("window", "exact", "uniform"), default="window",
                     help="the jagged-window recurrence (default), the exact, untruncated one, or "
                          "the uniform window of the same length")
+    ap.add_argument("--gate-groups", type=int, default=0,
+                    help="share b and c across this many groups of heads (0: no sharing)")
     ap.add_argument("--paper-shape", action="store_true",
                     help="forward-only sweep at the paper's own mixer-timing shape (B=1, D=2048 as "
                          "H=128 heads of d=16, block 16, bf16) over T = 1K .. 512K")
@@ -344,6 +354,13 @@ def main():
             print("the uniform window supports one decay per head only", file=sys.stderr)
             return 2
         cfg = cfg.with_(name=cfg.name + "_uniform")
+    groups = args.gate_groups
+    if groups:
+        if cfg.per_channel or exact or uniform or groups < 1 or cfg.H % groups:
+            print("--gate-groups needs the jagged window, one decay per head and a divisor of H",
+                  file=sys.stderr)
+            return 2
+        cfg = cfg.with_(name=cfg.name + f"_gates{groups}")
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -354,6 +371,14 @@ def main():
     da = torch.empty(a.shape, dtype=torch.float32, device=a.device)   # a's shape, contiguous
     carriers = torch.empty(swr.carrier_shape(x, cfg.block), dtype=torch.float32, device=x.device)
     stream = torch.cuda.current_stream()
+    if groups:   # each group's gates: those drawn for its first head
+        gsz = cfg.H // groups
+        b, c = b[:, :, ::gsz].contiguous(), c[:, :, ::gsz].contiguous()
+        db, dc = torch.empty_like(b), torch.empty_like(c)
+        gprob = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
+                                 x.stride()[:3], a.stride()[:3])
+        gws = torch.empty(swr.swr_shared_gates_workspace_bytes(gprob, gsz) // 4, dtype=torch.float32,
+                          device=x.device)
     if exact:
         wsp = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
                                x.stride()[:3], a.stride()[:3], False, args.run_len, cfg.per_channel)
@@ -369,6 +394,9 @@ def main():
                                   run_len=args.run_len, **feat)
         elif uniform:
             swr.swr_uniform_forward(x, a, b, c, cfg.block, y=y, run_len=args.run_len, **feat)
+        elif groups:
+            swr.swr_forward_shared_gates(x, a, b, c, cfg.block, gsz, y=y, carriers=carriers,
+                                         run_len=args.run_len, **feat)
         else:
             swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
         if ev is not None:
@@ -379,6 +407,9 @@ def main():
         elif uniform:
             swr.swr_uniform_backward(x, a, b, c, dy, cfg.block, outputs=(dx, da, db, dc),
                                      run_len=args.run_len, **feat)
+        elif groups:
+            swr.swr_backward_shared_gates(x, a, b, c, dy, carriers, cfg.block, gsz, outputs=(dx, da, db, dc),
+                                          workspace=gws, run_len=args.run_len, **feat)
         else:
             swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
                              run_len=args.run_len, **feat)
@@ -406,7 +437,8 @@ def main():
     tokens = cfg.B * cfg.T
     value = tokens / (ms_per_step * 1e-3)
 
-    fb, bb = algorithmic_bytes(cfg, False, not uniform), algorithmic_bytes(cfg, True, not uniform)
+    fb = algorithmic_bytes(cfg, False, not uniform, groups)
+    bb = algorithmic_bytes(cfg, True, not uniform, groups)
     f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
     dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
     dom_gbs = b_gbs if dominant_bwd else f_gbs
@@ -414,9 +446,11 @@ def main():
     dom_kernel = f"swr_bwd{pc}_kernel" if dominant_bwd else f"swr_fwd{pc}_kernel"
     if uniform:
         dom_kernel = "swr_uni_bwd_kernel" if dominant_bwd else "swr_uni_fwd_kernel"
+    if groups and dominant_bwd:   # two launches, timed together
+        dom_kernel = "swr_backward_shared_gates (swr_bwd_kernel + swr_gate_reduce_kernel)"
     # The exact recurrence's passes are three launches each; their time is
     # taken as a whole and no single kernel's counters stand for it.
-    traffic = None if exact else recorded_traffic(dom_kernel, cfg.name)
+    traffic = None if exact or groups else recorded_traffic(dom_kernel, cfg.name)
     if exact:
         dom_kernel = ("swr_exact_backward (swr_bwd_agg_kernel + swr_scan_kernel + swr_bwd_kernel)"
                       if dominant_bwd else
@@ -462,6 +496,7 @@ def main():
                    "featurisation": "fused sigmoid of a and b" if args.sigmoid else "none",
                    "recurrence": ("exact (untruncated)" if exact else
                                   "uniform window" if uniform else "jagged window"),
+                   "gate_groups": groups or None,
                    "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {
