@@ -88,7 +88,8 @@ def contraction_flops(cfg, backward, uniform=False):
 
 # The sources that decide what a launch does (kernels, grid policy): the
 # recorded traffic is stale once any of them changes.
-KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_device.h", "swr_api.cpp", "swr_launch.h")
+KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_groups.hip", "swr_device.h", "swr_api.cpp",
+                  "swr_launch.h")
 
 
 def recorded_traffic(kernel, workload):
@@ -377,8 +378,8 @@ def main():
         db, dc = torch.empty_like(b), torch.empty_like(c)
         gprob = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
                                  x.stride()[:3], a.stride()[:3])
-        gws = torch.empty(swr.swr_shared_gates_workspace_bytes(gprob, gsz) // 4, dtype=torch.float32,
-                          device=x.device)
+        gbytes = swr.swr_shared_gates_workspace_bytes(gprob, gsz)
+        gws = torch.empty(gbytes // 4, dtype=torch.float32, device=x.device) if gbytes else None
     if exact:
         wsp = swr.make_problem(cfg.B, cfg.T, cfg.H, cfg.D, cfg.block, 1 if cfg.dtype == "bf16" else 0,
                                x.stride()[:3], a.stride()[:3], False, args.run_len, cfg.per_channel)
@@ -447,7 +448,8 @@ def main():
     if uniform:
         dom_kernel = "swr_uni_bwd_kernel" if dominant_bwd else "swr_uni_fwd_kernel"
     if groups and dominant_bwd:   # two launches, timed together
-        dom_kernel = "swr_backward_shared_gates (swr_bwd_kernel + swr_gate_reduce_kernel)"
+        dom_kernel = ("swr_bwd_grouped_kernel" if not gbytes else
+                      "swr_backward_shared_gates (swr_bwd_kernel + swr_gate_reduce_kernel)")
     # The exact recurrence's passes are three launches each; their time is
     # taken as a whole and no single kernel's counters stand for it.
     traffic = None if exact or groups else recorded_traffic(dom_kernel, cfg.name)

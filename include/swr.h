@@ -260,15 +260,17 @@ int swr_decode_state(const swr_problem_t* problem, const void* a, const float* c
  * recurrence is the jagged window of swr_forward / swr_backward, with the
  * same carriers; db and dc are the gradients with respect to the shared
  * gates (sums over each group's heads, added in head order, so results are
- * reproducible).  The backward writes every head's share of db and dc in
- * float32 to a caller-provided workspace and sums the groups in a second
+ * reproducible).  For groups of up to 16 heads the backward sums a group's
+ * shares inside one pass and needs no workspace; larger groups write every
+ * head's float32 shares to a caller-provided workspace, summed in a second
  * launch.  One decay per head only (SWR_FLAG_PER_CHANNEL_DECAY is rejected);
  * heads of 16 and 32 channels are not packed.  group = 1 is the ordinary
  * layout with b, c at their own strides.
  * ------------------------------------------------------------------------ */
 
-/* Workspace bytes swr_backward_shared_gates needs: 2 * B * T * H * D float32
- * (the heads' shares of db and dc), or a negative SWR_ERR_* code. */
+/* Workspace bytes swr_backward_shared_gates needs: 0 for groups of up to 16
+ * heads, else 2 * B * T * H * D float32 (the heads' shares of db and dc); or a
+ * negative SWR_ERR_* code. */
 int64_t swr_shared_gates_workspace_bytes(const swr_problem_t* problem, int64_t group);
 
 /* Forward with shared gates: y = SWR(x, a, b, c) where head h reads
@@ -279,7 +281,8 @@ int swr_forward_shared_gates(const swr_problem_t* problem, int64_t group, const 
 
 /* Backward with shared gates: dx, da as for swr_backward; db and dc in the
  * gates' layout.  workspace: swr_shared_gates_workspace_bytes bytes of device
- * memory (16-byte aligned, no initialisation needed, overwritten). */
+ * memory (16-byte aligned, no initialisation needed, overwritten); may be NULL
+ * when that size is 0. */
 int swr_backward_shared_gates(const swr_problem_t* problem, int64_t group, const int64_t* gate_strides,
                               const void* x, const void* a, const void* b, const void* c, const void* dy,
                               const float* carriers, void* dx, float* da, void* db, void* dc,

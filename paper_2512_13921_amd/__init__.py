@@ -538,12 +538,12 @@ def swr_backward_shared_gates(x, a, b, c, dy, carriers, block, group, residual=F
             raise ValueError("da must be float32 with the shape and strides of a")
     nbytes = swr_shared_gates_workspace_bytes(problem, group)
     if workspace is None:
-        workspace = torch.empty(max(nbytes // 4, 1), dtype=torch.float32, device=x.device)
+        workspace = torch.empty(nbytes // 4, dtype=torch.float32, device=x.device) if nbytes else None
     elif workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous():
         raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes")
     rc = load().swr_backward_shared_gates(ctypes.byref(problem), int(group), _i64x3(b.stride()), _ptr(x),
                                           _ptr(a), _ptr(b), _ptr(c), _ptr(dy), _ptr(carriers), _ptr(dx),
-                                          _ptr(da), _ptr(db), _ptr(dc), _ptr(workspace),
+                                          _ptr(da), _ptr(db), _ptr(dc), _opt(workspace),
                                           _stream(stream, x.device))
     if rc != 0:
         raise SwrError(rc, "swr_backward_shared_gates")

@@ -788,7 +788,8 @@ int64_t swr_shared_gates_workspace_bytes(const swr_problem_t* p, int64_t group) 
     const int rc = resolve(p, &r, false);
     if (rc != SWR_OK) return rc;
     if (group < 1 || (p->H > 0 && p->H % group != 0)) return SWR_ERR_SHAPE;
-    return 2 * p->B * p->T * p->H * p->D * 4;
+    // groups of up to grouped_max_heads() heads are summed inside the backward
+    return group <= swr::grouped_max_heads() ? 0 : 2 * p->B * p->T * p->H * p->D * 4;
 }
 
 int swr_forward_shared_gates(const swr_problem_t* p, int64_t group, const int64_t* gate_strides,
@@ -825,13 +826,15 @@ int swr_backward_shared_gates(const swr_problem_t* p, int64_t group, const int64
     int rc = gates_resolve(p, group, gate_strides, &r, &gspan);
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
-    if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc || !workspace) return SWR_ERR_NULL;
+    const bool fused = group <= swr::grouped_max_heads();
+    if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc || (!fused && !workspace))
+        return SWR_ERR_NULL;
     for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
         if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
     if (!aligned(a, r.es) || !aligned(da, 4) || !aligned(carriers, 16) || !aligned(workspace, 16))
         return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
-    const int64_t wbytes = 2 * p->B * p->T * p->H * p->D * 4;
+    const int64_t wbytes = fused || !workspace ? 0 : 2 * p->B * p->T * p->H * p->D * 4;
     const Span outs[5] = {span(dx, r.xspan), span(db, gspan), span(dc, gspan), span(da, r.aspan * 4),
                           span(workspace, wbytes)};
     const Span ins[6] = {span(x, r.xspan), span(b, gspan), span(c, gspan), span(dy, r.xspan),
@@ -847,6 +850,19 @@ int swr_backward_shared_gates(const swr_problem_t* p, int64_t group, const int64
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
+    if (fused) {
+        // one workgroup per (batch, group, 64-channel half, run), whole blocks per step
+        k.hshift = p->D > 64 ? 1 : 0;
+        k.Hv = (p->H / group) << k.hshift;
+        const int64_t units = p->B * k.Hv;
+        const int tw = p->block >= 128 ? 8 : 4;
+        k.run_len = p->run_len > 0 ? p->run_len : pick_run_len(p->T, units, 16 * tw, 256);
+        k.nruns = (p->T + k.run_len - 1) / k.run_len;
+        if (k.nruns > kMaxWorkgroups / units) return SWR_ERR_UNSUPPORTED;
+        k.nwork = units * k.nruns;
+        const int cpl = (int)(std::min<int64_t>(p->D, 64) / 16);
+        return swr::launch_grouped_backward(k, p->dtype, cpl, tw, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    }
     k.gws = (float*)workspace;
     if (swr::launch(k, p->dtype, r.dk, r.bwd, true, false, 1, swr::kGrouped, stream) != hipSuccess)
         return SWR_ERR_HIP;

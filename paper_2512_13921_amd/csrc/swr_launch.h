@@ -70,6 +70,14 @@ enum Mode {
 // dc ([B, T, H / group, D], strides sg_*) in the I/O dtype.
 hipError_t launch_gate_reduce(const Params& p, int dtype, int D, void* stream);
 
+// Fused backward with shared gates: one workgroup per (batch, group, channel
+// half, run) goes through the group's heads at every step and stores db, dc
+// once per group.  p.Hv = (H / group) << hshift work units, 16 * cpl
+// channels each, tw waves per workgroup (whole blocks per step).  Groups of
+// at most grouped_max_heads() heads.
+int grouped_max_heads();
+hipError_t launch_grouped_backward(const Params& p, int dtype, int cpl, int tw, void* stream);
+
 // Stage II of the exact recurrence: for every (batch, head) and channel, the
 // carrier recurrence over a sequence's runs, S_r = P_r S_{r-1} + V_r forward
 // (reverse == 0) or S_r = P_r S_{r+1} + V_r backward, from `init` (or 0);

@@ -445,15 +445,22 @@ def test_shared_gates_validation():
     p = problem(B=B, T=T, H=H, D=D)
     gst = (T * 2 * D, 2 * D, D)          # [B, T, 2 groups, D]
     assert gfwd(p, 3, gst) == E_SHAPE and gfwd(p, 0, gst) == E_SHAPE
-    assert gfwd(p, 2, None) == E_NULL and gbwd(p, 2, gst, ws=0) == E_NULL
+    assert gfwd(p, 2, None) == E_NULL
     assert gfwd(problem(B=B, T=T, H=H, D=D, per_channel=True), 2, gst) == E_UNSUP
     assert gfwd(p, 2, (T * 2 * D, 2 * D, D - 4)) in (E_SHAPE, E_ALIGN)
     assert gfwd(p, 2, (T * 2 * D, 2 * D + 2, D)) == E_ALIGN       # 4-byte rows, 8-byte lane slices
     assert gfwd(p, 2, gst, b=B_ + 4) == E_ALIGN
     assert gfwd(p, 2, gst, y=B_) == E_ALIAS
-    assert gbwd(p, 2, gst, db=GB * 20) == E_ALIAS          # db inside the workspace
     assert gbwd(p, 2, gst, dc=C) == E_ALIAS
     assert gfwd(problem(B=0), 2, gst) == OK and gbwd(problem(T=0), 2, None) == OK
-    assert swr.swr_shared_gates_workspace_bytes(p, 2) == 2 * B * T * H * D * 4
+    # groups of up to 16 heads are summed inside the backward: no workspace
+    assert swr.swr_shared_gates_workspace_bytes(p, 2) == 0
     with pytest.raises(swr.SwrError):
         swr.swr_shared_gates_workspace_bytes(p, 3)
+    # larger groups go through a float32 workspace of every head's shares
+    H32 = 32
+    p32 = problem(B=B, T=T, H=H32, D=D)
+    g32 = (T * D, D, D)                  # [B, T, 1 group, D]
+    assert swr.swr_shared_gates_workspace_bytes(p32, 32) == 2 * B * T * H32 * D * 4
+    assert gbwd(p32, 32, g32, ws=0) == E_NULL
+    assert gbwd(p32, 32, g32, db=GB * 20) == E_ALIAS        # db inside the workspace
