@@ -27,7 +27,7 @@ __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error
            "swr_step", "swr_exact_step", "swr_decode_state",
            "swr_uniform_forward", "swr_uniform_backward", "swr_uniform_launch_info",
            "swr_forward_shared_gates", "swr_backward_shared_gates", "swr_shared_gates_workspace_bytes",
-           "SWRFunction", "library_path", "load"]
+           "SWRFunction", "SWRUniformFunction", "SWRSharedGatesFunction", "library_path", "load"]
 
 SWR_ABI_VERSION = 1
 SWR_DTYPE_F32 = 0
@@ -626,23 +626,55 @@ def _autograd_function():
             dx, da, db, dc = swr_backward(x, a, b, c, dy, v, ctx.block, ctx.residual, **ctx.feat)
             return dx, da.to(a.dtype), db, dc, None, None, None, None
 
-    return _SWRFunction
+    class _SWRUniformFunction(torch.autograd.Function):
+        """Autograd wrapper of the uniform window (nothing saved but the inputs)."""
+
+        @staticmethod
+        def forward(ctx, x, a, b, c, window, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+            ctx.window, ctx.residual = window, residual
+            ctx.feat = dict(sigmoid_decay=sigmoid_decay, sigmoid_pregate=sigmoid_pregate)
+            ctx.save_for_backward(x, a, b, c)
+            return swr_uniform_forward(x, a, b, c, window, residual, **ctx.feat)
+
+        @staticmethod
+        def backward(ctx, dy):
+            x, a, b, c = ctx.saved_tensors
+            dy = dy if dy.stride() == x.stride() else torch.empty_strided(
+                x.shape, x.stride(), dtype=x.dtype, device=x.device).copy_(dy)
+            dx, da, db, dc = swr_uniform_backward(x, a, b, c, dy, ctx.window, ctx.residual, **ctx.feat)
+            return dx, da.to(a.dtype), db, dc, None, None, None, None
+
+    class _SWRSharedGatesFunction(torch.autograd.Function):
+        """Autograd wrapper of the jagged window with b, c shared by groups of heads."""
+
+        @staticmethod
+        def forward(ctx, x, a, b, c, block, group, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+            ctx.block, ctx.group, ctx.residual = block, group, residual
+            ctx.feat = dict(sigmoid_decay=sigmoid_decay, sigmoid_pregate=sigmoid_pregate)
+            y, v = swr_forward_shared_gates(x, a, b, c, block, group, residual, save_carriers=True, **ctx.feat)
+            ctx.save_for_backward(x, a, b, c, v)
+            return y
+
+        @staticmethod
+        def backward(ctx, dy):
+            x, a, b, c, v = ctx.saved_tensors
+            dy = dy if dy.stride() == x.stride() else torch.empty_strided(
+                x.shape, x.stride(), dtype=x.dtype, device=x.device).copy_(dy)
+            dx, da, db, dc = swr_backward_shared_gates(x, a, b, c, dy, v, ctx.block, ctx.group, ctx.residual,
+                                                       **ctx.feat)
+            return dx, da.to(a.dtype), db, dc, None, None, None, None, None
+
+    return _SWRFunction, _SWRUniformFunction, _SWRSharedGatesFunction
 
 
-class _Lazy:
-    _fn = None
-
-    def __get__(self, obj, owner):
-        if _Lazy._fn is None:
-            _Lazy._fn = _autograd_function()
-        return _Lazy._fn
-
-
-class _Namespace:
-    SWRFunction = _Lazy()
+_FUNCTIONS = None
 
 
 def __getattr__(name):
-    if name == "SWRFunction":
-        return _Namespace.SWRFunction
+    global _FUNCTIONS
+    names = ("SWRFunction", "SWRUniformFunction", "SWRSharedGatesFunction")
+    if name in names:
+        if _FUNCTIONS is None:
+            _FUNCTIONS = dict(zip(names, _autograd_function()))
+        return _FUNCTIONS[name]
     raise AttributeError(name)

@@ -152,3 +152,18 @@ def test_shared_gates_headline_shape_sampled(swr):
             _say(f"[groups headline] ({bi}, {g}) {name}: {st}")
     for t in (y,) + tuple(grads):
         assert torch.isfinite(t.float()).all()
+
+
+def test_shared_gates_autograd_function(swr):
+    prob = W.random_problem(24, 2, 300, 4, 64, 64, "f32")
+    group = 2
+    bg, cg = _gated(prob, group)
+    x, a = (to_device(getattr(prob, n), "f32").requires_grad_(True) for n in ("x", "a"))
+    b, c = (to_device(v, "f32").requires_grad_(True) for v in (bg, cg))
+    y = swr.SWRSharedGatesFunction.apply(x, a, b, c, 64, group)
+    y.backward(to_device(prob.dy, "f32"))
+    torch.cuda.synchronize()
+    assert_close(to_host(y), oracle.grouped_forward(prob.x, prob.a, bg, cg, 64, group), "f32", "autograd y")
+    ref = oracle.grouped_backward(prob.x, prob.a, bg, cg, prob.dy, 64, group)
+    for name, t, r in zip(("dx", "da", "db", "dc"), (x, a, b, c), ref):
+        assert_close(to_host(t.grad), r, "f32", f"autograd {name}")

@@ -189,3 +189,15 @@ def test_uniform_headline_shape_sampled(swr):
         _say(f"[uniform headline] {name}: {st}")
     for t in (y,) + tuple(grads):
         assert torch.isfinite(t.float()).all()
+
+
+def test_uniform_autograd_function(swr):
+    prob = W.random_problem(12, 2, 300, 2, 64, 32, "f32")
+    x, a, b, c = (to_device(getattr(prob, n), "f32").requires_grad_(True) for n in ("x", "a", "b", "c"))
+    y = swr.SWRUniformFunction.apply(x, a, b, c, 32)
+    y.backward(to_device(prob.dy, "f32"))
+    torch.cuda.synchronize()
+    assert_close(to_host(y), oracle.uniform_forward(prob.x, prob.a, prob.b, prob.c, 32), "f32", "autograd y")
+    ref = oracle.uniform_backward(prob.x, prob.a, prob.b, prob.c, prob.dy, 32)
+    for name, t, r in zip(("dx", "da", "db", "dc"), (x, a, b, c), ref):
+        assert_close(to_host(t.grad), r, "f32", f"autograd {name}")
