@@ -167,3 +167,34 @@ def test_shared_gates_autograd_function(swr):
     ref = oracle.grouped_backward(prob.x, prob.a, bg, cg, prob.dy, 64, group)
     for name, t, r in zip(("dx", "da", "db", "dc"), (x, a, b, c), ref):
         assert_close(to_host(t.grad), r, "f32", f"autograd {name}")
+
+
+def test_shared_gates_in_a_captured_graph(swr):
+    prob = W.random_problem(25, 2, 600, 4, 128, 128, "bf16")
+    group = 2
+    bg, cg = _gated(prob, group)
+    x, a, dy = (to_device(getattr(prob, n), "bf16") for n in ("x", "a", "dy"))
+    b, c = to_device(bg, "bf16"), to_device(cg, "bf16")
+    y_e, v = swr.swr_forward_shared_gates(x, a, b, c, 128, group, save_carriers=True)
+    g_e = swr.swr_backward_shared_gates(x, a, b, c, dy, v, 128, group)
+    torch.cuda.synchronize()
+    y, v2 = torch.empty_like(y_e), torch.empty_like(v)
+    outs = tuple(torch.empty_like(t) for t in g_e)
+    graph = torch.cuda.CUDAGraph()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            swr.swr_forward_shared_gates(x, a, b, c, 128, group, y=y, carriers=v2)
+            swr.swr_backward_shared_gates(x, a, b, c, dy, v2, 128, group, outputs=outs)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (y, v2) + outs:
+            t.fill_(7.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_e), rep
+        for p_, q_ in zip(outs, g_e):
+            assert torch.equal(p_, q_), rep

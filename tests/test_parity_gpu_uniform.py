@@ -201,3 +201,34 @@ def test_uniform_autograd_function(swr):
     ref = oracle.uniform_backward(prob.x, prob.a, prob.b, prob.c, prob.dy, 32)
     for name, t, r in zip(("dx", "da", "db", "dc"), (x, a, b, c), ref):
         assert_close(to_host(t.grad), r, "f32", f"autograd {name}")
+
+
+def test_uniform_in_a_captured_graph(swr):
+    # Forward and backward (d = 128: a zero fill of da, then two halves adding
+    # to it) captured once in a HIP graph: every replay, with eager work and
+    # synchronisations between replays, reproduces the eager results bit for bit.
+    prob = W.random_problem(14, 2, 700, 2, 128, 64, "bf16")
+    x, a, b, c, dy = (to_device(getattr(prob, n), "bf16") for n in ("x", "a", "b", "c", "dy"))
+    y_e = swr.swr_uniform_forward(x, a, b, c, 64)
+    g_e = swr.swr_uniform_backward(x, a, b, c, dy, 64)
+    torch.cuda.synchronize()
+    y = torch.empty_like(y_e)
+    outs = tuple(torch.empty_like(t) for t in g_e)
+    graph = torch.cuda.CUDAGraph()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            swr.swr_uniform_forward(x, a, b, c, 64, y=y)
+            swr.swr_uniform_backward(x, a, b, c, dy, 64, outputs=outs)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (y,) + outs:
+            t.fill_(7.0)                  # eager work between the replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_e), rep
+        for p_, q_ in zip(outs, g_e):
+            assert torch.equal(p_, q_), rep
