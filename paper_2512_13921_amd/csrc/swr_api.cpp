@@ -68,6 +68,7 @@ struct Resolved {
     bool pc;            // per-channel decay: a and da have the [B, T, H, D] layout of x
     int hshift;         // per-channel kernels: log2 of the virtual heads per head
     int pack;           // > 1: heads of 64 / pack channels packed into 64-channel virtual heads
+    bool pair;          // forward: bf16 heads of 64 channels run two per kernel head (16-byte lane slices)
     int dk;             // channels a kernel's head covers (D, or D >> hshift)
     int64_t hv;         // heads the kernels split the work over (H << hshift)
     int64_t vbytes;     // bytes of one lane's slice of an x-like row (alignment unit)
@@ -82,7 +83,7 @@ struct Resolved {
     int64_t carriers;   // float32 carriers of the whole problem
 };
 
-int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true) {
+int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true, bool allow_pair = false) {
     if (!p) return SWR_ERR_NULL;
     if (p->abi_version != SWR_ABI_VERSION) return SWR_ERR_VERSION;
     if (p->dtype != SWR_DTYPE_F32 && p->dtype != SWR_DTYPE_BF16) return SWR_ERR_DTYPE;
@@ -107,8 +108,23 @@ int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true) {
         r->pack = (int)(64 / p->D);
         r->dk = 64;
     }
+    // The jagged window's forward runs bf16 heads of 64 channels two at a
+    // time, so that each lane moves 16-byte row slices as with 128-channel
+    // heads and the tiles can be copied through LDS (the caller's pointers may
+    // still veto it, see resolve_for).  The backward keeps them apart: two
+    // heads' operators do not fit its register budget.
+    // (Lane offsets then include the second head's share: sx_h of x and one
+    // head's carriers, which must keep every 32-bit lane offset below 2^31
+    // bytes.)
+    const int64_t lim32 = 0x7fffffffLL;
+    r->pair = allow_pair && !r->pc && p->D == 64 && p->dtype == SWR_DTYPE_BF16 && p->H % 2 == 0 &&
+              (p->sx_h * 2) % 16 == 0 && p->sx_h >= 0 && p->sx_h <= (int64_t)1 << 26 && p->sa_h >= 0 &&
+              p->sa_h <= (int64_t)1 << 26 && p->sx_t >= 0 && p->sx_t <= (lim32 - p->sx_h * 2 - 128) / 32 &&
+              p->sa_t >= 0 && p->sa_t <= (lim32 - p->sa_h * 4) / 64 &&
+              (p->T + p->block - 1) / p->block <= lim32 / (2 * 64 * 4);
+    if (r->pair) r->dk = 128;
     r->cpl = r->dk / 16;
-    r->hv = r->pack > 1 ? p->H / r->pack : p->H << r->hshift;
+    r->hv = r->pack > 1 ? p->H / r->pack : r->pair ? p->H / 2 : p->H << r->hshift;
     r->vbytes = std::min<int64_t>(16, (int64_t)(r->dk / 16) * r->es);
     r->bwd = swr::bwd_shape(p->block, r->hv);
     r->fwd = swr::fwd_shape(p->block, r->hv);
@@ -185,13 +201,16 @@ bool aligned(const void* ptr, int64_t bytes) { return ((uintptr_t)ptr % (uintptr
 // resolve() for a call with these [B,T,H,D] tensors: packed small heads need
 // each lane's 64-channel row slice aligned (8 or 16 bytes); otherwise the
 // heads run one by one.
-int resolve_for(const swr_problem_t* p, Resolved* r, std::initializer_list<const void*> xs) {
-    int rc = resolve(p, r, true);
-    if (rc != SWR_OK || r->pack == 1 || r->empty) return rc;
+// The same for paired 64-channel heads (allow_pair: the jagged window's
+// forward and backward), which need 16-byte aligned slices.
+int resolve_for(const swr_problem_t* p, Resolved* r, std::initializer_list<const void*> xs,
+                bool allow_pair = false) {
+    int rc = resolve(p, r, true, allow_pair);
+    if (rc != SWR_OK || (r->pack == 1 && !r->pair) || r->empty) return rc;
     bool ok = check_strides_aligned(p, *r) == SWR_OK;
     for (const void* q : xs)
         if (q && !aligned(q, r->vbytes)) ok = false;
-    return ok ? SWR_OK : resolve(p, r, false);
+    return ok ? SWR_OK : resolve(p, r, false, false);
 }
 
 struct Span {
@@ -245,11 +264,14 @@ const char* swr_error_string(int code) {
 
 int swr_launch_info(const swr_problem_t* problem, int64_t* fwd_run_len, int64_t* fwd_workgroups,
                     int64_t* bwd_run_len, int64_t* bwd_workgroups) {
-    Resolved r;
-    const int rc = resolve(problem, &r);
+    // the plans of swr_forward (which may pair heads) and swr_backward, with
+    // suitably aligned pointers
+    Resolved r, f;
+    int rc = resolve(problem, &r);
     if (rc != SWR_OK) return rc;
-    if (fwd_run_len) *fwd_run_len = r.run_len_f;
-    if (fwd_workgroups) *fwd_workgroups = r.nwork_f;
+    if ((rc = resolve(problem, &f, true, true)) != SWR_OK) return rc;
+    if (fwd_run_len) *fwd_run_len = f.run_len_f;
+    if (fwd_workgroups) *fwd_workgroups = f.nwork_f;
     if (bwd_run_len) *bwd_run_len = r.run_len;
     if (bwd_workgroups) *bwd_workgroups = r.nwork;
     return SWR_OK;
@@ -267,7 +289,7 @@ namespace {
 int forward_impl(const swr_problem_t* p, const void* x, const void* a, const void* b,
                  const void* c, void* y, float* carriers, void* stream) {
     Resolved r;
-    int rc = resolve_for(p, &r, {x, b, c, (const void*)y});
+    int rc = resolve_for(p, &r, {x, b, c, (const void*)y}, true);
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
     if (!x || !a || !b || (y && !c)) return SWR_ERR_NULL;
@@ -284,8 +306,8 @@ int forward_impl(const swr_problem_t* p, const void* x, const void* a, const voi
 
     swr::Params k = make_params(p, r, false);
     k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers;
-    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, swr::kSwr, stream) == hipSuccess ? SWR_OK
-                                                                                        : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, r.pair ? swr::kPaired : swr::kSwr,
+                       stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // namespace
@@ -337,8 +359,8 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, swr::kSwr, stream) == hipSuccess ? SWR_OK
-                                                                                       : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, swr::kSwr, stream) == hipSuccess
+               ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // extern "C"

@@ -70,17 +70,25 @@ namespace {
 // or the outputs from the exact state entering each run (kExact).  The exact
 // modes need no halo and never restart the carrier.  kGrouped is the jagged
 // window with b and c shared by groups of p.group heads (their own strides).
+// kPaired is the jagged window on heads of D/2 channels taken two at a time
+// (work item h = heads 2h, 2h+1): each 16-lane row holds both heads' rows,
+// lanes 0-7 the first head's channels and 8-15 the second's, so every lane
+// still moves 16-byte slices (and the tiles can be copied through LDS); each
+// head has its own decay operator, so the local solve runs once per head
+// and every lane keeps its own head's result.
 template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     constexpr bool GG = MODE == kGrouped;
-    constexpr bool SWR = MODE == kSwr || GG;
+    constexpr bool PAIR = MODE == kPaired;
+    constexpr bool SWR = MODE == kSwr || GG || PAIR;
+    constexpr int NH = PAIR ? 2 : 1;   // heads per kernel head
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
     constexpr int STEP = TW * SB;
     constexpr int ES = IO::ES;
     __shared__ float s_wl[2][NW][D];   // last row of each sub-block's local solve
-    __shared__ float s_c[2][NW];       // each sub-block's decay product
+    __shared__ float s_c[2][NW * NH];  // each sub-block's decay product (per head of a pair)
     // The next step's x, b, c tiles are copied into a wave-private LDS slot
     // while the current step computes (16-byte lane slices only; the slots of
     // a workgroup stay small enough for three workgroups per compute unit).
@@ -100,24 +108,32 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     const int64_t t_lo = SWR ? max(wk.t_begin - (int64_t)l, (int64_t)0) : wk.t_begin;
     const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
-    const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    const int hsel = PAIR ? n >> 3 : 0;                  // this lane's head of a pair
+    const int64_t h0 = PAIR ? 2 * wk.h : wk.h;           // (first) head of the work item
+    constexpr int DH = D / NH;                           // channels of a head
+    const int64_t xo = (wk.b * p.sx_b + h0 * p.sx_h) * ES;
     // b and c: this head's rows, or its group's with shared gates
     const int64_t go = GG ? (wk.b * p.sg_b + (wk.h / p.group) * p.sg_h) * ES : xo;
     const char* xb = (const char*)p.x + xo;
     const char* bb = (const char*)p.b + go;
     const char* cb = (const char*)p.c + go;
     char* yb = (char*)p.y + xo;
-    const char* ab = (const char*)p.a + (wk.b * p.sa_b + wk.h * p.sa_h) * ES;
+    const char* ab = (const char*)p.a + (wk.b * p.sa_b + h0 * p.sa_h) * ES;
     const int64_t rs = p.sx_t * ES;    // row stride in bytes
     const int64_t gs = GG ? p.sg_t * ES : rs;   // of b and c
     const int64_t as = p.sa_t * ES;
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    // this lane's channel slice: n * CPL, or (with a pair) its head's (n & 7) * CPL
+    const uint32_t lch = PAIR ? (uint32_t)(hsel * p.sx_h * ES) + (uint32_t)((n & 7) * CPL * ES)
+                              : (uint32_t)(n * CPL * ES);
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + lch;
     const uint32_t goff = GG ? (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES) : loff;
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     // false: only the block carriers (or the run aggregates) are produced
     const bool want_y = MODE != kAggregate && p.y != nullptr;
-    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D
+    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + (wk.b * p.H + h0) * p.nblocks * DH
                                                        : nullptr;
+    // this lane's carrier slice within the block's entry
+    const uint32_t vch = (uint32_t)(PAIR ? hsel * p.nblocks * DH + (n & 7) * CPL : n * CPL);
     const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
     const int64_t slot = (wk.b * p.H + wk.h) * p.nruns + wk.run;   // this run's aggregate / carry
 
@@ -197,25 +213,47 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
         // Past the end of the sequence the decay is 1 (and u = 0), so the
         // carrier of a partial last block is the state at its last token.
         if (ta >= p.T) a_n = 1.0f;
+        float a_n1 = 0.0f;   // the second head's decay of a pair
+        if constexpr (PAIR) {
+            a_n1 = load_scalar<IO, kFwdDecay>(rsrc(ab + p.sa_h * ES + r0 * as), in_range(a_ok, aoff));
+            if (sig_a) a_n1 = a_ok ? sigmoid(a_n1) : 0.0f;
+            if (ta >= p.T) a_n1 = 1.0f;
+        }
 
         // ---- local solve W = L U on the matrix cores ---------------------
         const Decay dk = build_decay(a_n, grp, n);
-        const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+        Decay dk1 = dk;
+        if constexpr (PAIR) dk1 = build_decay(a_n1, grp, n);
         f32x4 W[CPL];
+        {
+            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+            typename Contract<IO>::A A1 = A;
+            if constexpr (PAIR) A1 = Contract<IO>::prep(dk1.L);
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) {
-            float u[4];
+            for (int m = 0; m < CPL; ++m) {
+                float u[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);   // pre-gate b*x
-            W[m] = Contract<IO>::run(A, u);
+                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);   // pre-gate b*x
+                W[m] = Contract<IO>::run(A, u);
+                if constexpr (PAIR) {   // the second head's lanes keep its own operator's result
+                    const f32x4 W1 = Contract<IO>::run(A1, u);
+                    if (hsel) W[m] = W1;
+                }
+            }
         }
+        float Gl[4];   // this lane's head's prefix products at its rows
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Gl[r] = PAIR && hsel ? dk1.G[r] : dk.G[r];
 
         // ---- carriers through LDS ------------------------------------------
         if (grp == 3) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) s_wl[buf][wv][n * CPL + m] = W[m][3];
         }
-        if (lane == 63) s_c[buf][wv] = dk.c;
+        if (lane == 63) {
+            s_c[buf][wv * NH] = dk.c;
+            if constexpr (PAIR) s_c[buf][wv * NH + 1] = dk1.c;
+        }
         __syncthreads();
 
         // A step need not start at a block boundary: phase of its first sub-block.
@@ -236,7 +274,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
                 for (int m = 0; m < CPL; ++m) ein[m] = e[m];
             }
             const int src = hw * TW + r;
-            const float cr_ = s_c[buf][src];
+            const float cr_ = s_c[buf][src * NH + hsel];
             if constexpr (MODE == kAggregate) prod *= cr_;
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
@@ -256,7 +294,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;   // first token of the block (it may end past T)
             store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
-                                               (uint32_t)(blk * D + n * CPL) * 4u), vout);
+                                               (uint32_t)(blk * DH + vch) * 4u), vout);
         }
         if (!want_y) continue;
 
@@ -267,7 +305,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             float yv[CPL];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                const float hv = W[m][r] + dk.G[r] * ein[m];
+                const float hv = W[m][r] + Gl[r] * ein[m];
                 yv[m] = cr[r].get(m) * hv;
                 if (p.residual) yv[m] += xr[r].get(m);
             }
@@ -1682,6 +1720,9 @@ static hipError_t launch_pc_mode(const Params& p, const Shape& sh, bool backward
 
 template <class IO, int CPL, bool FEAT, int MODE>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
+    if constexpr (MODE == kPaired) {   // a forward-only mode
+        if (backward) return hipErrorInvalidValue;
+    }
     const dim3 grid((unsigned)p.nwork);
 #define SWR_LAUNCH(KERNEL, TW_, HW_)                                                                \
     else if (sh.tw == TW_ && sh.hw == HW_)                                                          \
@@ -1692,7 +1733,7 @@ static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, 
             SWR_LAUNCH((swr_bwd_agg_kernel<IO, CPL, 8, FEAT>), 8, 1)
             SWR_LAUNCH((swr_bwd_agg_kernel<IO, CPL, 4, FEAT>), 4, 1)
             else return hipErrorInvalidValue;
-        } else {
+        } else if constexpr (MODE != kPaired) {
             if (false) {}
             SWR_LAUNCH((swr_bwd_kernel<IO, CPL, 8, 1, FEAT, MODE>), 8, 1)
             SWR_LAUNCH((swr_bwd_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
@@ -1715,6 +1756,9 @@ static hipError_t launch_mode(const Params& p, const Shape& sh, bool backward, i
         case kAggregate: return launch_shape<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
         case kExact: return launch_shape<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
         case kGrouped: return launch_shape<IO, CPL, FEAT, kGrouped>(p, sh, backward, stream);
+        case kPaired:
+            if constexpr (CPL == 8 && IO::ES == 2) return launch_shape<IO, CPL, FEAT, kPaired>(p, sh, backward, stream);
+            return hipErrorInvalidValue;
         default: return hipErrorInvalidValue;
     }
 }

@@ -63,6 +63,8 @@ enum Mode {
     kAggregate = 1,  // exact, stage I: run aggregates only (no outputs)
     kExact = 2,      // exact, stage III: outputs from the carry entering each run
     kGrouped = 3,    // the jagged window with b and c shared by groups of heads
+    kPaired = 4,     // the jagged window's forward, two heads of D/2 channels per kernel
+                     // head (lanes 0-7 of a 16-lane row hold the first, 8-15 the second)
 };
 
 // Sums the per-head float32 shares of db and dc that a kGrouped backward left

@@ -464,3 +464,16 @@ def test_shared_gates_validation():
     assert swr.swr_shared_gates_workspace_bytes(p32, 32) == 2 * B * T * H32 * D * 4
     assert gbwd(p32, 32, g32, ws=0) == E_NULL
     assert gbwd(p32, 32, g32, db=GB * 20) == E_ALIAS        # db inside the workspace
+
+
+def test_forward_pairs_bf16_heads_of_64():
+    # the forward runs bf16 heads of 64 channels two at a time (16-byte lane
+    # slices); the backward and float32 keep one head per kernel head
+    p = problem(B=2, T=4096, H=8, D=64, block=128, run_len=1024)
+    info = swr.swr_launch_info(p)
+    assert info["fwd_workgroups"] == 2 * (8 // 2 // 2) * 4      # pairs, two per workgroup
+    assert info["bwd_workgroups"] == 2 * 8 * 4
+    p = problem(B=2, T=4096, H=8, D=64, block=128, run_len=1024, dtype=F32)
+    assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * (8 // 2) * 4
+    p = problem(B=2, T=4096, H=7, D=64, block=128, run_len=1024)   # odd H: no pairs
+    assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * 7 * 4
