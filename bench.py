@@ -121,51 +121,85 @@ def to_device(arr, dtype):
     return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
 
 
+def _cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(cfg, prob, budget_s=10.0, exact=False, uniform=False):
     """Oracle throughput on whole (batch, head) slices of the workload, in
     tokens/s of the full job (a token carries all H heads).  Slices are taken
     in a fixed shuffled order and revisited until about budget_s seconds of
-    oracle time have been spent."""
+    oracle time have been spent on all host cores (forward and backward timed
+    separately); then one slice's forward and backward run on one core."""
     import oracle
     threads = oracle.max_threads()
     nslices = cfg.B * cfg.H
     batch = max(1, min(threads, nslices))
     order = np.random.default_rng(0).permutation(nslices)
-    done, elapsed, passes = 0, 0.0, 0
-    pos = 0
-    while elapsed < budget_s or done == 0:
-        idx = order[pos:pos + batch]
+
+    def take_slices(idx):
         bi, hi = idx // cfg.H, idx % cfg.H
 
         def take(t):
             return np.ascontiguousarray(np.asarray(t)[bi, :, hi], dtype=np.float64)
 
-        xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
+        return [take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy")]
+
+    def run(xs, as_, bs, cs, dys):
+        """(forward seconds, backward seconds) of the oracle on these slices."""
         t0 = time.perf_counter()
         if cfg.logits:     # the featurisation is part of the timed work
             as_, bs = oracle.sigmoid(as_), oracle.sigmoid(bs)
         if exact:
             oracle.exact_forward_slices(xs, as_, bs, cs)
-            oracle.exact_backward_slices(xs, as_, bs, cs, dys)
         elif uniform:
             oracle.uniform_forward_slices(xs, as_, bs, cs, cfg.block)
-            oracle.uniform_backward_slices(xs, as_, bs, cs, dys, cfg.block)
         else:
             oracle.forward_slices(xs, as_, bs, cs, cfg.block)
+        t1 = time.perf_counter()
+        if exact:
+            oracle.exact_backward_slices(xs, as_, bs, cs, dys)
+        elif uniform:
+            oracle.uniform_backward_slices(xs, as_, bs, cs, dys, cfg.block)
+        else:
             oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
-        elapsed += time.perf_counter() - t0
+        return t1 - t0, time.perf_counter() - t1
+
+    done, t_fwd, t_bwd, passes, pos = 0, 0.0, 0.0, 0, 0
+    while t_fwd + t_bwd < budget_s or done == 0:
+        idx = order[pos:pos + batch]
+        f, b = run(*take_slices(idx))
+        t_fwd, t_bwd = t_fwd + f, t_bwd + b
         done += len(idx)
         pos += len(idx)
         if pos >= nslices:
             pos, passes = 0, passes + 1
-    token_heads = done * cfg.T
+    # one core, one slice
+    oracle.set_threads(1)
+    try:
+        f1, b1 = run(*take_slices(order[:1]))
+    finally:
+        oracle.set_threads(threads)
+    tokens = done * cfg.T / cfg.H          # full-job tokens the sample stands for
+    tok1 = cfg.T / cfg.H
     return {
-        "value": token_heads / cfg.H / elapsed,
+        "value": tokens / (t_fwd + t_bwd),
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
         "sample": f"{done} (batch, head) slices of {nslices} (full T={cfg.T}; {passes} full passes), "
-                  f"forward+backward in float64, OpenMP over slices; {elapsed:.1f} s of oracle time",
+                  f"forward+backward in float64, OpenMP over slices; {t_fwd + t_bwd:.1f} s of oracle time",
+        "forward_tokens_per_s": tokens / t_fwd,
+        "backward_tokens_per_s": tokens / t_bwd,
+        "single_core": {"value": tok1 / (f1 + b1), "forward_tokens_per_s": tok1 / f1,
+                        "backward_tokens_per_s": tok1 / b1, "sample": "one (batch, head) slice"},
+        "cpu_model": _cpu_model(),
     }
 
 
@@ -515,10 +549,12 @@ def main():
         },
         "kernels": {
             "forward": {"ms": float(fwd_ms.mean()), "ms_min": float(fwd_ms.min()),
+                        "ms_median": float(np.median(fwd_ms)),
                         "algorithmic_bytes": fb, "GB/s": f_gbs, "frac_hbm": f_gbs / HBM_PEAK_GBS,
                         "mfma_tflops": mfma_rate(False, fwd_ms.mean()),
                         "tokens_per_s": tokens / (fwd_ms.mean() * 1e-3)},
             "backward": {"ms": float(bwd_ms.mean()), "ms_min": float(bwd_ms.min()),
+                         "ms_median": float(np.median(bwd_ms)),
                          "algorithmic_bytes": bb, "GB/s": b_gbs, "frac_hbm": b_gbs / HBM_PEAK_GBS,
                          "mfma_tflops": mfma_rate(True, bwd_ms.mean()),
                          "tokens_per_s": tokens / (bwd_ms.mean() * 1e-3)},

@@ -59,6 +59,8 @@ def _load():
         lib.swr_oracle_step.argtypes = [i64, i64, i64, i64, i64, ci, ci] + [dp] * 6
         lib.swr_oracle_step.restype = ci
         lib.swr_oracle_max_threads.restype = ci
+        lib.swr_oracle_set_threads.argtypes = [ci]
+        lib.swr_oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
@@ -74,6 +76,11 @@ def _c64(arr):
 def max_threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().swr_oracle_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Sets the OpenMP threads of the oracle's later parallel loops."""
+    _load().swr_oracle_set_threads(int(n))
 
 
 def forward_slices(x, a, b, c, block, residual=False):

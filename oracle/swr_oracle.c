@@ -415,3 +415,11 @@ int swr_oracle_max_threads(void) {
     return 1;
 #endif
 }
+
+void swr_oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

@@ -147,6 +147,10 @@ int swr_oracle_uniform_backward(int64_t S, int64_t T, int64_t D, int64_t k, int 
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
 int swr_oracle_max_threads(void);
 
+/* Sets the number of OpenMP threads of later parallel regions (no-op without
+ * OpenMP); n < 1 is ignored. */
+void swr_oracle_set_threads(int n);
+
 #ifdef __cplusplus
 }
 #endif
