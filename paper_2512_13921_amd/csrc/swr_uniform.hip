@@ -240,14 +240,24 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
     constexpr int L = TW * SB;
     constexpr int ES = IO::ES;
     using RW = Row<IO, CPL>;
-    // Per sub-block quantities exchanged through LDS (block t unless noted):
-    __shared__ float s_wl[2][NW][DV];   // last row of the local solve L u
-    __shared__ float s_df[2][NW][DV];   // g-weighted column sum of dh
-    __shared__ float s_wp[2][NW][DV];   // block t-1: last row of its local solve
-    __shared__ float s_de[2][NW][DV];   // g-weighted column sum of dh * Q_{t-1}
-    __shared__ float s_wf[2][NW][DV];   // last row of the local solve L (u * C'_{t+1})
-    __shared__ float s_c[2][NW];        // decay product
-    __shared__ float s_cp[2][NW];       // block t-1: decay product
+    // Per sub-block quantities exchanged through LDS (block t unless noted),
+    // double buffered by step; one struct, so that one base address serves all.
+    struct Exchange {
+        float wl[NW][DV];   // last row of the local solve L u
+        float df[NW][DV];   // g-weighted column sum of dh
+        float wp[NW][DV];   // block t-1: last row of its local solve
+        float de[NW][DV];   // g-weighted column sum of dh * Q_{t-1}
+        float wf[NW][DV];   // last row of the local solve L (u * C'_{t+1})
+        float c[NW];        // decay product
+        float cp[NW];       // block t-1: decay product
+    };
+    __shared__ Exchange s_x[2];
+    // x and b rows of the step's block.  Block t-1's rows, which a step reads
+    // for the previous block's tail, are the next step's own: each lane keeps
+    // them in LDS slots of its own (no barrier involved) instead of reading
+    // them again.
+    __shared__ uint32_t s_xb[2][4][RW::NWORDS][NW * 64];
+    const int tid = threadIdx.x;
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
@@ -285,12 +295,20 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         return ok ? v : 0.0f;
     };
 
-    // C'_{t+1} at this lane's rows, for the block the next step processes.
-    float Cn[4][CPL];
+    // C'_{t+1} at this lane's rows, for the block the next step processes
+    // (kept from one step to the next in this lane's own LDS slots).
+    __shared__ float s_cn[4][NW * 64][CPL];
+    auto set_cn = [&](int r, const float (&v)[CPL]) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+        for (int m = 0; m < CPL; ++m) s_cn[r][tid][m] = v[m];
+    };
+    {
+        float z[CPL];
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) Cn[r][m] = 0.f;
+        for (int m = 0; m < CPL; ++m) z[m] = 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) set_cn(r, z);
+    }
     int buf = 0;
 
     // From block t (g prefix products G, sub-block product c) and its dh:
@@ -307,7 +325,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
 #pragma unroll
             for (int q = 0; q < 4; ++q) d4[q] = dh[q][m];
             Pe[m] = Contract<IO>::run(AP, d4);
-            if (grp == 3) s_df[buf][wv][n * CPL + m] = Pe[m][3] + dk.G[3] * dh[3][m];
+            if (grp == 3) s_x[buf].df[wv][n * CPL + m] = Pe[m][3] + dk.G[3] * dh[3][m];
         }
     };
     // Prefix over this head's sub-blocks before sg of the column sums: X = sum_{r < sg} G_<r df_r.
@@ -319,8 +337,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         for (int r = 0; r < sg; ++r) {
             const int src = hw * TW + r;
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) X[m] += gp * s_df[buf][src][n * CPL + m];
-            gp *= s_c[buf][src];
+            for (int m = 0; m < CPL; ++m) X[m] += gp * s_x[buf].df[src][n * CPL + m];
+            gp *= s_x[buf].c[src];
         }
     };
 
@@ -346,45 +364,77 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         const Decay dk = build_decay(a_n, grp, n);
         f32x4 Pe[CPL];
         c_prime(dk, dh, Pe);
-        if (lane == 63) s_c[buf][wv] = dk.c;
+        if (lane == 63) s_x[buf].c[wv] = dk.c;
         __syncthreads();
         float X[CPL], gp;
         prefix_df(X, gp);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 4; ++r) {
+            float v[CPL];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) Cn[r][m] = X[m] + gp * Pe[m][r];
+            for (int m = 0; m < CPL; ++m) v[m] = X[m] + gp * Pe[m][r];
+            set_cn(r, v);
+        }
         buf ^= 1;
     }
 
     const int64_t nsteps = (wk.t_end - wk.t_begin + L - 1) / L;
+    if (nsteps > 0) {   // x and b of the run's last block into this lane's slots
+        const int64_t r0 = wk.t_begin + (nsteps - 1) * L + sg * SB, tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t oc = in_range(wk.valid && tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+            RW xv, bv;
+            xv.template load<kBwdLoad>(rx, oc);
+            bv.template load<kBwdLoad>(rb, oc);
+#pragma unroll
+            for (int i = 0; i < RW::NWORDS; ++i) {
+                s_xb[0][r][i][tid] = xv.w[i];
+                s_xb[1][r][i][tid] = bv.w[i];
+            }
+        }
+    }
     for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
         const int64_t t0 = wk.t_begin + k * L;    // a block boundary
         const int64_t r0 = t0 + sg * SB, tr0 = r0 + 4 * grp;
         const int64_t rp = r0 - L;                // the same sub-block of block t-1
+        // The rows' offsets, recomputed every step (one add each) rather than
+        // kept across the loop: an empty asm hides that lo equals loff.
+        uint32_t lo = loff;
+        asm volatile("" : "+v"(lo));
 
         // ---- loads: block t, and x, b, a of block t-1 -----------------------------
         RW xr[4], br[4], dyr[4];
         float dh[4][CPL], up[4][CPL];
         {
             RW cr[4];
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                         rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
+            const __amdgpu_buffer_rsrc_t rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
             const int64_t rpb = max(rp, (int64_t)0);   // (rows before the sequence are masked)
             const __amdgpu_buffer_rsrc_t rxp = rsrc(xb + rpb * rs), rbp = rsrc(bb + rpb * rs);
             RW xp[4], bp[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const uint32_t o = loff + (uint32_t)(r * rs);
+                const uint32_t o = lo + (uint32_t)(r * rs);
                 const uint32_t oc = in_range(wk.valid && tr0 + r < wk.t_end, o);
                 const uint32_t opv = in_range(wk.valid && rp + 4 * grp + r >= 0, o);
-                xr[r].template load<kBwdLoad>(rx, oc);
-                br[r].template load<kBwdLoad>(rb, oc);
+#pragma unroll
+                for (int i = 0; i < RW::NWORDS; ++i) {
+                    xr[r].w[i] = s_xb[0][r][i][tid];
+                    br[r].w[i] = s_xb[1][r][i][tid];
+                }
                 cr[r].template load<kBwdLoad>(rc, oc);
                 dyr[r].template load<kBwdLoad>(rdy, oc);
                 xp[r].template load<kBwdLoad>(rxp, opv);
                 bp[r].template load<kBwdLoad>(rbp, opv);
             }
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int i = 0; i < RW::NWORDS; ++i) {
+                    s_xb[0][r][i][tid] = xp[r].w[i];
+                    s_xb[1][r][i][tid] = bp[r].w[i];
+                }
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -432,13 +482,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         const float cp = shfl(row_prefix_prod(ap_n), base + 15);
         if (grp == 3) {
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) s_wl[buf][wv][n * CPL + m] = W[m][3];
+            for (int m = 0; m < CPL; ++m) s_x[buf].wl[wv][n * CPL + m] = W[m][3];
         }
         if (grp == 0) {
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) s_wp[buf][wv][n * CPL + m] = wp0[m];
+            for (int m = 0; m < CPL; ++m) s_x[buf].wp[wv][n * CPL + m] = wp0[m];
         }
-        if (lane == 63) { s_c[buf][wv] = dk.c; s_cp[buf][wv] = cp; }
+        if (lane == 63) { s_x[buf].c[wv] = dk.c; s_x[buf].cp[wv] = cp; }
         __syncthreads();
 
         // ---- the block's other sub-blocks -------------------------------------------
@@ -450,21 +500,21 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
 #pragma unroll 1
         for (int r = 0; r < sg; ++r) {   // state entering this sub-block, restarted at the block start
             const int src = hw * TW + r;
-            const float c_ = s_c[buf][src];
+            const float c_ = s_x[buf].c[src];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) s[m] = c_ * s[m] + s_wl[buf][src][n * CPL + m];
+            for (int m = 0; m < CPL; ++m) s[m] = c_ * s[m] + s_x[buf].wl[src][n * CPL + m];
         }
 #pragma unroll 1
         for (int r = TW - 1; r > sg; --r) {   // adjoint entering from the block's later sub-blocks
             const int src = hw * TW + r;
-            const float c_ = s_c[buf][src];
+            const float c_ = s_x[buf].c[src];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                pin[m] = c_ * pin[m] + s_df[buf][src][n * CPL + m];
-                Vp[m] += rap * s_wp[buf][src][n * CPL + m];
+                pin[m] = c_ * pin[m] + s_x[buf].df[src][n * CPL + m];
+                Vp[m] += rap * s_x[buf].wp[src][n * CPL + m];
             }
             ra *= c_;
-            rap *= s_cp[buf][src];
+            rap *= s_x[buf].cp[src];
         }
 
         // ---- gradients of x, b, c ----------------------------------------------------
@@ -480,12 +530,15 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
             float vdx[4][CPL], vdb[4][CPL], vdc[4][CPL], eh[4][CPL], uc[4][CPL];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
+                float Cn[CPL], Cnext[CPL];
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) Cn[m] = s_cn[r][tid][m];
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     const float Qv = rap * Tp[m][r] + Vp[m];
                     const float Hv = W[m][r] + dk.G[r] * (s[m] + gp * Qv);
                     const float Dv = Dl[m][r] + rrow[r] * pin[m];
-                    const float du = Dv + Rv[r] * Cn[r][m];
+                    const float du = Dv + Rv[r] * Cn[m];
                     const float dyv = dyr[r].get(m);
                     const float zb = br[r].get(m);
                     const SigSlope g = p.sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
@@ -493,12 +546,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
                     vdx[r][m] = g.s * du + (p.residual ? dyv : 0.0f);
                     vdb[r][m] = xr[r].get(m) * du * g.ds;
                     eh[r][m] = dh[r][m] * Qv;
-                    uc[r][m] = xr[r].get(m) * g.s * Cn[r][m];
+                    uc[r][m] = xr[r].get(m) * g.s * Cn[m];
                     Dl[m][r] = Dv;                          // keep D for the decay gradient
                     W[m][r] += dk.G[r] * s[m];              // and the block-restarted state w
-                    Cn[r][m] = X[m] + gp * Pe[m][r];        // C'_t for the next step
+                    Cnext[m] = X[m] + gp * Pe[m][r];        // C'_t for the next step
                 }
-                const uint32_t o = in_range(wk.valid && tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+                set_cn(r, Cnext);
+                const uint32_t o = in_range(wk.valid && tr0 + r < wk.t_end, lo + (uint32_t)(r * rs));
                 store_row<IO, CPL, kBwdStore>(rdx, o, vdx[r]);
                 store_row<IO, CPL, kBwdStore>(rdb, o, vdb[r]);
                 store_row<IO, CPL, kBwdStore>(rdc, o, vdc[r]);
@@ -519,11 +573,11 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         const float a0 = shfl(a_n, base);
         if (grp == 0) {
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) s_de[buf][wv][n * CPL + m] = a0 * El[m][0];
+            for (int m = 0; m < CPL; ++m) s_x[buf].de[wv][n * CPL + m] = a0 * El[m][0];
         }
         if (grp == 3) {
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) s_wf[buf][wv][n * CPL + m] = Fl[m][3];
+            for (int m = 0; m < CPL; ++m) s_x[buf].wf[wv][n * CPL + m] = Fl[m][3];
         }
         __syncthreads();
         float pinE[CPL], sF[CPL];
@@ -532,16 +586,16 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
 #pragma unroll 1
         for (int r = 0; r < sg; ++r) {
             const int src = hw * TW + r;
-            const float c_ = s_c[buf][src];
+            const float c_ = s_x[buf].c[src];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) sF[m] = c_ * sF[m] + s_wf[buf][src][n * CPL + m];
+            for (int m = 0; m < CPL; ++m) sF[m] = c_ * sF[m] + s_x[buf].wf[src][n * CPL + m];
         }
 #pragma unroll 1
         for (int r = TW - 1; r > sg; --r) {
             const int src = hw * TW + r;
-            const float c_ = s_c[buf][src];
+            const float c_ = s_x[buf].c[src];
 #pragma unroll
-            for (int m = 0; m < CPL; ++m) pinE[m] = c_ * pinE[m] + s_de[buf][src][n * CPL + m];
+            for (int m = 0; m < CPL; ++m) pinE[m] = c_ * pinE[m] + s_x[buf].de[src][n * CPL + m];
         }
 
         // ---- decay gradient --------------------------------------------------------
