@@ -106,6 +106,13 @@ __device__ inline void build_suffix_operator(float a_n, int grp, int n, float (&
 
 template <class IO, int CPL, int TW, int HW>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_fwd_kernel(Params p) {
+    // Featurisation flags, read at run time (compiling them out measured
+    // slower for this kernel, unlike the backward).
+    const bool sig_a = p.sig_a, sig_b = p.sig_b;
+    // Both contractions take fp32 operands (the fp32 MFMA) whatever the I/O
+    // type: this kernel is bound by its VALU work, which the bf16 hi/lo
+    // operand split adds to, more than by MFMA cycles.
+    using Ct = Contract<IoF32>;
     constexpr int NW = TW * HW;
     constexpr int DV = CPL * SB;    // channels of a virtual head
     constexpr int L = TW * SB;      // block length = window length
@@ -158,7 +165,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_fwd_kernel(Params p) 
         }
         const bool a_ok = wk.valid && r0 + n < wk.t_end;
         float a_n = load_scalar<IO, kFwdDecay>(rsrc(ab + r0 * as), in_range(a_ok, aoff));
-        if (p.sig_a) a_n = a_ok ? sigmoid(a_n) : 0.0f;
+        if (sig_a) a_n = a_ok ? sigmoid(a_n) : 0.0f;
         // (rows past the end of the sequence have u = 0 and reach no output)
 
         // ---- local solve W = L u and strict suffix solve T = S u ------------
@@ -167,15 +174,15 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_fwd_kernel(Params p) 
         build_suffix_operator(a_n, grp, n, S, rrow);
         f32x4 W[CPL], Ts[CPL];
         {
-            const typename Contract<IO>::A AL = Contract<IO>::prep(dk.L);
-            const typename Contract<IO>::A AS = Contract<IO>::prep(S);
+            const typename Ct::A AL = Ct::prep(dk.L);
+            const typename Ct::A AS = Ct::prep(S);
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 float u[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), p.sig_b);
-                W[m] = Contract<IO>::run(AL, u);
-                Ts[m] = Contract<IO>::run(AS, u);
+                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
+                W[m] = Ct::run(AL, u);
+                Ts[m] = Ct::run(AS, u);
             }
         }
         if (grp == 3) {
@@ -233,8 +240,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_fwd_kernel(Params p) 
 // Backward
 // ---------------------------------------------------------------------------
 
-template <class IO, int CPL, int TW, int HW>
+template <class IO, int CPL, int TW, int HW, bool FEAT>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) {
+    // Featurisation flags; off at compile time unless FEAT.
+    const bool sig_a = FEAT && p.sig_a, sig_b = FEAT && p.sig_b;
     constexpr int NW = TW * HW;
     constexpr int DV = CPL * SB;
     constexpr int L = TW * SB;
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         const bool ok = wk.valid && r0 + n >= lo && r0 + n < hi;
         float v = load_scalar<IO, kBwdDecay>(rsrc(ab + max(r0, (int64_t)0) * as), in_range(ok, aoff));
         ds = 1.0f;
-        if (p.sig_a) {
+        if (sig_a) {
             const SigSlope g = sigmoid_slope(v);
             ds = g.ds;
             v = g.s;
@@ -440,7 +449,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     dh[r][m] = dyr[r].get(m) * cr[r].get(m);          // dh = dy * c
-                    up[r][m] = xp[r].get(m) * pregate(bp[r].get(m), p.sig_b);
+                    up[r][m] = xp[r].get(m) * pregate(bp[r].get(m), sig_b);
                 }
         }
         float ds_n, ds_unused;
@@ -469,7 +478,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
                 float u[4], d4[4], u4p[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    u[q] = xr[q].get(m) * pregate(br[q].get(m), p.sig_b);
+                    u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
                     d4[q] = dh[q][m];
                     u4p[q] = up[q][m];
                 }
@@ -541,7 +550,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
                     const float du = Dv + Rv[r] * Cn[m];
                     const float dyv = dyr[r].get(m);
                     const float zb = br[r].get(m);
-                    const SigSlope g = p.sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
+                    const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
                     vdc[r][m] = dyv * Hv;
                     vdx[r][m] = g.s * du + (p.residual ? dyv : 0.0f);
                     vdb[r][m] = xr[r].get(m) * du * g.ds;
@@ -655,10 +664,12 @@ template <class IO, int CPL, int TW>
 hipError_t launch_uni_tw(const Params& p, bool backward, hipStream_t st) {
     constexpr int HW = 8 / TW;
     const dim3 grid((uint32_t)p.nwork), block(TW * HW * 64);
-    if (backward)
-        hipLaunchKernelGGL((swr_uni_bwd_kernel<IO, CPL, TW, HW>), grid, block, 0, st, p);
-    else
+    if (!backward)
         hipLaunchKernelGGL((swr_uni_fwd_kernel<IO, CPL, TW, HW>), grid, block, 0, st, p);
+    else if (p.sig_a || p.sig_b)
+        hipLaunchKernelGGL((swr_uni_bwd_kernel<IO, CPL, TW, HW, true>), grid, block, 0, st, p);
+    else
+        hipLaunchKernelGGL((swr_uni_bwd_kernel<IO, CPL, TW, HW, false>), grid, block, 0, st, p);
     return hipGetLastError();
 }
 
