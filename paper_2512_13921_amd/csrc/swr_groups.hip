@@ -146,21 +146,72 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_grouped_kernel(Params p) {
     }
     __syncthreads();
 
+    // One head's inputs for one step: its x and dy rows, its decay (as
+    // stored) and the carrier of the block before the step.  Each head's are
+    // fetched while the head before it computes.
+    struct HeadIn {
+        R_ x[4], dy[4];
+        float a;
+        float v[CPL];
+    };
+    // (Straight-line code whatever the arguments: with live false every
+    // access is out of range and reads zero, so that the loads are issued on
+    // one path and not waited for where two paths would join.)
+    auto fetch = [&](int64_t kk, int jj, bool live, HeadIn& in) {
+        const int64_t t0 = wk.t_begin + kk * STEP, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+        const int64_t xo = head_x(jj);
+        const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
+                                     rdy = rsrc((const char*)p.dy + xo + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(live && tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+            in.x[r].template load<kBwdLoad>(rx, o);
+            in.dy[r].template load<kBwdLoad>(rdy, o);
+        }
+        in.a = load_scalar<IO, kBwdDecay>(rsrc((const char*)p.a + (head_a(jj) + r0 * p.sa_t) * ES),
+                                          in_range(live && r0 + n < wk.t_end, aoff));
+        Row<IoF32, CPL> vr;
+        const float* vb = p.carriers + ((wk.b * p.H + wk.g * K + jj) * p.nblocks) * D + (int64_t)wk.part * DV;
+        const int64_t blk = (t0 >> p.lshift) - 1;
+        vr.load(rsrc(vb), in_range(live && t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+    };
+
+    // The gates are fetched a step ahead (PG), each head's inputs a head
+    // ahead (PH), where the registers allow it: the featurised and the
+    // float32 64-channel kernels would spill.
+    constexpr bool PG = CPL <= 2 || (IO::ES == 2 && !FEAT);
+    constexpr bool PH = CPL <= 2 || IO::ES == 2 || !FEAT;
+    R_ gb[4], gc[4];   // PG: the group's gates of the coming step
+    auto fetch_gates = [&](int64_t kk, bool live, R_ (&ob)[4], R_ (&oc)[4]) {
+        const int64_t r0 = wk.t_begin + kk * STEP + tw * SB, tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rb = rsrc(bb + r0 * gs), rc = rsrc(cb + r0 * gs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t og = in_range(live && tr0 + r < wk.t_end, goff + (uint32_t)(r * gs));
+            ob[r].template load<kBwdLoad>(rb, og);
+            oc[r].template load<kBwdLoad>(rc, og);
+        }
+    };
+
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    if constexpr (PG) fetch_gates(max(nsteps - 1, (int64_t)0), nsteps > 0, gb, gc);
+    HeadIn cur;
+    if constexpr (PH) fetch(max(nsteps - 1, (int64_t)0), 0, nsteps > 0, cur);
     for (int64_t k = nsteps - 1; k >= 0; --k, par ^= 1) {
         const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
         const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
-        // The group's gates for this step, and the sums of the heads' shares.
+        // The group's gates for this step (with PG fetched during the step
+        // before, which then fetches the next step's); the sums of the heads' shares.
         R_ br[4], cr[4];
-        {
-            const __amdgpu_buffer_rsrc_t rb = rsrc(bb + r0 * gs), rc = rsrc(cb + r0 * gs);
+        if constexpr (PG) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const uint32_t og = in_range(tr0 + r < wk.t_end, goff + (uint32_t)(r * gs));
-                br[r].template load<kBwdLoad>(rb, og);
-                cr[r].template load<kBwdLoad>(rc, og);
-            }
+            for (int r = 0; r < 4; ++r) { br[r] = gb[r]; cr[r] = gc[r]; }
+            fetch_gates(max(k - 1, (int64_t)0), k > 0, gb, gc);
+        } else {
+            fetch_gates(k, true, br, cr);
         }
         float sdb[4][CPL], sdc[4][CPL];
 #pragma unroll
@@ -170,39 +221,27 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_grouped_kernel(Params p) {
 
 #pragma unroll 1
         for (int j = 0; j < K; ++j, buf ^= 1) {
-            const int64_t h = wk.g * K + j;
             const int64_t xo = head_x(j);
-            const char* xb = (const char*)p.x + xo;
-            const char* dyb = (const char*)p.dy + xo;
             char* dxb = (char*)p.dx + xo;
-            const char* ab = (const char*)p.a + head_a(j) * ES;
             float* const dab = p.da + head_a(j);
-            R_ xr[4], dyr[4];
-            {
-                const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rdy = rsrc(dyb + r0 * rs);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
-                    xr[r].template load<kBwdLoad>(rx, o);
-                    dyr[r].template load<kBwdLoad>(rdy, o);
-                }
+            // This head's inputs, fetched while the head before computed; then
+            // the next head's (or the next step's first head's).
+            if constexpr (!PH) fetch(k, j, true, cur);
+            const HeadIn in = cur;
+            if constexpr (PH) {
+                const bool same = j + 1 < K;   // the next head of this step, else the next step's first
+                fetch(same ? k : max(k - 1, (int64_t)0), same ? j + 1 : 0, same || k > 0, cur);
             }
-            float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+            const R_* const xr = in.x;
+            const R_* const dyr = in.dy;
+            float a_n = in.a;
             float ds_n = 1.0f;
             if (sig_a) {
                 const SigSlope g = sigmoid_slope(a_n);
                 ds_n = g.ds;
                 a_n = r0 + n < wk.t_end ? g.s : 0.0f;
             }
-            float vprev[CPL];   // carrier of the block before this step (zero at the start)
-            {
-                Row<IoF32, CPL> vr;
-                const float* vb = p.carriers + ((wk.b * p.H + h) * p.nblocks) * D + (int64_t)wk.part * DV;
-                const int64_t blk = (t0 >> p.lshift) - 1;
-                vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
-            }
+            const float* const vprev = in.v;   // carrier of the block before this step (zero at the start)
 
             // ---- local solves W = L u and Dl = L^T dh --------------------------------
             const Decay dk = build_decay(a_n, grp, n);
