@@ -1419,49 +1419,68 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         buf ^= 1;
     }
 
+    // A step's inputs: the rows of x, b, c, dy (and of a, one decay per
+    // channel) and the carrier of the block before it.  PF: fetched during
+    // the step before (bf16, one decay per channel, no featurisation: the
+    // float32 kernels would spill, the featurised ones measured no faster).
+    // The fetch is straight-line code (live false: every access out of
+    // range, reading zero), so the loads are not waited for where two paths
+    // would join.
+    constexpr bool PF = PK == 1 && IO::ES == 2 && !FEAT;
+    struct StepIn {
+        R_ x[4], b[4], c[4], dy[4], a[4];
+        float v[CPL];
+    };
+    auto fetch_step = [&](int64_t kk, bool live, StepIn& in) {
+        const int64_t t0 = wk.t_begin + kk * STEP, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs), rc = rsrc(cb + r0 * rs),
+                                     rdy = rsrc(dyb + r0 * rs), ra = rsrc(ab + r0 * as);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(live && tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
+            in.x[r].template load<kBwdLoad>(rx, o);
+            in.b[r].template load<kBwdLoad>(rb, o);
+            in.c[r].template load<kBwdLoad>(rc, o);
+            in.dy[r].template load<kBwdLoad>(rdy, o);
+            if constexpr (PK == 1) in.a[r].template load<kBwdLoad>(ra, o);
+        }
+        // the carrier: the initial state for the exact recurrence's first block
+        const bool from_h0 = MODE == kExact && t0 == 0;
+        const int64_t blk = (t0 >> p.lshift) - 1;
+        Row<IoF32, CPL> vr;
+        vr.load(rsrc(from_h0 ? p.h0 + hb * geo.Dr : vb),
+                from_h0 ? in_range(live && p.h0 != nullptr, geo.off(1, 0) * 4u)
+                        : in_range(live && t0 > 0, geo.off(p.nblocks, blk) * 4u));
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+    };
+
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    StepIn nxt;
+    if constexpr (PF) fetch_step(max(nsteps - 1, (int64_t)0), nsteps > 0, nxt);
     for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
         const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
         const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
 
-        R_ xr[4], br[4], dyr[4], ar[4];
+        if constexpr (!PF) fetch_step(k, true, nxt);
+        const StepIn in = nxt;
+        if constexpr (PF) fetch_step(max(k - 1, (int64_t)0), k > 0, nxt);
+        const R_* const xr = in.x;
+        const R_* const br = in.b;
+        const R_* const dyr = in.dy;
+        const R_* const ar = in.a;
         float av[4][CPL], dh[4][CPL], az[4];
-        {
-            R_ cr[4];
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs),
-                                         rc = rsrc(cb + r0 * rs), rdy = rsrc(dyb + r0 * rs),
-                                         ra = rsrc(ab + r0 * as);
+        if constexpr (PK > 1)
+            decay_rows_packed<IO, CPL, kBwdDecay>(rsrc(ab + r0 * as), aoffp, (uint32_t)as, tr0, wk.t_begin, wk.t_end,
+                                                  p.T, sig_a, az, av);
+        else
+            decay_rows<IO, CPL>(in.a, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const uint32_t o = in_range(tr0 + r < wk.t_end, loff + (uint32_t)(r * rs));
-                xr[r].template load<kBwdLoad>(rx, o);
-                br[r].template load<kBwdLoad>(rb, o);
-                cr[r].template load<kBwdLoad>(rc, o);
-                dyr[r].template load<kBwdLoad>(rdy, o);
-                if constexpr (PK == 1) ar[r].template load<kBwdLoad>(ra, o);
-            }
-            if constexpr (PK > 1)
-                decay_rows_packed<IO, CPL, kBwdDecay>(ra, aoffp, (uint32_t)as, tr0, wk.t_begin, wk.t_end, p.T, sig_a,
-                                                      az, av);
-            else
-                decay_rows<IO, CPL>(ar, tr0, wk.t_begin, wk.t_end, p.T, sig_a, av);
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);
-        }
-        float vprev[CPL];
-        {
-            Row<IoF32, CPL> vr;
-            const int64_t blk = (t0 >> p.lshift) - 1;
-            if (MODE == kExact && t0 == 0)
-                vr.load(rsrc(p.h0 + hb * geo.Dr), in_range(p.h0 != nullptr, geo.off(1, 0) * 4u));
-            else
-                vr.load(rsrc(vb), in_range(t0 > 0, geo.off(p.nblocks, blk) * 4u));
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
-        }
+            for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * in.c[r].get(m);
+        const float* const vprev = in.v;
 
         // ---- local solves: W = L (b*x), G; Dv = L^T (c*dy), Rr -------------------------
         float W[4][CPL], G[4][CPL], Dv[4][CPL], Rr[4][CPL];
