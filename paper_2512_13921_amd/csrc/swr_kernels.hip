@@ -467,38 +467,67 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         buf ^= 1;
     }
 
+    // A step's inputs: the rows of x, b, c, dy, the decays and the carrier of
+    // the block before it.  PF: fetched during the step before, where it costs
+    // no occupancy (bf16 heads of up to 64 channels in 8-wave groups, which
+    // run one group per compute unit either way; no featurisation).  The
+    // 128-channel kernel has no registers to spare for it.  The fetch is
+    // straight-line code (live false: every access out of range, reading
+    // zero), so the loads are not waited for where two paths would join.
+    constexpr bool PF = CPL <= 4 && TW == 8 && IO::ES == 2 && !FEAT;
+    struct StepIn {
+        R_ x[4], b[4], c[4], dy[4];
+        float a;
+        float v[CPL];
+    };
+    auto fetch_step = [&](int64_t kk, bool live, StepIn& in) {
+        const int64_t t0 = wk.t_begin + kk * STEP, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs), rc = rsrc(cb + r0 * gs),
+                                     rdy = rsrc(dyb + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const bool ok = live && tr0 + r < wk.t_end;
+            const uint32_t o = in_range(ok, loff + (uint32_t)(r * rs));
+            const uint32_t og = GG ? in_range(ok, goff + (uint32_t)(r * gs)) : o;
+            in.x[r].template load<kBwdLoad>(rx, o);
+            in.b[r].template load<kBwdLoad>(rb, og);
+            in.c[r].template load<kBwdLoad>(rc, og);
+            in.dy[r].template load<kBwdLoad>(rdy, o);
+        }
+        in.a = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(live && r0 + n < wk.t_end, aoff));
+        // Carrier of the block before the step (zero before the sequence
+        // start, or the initial state for the exact recurrence).
+        const bool from_h0 = MODE == kExact && t0 == 0;
+        const int64_t blk = (t0 >> p.lshift) - 1;
+        Row<IoF32, CPL> vr;
+        vr.load(rsrc(from_h0 ? (const void*)(p.h0 + seq * D) : (const void*)vb),
+                from_h0 ? in_range(live && p.h0 != nullptr, (uint32_t)(n * CPL) * 4u)
+                        : in_range(live && t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+    };
+
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
+    StepIn nxt;
+    if constexpr (PF) fetch_step(max(nsteps - 1, (int64_t)0), nsteps > 0, nxt);
     for (int64_t k = nsteps - 1; k >= 0; --k, buf ^= 1) {
         const int64_t t0 = wk.t_begin + k * STEP;      // a block boundary
         const int64_t r0 = t0 + tw * SB;
         const int64_t tr0 = r0 + 4 * grp;
 
         // ---- loads ---------------------------------------------------------------
-        R_ xr[4], br[4], dyr[4];
+        if constexpr (!PF) fetch_step(k, true, nxt);
+        const StepIn in = nxt;
+        if constexpr (PF) fetch_step(max(k - 1, (int64_t)0), k > 0, nxt);
+        const R_* const xr = in.x;
+        const R_* const br = in.b;
+        const R_* const dyr = in.dy;
         float dh[4][CPL];
-        {
-            // (Copying these tiles into LDS one step ahead, as the forward
-            // does, measured no faster here: the backward's eight waves keep
-            // enough loads in flight.)
-            R_ cr[4];
-            const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs),
-                                         rc = rsrc(cb + r0 * gs), rdy = rsrc(dyb + r0 * rs);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const bool ok = tr0 + r < wk.t_end;
-                const uint32_t o = in_range(ok, loff + (uint32_t)(r * rs));
-                const uint32_t og = GG ? in_range(ok, goff + (uint32_t)(r * gs)) : o;
-                xr[r].template load<kBwdLoad>(rx, o);
-                br[r].template load<kBwdLoad>(rb, og);
-                cr[r].template load<kBwdLoad>(rc, og);
-                dyr[r].template load<kBwdLoad>(rdy, o);
-            }
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * cr[r].get(m);   // dh = dy * c
-        }
-        float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(r0 + n < wk.t_end, aoff));
+            for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * in.c[r].get(m);   // dh = dy * c
+        float a_n = in.a;
         float ds_n = 1.0f;      // d a / d(input) of token n: 1, or sigma'(z) for a logit z
         if (sig_a) {
             const SigSlope g = sigmoid_slope(a_n);
@@ -508,19 +537,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         // Exact recurrence: past the end of the sequence the decay is 1, so
         // the adjoint entering from the end reaches the last token intact.
         if (MODE == kExact && r0 + n >= p.T) a_n = 1.0f;
-        // Carrier of the block before this step (zero before the sequence
-        // start, or the initial state for the exact recurrence).
-        float vprev[CPL];
-        {
-            Row<IoF32, CPL> vr;
-            const int64_t blk = (t0 >> p.lshift) - 1;
-            if (MODE == kExact && t0 == 0)
-                vr.load(rsrc(p.h0 + seq * D), in_range(p.h0 != nullptr, (uint32_t)(n * CPL) * 4u));
-            else
-                vr.load(rsrc(vb), in_range(t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) vprev[m] = vr.get(m);
-        }
+        const float* const vprev = in.v;
 
         // ---- local solves: W = L (b*x) and Dl = L^T (c*dy) ---------------------------
         const Decay dk = build_decay(a_n, grp, n);
