@@ -468,13 +468,14 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     }
 
     // A step's inputs: the rows of x, b, c, dy, the decays and the carrier of
-    // the block before it.  PF: fetched during the step before, where it costs
-    // no occupancy (bf16 heads of up to 64 channels in 8-wave groups, which
-    // run one group per compute unit either way; no featurisation).  The
-    // 128-channel kernel has no registers to spare for it.  The fetch is
-    // straight-line code (live false: every access out of range, reading
-    // zero), so the loads are not waited for where two paths would join.
-    constexpr bool PF = CPL <= 4 && TW == 8 && IO::ES == 2 && !FEAT;
+    // the block before it.  PF: fetched during the step before (bf16 heads of
+    // up to 64 channels, no featurisation; 147 -> 186 VGPRs, which keeps
+    // 8-wave groups at one per compute unit and leaves 4-wave groups two of
+    // their three, measured faster either way).  The 128-channel kernel has
+    // no registers to spare for it.  The fetch is straight-line code (live
+    // false: every access out of range, reading zero), so the loads are not
+    // waited for where two paths would join.
+    constexpr bool PF = CPL <= 4 && IO::ES == 2 && !FEAT;
     struct StepIn {
         R_ x[4], b[4], c[4], dy[4];
         float a;

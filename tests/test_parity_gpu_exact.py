@@ -92,6 +92,7 @@ SMALL = [
     (1, 1, 1, 64, 64, "bf16"),      # a single token: the recurrent decoding step
     (1, 17, 1, 128, 128, "bf16"),
     (2, 700, 4, 64, 64, "bf16"),
+    (1, 700, 2, 64, 128, "bf16"),   # 8-wave groups of 64 channels (inputs fetched a step ahead)
     (3, 300, 6, 128, 32, "f32"),
 ]
 
