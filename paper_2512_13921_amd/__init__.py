@@ -189,6 +189,12 @@ def _dtype_code(t):
 def _problem_from(x, a, block, residual, run_len, sigmoid_decay=False, sigmoid_pregate=False):
     if x.dim() != 4:
         raise ValueError("x must be [B, T, H, D]")
+    # The kernels dereference every pointer on the GPU: a host tensor would be
+    # a memory fault, not an error, so it is refused here.
+    if not x.is_cuda:
+        raise ValueError("x must be a GPU tensor")
+    if a.device != x.device:
+        raise ValueError("a must be on x's device")
     per_channel = a.dim() == 4
     if per_channel:
         if a.shape != x.shape or a.stride() != x.stride():
@@ -221,6 +227,13 @@ def _stream(stream, device):
 
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _da_check(da, a):
+    torch = _torch()
+    if (da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride()
+            or da.device != a.device):
+        raise ValueError("da must be float32 with the shape, strides and device of a")
 
 
 def _carrier_tensor(x, block, carriers):
@@ -287,8 +300,7 @@ def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, 
     else:
         dx, da, db, dc = outputs
         _same_layout(x, dx, db, dc)
-        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
-            raise ValueError("da must be float32 with the shape and strides of a")
+        _da_check(da, a)
     rc = load().swr_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
                              _ptr(carriers), _ptr(dx), _ptr(da), _ptr(db), _ptr(dc),
                              _stream(stream, x.device))
@@ -313,8 +325,9 @@ def _workspace(problem, device, workspace):
     nbytes = swr_exact_workspace_bytes(problem)
     if workspace is None:
         return torch.empty(max(nbytes // 4, 1), dtype=torch.float32, device=device)
-    if workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous():
-        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes")
+    if (workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous()
+            or workspace.device != device):
+        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes on x's device")
     return workspace
 
 
@@ -382,8 +395,7 @@ def swr_exact_backward(x, a, b, c, dy, carriers, block, h0=None, dh_last=None, r
     else:
         dx, da, db, dc = outputs
         _same_layout(x, dx, db, dc)
-        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
-            raise ValueError("da must be float32 with the shape and strides of a")
+        _da_check(da, a)
     B, T, H, D = x.shape
     dh0 = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if want_dh0 else None
     ws = _workspace(problem, x.device, workspace)
@@ -534,13 +546,13 @@ def swr_backward_shared_gates(x, a, b, c, dy, carriers, block, group, residual=F
         dx, da, db, dc = outputs
         _same_layout(x, dx)
         _same_layout(b, db, dc)
-        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
-            raise ValueError("da must be float32 with the shape and strides of a")
+        _da_check(da, a)
     nbytes = swr_shared_gates_workspace_bytes(problem, group)
     if workspace is None:
         workspace = torch.empty(nbytes // 4, dtype=torch.float32, device=x.device) if nbytes else None
-    elif workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous():
-        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes")
+    elif (workspace.numel() * workspace.element_size() < nbytes or not workspace.is_contiguous()
+          or workspace.device != x.device):
+        raise ValueError(f"workspace must be a contiguous tensor of at least {nbytes} bytes on x's device")
     rc = load().swr_backward_shared_gates(ctypes.byref(problem), int(group), _i64x3(b.stride()), _ptr(x),
                                           _ptr(a), _ptr(b), _ptr(c), _ptr(dy), _ptr(carriers), _ptr(dx),
                                           _ptr(da), _ptr(db), _ptr(dc), _opt(workspace),
@@ -594,8 +606,7 @@ def swr_uniform_backward(x, a, b, c, dy, window, residual=False, outputs=None, r
     else:
         dx, da, db, dc = outputs
         _same_layout(x, dx, db, dc)
-        if da.dtype != torch.float32 or da.shape != a.shape or da.stride() != a.stride():
-            raise ValueError("da must be float32 with the shape and strides of a")
+        _da_check(da, a)
     rc = load().swr_uniform_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
                                      _ptr(dx), _ptr(da), _ptr(db), _ptr(dc), _stream(stream, x.device))
     if rc != 0:

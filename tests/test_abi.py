@@ -477,3 +477,30 @@ def test_forward_pairs_bf16_heads_of_64():
     assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * (8 // 2) * 4
     p = problem(B=2, T=4096, H=7, D=64, block=128, run_len=1024)   # odd H: no pairs
     assert swr.swr_launch_info(p)["fwd_workgroups"] == 2 * 7 * 4
+
+
+# ---- the Python binding refuses host tensors (the kernels would dereference
+# their host addresses on the GPU); checked before the library is called.
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 64, 2, 16, dtype=torch.bfloat16)
+    a = torch.zeros(1, 64, 2, dtype=torch.bfloat16)
+    gates = torch.zeros(1, 64, 1, 16, dtype=torch.bfloat16)
+    calls = [
+        lambda: swr.swr_forward(x, a, x, x, 16),
+        lambda: swr.swr_carriers(x, a, x, 16),
+        lambda: swr.swr_backward(x, a, x, x, x, torch.zeros(1), 16),
+        lambda: swr.swr_exact_forward(x, a, x, x, 16),
+        lambda: swr.swr_exact_backward(x, a, x, x, x, torch.zeros(1), 16),
+        lambda: swr.swr_step(x, a, x, x, 16, 0),
+        lambda: swr.swr_exact_step(x, a, x, x),
+        lambda: swr.swr_decode_state(x, a, torch.zeros(1), 16),
+        lambda: swr.swr_uniform_forward(x, a, x, x, 16),
+        lambda: swr.swr_uniform_backward(x, a, x, x, x, 16),
+        lambda: swr.swr_forward_shared_gates(x, a, gates, gates, 16, 2),
+        lambda: swr.swr_backward_shared_gates(x, a, gates, gates, x, torch.zeros(1), 16, 2),
+    ]
+    for call in calls:
+        with pytest.raises(ValueError, match="GPU tensor"):
+            call()
