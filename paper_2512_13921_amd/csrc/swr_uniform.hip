@@ -461,15 +461,22 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         float rrow[4];   // r_q of this lane's rows: a_{q+1} ... a_15 of the sub-block
         f32x4 W[CPL], Dl[CPL], Pe[CPL], Tp[CPL];
         float wp0[CPL];
+        // L and L^T as MFMA operands, kept for the step's second solves
+        // (rebuilt for them in the featurised kernel, which has no registers
+        // to spare)
+        typename Contract<IO>::A AL, ALT;
+        auto prep_L = [&] {
+            float LT[4];
+            build_decay_transposed(a_n, grp, n, LT);
+            AL = Contract<IO>::prep(dk.L);
+            ALT = Contract<IO>::prep(LT);
+        };
+        prep_L();
         {
             float S[4];
             build_suffix_operator(a_n, grp, n, S, rrow);
             float Sp[4], rrow_p[4];
             build_suffix_operator(ap_n, grp, n, Sp, rrow_p);
-            float LT[4];
-            build_decay_transposed(a_n, grp, n, LT);
-            const typename Contract<IO>::A AL = Contract<IO>::prep(dk.L);
-            const typename Contract<IO>::A ALT = Contract<IO>::prep(LT);
             const typename Contract<IO>::A ASp = Contract<IO>::prep(Sp);
             c_prime(dk, dh, Pe);
             const float rp0 = shfl(rrow_p[0], base);   // r'_0 (lane n = 0 holds row 0's value)
@@ -566,10 +573,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
                 store_row<IO, CPL, kBwdStore>(rdb, o, vdb[r]);
                 store_row<IO, CPL, kBwdStore>(rdc, o, vdc[r]);
             }
-            float LT[4];
-            build_decay_transposed(a_n, grp, n, LT);
-            const typename Contract<IO>::A AL = Contract<IO>::prep(dk.L);
-            const typename Contract<IO>::A ALT = Contract<IO>::prep(LT);
+            if constexpr (FEAT) prep_L();
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 float e4[4], f4[4];
