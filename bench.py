@@ -72,8 +72,9 @@ def algorithmic_bytes(cfg, backward, with_carriers=True, gate_groups=0):
 
 def contraction_flops(cfg, backward, uniform=False):
     """Dense flops of the intra-block contractions (16x16 sub-block tiles):
-    2 * 16 * D per token-head per contraction; the jagged backward runs three
-    (forward recompute, reverse solve, look-ahead reverse solve); the uniform
+    2 * 16 * D per token-head per contraction; the jagged backward runs two
+    (the forward's local solve recomputed, and the reverse solve; the one
+    reverse solve per run for the block after it is left out); the uniform
     window's forward two (local and strict-suffix solves) and its backward six
     (local, reverse, prefix and previous block's suffix solves, and the two
     solves of its decay gradient).  None for a per-channel decay, whose local
@@ -83,7 +84,7 @@ def contraction_flops(cfg, backward, uniform=False):
     per = 2 * 16 * cfg.D * cfg.B * cfg.T * cfg.H
     if uniform:
         return per * (6 if backward else 2)
-    return per * (3 if backward else 1)
+    return per * (2 if backward else 1)
 
 
 # The sources that decide what a launch does (kernels, grid policy): the
