@@ -98,11 +98,23 @@ def test_uniform_residual_and_layout(swr, dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("block", [32, 128])
-def test_uniform_featurisation(swr, dtype, block):
+@pytest.mark.parametrize("flags", ["both", "decay", "pregate"])
+def test_uniform_featurisation(swr, dtype, block, flags):
     prob = W.random_problem(4, 2, 500, 2, 64, block, dtype, logits=True)
-    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    feat = dict(sigmoid_decay=flags != "pregate", sigmoid_pregate=flags != "decay")
+    if not feat["sigmoid_decay"]:      # the kernels take the decay itself: hand them sigma(z)
+        prob.a[...] = W.round_to(oracle.sigmoid(prob.a).astype(np.float32), dtype)
     y, grads = _run(swr, prob, **feat)
-    _check(prob, y, grads, what="uniform featurised", **feat)
+    _check(prob, y, grads, what=f"uniform featurised ({flags})", **feat)
+
+
+def test_uniform_featurised_headline_width(swr):
+    # 128 channels as two 64-channel halves, several runs of several steps:
+    # the pre-gate's e^-z carried from step to step.
+    prob = W.random_problem(5, 1, 1536, 2, 128, 128, "bf16", logits=True)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    y, grads = _run(swr, prob, run_len=512, **feat)
+    _check(prob, y, grads, what="uniform featurised d128 runs", **feat)
 
 
 @pytest.mark.parametrize("value", [0.0, 1.0])
