@@ -20,7 +20,7 @@ constexpr int64_t kMaxExtent = (int64_t)1 << 62;
 // Longer runs mean fewer halo re-reads.
 int64_t fwd_workgroups(const swr::Shape& s) { return s.tw * s.hw == 4 ? 512 : 256; }
 int64_t bwd_workgroups(const swr::Shape& s, int cpl) {
-    return s.tw * s.hw == 8 ? 256 : (cpl == 8 ? 1024 : 4096);
+    return s.tw * s.hw == 8 ? 256 : (cpl == 8 ? 1024 : 8192);
 }
 
 // Run length (tokens, a multiple of step) that splits each sequence into
