@@ -196,6 +196,17 @@ def test_per_channel_launch_shape():
     assert swr.swr_carrier_elems(p) == 8 * 16 * 128 * 128
 
 
+def test_backward_grid_targets():
+    # the backward's default grid: one 8-wave group per CU at block 128 (256),
+    # 4-wave groups at block 64 about 1024 (128 channels) or 8192 (64)
+    info = swr.swr_launch_info(problem(B=8, T=4096, H=16, D=128, block=64))
+    assert info["bwd_workgroups"] == 8 * 16 * (-(-4096 // info["bwd_run_len"]))
+    assert 1024 <= info["bwd_workgroups"] < 2048
+    info = swr.swr_launch_info(problem(B=16, T=8192, H=32, D=64, block=64))
+    assert info["bwd_workgroups"] == 16 * 32 * (-(-8192 // info["bwd_run_len"]))
+    assert 8192 <= info["bwd_workgroups"] < 16384
+
+
 def test_carrier_elems():
     p = problem(B=2, T=250, H=3, D=64, block=64)
     assert swr.swr_carrier_elems(p) == 2 * 3 * 4 * 64     # ceil(250 / 64) = 4 blocks
