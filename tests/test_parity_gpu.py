@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 import workloads as W
-from parity import assert_close, check_full, run_gpu, to_device, to_host
+from parity import assert_close, check_full, compare_whole, run_gpu, to_device, to_host, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -195,38 +195,29 @@ def test_config1_full(swr):
     check_full(prob, y, grads, what="config 1")
 
 
-def _slices(cfg):
-    B, H = cfg.B, cfg.H
-    picks = {(0, 0), (B - 1, H - 1), (B // 2, H // 3), (B // 3, H - 1)}
-    return sorted(picks)
+def _heads(t, b, h0, h1):
+    """tensor[b:b+1, :, h0:h1] of a host array in [B, T, H, ...] layout."""
+    return np.asarray(t)[b:b + 1, :, h0:h1]
 
 
 @pytest.mark.parametrize("cid", [2, 3, 4, 5])
-def test_full_size_sampled(swr, cid):
-    """Full-size run in the default launch configuration; whole (batch, head)
-    slices (every token, every channel) are compared with the oracle."""
+def test_full_size_whole_tensors(swr, cid):
+    """Full-size run in the default launch configuration; every element of y,
+    dx, da, db and dc is compared with the oracle (streamed over chunks of
+    heads), and the whole-tensor error figures are reported."""
     cfg = W.CONFIGS[cid]
     _say(f"[config {cid}] {cfg.name}: generating inputs")
-    prob = W.generate(cfg)
+    prob = workload(cfg)
     _say(f"[config {cid}] running on the GPU")
     y, grads = run_gpu(swr, prob)
-    picks = _slices(cfg)
-    bi = np.array([p[0] for p in picks])
-    hi = np.array([p[1] for p in picks])
 
-    def take(t):   # [B, T, H, ...] -> [S, T, ...] on the sampled slices
-        return np.ascontiguousarray(np.asarray(t)[bi, :, hi])
+    def ref_chunk(b, h0, h1):
+        args = [_heads(getattr(prob, n), b, h0, h1) for n in ("x", "a", "b", "c")]
+        ref = dict(y=oracle.forward(*args, cfg.block))
+        ref.update(zip(("dx", "da", "db", "dc"),
+                       oracle.backward(*args, _heads(prob.dy, b, h0, h1), cfg.block)))
+        return ref
 
-    xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
-    _say(f"[config {cid}] oracle on {len(picks)} slices")
-    ref_y = oracle.forward_slices(xs, as_, bs, cs, cfg.block)
-    ref = oracle.backward_slices(xs, as_, bs, cs, dys, cfg.block)
-    got_y = np.stack([to_host(y[b_, :, h_]) for b_, h_ in picks])
-    assert_close(got_y, ref_y, cfg.dtype, f"config {cid} y")
-    for name, g, r in zip(("dx", "da", "db", "dc"), grads, ref):
-        got = np.stack([to_host(g[b_, :, h_]) for b_, h_ in picks])
-        st = assert_close(got, r, cfg.dtype, f"config {cid} {name}")
-        _say(f"[config {cid}] {name}: {st}")
-    # properties over the whole output: finite everywhere
-    for t in (y,) + tuple(grads):
-        assert torch.isfinite(t.float()).all()
+    outs = [("y", y, 2, 1)] + [(n, g, 2, 1) for n, g in zip(("dx", "da", "db", "dc"), grads)]
+    _say(f"[config {cid}] comparing whole tensors with the oracle")
+    compare_whole(f"config {cid} {cfg.name}", cfg.dtype, cfg.B, cfg.H, outs, ref_chunk)

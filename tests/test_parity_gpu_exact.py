@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import workloads as W
-from parity import assert_close, to_device, to_host
+from parity import assert_close, compare_whole, to_device, to_host, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -238,35 +238,33 @@ def test_exact_deterministic(swr):
         assert torch.equal(t1, t2)
 
 
-@pytest.mark.parametrize("cid", [3, 4])
-def test_exact_full_size_sampled(swr, cid):
+@pytest.mark.parametrize("cid", [3, 4, 5])
+def test_exact_full_size_whole_tensors(swr, cid):
     """Full-size exact forward and backward in the default launch
-    configuration; whole (batch, head) slices compared with the oracle."""
+    configuration, with an initial state and a final-state gradient; every
+    element of y, h_last, dx, da, db, dc and dh0 is compared with the oracle."""
     cfg = W.CONFIGS[cid]
     _say(f"[exact config {cid}] {cfg.name}: generating inputs")
-    prob = W.generate(cfg)
+    prob = workload(cfg)
     rng = np.random.default_rng(cid)
     h0, dhl = _state(rng, cfg), _state(rng, cfg)
     _say(f"[exact config {cid}] running on the GPU")
     y, v, hl, grads = run_exact(swr, prob, h0, dhl)
-    picks = sorted({(0, 0), (cfg.B - 1, cfg.H - 1), (cfg.B // 2, cfg.H // 3)})
-    bi = np.array([p[0] for p in picks])
-    hi = np.array([p[1] for p in picks])
 
-    def take(t):
-        return np.ascontiguousarray(np.asarray(t)[bi, :, hi])
+    def ref_chunk(b, h0_, h1_):
+        args = [np.asarray(getattr(prob, n))[b:b + 1, :, h0_:h1_] for n in ("x", "a", "b", "c")]
+        st0, dst = h0[b:b + 1, h0_:h1_], dhl[b:b + 1, h0_:h1_]
+        ref = dict(zip(("y", "h_last"), oracle.exact_forward(*args, st0)))
+        ref.update(zip(("dx", "da", "db", "dc", "dh0"),
+                       oracle.exact_backward(*args, prob.dy[b:b + 1, :, h0_:h1_], st0, dst)))
+        states, _ = oracle.exact_forward(args[0], args[1], args[2], np.ones_like(args[3]), st0)
+        nb = -(-cfg.T // cfg.block)
+        ends = [min((t + 1) * cfg.block, cfg.T) - 1 for t in range(nb)]
+        ref["carriers"] = np.transpose(states[:, ends], (0, 2, 1, 3))     # [1, heads, nb, D]
+        return ref
 
-    xs, as_, bs, cs, dys = (take(getattr(prob, n)) for n in ("x", "a", "b", "c", "dy"))
-    h0s, dhls = h0[bi, hi], dhl[bi, hi]
-    _say(f"[exact config {cid}] oracle on {len(picks)} slices")
-    ref_y, ref_hl = oracle.exact_forward_slices(xs, as_, bs, cs, h0s)
-    ref = oracle.exact_backward_slices(xs, as_, bs, cs, dys, h0s, dhls)
-    assert_close(np.stack([to_host(y[b_, :, h_]) for b_, h_ in picks]), ref_y, cfg.dtype, "exact y")
-    assert_close(np.stack([to_host(hl[b_, h_]) for b_, h_ in picks]), ref_hl, cfg.dtype, "exact h_last")
-    for name, g, r in zip(("dx", "da", "db", "dc"), grads[:4], ref[:4]):
-        got = np.stack([to_host(g[b_, :, h_]) for b_, h_ in picks])
-        st = assert_close(got, r, cfg.dtype, f"exact config {cid} {name}")
-        _say(f"[exact config {cid}] {name}: {st}")
-    assert_close(np.stack([to_host(grads[4][b_, h_]) for b_, h_ in picks]), ref[4], cfg.dtype, "exact dh0")
-    for t in (y, v, hl) + tuple(grads):
-        assert torch.isfinite(t.float()).all()
+    outs = [("y", y, 2, 1), ("h_last", hl, 1, 1)]
+    outs += [(n, g, 2, 1) for n, g in zip(("dx", "da", "db", "dc"), grads[:4])]
+    outs += [("dh0", grads[4], 1, 1), ("carriers", v, 1, 1)]
+    _say(f"[exact config {cid}] comparing whole tensors with the oracle")
+    compare_whole(f"exact config {cid} {cfg.name}", cfg.dtype, cfg.B, cfg.H, outs, ref_chunk)

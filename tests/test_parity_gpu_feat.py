@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 import workloads as W
-from parity import assert_close, check_full, run_gpu, to_device, to_host
+from parity import assert_close, check_full, compare_whole, run_gpu, to_device, to_host, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -101,29 +101,23 @@ def test_autograd_function(swr):
         assert_close(to_host(t.grad), r, "f32", "feat autograd d" + n)
 
 
-def test_full_size_sampled_with_logits(swr):
+def test_full_size_whole_tensors_with_logits(swr):
     """B=8, T=4096, H=16, d=128, block 64 with the decay's logits N(3, 1) and
-    pre-gate logits, both through the kernels' sigmoid; whole sampled slices."""
+    pre-gate logits, both through the kernels' sigmoid; every element of every
+    output is compared with the oracle."""
     cfg = W.CONFIGS[2].with_(logits=True)
     _say(f"[feat] {cfg.name} (logits): generating inputs")
-    prob = W.generate(cfg)
+    prob = workload(cfg)
     kw = FEATS[2]
     y, grads = run_gpu(swr, prob, **kw)
-    picks = sorted({(0, 0), (cfg.B - 1, cfg.H - 1), (cfg.B // 2, cfg.H // 3)})
-    bi = np.array([p_[0] for p_ in picks])
-    hi = np.array([p_[1] for p_ in picks])
 
-    def take(t):   # keep singleton batch and head axes: [S, T, 1, ...] slices in [B, T, H, ...] form
-        return np.stack([np.asarray(t)[b_, :, h_][None, :, None] for b_, h_ in zip(bi, hi)])
+    def ref_chunk(b, h0, h1):
+        args = [np.asarray(getattr(prob, n))[b:b + 1, :, h0:h1] for n in ("x", "a", "b", "c")]
+        ref = dict(y=oracle.forward(*args, cfg.block, **kw))
+        ref.update(zip(("dx", "da", "db", "dc"),
+                       oracle.backward(*args, prob.dy[b:b + 1, :, h0:h1], cfg.block, **kw)))
+        return ref
 
-    refs_y, refs_g = [], []
-    for k in range(len(picks)):
-        xs, as_, bs, cs, dys = (take(getattr(prob, n))[k] for n in ("x", "a", "b", "c", "dy"))
-        refs_y.append(oracle.forward(xs, as_, bs, cs, cfg.block, **kw)[0, :, 0])
-        refs_g.append([g[0, :, 0] for g in oracle.backward(xs, as_, bs, cs, dys, cfg.block, **kw)])
-    got = np.stack([to_host(y[b_, :, h_]) for b_, h_ in picks])
-    assert_close(got, np.stack(refs_y), cfg.dtype, "feat full y")
-    for i, name in enumerate(("dx", "da", "db", "dc")):
-        got = np.stack([to_host(grads[i][b_, :, h_]) for b_, h_ in picks])
-        st = assert_close(got, np.stack([r[i] for r in refs_g]), cfg.dtype, f"feat full {name}")
-        _say(f"[feat full] {name}: {st}")
+    outs = [("y", y, 2, 1)] + [(n, g, 2, 1) for n, g in zip(("dx", "da", "db", "dc"), grads)]
+    _say("[feat] comparing whole tensors with the oracle")
+    compare_whole(f"featurised {cfg.name} (logits)", cfg.dtype, cfg.B, cfg.H, outs, ref_chunk)

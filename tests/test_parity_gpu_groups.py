@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 import workloads as W
-from parity import assert_close, to_device, to_host
+from parity import assert_close, compare_whole, to_device, to_host, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -125,33 +125,31 @@ def test_shared_gates_deterministic(swr, D):
         assert torch.equal(p_, q_)
 
 
-def test_shared_gates_headline_shape_sampled(swr):
+def test_shared_gates_headline_shape_whole_tensors(swr):
     """The headline shape (B=8, T=16384, H=16, d=128, l=128) with 8 gate groups
-    of 2 heads; whole (batch, group) slices of db, dc and (batch, head) slices
-    of y, dx, da compared with the oracle."""
+    of 2 heads; every element of y, dx, da and of the groups' db, dc is
+    compared with the oracle."""
     cfg = W.CONFIGS[3]
     group = 2
     _say(f"[groups headline] {cfg.name}: generating inputs")
-    prob = W.generate(cfg)
+    prob = workload(cfg)
     y, grads = _run(swr, prob, group)
     bg, cg = _gated(prob, group)
-    for bi, g in [(0, 0), (5, 3), (7, 7)]:
-        heads = [g * group + j for j in range(group)]
-        sl = lambda t, h: np.ascontiguousarray(np.asarray(t)[bi:bi + 1, :, h:h + 1])
-        xs = np.concatenate([sl(prob.x, h) for h in heads], axis=2)
-        as_ = np.concatenate([sl(prob.a, h) for h in heads], axis=2)
-        dys = np.concatenate([sl(prob.dy, h) for h in heads], axis=2)
-        bs, cs = sl(bg, g), sl(cg, g)
-        ref_y = oracle.grouped_forward(xs, as_, bs, cs, cfg.block, group)
-        ref = oracle.grouped_backward(xs, as_, bs, cs, dys, cfg.block, group)
-        h0, h1 = heads[0], heads[-1] + 1
-        assert_close(to_host(y[bi:bi + 1, :, h0:h1]), ref_y, cfg.dtype, "groups headline y")
-        for name, got, r in zip(("dx", "da", "db", "dc"), grads, ref):
-            part = got[bi:bi + 1, :, g:g + 1] if name in ("db", "dc") else got[bi:bi + 1, :, h0:h1]
-            st = assert_close(to_host(part), r, cfg.dtype, f"groups headline {name}")
-            _say(f"[groups headline] ({bi}, {g}) {name}: {st}")
-    for t in (y,) + tuple(grads):
-        assert torch.isfinite(t.float()).all()
+
+    def ref_chunk(b, h0, h1):
+        per_head = [np.asarray(getattr(prob, n))[b:b + 1, :, h0:h1] for n in ("x", "a", "dy")]
+        bs, cs = bg[b:b + 1, :, h0 // group:h1 // group], cg[b:b + 1, :, h0 // group:h1 // group]
+        xs, as_, dys = per_head
+        ref = dict(y=oracle.grouped_forward(xs, as_, bs, cs, cfg.block, group))
+        ref.update(zip(("dx", "da", "db", "dc"),
+                       oracle.grouped_backward(xs, as_, bs, cs, dys, cfg.block, group)))
+        return ref
+
+    outs = [("y", y, 2, 1), ("dx", grads[0], 2, 1), ("da", grads[1], 2, 1),
+            ("db", grads[2], 2, group), ("dc", grads[3], 2, group)]
+    _say("[groups headline] comparing whole tensors with the oracle")
+    compare_whole(f"shared gates {cfg.H // group}x{group} {cfg.name}", cfg.dtype, cfg.B, cfg.H, outs,
+                  ref_chunk, quantum=group)
 
 
 def test_shared_gates_autograd_function(swr):
