@@ -39,9 +39,11 @@
  * `dtype`; accumulation is always float32.
  *
  * Ownership.  Every pointer is device memory owned by the caller.  The library
- * allocates no memory and keeps no mutable global state; calls from several
- * host threads are safe.  Only the exact-recurrence calls and the backward
- * with shared gates need a workspace, which the caller provides.  Outputs are
+ * allocates no memory.  Its only global state is the static device array that
+ * swr_exact_forward_noalloc uses as its workspace (and that array's address
+ * per device); every other call keeps no state, and calls from several host
+ * threads are safe.  Only the exact-recurrence calls and the backward with
+ * shared gates need a workspace, which the caller provides.  Outputs are
  * fully overwritten.
  *
  * Asynchrony.  Work is enqueued on `stream` (a hipStream_t passed as void*;
@@ -74,7 +76,9 @@ typedef enum swr_status {
     SWR_ERR_UNSUPPORTED = -7, /* D not in {16, 32, 64, 128}, unknown flags, bad run_len,
                                  or strides/sizes beyond the kernels' 32-bit offsets       */
     SWR_ERR_HIP = -8,         /* the HIP runtime rejected the launch                      */
-    SWR_ERR_VERSION = -9      /* problem->abi_version != SWR_ABI_VERSION                  */
+    SWR_ERR_VERSION = -9,     /* problem->abi_version != SWR_ABI_VERSION                  */
+    SWR_ERR_SCRATCH = -10     /* swr_exact_forward_noalloc: the problem needs more than
+                                 SWR_NOALLOC_SCRATCH_BYTES of workspace                    */
 } swr_status_t;
 
 typedef enum swr_dtype {
@@ -197,6 +201,26 @@ int64_t swr_exact_workspace_bytes(const swr_problem_t* problem);
 int swr_exact_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
                       const void* c, const float* h0, void* y, float* carriers, float* h_last,
                       void* workspace, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the exact
+ * forward with the arguments and results of swr_exact_forward, but with its
+ * workspace in a device array that the library owns instead of a caller's
+ * buffer.  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).  The array is a static device array of SWR_NOALLOC_SCRATCH_BYTES
+ * bytes, one per GPU, held from the library's first use of that GPU until the
+ * process ends; its address is looked up once per device, on the first call
+ * on it.  A problem whose swr_exact_workspace_bytes exceeds that size is
+ * rejected with SWR_ERR_SCRATCH before any HIP runtime call.  The kernels
+ * write every workspace entry they read, so nothing is cleared between calls.
+ * All calls on one GPU share its array: calls whose work overlaps in time on
+ * one GPU (different streams, or host threads racing on the same stream)
+ * race on it and give wrong results; calls ordered on one stream are safe.
+ * Launches go to the device of `stream` (NULL: the current device). */
+#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)16 << 20)
+int swr_exact_forward_noalloc(const swr_problem_t* problem, const void* x, const void* a,
+                              const void* b, const void* c, const float* h0, void* y,
+                              float* carriers, float* h_last, void* stream);
 
 /* Exact backward: gradients of  sum(dy * y) + sum(dh_last * h_last)  with
  * respect to x, a (float32 with a's shape and strides), b, c and h0.  x, a, b,

@@ -23,7 +23,7 @@ from . import build as _build
 
 __all__ = ["SwrError", "swr_forward", "swr_backward", "swr_carriers", "swr_error_string",
            "swr_abi_version", "swr_launch_info", "swr_carrier_elems", "carrier_shape",
-           "swr_exact_forward", "swr_exact_backward", "swr_exact_workspace_bytes",
+           "swr_exact_forward", "swr_exact_forward_noalloc", "swr_exact_backward", "swr_exact_workspace_bytes",
            "swr_step", "swr_exact_step", "swr_decode_state",
            "swr_uniform_forward", "swr_uniform_backward", "swr_uniform_launch_info",
            "swr_forward_shared_gates", "swr_backward_shared_gates", "swr_shared_gates_workspace_bytes",
@@ -36,6 +36,8 @@ SWR_FLAG_RESIDUAL = 1
 SWR_FLAG_PER_CHANNEL_DECAY = 2
 SWR_FLAG_SIGMOID_DECAY = 4
 SWR_FLAG_SIGMOID_PREGATE = 8
+SWR_ERR_SCRATCH = -10
+SWR_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class SwrProblem(ctypes.Structure):
@@ -92,6 +94,8 @@ def load():
         lib.swr_exact_workspace_bytes.restype = ctypes.c_int64
         lib.swr_exact_forward.argtypes = [P] + [vp] * 10
         lib.swr_exact_forward.restype = ctypes.c_int
+        lib.swr_exact_forward_noalloc.argtypes = [P] + [vp] * 9
+        lib.swr_exact_forward_noalloc.restype = ctypes.c_int
         lib.swr_exact_backward.argtypes = [P] + [vp] * 15
         lib.swr_exact_backward.restype = ctypes.c_int
         lib.swr_step.argtypes = [P, ctypes.c_int64] + [vp] * 7
@@ -347,13 +351,8 @@ def _opt(t):
     return None if t is None else _ptr(t)
 
 
-def swr_exact_forward(x, a, b, c, block, h0=None, residual=False, y=None, carriers=None,
-                      save_carriers=False, want_h_last=False, workspace=None, run_len=0, stream=None,
-                      sigmoid_decay=False, sigmoid_pregate=False):
-    """The exact (untruncated) recurrence on the GPU (see ``include/swr.h``):
-    returns y, plus the exact block carriers (``save_carriers`` or a
-    ``carriers`` tensor) and the final state h_last ([B, H, D] float32,
-    ``want_h_last``), in that order.  ``h0`` is the initial state or None."""
+def _exact_forward(noalloc, x, a, b, c, block, h0, residual, y, carriers, save_carriers, h_last,
+                   want_h_last, workspace, run_len, stream, sigmoid_decay, sigmoid_pregate):
     torch = _torch()
     problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
     _same_layout(x, b, c)
@@ -365,14 +364,46 @@ def swr_exact_forward(x, a, b, c, block, h0=None, residual=False, y=None, carrie
     want_v = save_carriers or carriers is not None
     v = _carrier_tensor(x, block, carriers) if want_v else None
     B, T, H, D = x.shape
-    hl = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if want_h_last else None
-    ws = _workspace(problem, x.device, workspace)
-    rc = load().swr_exact_forward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _opt(h0),
-                                  _ptr(y), _opt(v), _opt(hl), _ptr(ws), _stream(stream, x.device))
+    want_h_last = want_h_last or h_last is not None
+    if h_last is None:
+        hl = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if want_h_last else None
+    else:
+        hl = _state(h_last, x, "h_last")
+    if noalloc:
+        rc = load().swr_exact_forward_noalloc(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c),
+                                              _opt(h0), _ptr(y), _opt(v), _opt(hl), _stream(stream, x.device))
+    else:
+        ws = _workspace(problem, x.device, workspace)
+        rc = load().swr_exact_forward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _opt(h0),
+                                      _ptr(y), _opt(v), _opt(hl), _ptr(ws), _stream(stream, x.device))
     if rc != 0:
-        raise SwrError(rc, "swr_exact_forward")
+        raise SwrError(rc, "swr_exact_forward_noalloc" if noalloc else "swr_exact_forward")
     out = (y,) + ((v,) if want_v else ()) + ((hl,) if want_h_last else ())
     return out[0] if len(out) == 1 else out
+
+
+def swr_exact_forward(x, a, b, c, block, h0=None, residual=False, y=None, carriers=None,
+                      save_carriers=False, want_h_last=False, workspace=None, run_len=0, stream=None,
+                      sigmoid_decay=False, sigmoid_pregate=False, h_last=None):
+    """The exact (untruncated) recurrence on the GPU (see ``include/swr.h``):
+    returns y, plus the exact block carriers (``save_carriers`` or a
+    ``carriers`` tensor) and the final state h_last ([B, H, D] float32,
+    ``want_h_last`` or an ``h_last`` tensor), in that order.  ``h0`` is the
+    initial state or None."""
+    return _exact_forward(False, x, a, b, c, block, h0, residual, y, carriers, save_carriers, h_last,
+                          want_h_last, workspace, run_len, stream, sigmoid_decay, sigmoid_pregate)
+
+
+def swr_exact_forward_noalloc(x, a, b, c, block, h0=None, residual=False, y=None, carriers=None,
+                              save_carriers=False, want_h_last=False, run_len=0, stream=None,
+                              sigmoid_decay=False, sigmoid_pregate=False, h_last=None):
+    """swr_exact_forward with its workspace in the library's static device
+    array (``SWR_NOALLOC_SCRATCH_BYTES`` per GPU): the C call allocates no
+    device memory.  Pass ``y`` (and ``carriers`` / ``h_last``) to make the
+    whole call allocation-free; calls that overlap in time on one GPU race on
+    the shared array."""
+    return _exact_forward(True, x, a, b, c, block, h0, residual, y, carriers, save_carriers, h_last,
+                          want_h_last, None, run_len, stream, sigmoid_decay, sigmoid_pregate)
 
 
 def swr_exact_backward(x, a, b, c, dy, carriers, block, h0=None, dh_last=None, residual=False,

@@ -7,6 +7,7 @@
 #include <initializer_list>
 
 #include "../../include/swr.h"
+#include "swr_internal.h"
 #include "swr_launch.h"
 
 namespace {
@@ -258,6 +259,7 @@ const char* swr_error_string(int code) {
         case SWR_ERR_UNSUPPORTED: return "unsupported: D must be 16, 32, 64 or 128; unknown flags; bad run_len; or offsets beyond 32 bits";
         case SWR_ERR_HIP: return "the HIP runtime rejected the kernel launch";
         case SWR_ERR_VERSION: return "ABI version mismatch";
+        case SWR_ERR_SCRATCH: return "the problem needs more workspace than the library's static scratch array holds (SWR_NOALLOC_SCRATCH_BYTES)";
         default: return "unknown status code";
     }
 }
@@ -429,6 +431,14 @@ int64_t swr_exact_workspace_bytes(const swr_problem_t* problem) {
 int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
                       const void* c, const float* h0, void* y, float* carriers, float* h_last,
                       void* workspace, void* stream) {
+    return swr::exact_forward_impl(p, x, a, b, c, h0, y, carriers, h_last, workspace, nullptr, 0, stream);
+}
+
+}  // extern "C"
+
+int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a, const void* b,
+                            const void* c, const float* h0, void* y, float* carriers, float* h_last,
+                            void* workspace, ScratchFn scratch, int64_t scratch_bytes, void* stream) {
     Resolved r;
     int rc = resolve_for(p, &r, {x, b, c, (const void*)y});
     if (rc != SWR_OK) return rc;
@@ -436,7 +446,13 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
     if (!r.empty && (!x || !a || !b || !c || !y)) return SWR_ERR_NULL;
-    if (w.floats > 0 && !workspace) return SWR_ERR_NULL;
+    if (scratch) {
+        // the library's own array: disjoint from every caller buffer, located later
+        if (w.floats * 4 > scratch_bytes) return SWR_ERR_SCRATCH;
+        workspace = nullptr;
+    } else if (w.floats > 0 && !workspace) {
+        return SWR_ERR_NULL;
+    }
     for (const void* q : {(const void*)h0, (const void*)h_last, (const void*)carriers, (const void*)workspace})
         if (q && !aligned(q, 16)) return SWR_ERR_ALIGN;
     if (!r.empty) {
@@ -448,7 +464,7 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es),
                          span(h0, h0 ? sbytes : 0)};
     const Span outs[4] = {span(y, r.xspan), span(carriers, carriers ? r.carriers * 4 : 0),
-                          span(h_last, h_last ? sbytes : 0), span(workspace, w.floats * 4)};
+                          span(h_last, h_last ? sbytes : 0), span(workspace, workspace ? w.floats * 4 : 0)};
     for (int i = 0; i < 4; ++i) {
         for (const Span& s : ins)
             if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
@@ -456,6 +472,7 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
             if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
     }
 
+    if (scratch && w.floats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
     float *wv = nullptr, *wc = nullptr, *wp = nullptr;
     if (w.floats > 0) exact_arrays(p, w, workspace, &wv, &wc, &wp);
     swr::Params k = make_params(p, r, false);
@@ -477,6 +494,8 @@ int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, cons
     return swr::launch(k, p->dtype, r.dk, r.fwd, false, r.pc, r.pack, swr::kExact, stream) == hipSuccess ? SWR_OK
                                                                                           : SWR_ERR_HIP;
 }
+
+extern "C" {
 
 int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, const void* b,
                        const void* c, const void* dy, const float* h0, const float* carriers,

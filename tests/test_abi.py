@@ -12,8 +12,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "swr.h")
 
 BF16, F32 = swr.SWR_DTYPE_BF16, swr.SWR_DTYPE_F32
-OK, E_NULL, E_SHAPE, E_DTYPE, E_BLOCK, E_ALIGN, E_ALIAS, E_UNSUP, E_HIP, E_VER = (
-    0, -1, -2, -3, -4, -5, -6, -7, -8, -9)
+OK, E_NULL, E_SHAPE, E_DTYPE, E_BLOCK, E_ALIGN, E_ALIAS, E_UNSUP, E_HIP, E_VER, E_SCRATCH = (
+    0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10)
 
 # Fake, well-aligned "device" addresses far apart: validation never dereferences them.
 GB = 1 << 30
@@ -63,7 +63,7 @@ def test_abi_version_and_struct_layout():
 
 
 @pytest.mark.parametrize("code", [OK, E_NULL, E_SHAPE, E_DTYPE, E_BLOCK, E_ALIGN, E_ALIAS,
-                                  E_UNSUP, E_HIP, E_VER, 17])
+                                  E_UNSUP, E_HIP, E_VER, E_SCRATCH, 17])
 def test_error_strings(code):
     s = swr.swr_error_string(code)
     assert isinstance(s, str) and s
@@ -324,6 +324,36 @@ def test_exact_validation():
     for kw in (dict(B=0), dict(H=0)):
         assert xfwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
         assert xbwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0) == OK
+
+
+def nfwd(p, x=X, a=A, b=B_, c=C, h0=H0, y=Y, v_=V, hl=HL):
+    v = ctypes.c_void_p
+    return swr.load().swr_exact_forward_noalloc(ctypes.byref(p), v(x), v(a), v(b), v(c), v(h0), v(y),
+                                                v(v_), v(hl), None)
+
+
+def test_exact_forward_noalloc_validation():
+    # validated as swr_exact_forward is, every check before any HIP runtime call
+    p = problem()
+    for kw in ("x", "a", "b", "c", "y"):
+        assert nfwd(p, **{kw: 0}) == E_NULL, kw
+    for kw in ("h0", "hl", "v_"):
+        assert nfwd(p, **{kw: GB * 40 + 8}) == E_ALIGN, kw
+    assert nfwd(p, x=X + 4) == E_ALIGN
+    assert nfwd(p, hl=H0) == E_ALIAS and nfwd(p, hl=V) == E_ALIAS and nfwd(p, y=X) == E_ALIAS
+    assert nfwd(problem(D=48)) == E_UNSUP and nfwd(problem(block=48)) == E_BLOCK
+    # a problem whose workspace exceeds the static array is refused with its own code
+    assert swr.SWR_NOALLOC_SCRATCH_BYTES == 16 << 20
+    assert "#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)16 << 20)" in open(HEADER).read()
+    big = problem(B=128, T=128, H=128, D=128, block=128)
+    assert swr.swr_exact_workspace_bytes(big) > swr.SWR_NOALLOC_SCRATCH_BYTES
+    assert nfwd(big) == E_SCRATCH
+    assert "SWR_NOALLOC_SCRATCH_BYTES" in swr.swr_error_string(E_SCRATCH)
+    # the headline shape fits
+    assert swr.swr_exact_workspace_bytes(problem(B=8, T=16384, H=16, D=128, block=128)) <= 16 << 20
+    # nothing to do for an empty batch or head set, even with NULL pointers
+    for kw in (dict(B=0), dict(H=0)):
+        assert nfwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0) == OK
 
 
 # ----------------------------------------------------------------------------- recurrent decoding

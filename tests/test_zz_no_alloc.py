@@ -1,0 +1,85 @@
+"""The allocation-free exact forward, swr_exact_forward_noalloc (its workspace
+is the library's static device array), against swr_exact_forward with a
+caller-provided workspace, both called through the C ABI on the same inputs:
+consecutive calls, each smaller than the one before, whose outputs start out
+as NaN; every call must give the same results bit for bit, and match the
+oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from parity import assert_close, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def swr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2512_13921_amd as lib
+    lib.load()
+    return lib
+
+
+# (B, T, H, D, block, dtype, per-channel decay): each call smaller than the one before
+CALLS = [
+    (2, 3000, 4, 128, 128, "bf16", False),
+    (1, 700, 2, 64, 64, "bf16", False),
+    (1, 333, 3, 32, 32, "f32", True),
+]
+
+
+def _run_both(swr, seed, B, T, H, D, block, dtype, per_channel):
+    prob = W.random_problem(seed, B, T, H, D, block, dtype, "sigmoid", 3.0, per_channel=per_channel)
+    x, a, b, c = (to_device(getattr(prob, n), dtype) for n in "xabc")
+    h0 = np.random.default_rng(seed).standard_normal((B, H, D)).astype(np.float32)
+    h0_t = torch.from_numpy(h0).cuda()
+    nb = -(-T // block)
+    y = torch.full_like(x, float("nan"))
+    v = torch.full((B, H, nb, D), float("nan"), dtype=torch.float32, device="cuda")
+    hl = torch.full((B, H, D), float("nan"), dtype=torch.float32, device="cuda")
+    out = swr.swr_exact_forward_noalloc(x, a, b, c, block, h0=h0_t, y=y, carriers=v, h_last=hl)
+    assert out[0] is y and out[1] is v and out[2] is hl
+    y2, v2, hl2 = swr.swr_exact_forward(x, a, b, c, block, h0=h0_t, save_carriers=True, want_h_last=True)
+    torch.cuda.synchronize()
+    return prob, h0, (y, v, hl), (y2, v2, hl2)
+
+
+def test_noalloc_matches_the_workspace_call_on_consecutive_calls(swr):
+    for i, call in enumerate(CALLS):
+        B, T, H, D, block, dtype, pc = call
+        print(f"[noalloc] call {i}: B={B} T={T} H={H} D={D} l={block} {dtype} per_channel={pc}", flush=True)
+        prob, h0, got, ref = _run_both(swr, 70 + i, *call)
+        for name, p_, q_ in zip(("y", "carriers", "h_last"), got, ref):
+            assert torch.equal(p_, q_), (i, name)
+        ry, rhl = oracle.exact_forward(prob.x, prob.a, prob.b, prob.c, h0)
+        assert_close(to_host(got[0]), ry, dtype, f"noalloc call {i} y")
+        assert_close(to_host(got[2]), rhl, dtype, f"noalloc call {i} h_last")
+
+
+def test_noalloc_after_a_larger_call_on_another_stream(swr):
+    # calls ordered through one stream after work on another stream that the
+    # caller synchronised with: the array's contents from the earlier call do
+    # not leak into the later one
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        _run_both(swr, 80, *CALLS[0])
+    torch.cuda.current_stream().wait_stream(side)
+    prob, h0, got, ref = _run_both(swr, 81, *CALLS[1])
+    for name, p_, q_ in zip(("y", "carriers", "h_last"), got, ref):
+        assert torch.equal(p_, q_), name
+
+
+def test_noalloc_refuses_problems_beyond_the_static_array(swr):
+    # refused during validation, before any HIP call
+    x = torch.zeros((128, 128, 128, 128), dtype=torch.bfloat16, device="cuda")
+    a = torch.zeros((128, 128, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(swr.SwrError) as err:
+        swr.swr_exact_forward_noalloc(x, a, x, x, 128, y=torch.empty_like(x))
+    assert err.value.code == swr.SWR_ERR_SCRATCH
+    assert "SWR_NOALLOC_SCRATCH_BYTES" in str(err.value)
