@@ -93,17 +93,19 @@ KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_groups.hip", "swr_d
                   "swr_launch.h")
 
 
-def recorded_traffic(kernel, workload):
-    """HBM bytes per launch measured with rocprofv3 counters for this kernel and
-    workload, as recorded in profiles/, or None when a kernel or launch-policy
-    source has changed since the counters were taken."""
+def recorded(kernel, workload, what="traffic"):
+    """A record measured with rocprofv3 counters for this kernel and workload
+    and kept in profiles/ -- "traffic" (HBM bytes per launch) or "counters"
+    (matrix-pipe utilisation, executed MFMA flops, VALU busy, occupancy) --
+    or None when a kernel or launch-policy source has changed since the
+    counters were taken."""
     import hashlib
     import re
     csrc = os.path.join(ROOT, "paper_2512_13921_amd", "csrc")
     prof = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(prof):
         return None
-    m = re.search(r"<!-- traffic: (\{.*\}) -->", open(prof).read())
+    m = re.search(r"<!-- " + what + r": (\{.*\}) -->", open(prof).read())
     if not m:
         return None
     rec = json.loads(m.group(1))
@@ -487,7 +489,8 @@ def main():
                       "swr_backward_shared_gates (swr_bwd_kernel + swr_gate_reduce_kernel)")
     # The exact recurrence's passes are three launches each; their time is
     # taken as a whole and no single kernel's counters stand for it.
-    traffic = None if exact or groups else recorded_traffic(dom_kernel, cfg.name)
+    traffic = None if exact or groups else recorded(dom_kernel, cfg.name, "traffic")
+    counters = None if exact or groups else recorded(dom_kernel, cfg.name, "counters")
     if exact:
         dom_kernel = ("swr_exact_backward (swr_bwd_agg_kernel + swr_scan_kernel + swr_bwd_kernel)"
                       if dominant_bwd else
@@ -547,6 +550,16 @@ def main():
             "traffic_unit": "GB per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
             "traffic_vs_algorithmic": None if traffic is None else
                 traffic["traffic_bytes"] / (bb if dominant_bwd else fb),
+            # the same kernel's compute counters (rocprofv3 --pmc, recorded in
+            # profiles/ for these sources): matrix-pipe busy fraction
+            # (MfmaUtil), executed MFMA flops (SQ_INSTS_VALU_MFMA_MOPS_* x 512)
+            # at the profiled average duration against the dense peak of their
+            # dtype, VALU busy fraction and mean resident waves per CU
+            "mfma_util": None if counters is None else counters.get("mfma_util"),
+            "mfma_tflops_counted": None if counters is None else counters.get("mfma_tflops"),
+            "mfma_frac_counted": None if counters is None else counters.get("mfma_frac"),
+            "valu_busy": None if counters is None else counters.get("valu_busy"),
+            "occupancy_waves_per_cu": None if counters is None else counters.get("occupancy_waves_per_cu"),
         },
         "kernels": {
             "forward": {"ms": float(fwd_ms.mean()), "ms_min": float(fwd_ms.min()),
