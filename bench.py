@@ -351,6 +351,9 @@ def main():
     ap.add_argument("--paper-shape", action="store_true",
                     help="forward-only sweep at the paper's own mixer-timing shape (B=1, D=2048 as "
                          "H=128 heads of d=16, block 16, bf16) over T = 1K .. 512K")
+    ap.add_argument("--no-carriers", action="store_true",
+                    help="the jagged window without saved block carriers: the forward keeps none "
+                         "and the backward recomputes them (the problem statement's call shape)")
     ap.add_argument("--decode", action="store_true",
                     help="time recurrent decoding instead: one token per sequence per call "
                          "(swr_step / swr_exact_step) after a prompt of the workload's length")
@@ -399,6 +402,12 @@ def main():
                   file=sys.stderr)
             return 2
         cfg = cfg.with_(name=cfg.name + f"_gates{groups}")
+    nocar = args.no_carriers
+    if nocar:
+        if exact or uniform or groups:
+            print("--no-carriers applies to the jagged window's own entry points only", file=sys.stderr)
+            return 2
+        cfg = cfg.with_(name=cfg.name + "_nocarriers")
     if not cfg.backward:
         cfg = cfg.with_(backward=True)
     log(f"[bench] workload {cfg.name}: generating inputs")
@@ -436,7 +445,8 @@ def main():
             swr.swr_forward_shared_gates(x, a, b, c, cfg.block, gsz, y=y, carriers=carriers,
                                          run_len=args.run_len, **feat)
         else:
-            swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=carriers, run_len=args.run_len, **feat)
+            swr.swr_forward(x, a, b, c, cfg.block, y=y, carriers=None if nocar else carriers,
+                            run_len=args.run_len, **feat)
         if ev is not None:
             ev[1].record(stream)
         if exact:
@@ -449,7 +459,7 @@ def main():
             swr.swr_backward_shared_gates(x, a, b, c, dy, carriers, cfg.block, gsz, outputs=(dx, da, db, dc),
                                           workspace=gws, run_len=args.run_len, **feat)
         else:
-            swr.swr_backward(x, a, b, c, dy, carriers, cfg.block, outputs=(dx, da, db, dc),
+            swr.swr_backward(x, a, b, c, dy, None if nocar else carriers, cfg.block, outputs=(dx, da, db, dc),
                              run_len=args.run_len, **feat)
         if ev is not None:
             ev[2].record(stream)
@@ -475,8 +485,8 @@ def main():
     tokens = cfg.B * cfg.T
     value = tokens / (ms_per_step * 1e-3)
 
-    fb = algorithmic_bytes(cfg, False, not uniform, groups)
-    bb = algorithmic_bytes(cfg, True, not uniform, groups)
+    fb = algorithmic_bytes(cfg, False, not (uniform or nocar), groups)
+    bb = algorithmic_bytes(cfg, True, not (uniform or nocar), groups)
     f_gbs, b_gbs = fb / (fwd_ms.mean() * 1e-3) / 1e9, bb / (bwd_ms.mean() * 1e-3) / 1e9
     dominant_bwd = bwd_ms.mean() >= fwd_ms.mean()
     dom_gbs = b_gbs if dominant_bwd else f_gbs
@@ -537,6 +547,8 @@ def main():
                    "recurrence": ("exact (untruncated)" if exact else
                                   "uniform window" if uniform else "jagged window"),
                    "gate_groups": groups or None,
+                   "block_carriers": None if (exact or uniform or groups) else
+                                     ("recomputed by the backward" if nocar else "saved by the forward"),
                    "global_batch": cfg.B, "seq_len": cfg.T,
                    "parallelism": "single GPU", "launch": launch},
         "roofline": {

@@ -27,8 +27,10 @@
  * t+1; the paper suggests checkpointing only this carrier).  They are D
  * float32 values per block: a [B][H][ceil(T/block)][D] array, contiguous,
  * 0.4% of the forward's traffic at D = 128, block = 128.  swr_backward reads
- * them instead of re-reading the previous block's x, b and a; swr_carriers
- * recomputes them for callers that did not keep them.
+ * them instead of re-reading the previous block's x, b and a; given none, it
+ * recomputes each one from those rows itself (the call shape of the paper's
+ * problem statement, Alg. "Block Two-Pass": inputs and coefficients only),
+ * with the same results bit for bit.  swr_carriers computes them alone.
  *
  * Tensor layout.  x, b, c, y, dy, dx, db, dc are [B, T, H, D] with the channel
  * dimension D contiguous (stride 1) and element strides sx_b, sx_t, sx_h for
@@ -140,10 +142,13 @@ int swr_carriers(const swr_problem_t* problem, const void* x, const void* a, con
                  float* carriers, void* stream);
 
 /* Backward: given dy = dL/dy, writes dx, da (float32 with a's shape and strides),
- * db and dc.  x, a, b, c are the forward's inputs and `carriers` the block
- * carriers of those same inputs (from swr_forward or swr_carriers; required).
- * Nothing else from the forward is needed: the kernel recomputes the local
- * solves it uses. */
+ * db and dc.  x, a, b, c are the forward's inputs.  carriers: the block
+ * carriers of those same inputs (from swr_forward or swr_carriers; 16-byte
+ * aligned), or NULL, in which case the kernel recomputes the carrier of the
+ * block before each of its steps from that block's x, b and a (the rows it
+ * processes next; no workspace, no allocation; identical results, at the
+ * cost of reading those rows once more).  Nothing else from the forward is
+ * needed: the kernel recomputes the local solves it uses. */
 int swr_backward(const swr_problem_t* problem, const void* x, const void* a, const void* b,
                  const void* c, const void* dy, const float* carriers, void* dx, float* da,
                  void* db, void* dc, void* stream);

@@ -289,14 +289,13 @@ def swr_carriers(x, a, b, block, carriers=None, run_len=0, stream=None, sigmoid_
 def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, run_len=0,
                  stream=None, sigmoid_decay=False, sigmoid_pregate=False):
     """(dx, da, db, dc) of the SWR forward given dy and the forward's block
-    carriers (see ``include/swr.h``)."""
+    carriers (see ``include/swr.h``), or carriers=None: the kernel then
+    recomputes each carrier from the previous block's x, b, a."""
     torch = _torch()
     problem = _problem_from(x, a, block, residual, run_len, sigmoid_decay, sigmoid_pregate)
     _same_layout(x, b, c, dy)
-    if carriers is None:
-        raise ValueError("swr_backward needs the forward's block carriers: "
-                         "swr_forward(..., save_carriers=True) or swr_carriers(x, a, b, block)")
-    carriers = _carrier_tensor(x, block, carriers)
+    if carriers is not None:
+        carriers = _carrier_tensor(x, block, carriers)
     if outputs is None:
         dx, db, dc = (torch.empty_strided(x.shape, x.stride(), dtype=x.dtype, device=x.device)
                       for _ in range(3))
@@ -306,7 +305,7 @@ def swr_backward(x, a, b, c, dy, carriers, block, residual=False, outputs=None, 
         _same_layout(x, dx, db, dc)
         _da_check(da, a)
     rc = load().swr_backward(ctypes.byref(problem), _ptr(x), _ptr(a), _ptr(b), _ptr(c), _ptr(dy),
-                             _ptr(carriers), _ptr(dx), _ptr(da), _ptr(db), _ptr(dc),
+                             _opt(carriers), _ptr(dx), _ptr(da), _ptr(db), _ptr(dc),
                              _stream(stream, x.device))
     if rc != 0:
         raise SwrError(rc, "swr_backward")
@@ -650,23 +649,32 @@ def _autograd_function():
 
     class _SWRFunction(torch.autograd.Function):
         """Autograd wrapper: forward and backward both run the HIP kernels;
-        the backward recomputes what it needs from the saved inputs."""
+        the backward recomputes what it needs from the saved inputs (and the
+        block carriers, unless save_carriers is False: then it recomputes
+        those too, and nothing but the inputs is kept)."""
 
         @staticmethod
-        def forward(ctx, x, a, b, c, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False):
+        def forward(ctx, x, a, b, c, block, residual=False, sigmoid_decay=False, sigmoid_pregate=False,
+                    save_carriers=True):
             ctx.block, ctx.residual = block, residual
             ctx.feat = dict(sigmoid_decay=sigmoid_decay, sigmoid_pregate=sigmoid_pregate)
-            y, v = swr_forward(x, a, b, c, block, residual, save_carriers=True, **ctx.feat)
-            ctx.save_for_backward(x, a, b, c, v)     # the carriers are the only extra state
+            if save_carriers:
+                y, v = swr_forward(x, a, b, c, block, residual, save_carriers=True, **ctx.feat)
+            else:
+                y, v = swr_forward(x, a, b, c, block, residual, **ctx.feat), None
+            ctx.has_v = v is not None
+            # the carriers are the only extra state
+            ctx.save_for_backward(x, a, b, c, *((v,) if ctx.has_v else ()))
             return y
 
         @staticmethod
         def backward(ctx, dy):
-            x, a, b, c, v = ctx.saved_tensors
+            x, a, b, c, *rest = ctx.saved_tensors
+            v = rest[0] if ctx.has_v else None
             dy = dy if dy.stride() == x.stride() else torch.empty_strided(
                 x.shape, x.stride(), dtype=x.dtype, device=x.device).copy_(dy)
             dx, da, db, dc = swr_backward(x, a, b, c, dy, v, ctx.block, ctx.residual, **ctx.feat)
-            return dx, da.to(a.dtype), db, dc, None, None, None, None
+            return dx, da.to(a.dtype), db, dc, None, None, None, None, None
 
     class _SWRUniformFunction(torch.autograd.Function):
         """Autograd wrapper of the uniform window (nothing saved but the inputs)."""

@@ -339,17 +339,18 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     int rc = resolve_for(p, &r, {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc});
     if (rc != SWR_OK) return rc;
     if (r.empty) return SWR_OK;
-    if (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc) return SWR_ERR_NULL;
+    // (carriers may be NULL: the kernels then recompute them)
+    if (!x || !a || !b || !c || !dy || !dx || !da || !db || !dc) return SWR_ERR_NULL;
     for (const void* q : {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc})
         if (!aligned(q, r.vbytes)) return SWR_ERR_ALIGN;
     const int64_t va = r.pc ? r.vbytes : r.es;
     const int64_t vda = r.pc ? std::min<int64_t>(16, (int64_t)(r.dk / 16) * 4) : 4;
-    if (!aligned(a, va) || !aligned(da, vda) || !aligned(carriers, 16)) return SWR_ERR_ALIGN;
+    if (!aligned(a, va) || !aligned(da, vda) || (carriers && !aligned(carriers, 16))) return SWR_ERR_ALIGN;
     if ((rc = check_strides_aligned(p, r)) != SWR_OK) return rc;
     const Span outs[4] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan),
                           span(da, r.aspan * 4)};
     const Span ins[6] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(dy, r.xspan),
-                         span(a, r.aspan * r.es), span(carriers, r.carriers * 4)};
+                         span(a, r.aspan * r.es), span(carriers, carriers ? r.carriers * 4 : 0)};
     for (int i = 0; i < 4; ++i) {
         for (const Span& s : ins)
             if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
@@ -361,8 +362,8 @@ int swr_backward(const swr_problem_t* p, const void* x, const void* a, const voi
     k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
     k.dx = dx; k.da = da; k.db = db; k.dc = dc;
     k.carriers = const_cast<float*>(carriers);
-    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, swr::kSwr, stream) == hipSuccess
-               ? SWR_OK : SWR_ERR_HIP;
+    return swr::launch(k, p->dtype, r.dk, r.bwd, true, r.pc, r.pack, carriers ? swr::kSwr : swr::kRecompute,
+                       stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
 }
 
 }  // extern "C"

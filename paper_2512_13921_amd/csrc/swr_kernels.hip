@@ -276,11 +276,14 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             const int src = hw * TW + r;
             const float cr_ = s_c[buf][src * NH + hsel];
             if constexpr (MODE == kAggregate) prod *= cr_;
+            // One fused multiply-add per carrier step, so that the backward's
+            // recomputation of a block's carrier (mode kRecompute) rounds exactly
+            // as this walk does.
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 const float wl = s_wl[buf][src][n * CPL + m];
-                e[m] = cr_ * e[m] + wl;
-                if constexpr (SWR) s[m] = cr_ * s[m] + wl;
+                e[m] = __builtin_fmaf(cr_, e[m], wl);
+                if constexpr (SWR) s[m] = __builtin_fmaf(cr_, s[m], wl);
             }
             if (r == tw) {
 #pragma unroll
@@ -353,10 +356,17 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
 // MODE kGrouped: the jagged window with b and c shared by groups of heads;
 // this head's shares of db and dc go to the float32 workspace p.gws, summed
 // over each group afterwards (swr_gate_reduce_kernel).
+//
+// MODE kRecompute: the jagged window without saved carriers.  The carrier of
+// the block before each step is recomputed during the step from that
+// block's x, b and a (the rows the next step processes): the same local
+// solves and the same walk over its sub-blocks as in the forward, so the
+// result equals the saved carrier bit for bit.
 template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     constexpr bool GG = MODE == kGrouped;
-    constexpr bool SWR = MODE == kSwr || GG;
+    constexpr bool VREC = MODE == kRecompute;
+    constexpr bool SWR = MODE == kSwr || GG || VREC;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -366,6 +376,9 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve L u
     __shared__ float s_df[2][NW][D];    // a_0 * first row of each sub-block's L^T dh
     __shared__ float s_c[2][NW];        // decay product of each sub-block
+    // kRecompute: the same two for the sub-blocks of the step before
+    __shared__ float s_wlp[VREC ? 2 : 1][VREC ? NW : 1][VREC ? D : 1];
+    __shared__ float s_cp[VREC ? 2 : 1][VREC ? NW : 1];
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
@@ -460,8 +473,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 const float df = s_df[buf][src][n * CPL + m];
-                eps[m] = c_ * eps[m] + df;
-                pr[m] = c_ * pr[m] + df;
+                eps[m] = __builtin_fmaf(c_, eps[m], df);
+                pr[m] = __builtin_fmaf(c_, pr[m], df);
             }
         }
         buf ^= 1;
@@ -498,14 +511,47 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         in.a = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(live && r0 + n < wk.t_end, aoff));
         // Carrier of the block before the step (zero before the sequence
         // start, or the initial state for the exact recurrence).
-        const bool from_h0 = MODE == kExact && t0 == 0;
-        const int64_t blk = (t0 >> p.lshift) - 1;
-        Row<IoF32, CPL> vr;
-        vr.load(rsrc(from_h0 ? (const void*)(p.h0 + seq * D) : (const void*)vb),
-                from_h0 ? in_range(live && p.h0 != nullptr, (uint32_t)(n * CPL) * 4u)
-                        : in_range(live && t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+        if constexpr (!VREC) {
+            const bool from_h0 = MODE == kExact && t0 == 0;
+            const int64_t blk = (t0 >> p.lshift) - 1;
+            Row<IoF32, CPL> vr;
+            vr.load(rsrc(from_h0 ? (const void*)(p.h0 + seq * D) : (const void*)vb),
+                    from_h0 ? in_range(live && p.h0 != nullptr, (uint32_t)(n * CPL) * 4u)
+                            : in_range(live && t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+            for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+        }
+    };
+
+    // kRecompute: the local solves of the step before the one starting at t0
+    // (rows of its last block only; none before the sequence), whose last
+    // rows and decay products go to LDS for the walk that yields the carrier
+    // of the block before t0.  As in the forward sweep.
+    auto prev_solve = [&](int64_t t0, int pb) {
+        const int64_t r0 = t0 - STEP + tw * SB, tr0 = r0 + 4 * grp;
+        const int64_t t_pl = max(t0 - (int64_t)l, (int64_t)0);   // first row needed
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * gs);
+        R_ xr[4], br[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const bool ok = tr0 + r >= t_pl;   // (every row lies before t0)
+            xr[r].template load<kBwdLoad>(rx, in_range(ok, loff + (uint32_t)(r * rs)));
+            br[r].template load<kBwdLoad>(rb, in_range(ok, goff + (uint32_t)(r * gs)));
+        }
+        const bool a_ok = r0 + n >= t_pl;
+        float a_n = load_scalar<IO, kBwdDecay>(rsrc(ab + r0 * as), in_range(a_ok, aoff));
+        if (sig_a) a_n = a_ok ? sigmoid(a_n) : 0.0f;
+        const Decay dk = build_decay(a_n, grp, n);
+        const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            float u[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
+            const f32x4 W = Contract<IO>::run(A, u);
+            if (grp == 3) s_wlp[pb][wv][n * CPL + m] = W[3];
+        }
+        if (lane == 63) s_cp[pb][wv] = dk.c;
     };
 
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
@@ -517,6 +563,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         const int64_t tr0 = r0 + 4 * grp;
 
         // ---- loads ---------------------------------------------------------------
+        // (kRecompute: the step before is solved first, while few registers are live)
+        if constexpr (VREC) prev_solve(t0, buf);
         if constexpr (!PF) fetch_step(k, true, nxt);
         const StepIn in = nxt;
         if constexpr (PF) fetch_step(max(k - 1, (int64_t)0), k > 0, nxt);
@@ -538,7 +586,6 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         // Exact recurrence: past the end of the sequence the decay is 1, so
         // the adjoint entering from the end reaches the last token intact.
         if (MODE == kExact && r0 + n >= p.T) a_n = 1.0f;
-        const float* const vprev = in.v;
 
         // ---- local solves: W = L (b*x) and Dl = L^T (c*dy) ---------------------------
         const Decay dk = build_decay(a_n, grp, n);
@@ -574,6 +621,23 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 
         // ---- forward carriers entering this wave's sub-block ---------------------------
         float ein[CPL], sin_[CPL];
+        float vrec[CPL];   // kRecompute: the carrier of the block before the step
+        if constexpr (VREC) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) vrec[m] = 0.f;
+#pragma unroll 1
+            for (int r = 0; r < TW; ++r) {   // the step before starts a block
+                if ((r & smask) == 0) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) vrec[m] = 0.f;
+                }
+                const int src = hw * TW + r;
+                const float c_ = s_cp[buf][src];
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) vrec[m] = __builtin_fmaf(c_, vrec[m], s_wlp[buf][src][n * CPL + m]);
+            }
+        }
+        const float* const vprev = VREC ? vrec : in.v;
         {
             // Exact: e is the exact state (never restarted) and s is unused.
             float e[CPL], s[CPL];
@@ -590,8 +654,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     const float wl = s_wl[buf][src][n * CPL + m];
-                    e[m] = c_ * e[m] + wl;
-                    if constexpr (SWR) s[m] = c_ * s[m] + wl;
+                    e[m] = __builtin_fmaf(c_, e[m], wl);
+                    if constexpr (SWR) s[m] = __builtin_fmaf(c_, s[m], wl);
                 }
             }
             if (SWR && (tw & smask) == 0) {
@@ -614,7 +678,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
                     epsin[m] = eps[m];
-                    if constexpr (SWR) kd += (ein[m] - sin_[m]) * (eps[m] - pr[m]);
+                    if constexpr (SWR) kd = __builtin_fmaf(ein[m] - sin_[m], eps[m] - pr[m], kd);
                 }
             }
             const int src = hw * TW + r;
@@ -622,8 +686,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
                 const float df = s_df[buf][src][n * CPL + m];
-                eps[m] = c_ * eps[m] + df;
-                if constexpr (SWR) pr[m] = c_ * pr[m] + df;
+                eps[m] = __builtin_fmaf(c_, eps[m], df);
+                if constexpr (SWR) pr[m] = __builtin_fmaf(c_, pr[m], df);
             }
         }
 
@@ -632,7 +696,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
 #pragma unroll
         for (int m = 0; m < CPL; ++m)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) W[m][r] += dk.G[r] * ein[m];
+            for (int r = 0; r < 4; ++r) W[m][r] = __builtin_fmaf(dk.G[r], ein[m], W[m][r]);
         float hup[CPL];   // state entering this lane's first row
 #pragma unroll
         for (int m = 0; m < CPL; ++m) {
@@ -658,13 +722,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float dyv = dyr[r].get(m);
                 vdc[m] = dyv * W[m][r];
-                const float du = Dl[m][r] + Rr[r] * epsin[m];          // adjoint of u
+                const float du = __builtin_fmaf(Rr[r], epsin[m], Dl[m][r]);   // adjoint of u
                 const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
                 const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
                 vdx[m] = g.s * du;
                 if (p.residual) vdx[m] += dyv;
                 vdb[m] = xr[r].get(m) * du * g.ds;
-                acc += (r == 0 ? hup[m] : W[m][r - 1]) * du;
+                acc = __builtin_fmaf(r == 0 ? hup[m] : W[m][r - 1], du, acc);
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
@@ -1040,6 +1104,9 @@ __global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
 // k = 4*grp + r.  A state is carried through a stretch of tokens by
 // s -> G s + w, so stretches compose as (G1, w1) then (G2, w2) =
 // (G1 G2, G2 w1 + w2).
+// Every multiply-add is one explicit fused operation, so that the same scan
+// rounds identically in every kernel it is inlined into (the backward's
+// recomputation of a block carrier matches the forward's bit for bit).
 template <int CPL>
 __device__ inline void chan_scan_fwd(const float (&a)[4][CPL], const float (&u)[4][CPL],
                                      float (&w)[4][CPL], float (&G)[4][CPL], int grp, int lane) {
@@ -1050,20 +1117,20 @@ __device__ inline void chan_scan_fwd(const float (&a)[4][CPL], const float (&u)[
 #pragma unroll
         for (int r = 1; r < 4; ++r) {
             G[r][m] = a[r][m] * G[r - 1][m];
-            w[r][m] = a[r][m] * w[r - 1][m] + u[r][m];
+            w[r][m] = __builtin_fmaf(a[r][m], w[r - 1][m], u[r][m]);
         }
         // Inclusive scan of the row totals over rows 0..grp.
         float tg = G[3][m], tw = w[3][m];
         float pg = shfl(tg, (lane - 16) & 63), pw = shfl(tw, (lane - 16) & 63);
-        if (grp >= 1) { tw = tg * pw + tw; tg = pg * tg; }
+        if (grp >= 1) { tw = __builtin_fmaf(tg, pw, tw); tg = pg * tg; }
         pg = shfl(tg, (lane - 32) & 63); pw = shfl(tw, (lane - 32) & 63);
-        if (grp >= 2) { tw = tg * pw + tw; tg = pg * tg; }
+        if (grp >= 2) { tw = __builtin_fmaf(tg, pw, tw); tg = pg * tg; }
         // Exclusive: the stretch from the sub-block start to this row.
         pg = shfl(tg, (lane - 16) & 63); pw = shfl(tw, (lane - 16) & 63);
         const float gin = grp >= 1 ? pg : 1.0f, win = grp >= 1 ? pw : 0.0f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            w[r][m] += G[r][m] * win;
+            w[r][m] = __builtin_fmaf(G[r][m], win, w[r][m]);
             G[r][m] *= gin;
         }
     }
@@ -1285,8 +1352,8 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float c_ = s_cc[buf][src][n * CPL + m];
                 const float wl = s_wl[buf][src][n * CPL + m];
-                e[m] = c_ * e[m] + wl;
-                if constexpr (SWR) s[m] = c_ * s[m] + wl;
+                e[m] = __builtin_fmaf(c_, e[m], wl);
+                if constexpr (SWR) s[m] = __builtin_fmaf(c_, s[m], wl);
                 if constexpr (MODE == kAggregate) prod[m] *= c_;
             }
             if (r == tw) {
@@ -1327,9 +1394,11 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
 //     da_{k,mu} = H_{k-1,mu} du_{k,mu} - g_{k-1,mu} r_{k,mu} (e - s)_mu (eps - p)_mu,
 // and is stored per channel (no sum over the head's channels).
 // MODE kExact: the gradient of the exact recurrence, as in swr_bwd_kernel.
+// MODE kRecompute: without saved carriers, as in swr_bwd_kernel.
 template <class IO, int CPL, int TW, int HW, bool FEAT, int MODE, int PK>
 __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
-    constexpr bool SWR = MODE == kSwr;
+    constexpr bool VREC = MODE == kRecompute;
+    constexpr bool SWR = MODE == kSwr || VREC;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;   // fused featurisation
     constexpr int NW = TW * HW;
     constexpr int D = CPL * SB;
@@ -1339,6 +1408,9 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     __shared__ float s_wl[2][NW][D];    // last row of each sub-block's local solve L u
     __shared__ float s_df[2][NW][D];    // E_0 = a_0 D_0 of each sub-block's L^T dh
     __shared__ float s_cc[2][NW][D];    // decay product of each sub-block, per channel
+    // kRecompute: the same two for the sub-blocks of the step before
+    __shared__ float s_wlp[VREC ? 2 : 1][VREC ? NW : 1][VREC ? D : 1];
+    __shared__ float s_ccp[VREC ? 2 : 1][VREC ? NW : 1][VREC ? D : 1];
 
     const Lanes ln = lanes();
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
@@ -1430,8 +1502,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float c_ = s_cc[buf][src][n * CPL + m];
                 const float df = s_df[buf][src][n * CPL + m];
-                eps[m] = c_ * eps[m] + df;
-                pr[m] = c_ * pr[m] + df;
+                eps[m] = __builtin_fmaf(c_, eps[m], df);
+                pr[m] = __builtin_fmaf(c_, pr[m], df);
             }
         }
         buf ^= 1;
@@ -1463,14 +1535,53 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             if constexpr (PK == 1) in.a[r].template load<kBwdLoad>(ra, o);
         }
         // the carrier: the initial state for the exact recurrence's first block
-        const bool from_h0 = MODE == kExact && t0 == 0;
-        const int64_t blk = (t0 >> p.lshift) - 1;
-        Row<IoF32, CPL> vr;
-        vr.load(rsrc(from_h0 ? p.h0 + hb * geo.Dr : vb),
-                from_h0 ? in_range(live && p.h0 != nullptr, geo.off(1, 0) * 4u)
-                        : in_range(live && t0 > 0, geo.off(p.nblocks, blk) * 4u));
+        if constexpr (!VREC) {
+            const bool from_h0 = MODE == kExact && t0 == 0;
+            const int64_t blk = (t0 >> p.lshift) - 1;
+            Row<IoF32, CPL> vr;
+            vr.load(rsrc(from_h0 ? p.h0 + hb * geo.Dr : vb),
+                    from_h0 ? in_range(live && p.h0 != nullptr, geo.off(1, 0) * 4u)
+                            : in_range(live && t0 > 0, geo.off(p.nblocks, blk) * 4u));
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+            for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
+        }
+    };
+
+    // kRecompute: the local solves of the step before the one starting at t0
+    // (rows of its last block only; none before the sequence), whose last
+    // rows and decay products go to LDS for the walk that yields the carrier
+    // of the block before t0.  As in the forward sweep.
+    auto prev_solve = [&](int64_t t0, int pb) {
+        const int64_t r0 = t0 - STEP + tw * SB, tr0 = r0 + 4 * grp;
+        const int64_t t_pl = max(t0 - (int64_t)l, (int64_t)0);   // first row needed
+        const __amdgpu_buffer_rsrc_t rx = rsrc(xb + r0 * rs), rb = rsrc(bb + r0 * rs), ra = rsrc(ab + r0 * as);
+        R_ xr[4], br[4], ar[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t o = in_range(tr0 + r >= t_pl, loff + (uint32_t)(r * rs));   // (all before t0)
+            xr[r].template load<kBwdLoad>(rx, o);
+            br[r].template load<kBwdLoad>(rb, o);
+            if constexpr (PK == 1) ar[r].template load<kBwdLoad>(ra, o);
+        }
+        float av[4][CPL], u[4][CPL], W[4][CPL], G[4][CPL];
+        if constexpr (PK > 1) {
+            float az[4];
+            decay_rows_packed<IO, CPL, kBwdDecay>(ra, aoffp, (uint32_t)as, tr0, t_pl, t0, p.T, sig_a, az, av);
+        } else {
+            decay_rows<IO, CPL>(ar, tr0, t_pl, t0, p.T, sig_a, av);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * pregate(br[r].get(m), sig_b);
+        chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_wlp[pb][wv][n * CPL + m] = W[3][m];
+                s_ccp[pb][wv][n * CPL + m] = G[3][m];
+            }
+        }
     };
 
     const int64_t nsteps = (wk.t_end - wk.t_begin + STEP - 1) / STEP;
@@ -1498,7 +1609,6 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
         for (int r = 0; r < 4; ++r)
 #pragma unroll
             for (int m = 0; m < CPL; ++m) dh[r][m] = dyr[r].get(m) * in.c[r].get(m);
-        const float* const vprev = in.v;
 
         // ---- local solves: W = L (b*x), G; Dv = L^T (c*dy), Rr -------------------------
         float W[4][CPL], G[4][CPL], Dv[4][CPL], Rr[4][CPL];
@@ -1522,7 +1632,25 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) s_df[buf][wv][n * CPL + m] = av[0][m] * Dv[0][m];
         }
+        if constexpr (VREC) prev_solve(t0, buf);
         __syncthreads();
+        float vrec[CPL];   // kRecompute: the carrier of the block before the step
+        if constexpr (VREC) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) vrec[m] = 0.f;
+#pragma unroll 1
+            for (int r = 0; r < TW; ++r) {   // the step before starts a block
+                if ((r & smask) == 0) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) vrec[m] = 0.f;
+                }
+                const int src = hw * TW + r;
+#pragma unroll
+                for (int m = 0; m < CPL; ++m)
+                    vrec[m] = __builtin_fmaf(s_ccp[buf][src][n * CPL + m], vrec[m], s_wlp[buf][src][n * CPL + m]);
+            }
+        }
+        const float* const vprev = VREC ? vrec : in.v;
 
         // ---- forward carriers entering this wave's sub-block ---------------------------
         float ein[CPL], sin_[CPL];
@@ -1541,8 +1669,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 for (int m = 0; m < CPL; ++m) {
                     const float c_ = s_cc[buf][src][n * CPL + m];
                     const float wl = s_wl[buf][src][n * CPL + m];
-                    e[m] = c_ * e[m] + wl;
-                    if constexpr (SWR) s[m] = c_ * s[m] + wl;
+                    e[m] = __builtin_fmaf(c_, e[m], wl);
+                    if constexpr (SWR) s[m] = __builtin_fmaf(c_, s[m], wl);
                 }
             }
             if (SWR && (tw & smask) == 0) {
@@ -1573,8 +1701,8 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float c_ = s_cc[buf][src][n * CPL + m];
                 const float df = s_df[buf][src][n * CPL + m];
-                eps[m] = c_ * eps[m] + df;
-                if constexpr (SWR) pr[m] = c_ * pr[m] + df;
+                eps[m] = __builtin_fmaf(c_, eps[m], df);
+                if constexpr (SWR) pr[m] = __builtin_fmaf(c_, pr[m], df);
             }
         }
 
@@ -1587,7 +1715,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
 #pragma unroll
             for (int r = 1; r < 4; ++r) Gsh[r][m] = G[r - 1][m];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) W[r][m] += G[r][m] * ein[m];   // H: the jagged-window state
+            for (int r = 0; r < 4; ++r) W[r][m] = __builtin_fmaf(G[r][m], ein[m], W[r][m]);   // H: the jagged-window state
             const float hv = shfl(W[3][m], (lane - 16) & 63);
             hup[m] = grp == 0 ? ein[m] : hv;
         }
@@ -1601,13 +1729,13 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) {
                 const float dyv = dyr[r].get(m);
                 vdc[m] = dyv * W[r][m];
-                const float du = Dv[r][m] + Rr[r][m] * epsin[m];
+                const float du = __builtin_fmaf(Rr[r][m], epsin[m], Dv[r][m]);
                 const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
                 const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
                 vdx[m] = g.s * du;
                 if (p.residual) vdx[m] += dyv;
                 vdb[m] = xr[r].get(m) * du * g.ds;
-                vda[m] = (r == 0 ? hup[m] : W[r - 1][m]) * du - Gsh[r][m] * Rr[r][m] * kd[m];
+                vda[m] = __builtin_fmaf(r == 0 ? hup[m] : W[r - 1][m], du, -(Gsh[r][m] * Rr[r][m] * kd[m]));
                 if (PK == 1 && sig_a) vda[m] *= sigmoid_slope(ar[r].get(m)).ds;
             }
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
@@ -1735,7 +1863,7 @@ static hipError_t launch_pc(const Params& p, const Shape& sh, bool backward, hip
             SWR_LAUNCH((swr_bwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE, PK>), 4, 1)
             else return hipErrorInvalidValue;
         }
-    } else {
+    } else if constexpr (MODE != kRecompute) {   // (a backward-only mode)
         if (false) {}
         SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 4, 1, FEAT, MODE, PK>), 4, 1)
         SWR_LAUNCH((swr_fwd_pc_kernel<IO, CPL, 2, 2, FEAT, MODE, PK>), 2, 2)
@@ -1751,6 +1879,9 @@ static hipError_t launch_pc_mode(const Params& p, const Shape& sh, bool backward
         case kSwr: return launch_pc<IO, CPL, FEAT, kSwr, PK>(p, sh, backward, stream);
         case kAggregate: return launch_pc<IO, CPL, FEAT, kAggregate, PK>(p, sh, backward, stream);
         case kExact: return launch_pc<IO, CPL, FEAT, kExact, PK>(p, sh, backward, stream);
+        case kRecompute:
+            if (!backward) return hipErrorInvalidValue;
+            return launch_pc<IO, CPL, FEAT, kRecompute, PK>(p, sh, backward, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1759,6 +1890,9 @@ template <class IO, int CPL, bool FEAT, int MODE>
 static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, hipStream_t stream) {
     if constexpr (MODE == kPaired) {   // a forward-only mode
         if (backward) return hipErrorInvalidValue;
+    }
+    if constexpr (MODE == kRecompute) {
+        if (!backward) return hipErrorInvalidValue;
     }
     const dim3 grid((unsigned)p.nwork);
 #define SWR_LAUNCH(KERNEL, TW_, HW_)                                                                \
@@ -1776,7 +1910,7 @@ static hipError_t launch_shape(const Params& p, const Shape& sh, bool backward, 
             SWR_LAUNCH((swr_bwd_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
             else return hipErrorInvalidValue;
         }
-    } else {
+    } else if constexpr (MODE != kRecompute) {   // (a backward-only mode)
         if (false) {}
         SWR_LAUNCH((swr_fwd_kernel<IO, CPL, 4, 1, FEAT, MODE>), 4, 1)
         SWR_LAUNCH((swr_fwd_kernel<IO, CPL, 2, 2, FEAT, MODE>), 2, 2)
@@ -1793,6 +1927,7 @@ static hipError_t launch_mode(const Params& p, const Shape& sh, bool backward, i
         case kAggregate: return launch_shape<IO, CPL, FEAT, kAggregate>(p, sh, backward, stream);
         case kExact: return launch_shape<IO, CPL, FEAT, kExact>(p, sh, backward, stream);
         case kGrouped: return launch_shape<IO, CPL, FEAT, kGrouped>(p, sh, backward, stream);
+        case kRecompute: return launch_shape<IO, CPL, FEAT, kRecompute>(p, sh, backward, stream);
         case kPaired:
             if constexpr (CPL == 8 && IO::ES == 2) return launch_shape<IO, CPL, FEAT, kPaired>(p, sh, backward, stream);
             return hipErrorInvalidValue;

@@ -21,7 +21,7 @@ struct Params {
     void* db;
     void* dc;
     float* carriers;    // [B][H][nblocks][D] float32 block carriers v_t (forward: optional output;
-                        // backward: input)
+                        // backward: input, unused by mode kRecompute)
     int64_t B, T, H;
     int64_t Hv;         // heads the work is split over: H, or H << hshift virtual heads
     int64_t sx_b, sx_t, sx_h;
@@ -65,6 +65,8 @@ enum Mode {
     kGrouped = 3,    // the jagged window with b and c shared by groups of heads
     kPaired = 4,     // the jagged window's forward, two heads of D/2 channels per kernel
                      // head (lanes 0-7 of a 16-lane row hold the first, 8-15 the second)
+    kRecompute = 5,  // the jagged window's backward without saved block carriers: each step
+                     // recomputes the carrier of the block before it from that block's x, b, a
 };
 
 // Sums the per-head float32 shares of db and dc that a kGrouped backward left

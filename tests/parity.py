@@ -62,8 +62,9 @@ def assert_close(got, ref, dtype, what=""):
     return st
 
 
-def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd", **feat):
-    """Forward (saving the block carriers) and backward through the library."""
+def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd", carriers=True, **feat):
+    """Forward (saving the block carriers) and backward through the library
+    (carriers=False: the backward is called without them and recomputes them)."""
     import torch
     cfg = prob.cfg
     dt = cfg.dtype
@@ -80,7 +81,7 @@ def run_gpu(swr, prob, residual=False, run_len=0, backward=True, layout="bthd", 
             dy = bhtd(dy)
     y, v = swr.swr_forward(x, a, b, c, cfg.block, residual=residual, run_len=run_len,
                            save_carriers=True, **feat)
-    grads = swr.swr_backward(x, a, b, c, dy, v, cfg.block, residual=residual,
+    grads = swr.swr_backward(x, a, b, c, dy, v if carriers else None, cfg.block, residual=residual,
                              run_len=run_len, **feat) if backward else None
     torch.cuda.synchronize()
     return y, grads
