@@ -75,8 +75,10 @@ typedef enum swr_status {
     SWR_ERR_BLOCK = -4,       /* block is not 16, 32, 64 or 128                           */
     SWR_ERR_ALIGN = -5,       /* a pointer or stride breaks the vector alignment          */
     SWR_ERR_ALIAS = -6,       /* an output overlaps an input or another output            */
-    SWR_ERR_UNSUPPORTED = -7, /* D not in {16, 32, 64, 128}, unknown flags, bad run_len,
-                                 or strides/sizes beyond the kernels' 32-bit offsets       */
+    SWR_ERR_UNSUPPORTED = -7, /* D not a multiple of 16 up to 256 (not in {16, 32, 64,
+                                 128} outside swr_forward / swr_carriers / swr_backward),
+                                 unknown flags, bad run_len, or strides/sizes beyond the
+                                 kernels' 32-bit offsets                                  */
     SWR_ERR_HIP = -8,         /* the HIP runtime rejected the launch                      */
     SWR_ERR_VERSION = -9,     /* problem->abi_version != SWR_ABI_VERSION                  */
     SWR_ERR_SCRATCH = -10     /* swr_exact_forward_noalloc: the problem needs more than
@@ -116,7 +118,8 @@ typedef enum swr_dtype {
 typedef struct swr_problem {
     int32_t abi_version;   /* must be SWR_ABI_VERSION                                     */
     int32_t dtype;         /* swr_dtype_t of every tensor except da                       */
-    int64_t B, T, H, D;    /* batch, tokens, heads, channels per head; B, T or H may be 0 */
+    int64_t B, T, H, D;    /* batch, tokens, heads, channels per head; B, T or H may be 0;
+                              D a multiple of 16 up to 256 (see "Head width")             */
     int64_t block;         /* l, the block (= window unit) length: 16, 32, 64 or 128       */
     uint32_t flags;        /* SWR_FLAG_* bits                                              */
     int32_t reserved;      /* must be 0                                                    */
@@ -129,9 +132,21 @@ typedef struct swr_problem {
                               change results beyond float32 rounding order              */
 } swr_problem_t;
 
-/* Forward: y = SWR(x, a, b, c).  Alignment: x, b, c, y and every sx_* must be
- * multiples of min(16 bytes, D/16 elements) (i.e. each lane's slice of a row is
- * a naturally aligned vector); a needs the alignment of one element.
+/* Head width.  The kernels process heads of W = 16, 32, 64 or 128 channels
+ * (a lane holds W/16 channels of a token row).  swr_forward, swr_carriers and
+ * swr_backward take any D that is a multiple of 16 up to 256 (the paper's
+ * heads are d = D_model / h, Sec. 5): a head wider than 128 channels (64 with
+ * SWR_FLAG_PER_CHANNEL_DECAY) runs as 2 (or 4) virtual heads of D/2 (D/4)
+ * channels, and a (virtual) head narrower than the next of the widths W
+ * leaves the lanes past its channels idle.  With one decay per head, the
+ * decay gradient of a head split in two is the sum of the halves' shares,
+ * added onto a zeroed da by two float32 atomic adds (the same sum in either
+ * order).  Every other entry point takes D in {16, 32, 64, 128}.
+ *
+ * Forward: y = SWR(x, a, b, c).  Alignment: x, b, c, y and every sx_* must be
+ * multiples of min(16 bytes, W/16 elements), W the kernel width above (each
+ * lane's slice of a row is a naturally aligned vector; W = D for D in {16,
+ * 32, 64, 128}); a needs the alignment of one element.
  * carriers: NULL, or swr_carrier_elems(problem) float32 values (16-byte
  * aligned) that receive the block carriers for swr_backward. */
 int swr_forward(const swr_problem_t* problem, const void* x, const void* a, const void* b,

@@ -4,6 +4,7 @@ Usage: ``python -m paper_2512_13921_amd.build`` (or ``python paper_2512_13921_am
 Cross-compiles on a machine without a GPU.
 """
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -33,8 +34,30 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
          "-Wall", "-Wno-unused-function"]
 
 
+# Kernels that must compile without register spills: the forward sweeps copy
+# their next tiles straight into LDS, and a forward instantiation that spilled
+# was once measured writing wrong outputs; the build refuses any such spill.
+NO_SPILL = ("swr_fwd_kernel",)
+RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
+
+
 def compile_command(src: str, obj: str, extra=()) -> list:
-    return [hipcc(), *FLAGS, *extra, "-c", src, "-o", obj]
+    remarks = [RESOURCE_REMARKS] if os.path.basename(src) == "swr_kernels.hip" else []
+    return [hipcc(), *FLAGS, *remarks, *extra, "-c", src, "-o", obj]
+
+
+def spilled_kernels(text: str) -> list:
+    """Mangled names of NO_SPILL kernels whose resource remarks report scratch."""
+    bad, name = [], None
+    for line in text.splitlines():
+        if "Function Name: " in line:
+            name = line.split("Function Name: ", 1)[1].split()[0]
+        elif name and "ScratchSize [bytes/lane]: " in line:
+            size = int(line.split("ScratchSize [bytes/lane]: ", 1)[1].split()[0])
+            if size > 0 and any(k in name for k in NO_SPILL):
+                bad.append(f"{name} ({size} bytes/lane)")
+            name = None
+    return bad
 
 
 def link_command(objs, out: str) -> list:
@@ -42,9 +65,12 @@ def link_command(objs, out: str) -> list:
 
 
 def _messages(res) -> list:
-    # hipcc's host pass warns that it does not know the packed-fp32 feature
-    noise = "is not a recognized feature for this target"
-    return [ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln]
+    # hipcc's host pass warns that it does not know the packed-fp32 feature;
+    # the resource remarks are read by spilled_kernels, not shown
+    noise = ("is not a recognized feature for this target", "remark: ", "-Rpass-analysis")
+    quoted = re.compile(r"^\s*\d*\s*\|")   # the source lines a remark quotes
+    return [ln for ln in (res.stdout + res.stderr).splitlines()
+            if not any(n in ln for n in noise) and not quoted.match(ln)]
 
 
 def build(verbose: bool = False, extra=(), out: str = LIB) -> str:
@@ -66,6 +92,9 @@ def build(verbose: bool = False, extra=(), out: str = LIB) -> str:
                 failed.append("\n".join(msgs))
             elif verbose and msgs:
                 print("\n".join(msgs))
+            spills = spilled_kernels(res.stdout + res.stderr)
+            if spills:
+                failed.append("kernels that must not spill registers do:\n  " + "\n  ".join(spills))
         if failed:
             raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
         cmd = link_command(objs, out + ".tmp")

@@ -13,6 +13,10 @@
 namespace {
 
 constexpr int64_t kMaxWorkgroups = 0x7fffffffLL;
+// Widest head: two virtual heads of 128 channels (one decay per head; their
+// decay-gradient shares meet in two float32 atomic adds, which give the same
+// sum in either order) or four of 64 (per-channel decay).
+constexpr int64_t kMaxD = 256;
 constexpr int64_t kMaxExtent = (int64_t)1 << 62;
 // Default grid sizes, measured on the MI355X (256 compute units) over the
 // benchmark workloads: the forward runs best with two 4-wave workgroups per
@@ -70,7 +74,12 @@ struct Resolved {
     int hshift;         // per-channel kernels: log2 of the virtual heads per head
     int pack;           // > 1: heads of 64 / pack channels packed into 64-channel virtual heads
     bool pair;          // forward: bf16 heads of 64 channels run two per kernel head (16-byte lane slices)
-    int dk;             // channels a kernel's head covers (D, or D >> hshift)
+    int dk;             // channels a kernel's head covers (16, 32, 64 or 128)
+    int dv;             // channels of a virtual head (D >> hshift), at most dk
+    int nlane;          // lanes of a 16-lane row holding channels (dv / cpl)
+    bool natural;       // D is 16, 32, 64 or 128, the widths every entry point accepts (the
+                        // jagged window's forward, carriers and backward take any multiple of
+                        // 16 up to kMaxD)
     int64_t hv;         // heads the kernels split the work over (H << hshift)
     int64_t vbytes;     // bytes of one lane's slice of an x-like row (alignment unit)
     swr::Shape bwd;     // backward workgroup shape
@@ -90,7 +99,7 @@ int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true, bool al
     if (p->dtype != SWR_DTYPE_F32 && p->dtype != SWR_DTYPE_BF16) return SWR_ERR_DTYPE;
     if (p->B < 0 || p->T < 0 || p->H < 0 || p->D < 1) return SWR_ERR_SHAPE;
     if (p->block != 16 && p->block != 32 && p->block != 64 && p->block != 128) return SWR_ERR_BLOCK;
-    if (p->D != 16 && p->D != 32 && p->D != 64 && p->D != 128) return SWR_ERR_UNSUPPORTED;
+    if (p->D % 16 != 0 || p->D > kMaxD) return SWR_ERR_UNSUPPORTED;
     const uint32_t known = SWR_FLAG_RESIDUAL | SWR_FLAG_PER_CHANNEL_DECAY | SWR_FLAG_SIGMOID_DECAY |
                            SWR_FLAG_SIGMOID_PREGATE;
     if ((p->flags & ~known) != 0 || p->reserved != 0)
@@ -98,8 +107,13 @@ int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true, bool al
 
     r->es = p->dtype == SWR_DTYPE_BF16 ? 2 : 4;
     r->pc = (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) != 0;
-    r->hshift = r->pc ? swr::pc_hshift(p->D) : 0;
-    r->dk = (int)(p->D >> r->hshift);
+    // A head wider than one kernel head is split into 2^hshift virtual heads
+    // of dv channels; a virtual head narrower than the kernel's width dk (a
+    // power of two) leaves the lanes past nlane idle.
+    r->hshift = r->pc ? swr::pc_hshift(p->D) : swr::head_hshift(p->D);
+    r->dv = (int)(p->D >> r->hshift);
+    r->dk = r->dv <= 16 ? 16 : r->dv <= 32 ? 32 : r->dv <= 64 ? 64 : 128;
+    r->natural = p->D == 16 || p->D == 32 || p->D == 64 || p->D == 128;
     r->pack = 1;
     // Heads of 16 or 32 channels stored next to each other run as packed
     // 64-channel virtual heads on the per-channel kernels (a lane slice of one
@@ -125,6 +139,7 @@ int resolve(const swr_problem_t* p, Resolved* r, bool allow_pack = true, bool al
               (p->T + p->block - 1) / p->block <= lim32 / (2 * 64 * 4);
     if (r->pair) r->dk = 128;
     r->cpl = r->dk / 16;
+    r->nlane = r->pack > 1 || r->pair ? 16 : r->dv / r->cpl;
     r->hv = r->pack > 1 ? p->H / r->pack : r->pair ? p->H / 2 : p->H << r->hshift;
     r->vbytes = std::min<int64_t>(16, (int64_t)(r->dk / 16) * r->es);
     r->bwd = swr::bwd_shape(p->block, r->hv);
@@ -193,7 +208,7 @@ int check_strides_aligned(const swr_problem_t* p, const Resolved& r) {
         if (d.size > 1 && (d.stride * r.es) % r.vbytes != 0) return SWR_ERR_ALIGN;
         if (r.pc && d.size > 1 && (d.stride * 4) % vda != 0) return SWR_ERR_ALIGN;
     }
-    if (r.pc && (r.dk * r.es) % r.vbytes != 0) return SWR_ERR_ALIGN;   // a virtual head's offset
+    if ((r.pc || r.hshift) && (r.dv * r.es) % r.vbytes != 0) return SWR_ERR_ALIGN;   // a virtual head's offset
     return SWR_OK;
 }
 
@@ -227,6 +242,9 @@ swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward
     k.B = p->B; k.T = p->T; k.H = p->H;
     k.Hv = r.hv;
     k.hshift = r.hshift;
+    k.dh = (int32_t)p->D;
+    k.dv = r.pack > 1 ? 64 : r.pair ? 128 : r.dv;
+    k.nlane = r.nlane;
     k.sx_b = p->sx_b; k.sx_t = p->sx_t; k.sx_h = p->sx_h;
     k.sa_b = p->sa_b; k.sa_t = p->sa_t; k.sa_h = p->sa_h;
     k.block = (int32_t)p->block;
@@ -256,7 +274,7 @@ const char* swr_error_string(int code) {
         case SWR_ERR_BLOCK: return "block must be 16, 32, 64 or 128";
         case SWR_ERR_ALIGN: return "pointer or stride not aligned to the per-lane vector width";
         case SWR_ERR_ALIAS: return "an output overlaps an input or another output";
-        case SWR_ERR_UNSUPPORTED: return "unsupported: D must be 16, 32, 64 or 128; unknown flags; bad run_len; or offsets beyond 32 bits";
+        case SWR_ERR_UNSUPPORTED: return "unsupported: D must be a multiple of 16 up to 256 (16, 32, 64 or 128 except for swr_forward, swr_carriers and swr_backward); unknown flags; bad run_len; or offsets beyond 32 bits";
         case SWR_ERR_HIP: return "the HIP runtime rejected the kernel launch";
         case SWR_ERR_VERSION: return "ABI version mismatch";
         case SWR_ERR_SCRATCH: return "the problem needs more workspace than the library's static scratch array holds (SWR_NOALLOC_SCRATCH_BYTES)";
@@ -425,6 +443,7 @@ int64_t swr_exact_workspace_bytes(const swr_problem_t* problem) {
     Resolved r, u;
     int rc = resolve(problem, &r, true);
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     if ((rc = resolve(problem, &u, false)) != SWR_OK) return rc;
     return std::max(exact_ws(problem, r).floats, exact_ws(problem, u).floats) * 4;
 }
@@ -443,6 +462,7 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     Resolved r;
     int rc = resolve_for(p, &r, {x, b, c, (const void*)y});
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
@@ -505,6 +525,7 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     Resolved r;
     int rc = resolve_for(p, &r, {x, b, c, dy, (const void*)dx, (const void*)db, (const void*)dc});
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
@@ -590,6 +611,7 @@ int step_impl(const swr_problem_t* p, int64_t t0, const void* x, const void* a, 
     Resolved r;
     int rc = resolve(p, &r);
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     if (t0 < 0) return SWR_ERR_SHAPE;
     const int64_t seqs = p->B * p->H;
     if (seqs == 0 || p->T == 0) return SWR_OK;   // no token: the state is unchanged
@@ -638,6 +660,7 @@ int swr_decode_state(const swr_problem_t* p, const void* a, const float* carrier
     Resolved r;
     const int rc = resolve(p, &r);
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const int64_t seqs = p->B * p->H;
     if (seqs == 0) return SWR_OK;
     if (!state || (p->T > 0 && (!a || !carriers))) return SWR_ERR_NULL;
@@ -683,6 +706,7 @@ struct UniPlan {
 int uni_resolve(const swr_problem_t* p, UniPlan* u, bool backward) {
     int rc = resolve(p, &u->r, false);
     if (rc != SWR_OK) return rc;
+    if (!u->r.natural) return SWR_ERR_UNSUPPORTED;
     if (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) return SWR_ERR_UNSUPPORTED;
     u->hshift = p->D > 64 ? 1 : 0;
     u->dk = (int)(p->D >> u->hshift);
@@ -799,6 +823,7 @@ namespace {
 int gates_resolve(const swr_problem_t* p, int64_t group, const int64_t* gst, Resolved* r, int64_t* gspan) {
     int rc = resolve(p, r, false);
     if (rc != SWR_OK) return rc;
+    if (!r->natural) return SWR_ERR_UNSUPPORTED;
     if (p->flags & SWR_FLAG_PER_CHANNEL_DECAY) return SWR_ERR_UNSUPPORTED;
     if (group < 1 || (p->H > 0 && p->H % group != 0)) return SWR_ERR_SHAPE;
     *gspan = 0;
@@ -829,6 +854,7 @@ int64_t swr_shared_gates_workspace_bytes(const swr_problem_t* p, int64_t group) 
     Resolved r;
     const int rc = resolve(p, &r, false);
     if (rc != SWR_OK) return rc;
+    if (!r.natural) return SWR_ERR_UNSUPPORTED;
     if (group < 1 || (p->H > 0 && p->H % group != 0)) return SWR_ERR_SHAPE;
     // groups of up to grouped_max_heads() heads are summed inside the backward
     return group <= swr::grouped_max_heads() ? 0 : 2 * p->B * p->T * p->H * p->D * 4;

@@ -109,9 +109,13 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
     const int hsel = PAIR ? n >> 3 : 0;                  // this lane's head of a pair
-    const int64_t h0 = PAIR ? 2 * wk.h : wk.h;           // (first) head of the work item
-    constexpr int DH = D / NH;                           // channels of a head
-    const int64_t xo = (wk.b * p.sx_b + h0 * p.sx_h) * ES;
+    // (first) head of the work item; a head wider than the kernel is split
+    // into virtual heads of p.dv channels, starting at channel coff
+    const int64_t h0 = PAIR ? 2 * wk.h : wk.h >> p.hshift;
+    const int64_t coff = PAIR ? 0 : (wk.h & ((1 << p.hshift) - 1)) * (int64_t)p.dv;
+    const bool lane_ok = PAIR || n < p.nlane;            // this lane holds channels of the head
+    const int64_t DH = PAIR ? D / NH : p.dh;             // channels of a head (carrier rows)
+    const int64_t xo = (wk.b * p.sx_b + h0 * p.sx_h + coff) * ES;
     // b and c: this head's rows, or its group's with shared gates
     const int64_t go = GG ? (wk.b * p.sg_b + (wk.h / p.group) * p.sg_h) * ES : xo;
     const char* xb = (const char*)p.x + xo;
@@ -125,15 +129,17 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
     // this lane's channel slice: n * CPL, or (with a pair) its head's (n & 7) * CPL
     const uint32_t lch = PAIR ? (uint32_t)(hsel * p.sx_h * ES) + (uint32_t)((n & 7) * CPL * ES)
                               : (uint32_t)(n * CPL * ES);
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + lch;
-    const uint32_t goff = GG ? (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES) : loff;
+    // (every access of an idle lane is out of range: it reads zeros, stores nothing)
+    const uint32_t loff = in_range(lane_ok, (uint32_t)(4 * grp) * (uint32_t)rs + lch);
+    const uint32_t goff = GG ? in_range(lane_ok, (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES))
+                             : loff;
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     // false: only the block carriers (or the run aggregates) are produced
     const bool want_y = MODE != kAggregate && p.y != nullptr;
-    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + (wk.b * p.H + h0) * p.nblocks * DH
+    float* const vb = MODE != kAggregate && p.carriers ? p.carriers + (wk.b * p.H + h0) * p.nblocks * DH + coff
                                                        : nullptr;
-    // this lane's carrier slice within the block's entry
-    const uint32_t vch = (uint32_t)(PAIR ? hsel * p.nblocks * DH + (n & 7) * CPL : n * CPL);
+    // this lane's carrier slice within the block's entry, in bytes (idle lanes: out of range)
+    const uint32_t vch = in_range(lane_ok, (uint32_t)(PAIR ? hsel * p.nblocks * DH + (n & 7) * CPL : n * CPL) * 4u);
     const __amdgpu_buffer_rsrc_t rv = rsrc(vb);
     const int64_t slot = (wk.b * p.H + wk.h) * p.nruns + wk.run;   // this run's aggregate / carry
 
@@ -189,6 +195,8 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
                 LR::read(s_tile[wv][0][r], lane, xr[r].w);
                 LR::read(s_tile[wv][1][r], lane, br[r].w);
                 LR::read(s_tile[wv][2][r], lane, cr[r].w);
+                // (an idle lane's slot holds whatever it held: its values stay in
+                // its own MFMA column and channels and are never stored)
                 if (!ok_xb(tr0 + r)) { xr[r].zero(); br[r].zero(); }
                 if (!ok_c(tr0 + r)) cr[r].zero();
             }
@@ -297,7 +305,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;   // first token of the block (it may end past T)
             store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
-                                               (uint32_t)(blk * DH + vch) * 4u), vout);
+                                               (uint32_t)(blk * DH) * 4u + vch), vout);
         }
         if (!want_y) continue;
 
@@ -389,7 +397,16 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     const int smask = S - 1;
     const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);   // end (excl.) of the halo block
 
-    const int64_t xo = (wk.b * p.sx_b + wk.h * p.sx_h) * ES;
+    // The head of the work item; a head wider than the kernel is split into
+    // virtual heads of p.dv channels, starting at channel coff, whose shares of
+    // the decay gradient meet in two atomic adds onto a zeroed da (split).
+    const int64_t head = wk.h >> p.hshift;
+    const int64_t coff = (wk.h & ((1 << p.hshift) - 1)) * (int64_t)p.dv;
+    const bool split = p.hshift > 0;
+    const bool lane_ok = n < p.nlane;    // this lane holds channels of the head
+    // this lane's slice of a carrier row, in bytes (idle lanes: out of range)
+    const uint32_t vlane = in_range(lane_ok, (uint32_t)(n * CPL) * 4u);
+    const int64_t xo = (wk.b * p.sx_b + head * p.sx_h + coff) * ES;
     // b and c: this head's rows, or its group's with shared gates
     const int64_t go = GG ? (wk.b * p.sg_b + (wk.h / p.group) * p.sg_h) * ES : xo;
     const char* xb = (const char*)p.x + xo;
@@ -401,17 +418,19 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
     const int64_t wso = ((wk.b * p.T) * p.H + wk.h) * D;
     char* dbb = GG ? (char*)(p.gws + wso) : (char*)p.db + xo;
     char* dcb = GG ? (char*)(p.gws + p.B * p.T * p.H * D + wso) : (char*)p.dc + xo;
-    const int64_t ao = wk.b * p.sa_b + wk.h * p.sa_h;
+    const int64_t ao = wk.b * p.sa_b + head * p.sa_h;
     const char* ab = (const char*)p.a + ao * ES;
     char* dab = (char*)(p.da + ao);
-    const float* vb = p.carriers + (wk.b * p.H + wk.h) * p.nblocks * D;
+    const float* vb = p.carriers + (wk.b * p.H + head) * p.nblocks * p.dh + coff;
     const int64_t rs = p.sx_t * ES;
     const int64_t gs = GG ? p.sg_t * ES : rs;        // row stride of b and c
     const int64_t ws = GG ? p.H * D * 4 : rs;         // row stride of db and dc
     const int64_t as = p.sa_t * ES;
     const int64_t das = p.sa_t * 4;
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
-    const uint32_t goff = GG ? (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES) : loff;
+    // (every row access of an idle lane is out of range: it reads zeros, stores nothing)
+    const uint32_t loff = in_range(lane_ok, (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES));
+    const uint32_t goff = GG ? in_range(lane_ok, (uint32_t)(4 * grp) * (uint32_t)gs + (uint32_t)(n * CPL * ES))
+                             : loff;
     const uint32_t woff = GG ? (uint32_t)(4 * grp) * (uint32_t)ws + (uint32_t)(n * CPL * 4) : loff;
     const uint32_t aoff = (uint32_t)n * (uint32_t)as;
     const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das;
@@ -517,7 +536,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             Row<IoF32, CPL> vr;
             vr.load(rsrc(from_h0 ? (const void*)(p.h0 + seq * D) : (const void*)vb),
                     from_h0 ? in_range(live && p.h0 != nullptr, (uint32_t)(n * CPL) * 4u)
-                            : in_range(live && t0 > 0, (uint32_t)(blk * D + n * CPL) * 4u));
+                            : in_range(live && t0 > 0, (uint32_t)(blk * p.dh) * 4u + vlane));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
         }
@@ -741,9 +760,11 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
             }
             const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
-            __builtin_amdgcn_raw_buffer_store_b32(
-                __builtin_bit_cast(int, tot), rda,
-                (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das)), 0, kBwdStore);
+            const int oda = (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das));
+            if (split)   // this virtual head's share: two addends onto zero, order-independent
+                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(tot, rda, oda, 0, 0);
+            else
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, tot), rda, oda, 0, kBwdStore);
         }
     }
 }
@@ -1204,17 +1225,19 @@ template <int PK, int CPL>
 struct Geo {
     static constexpr int LPH = 16 / PK;   // lanes per real head when packed
     int64_t head;   // first real head of the virtual head
-    int64_t half;   // channel half of a split real head, else 0
+    int64_t coff;   // first channel of the virtual head within its real head
     int64_t Dr;     // channels of a real head (the row length of carriers and states)
     int lh;         // real head of this lane within the virtual head
     int lch;        // first channel of this lane within its real head
-    __device__ Geo(int64_t vh, int hshift, int n) {
+    bool ok;        // the lane holds channels (a virtual head of p.dv < D channels
+                    // leaves lanes n >= p.nlane idle)
+    __device__ Geo(int64_t vh, const Params& p, int n) {
         constexpr int D = CPL * SB;
         if constexpr (PK > 1) {
-            head = vh * PK; half = 0; Dr = D / PK; lh = n / LPH; lch = (n % LPH) * CPL;
+            head = vh * PK; coff = 0; Dr = D / PK; lh = n / LPH; lch = (n % LPH) * CPL; ok = true;
         } else {
-            head = vh >> hshift; half = vh & ((1 << hshift) - 1); Dr = (int64_t)D << hshift;
-            lh = 0; lch = (int)half * D + n * CPL;
+            head = vh >> p.hshift; coff = (vh & ((1 << p.hshift) - 1)) * (int64_t)p.dv; Dr = p.dh;
+            lh = 0; lch = (int)coff + n * CPL; ok = n < p.nlane;
         }
     }
     // Offset (in float32 elements) of this lane's slice of row `row` of a
@@ -1261,13 +1284,13 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const int hw = wv / TW, tw = wv % TW;
     const Work wk = decode_work<HW>(p, hw);
-    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
+    const Geo<PK, CPL> geo(wk.h, p, n);
     const int l = p.block;
     const int smask = l / SB - 1;
     const int64_t t_lo = SWR ? max(wk.t_begin - (int64_t)l, (int64_t)0) : wk.t_begin;
     const int64_t halo = SWR && wk.t_begin > 0 ? (l + STEP - 1) / STEP : 0;
 
-    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D) * ES;
+    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.coff) * ES;
     const char* xb = (const char*)p.x + xo;
     const char* bb = (const char*)p.b + xo;
     const char* cb = (const char*)p.c + xo;
@@ -1276,7 +1299,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
     char* yb = (char*)p.y + xo;
     const int64_t rs = p.sx_t * ES;
     const int64_t as = PK > 1 ? p.sa_t * ES : rs;
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t loff = in_range(geo.ok, (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES));
     const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
     const bool want_y = MODE != kAggregate && p.y != nullptr;
     const int64_t hb = wk.b * p.H + geo.head;   // first real (batch, head) of the virtual head
@@ -1364,7 +1387,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
         if (vb && ((ph + tw) & smask) == smask) {
             const int64_t blk = r0 >> p.lshift;
             const int64_t t_blk = blk << p.lshift;
-            store_row<IoF32, CPL>(rv, in_range(grp == 0 && t_blk >= wk.t_begin && t_blk < wk.t_end,
+            store_row<IoF32, CPL>(rv, in_range(grp == 0 && geo.ok && t_blk >= wk.t_begin && t_blk < wk.t_end,
                                                geo.off(p.nblocks, blk) * 4u), vout);
         }
         if (!want_y) continue;
@@ -1416,12 +1439,12 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     const int lane = ln.lane, wv = ln.wv, grp = ln.grp, n = ln.n;
     const int hw = wv / TW, tw = wv % TW;
     const Work wk = decode_work<HW>(p, hw);
-    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
+    const Geo<PK, CPL> geo(wk.h, p, n);
     const int l = p.block;
     const int smask = l / SB - 1;
     const int64_t t_la = min(wk.t_end + (int64_t)l, p.T);
 
-    const int64_t xe = wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D;   // element offset
+    const int64_t xe = wk.b * p.sx_b + geo.head * p.sx_h + geo.coff;   // element offset
     const int64_t xo = xe * ES;
     const char* xb = (const char*)p.x + xo;
     const char* bb = (const char*)p.b + xo;
@@ -1440,10 +1463,10 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
     const int64_t rs = p.sx_t * ES;
     const int64_t as = PK > 1 ? p.sa_t * ES : rs;
     const int64_t das = PK > 1 ? p.sa_t * 4 : p.sx_t * 4;
-    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t loff = in_range(geo.ok, (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES));
     const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
     const uint32_t daoff = PK > 1 ? (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(geo.lh * p.sa_h * 4)
-                                  : (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(n * CPL * 4);
+                                  : in_range(geo.ok, (uint32_t)(4 * grp) * (uint32_t)das + (uint32_t)(n * CPL * 4));
 
     float eps[CPL], pr[CPL];
 #pragma unroll
@@ -1541,7 +1564,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             Row<IoF32, CPL> vr;
             vr.load(rsrc(from_h0 ? p.h0 + hb * geo.Dr : vb),
                     from_h0 ? in_range(live && p.h0 != nullptr, geo.off(1, 0) * 4u)
-                            : in_range(live && t0 > 0, geo.off(p.nblocks, blk) * 4u));
+                            : in_range(live && t0 > 0 && geo.ok, geo.off(p.nblocks, blk) * 4u));
 #pragma unroll
             for (int m = 0; m < CPL; ++m) in.v[m] = vr.get(m);
         }
@@ -1776,8 +1799,8 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
     const Lanes ln = lanes();
     const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
     const Work wk = decode_work<1>(p, 0);
-    const Geo<PK, CPL> geo(wk.h, p.hshift, n);
-    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.half * D) * ES;
+    const Geo<PK, CPL> geo(wk.h, p, n);
+    const int64_t xo = (wk.b * p.sx_b + geo.head * p.sx_h + geo.coff) * ES;
     const char* cb = (const char*)p.c + xo;
     const char* dyb = (const char*)p.dy + xo;
     const char* ab = PK > 1 ? (const char*)p.a + (wk.b * p.sa_b + geo.head * p.sa_h) * ES : (const char*)p.a + xo;
@@ -1969,9 +1992,28 @@ static hipError_t launch_feat(const Params& p, int D, const Shape& sh, bool back
     return launch_cpl<IO, false>(p, D, sh, backward, per_channel, pack, mode, stream);
 }
 
+// Zeroes da ([B, T, H] float32 with a's strides) before the virtual heads of
+// a split head add their shares of the decay gradient.
+__global__ __launch_bounds__(256) void swr_da_zero_kernel(float* da, int64_t T, int64_t H, int64_t sa_b,
+                                                          int64_t sa_t, int64_t sa_h, int64_t total) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t h = i % H, t = (i / H) % T, b = i / (H * T);
+        da[b * sa_b + t * sa_t + h * sa_h] = 0.0f;
+    }
+}
+
 hipError_t launch(const Params& p, int dtype, int D, const Shape& sh, bool backward, bool per_channel,
                   int pack, int mode, void* stream) {
     hipStream_t st = (hipStream_t)stream;
+    if (backward && !per_channel && pack == 1 && p.hshift > 0) {
+        if (mode != kSwr && mode != kRecompute) return hipErrorInvalidValue;
+        const int64_t total = p.B * p.T * p.H;
+        const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+        hipLaunchKernelGGL(swr_da_zero_kernel, dim3((uint32_t)blocks), dim3(256), 0, st, p.da, p.T, p.H, p.sa_b,
+                           p.sa_t, p.sa_h, total);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (dtype == 1) return launch_feat<IoBf16>(p, D, sh, backward, per_channel, pack, mode, st);
     return launch_feat<IoF32>(p, D, sh, backward, per_channel, pack, mode, st);
 }

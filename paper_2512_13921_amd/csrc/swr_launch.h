@@ -31,7 +31,13 @@ struct Params {
     int32_t residual;   // 0 or 1
     int32_t sig_a;      // 1: a holds logits, the decay is sigmoid(a) (da is then d/d logit)
     int32_t sig_b;      // 1: b holds logits, the pre-gate is sigmoid(b) (db is then d/d logit)
-    int32_t hshift;     // per-channel decay: log2 of the virtual heads per head (0 or 1)
+    int32_t hshift;     // log2 of the virtual heads per head: a head of more channels than a
+                        // kernel covers (per-channel decay: 64, else 128) is split into 2^hshift
+                        // virtual heads of dv channels each
+    int32_t dh;         // channels of a (real) head: the row length of the carrier array
+    int32_t dv;         // channels of a virtual head (at most the kernel's D = 16 * CPL)
+    int32_t nlane;      // lanes n of a 16-lane row that hold channels: dv / CPL (16 when the
+                        // virtual head fills the kernel; the others load zeros, store nothing)
     int64_t run_len;    // tokens per workgroup run, a multiple of the step and of l
     int64_t nruns;      // runs per (batch, head) sequence
     int64_t nwork;      // B * H * nruns workgroups
@@ -151,9 +157,12 @@ inline Shape fwd_shape(int64_t /*block*/, int64_t H) {
     return fwd_shape_single();
 }
 
-// Per-channel decay: a head is processed as 2^hshift independent virtual
-// heads of at most 64 channels (nothing couples the channels there).
-inline int pc_hshift(int64_t D) { return D > 64 ? 1 : 0; }
+// Heads of more channels than one kernel head covers are processed as 2^hshift
+// virtual heads of D >> hshift channels: at most 64 with a per-channel decay
+// (nothing couples the channels there), at most 128 with a decay per head
+// (whose decay gradient then sums the virtual heads' shares).
+inline int pc_hshift(int64_t D) { return D > 128 ? 2 : D > 64 ? 1 : 0; }
+inline int head_hshift(int64_t D) { return D > 128 ? 1 : 0; }
 
 // Launches the forward or backward kernel for (dtype, D, shape) on `stream`;
 // for the per-channel kernels D is the channel count of a virtual head.

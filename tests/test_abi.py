@@ -83,7 +83,7 @@ def test_version_mismatch():
     (dict(dtype=7), E_DTYPE),
     (dict(T=-1), E_SHAPE), (dict(B=-3), E_SHAPE), (dict(D=0), E_SHAPE),
     (dict(block=48), E_BLOCK), (dict(block=256), E_BLOCK), (dict(block=0), E_BLOCK),
-    (dict(D=48), E_UNSUP), (dict(D=256), E_UNSUP),
+    (dict(D=24), E_UNSUP), (dict(D=8), E_UNSUP), (dict(D=272), E_UNSUP), (dict(D=4096), E_UNSUP),
     (dict(run_len=100), E_UNSUP), (dict(run_len=-64), E_UNSUP),
     (dict(block=128, run_len=64), E_UNSUP),
     (dict(x_strides=(256 * 4 * 64, 4 * 64, 1)), E_SHAPE),           # heads overlap channels
@@ -92,6 +92,34 @@ def test_version_mismatch():
 def test_shape_validation(kw, code):
     p = problem(**kw)
     assert fwd(p) == code and bwd(p) == code and car(p) == code
+
+
+@pytest.mark.parametrize("D", [48, 80, 96, 112, 144, 160, 192, 208, 240, 256])
+@pytest.mark.parametrize("per_channel", [False, True])
+def test_any_multiple_of_16_up_to_256(D, per_channel):
+    # the jagged window's forward, carriers and backward take any D % 16 == 0 up
+    # to 256 (past validation only the launch is left, which fails without a GPU)
+    for dtype in (BF16, F32):
+        p = problem(D=D, dtype=dtype, per_channel=per_channel)
+        assert fwd(p) in (OK, E_HIP) and bwd(p) in (OK, E_HIP) and car(p) in (OK, E_HIP)
+        assert bwd(p, v_=0) in (OK, E_HIP)
+        assert swr.swr_carrier_elems(p) == 2 * 4 * (256 // 64) * D
+    # the other entry points keep the kernels' own widths
+    p = problem(D=D)
+    assert swr.load().swr_exact_workspace_bytes(ctypes.byref(p)) == E_UNSUP
+
+
+@pytest.mark.parametrize("D,per_channel,heads_x", [
+    (48, False, 1), (112, False, 1), (144, False, 2), (256, False, 2),
+    (48, True, 1), (96, True, 2), (144, True, 4), (256, True, 4)])
+def test_wide_and_odd_heads_launch_plan(D, per_channel, heads_x):
+    # heads wider than a kernel head (128 channels, 64 with a per-channel
+    # decay) run as 2 or 4 virtual heads: the backward's grid grows with them
+    base = swr.swr_launch_info(problem(B=2, T=4096, H=4, D=64, block=64, per_channel=per_channel))
+    info = swr.swr_launch_info(problem(B=2, T=4096, H=4, D=D, block=64, per_channel=per_channel))
+    seqs = 2 * 4 * heads_x
+    assert info["bwd_workgroups"] == seqs * -(-4096 // info["bwd_run_len"])
+    assert info["bwd_workgroups"] >= base["bwd_workgroups"] * heads_x // 2
 
 
 def test_unknown_flags_and_reserved():
@@ -180,7 +208,7 @@ def test_aliasing():
 def test_per_channel_validation():
     # a and da take the [B, T, H, D] layout of x; every call below fails before any launch
     pc = dict(per_channel=True)
-    assert fwd(problem(D=48, **pc)) == E_UNSUP and bwd(problem(block=48, **pc)) == E_BLOCK
+    assert fwd(problem(D=40, **pc)) == E_UNSUP and bwd(problem(block=48, **pc)) == E_BLOCK
     assert fwd(problem(**pc), a=A + 2) == E_ALIGN          # a needs x's 8-byte lane vectors
     assert fwd(problem(dtype=F32, **pc), a=A + 8) == E_ALIGN
     assert bwd(problem(**pc), da=DA + 8) == E_ALIGN        # 4 fp32 channels per lane: 16 bytes
