@@ -136,35 +136,49 @@ struct Row {
     }
 };
 
+// CPL floats of one lane's row slice converted to the I/O type (bf16: round to
+// nearest even), kept as the words a vector store writes.
+template <class IO, int CPL>
+struct Packed {
+    static constexpr int BYTES = CPL * IO::ES;
+    uint32_t w[BYTES >= 4 ? BYTES / 4 : 1];
+    Packed() = default;
+    __device__ explicit Packed(const float (&v)[CPL]) {
+        if constexpr (IO::ES == 2) {
+            if constexpr (CPL == 1) {
+                w[0] = IoBf16::from_f32(v[0]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < CPL / 2; ++i)
+                    w[i] = IoBf16::from_f32(v[2 * i]) | (IoBf16::from_f32(v[2 * i + 1]) << 16);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) w[i] = __builtin_bit_cast(uint32_t, v[i]);
+        }
+    }
+    template <int POL = 0>
+    __device__ void store(__amdgpu_buffer_rsrc_t r, uint32_t off) const {
+        if constexpr (BYTES == 2) {
+            __builtin_amdgcn_raw_buffer_store_b16((short)w[0], r, (int)off, 0, POL);
+        } else if constexpr (BYTES == 4) {
+            __builtin_amdgcn_raw_buffer_store_b32((int)w[0], r, (int)off, 0, POL);
+        } else if constexpr (BYTES == 8) {
+            __builtin_amdgcn_raw_buffer_store_b64(i32x2{(int)w[0], (int)w[1]}, r, (int)off, 0, POL);
+        } else {
+#pragma unroll
+            for (int i = 0; i < BYTES / 16; ++i)
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    i32x4{(int)w[4 * i], (int)w[4 * i + 1], (int)w[4 * i + 2], (int)w[4 * i + 3]}, r,
+                    (int)(off + 16 * i), 0, POL);
+        }
+    }
+};
+
 // Packs CPL floats to the I/O type and stores them as one vector.
 template <class IO, int CPL, int POL = 0>
 __device__ inline void store_row(__amdgpu_buffer_rsrc_t r, uint32_t off, const float (&v)[CPL]) {
-    constexpr int BYTES = CPL * IO::ES;
-    uint32_t w[BYTES >= 4 ? BYTES / 4 : 1];
-    if constexpr (IO::ES == 2) {
-        if constexpr (CPL == 1) {
-            __builtin_amdgcn_raw_buffer_store_b16((short)IoBf16::from_f32(v[0]), r, (int)off, 0, POL);
-            return;
-        } else {
-#pragma unroll
-            for (int i = 0; i < CPL / 2; ++i)
-                w[i] = IoBf16::from_f32(v[2 * i]) | (IoBf16::from_f32(v[2 * i + 1]) << 16);
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) w[i] = __builtin_bit_cast(uint32_t, v[i]);
-    }
-    if constexpr (BYTES == 4) {
-        __builtin_amdgcn_raw_buffer_store_b32((int)w[0], r, (int)off, 0, POL);
-    } else if constexpr (BYTES == 8) {
-        __builtin_amdgcn_raw_buffer_store_b64(i32x2{(int)w[0], (int)w[1]}, r, (int)off, 0, POL);
-    } else if constexpr (BYTES >= 16) {
-#pragma unroll
-        for (int i = 0; i < BYTES / 16; ++i)
-            __builtin_amdgcn_raw_buffer_store_b128(
-                i32x4{(int)w[4 * i], (int)w[4 * i + 1], (int)w[4 * i + 2], (int)w[4 * i + 3]}, r,
-                (int)(off + 16 * i), 0, POL);
-    }
+    Packed<IO, CPL>(v).template store<POL>(r, off);
 }
 
 // Asynchronous copy of one row slice per lane from a buffer straight into
@@ -240,6 +254,29 @@ __device__ inline SigSlope sigmoid_slope(float z) {
 __device__ inline float fresh(float v) {
     asm volatile("" : "+v"(v));
     return v;
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup barrier
+// ---------------------------------------------------------------------------
+
+// The waves of a workgroup exchange data through LDS only (no wave reads what
+// another wrote to global memory), so a barrier needs to order LDS accesses
+// alone: the release / acquire fences of the local address space wait for
+// this wave's LDS operations (lgkmcnt) but not for its global loads and
+// stores, so loads issued ahead of the barrier (the next step's inputs) stay
+// in flight across it.  (__syncthreads also waits for every global access.)
+#ifndef SWR_LDS_BARRIER
+#define SWR_LDS_BARRIER 1
+#endif
+__device__ inline void lds_barrier() {
+#if SWR_LDS_BARRIER
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+#else
+    __syncthreads();
+#endif
 }
 
 // ---------------------------------------------------------------------------

@@ -119,7 +119,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_grouped_kernel(Params p) {
             }
             const float cq = shfl(row_prefix_prod(a_n), 15);
             if (lane == 0) s_c[buf][tw] = cq;
-            __syncthreads();
+            lds_barrier();
 #pragma unroll 1
             for (int r = TW - 1; r >= 0; --r) {
                 if ((r & smask) == smask) {
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_grouped_kernel(Params p) {
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     // One head's inputs for one step: its x and dy rows, its decay (as
     // stored) and the carrier of the block before the step.  Each head's are
@@ -273,7 +273,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_grouped_kernel(Params p) {
                 for (int m = 0; m < CPL; ++m) s_df[buf][tw][n * CPL + m] = a0 * Dl[m][0];
             }
             if (lane == 63) s_c[buf][tw] = dk.c;
-            __syncthreads();
+            lds_barrier();
 
             // ---- forward carriers entering this wave's sub-block -------------------------
             float ein[CPL], sin_[CPL];

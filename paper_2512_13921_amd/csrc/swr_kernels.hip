@@ -262,7 +262,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
             s_c[buf][wv * NH] = dk.c;
             if constexpr (PAIR) s_c[buf][wv * NH + 1] = dk1.c;
         }
-        __syncthreads();
+        lds_barrier();
 
         // A step need not start at a block boundary: phase of its first sub-block.
         const int ph = (int)(t0 >> 4) & smask;
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         }
         const float cq = shfl(row_prefix_prod(a_n), 15);
         if (lane == 0) s_c[buf][wv] = cq;
-        __syncthreads();
+        lds_barrier();
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
             if ((r & smask) == smask) {
@@ -636,7 +636,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) s_df[buf][wv][n * CPL + m] = a0 * Dl[m][0];
         }
         if (lane == 63) s_c[buf][wv] = dk.c;
-        __syncthreads();
+        lds_barrier();
 
         // ---- forward carriers entering this wave's sub-block ---------------------------
         float ein[CPL], sin_[CPL];
@@ -732,10 +732,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
         }
         const __amdgpu_buffer_rsrc_t rdx = rsrc(dxb + r0 * rs), rdb = rsrc(dbb + r0 * ws),
                                      rdc = rsrc(dcb + r0 * ws), rda = rsrc(dab + r0 * das);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t t = tr0 + r;
-            float vdx[CPL], vdb[CPL], vdc[CPL];
+        auto out_row = [&](int r, float (&vdx)[CPL], float (&vdb)[CPL], float (&vdc)[CPL], float& tot) {
             float acc = SWR ? -Gsh[r] * Rr[r] * kd : 0.0f;
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
@@ -749,6 +746,20 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 vdb[m] = xr[r].get(m) * du * g.ds;
                 acc = __builtin_fmaf(r == 0 ? hup[m] : W[m][r - 1], du, acc);
             }
+            tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
+        };
+        auto store_da = [&](int r, float tot) {
+            const int oda = (int)in_range(n == 0 && tr0 + r < wk.t_end, daoff + (uint32_t)(r * das));
+            if (split)   // this virtual head's share: two addends onto zero, order-independent
+                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(tot, rda, oda, 0, 0);
+            else
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, tot), rda, oda, 0, kBwdStore);
+        };
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t t = tr0 + r;
+            float vdx[CPL], vdb[CPL], vdc[CPL], tot;
+            out_row(r, vdx, vdb, vdc, tot);
             const uint32_t o = in_range(t < wk.t_end, loff + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
             if constexpr (GG) {   // this head's float32 shares, summed over the group later
@@ -759,12 +770,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_kernel(Params p) {
                 store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
                 store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
             }
-            const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
-            const int oda = (int)in_range(n == 0 && t < wk.t_end, daoff + (uint32_t)(r * das));
-            if (split)   // this virtual head's share: two addends onto zero, order-independent
-                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(tot, rda, oda, 0, 0);
-            else
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, tot), rda, oda, 0, kBwdStore);
+            store_da(r, tot);
         }
     }
 }
@@ -831,7 +837,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_agg_kernel(Params p) {
         }
         const float cq = shfl(row_prefix_prod(a_n), 15);
         if (lane == 0) s_c[buf][tw] = cq;
-        __syncthreads();
+        lds_barrier();
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
             const float c_ = s_c[buf][r];
@@ -1354,7 +1360,7 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_pc_kernel(Params p) {
                 s_cc[buf][wv][n * CPL + m] = G[3][m];
             }
         }
-        __syncthreads();
+        lds_barrier();
 
         const int ph = (int)(t0 >> 4) & smask;
         float ein[CPL], vout[CPL];
@@ -1513,7 +1519,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
                 s_cc[buf][wv][n * CPL + m] = av[0][m] * R[0][m];   // a_0 ... a_15
             }
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
             if ((r & smask) == smask) {
@@ -1656,7 +1662,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_bwd_pc_kernel(Params p) {
             for (int m = 0; m < CPL; ++m) s_df[buf][wv][n * CPL + m] = av[0][m] * Dv[0][m];
         }
         if constexpr (VREC) prev_solve(t0, buf);
-        __syncthreads();
+        lds_barrier();
         float vrec[CPL];   // kRecompute: the carrier of the block before the step
         if constexpr (VREC) {
 #pragma unroll
@@ -1846,7 +1852,7 @@ __global__ __launch_bounds__(TW * 64, 2) void swr_bwd_pc_agg_kernel(Params p) {
                 s_cc[buf][tw][n * CPL + m] = av[0][m] * R[0][m];
             }
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll 1
         for (int r = TW - 1; r >= 0; --r) {
 #pragma unroll

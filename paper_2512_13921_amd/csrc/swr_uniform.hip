@@ -190,7 +190,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_fwd_kernel(Params p) 
             for (int m = 0; m < CPL; ++m) s_wl[buf][wv][n * CPL + m] = W[m][3];
         }
         if (lane == 63) s_c[buf][wv] = dk.c;
-        __syncthreads();
+        lds_barrier();
 
         // ---- the block's earlier sub-blocks (state entering this one, their
         //      decay product) and later ones (the tail that Q carries) -------
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
         f32x4 Pe[CPL];
         c_prime(dk, dh, Pe);
         if (lane == 63) s_x[buf].c[wv] = dk.c;
-        __syncthreads();
+        lds_barrier();
         float X[CPL], gp;
         prefix_df(X, gp);
 #pragma unroll
@@ -505,7 +505,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
             for (int m = 0; m < CPL; ++m) s_x[buf].wp[wv][n * CPL + m] = wp0[m];
         }
         if (lane == 63) { s_x[buf].c[wv] = dk.c; s_x[buf].cp[wv] = cp; }
-        __syncthreads();
+        lds_barrier();
 
         // ---- the block's other sub-blocks -------------------------------------------
         float s[CPL], X[CPL], pin[CPL], Vp[CPL];
@@ -592,7 +592,7 @@ __global__ __launch_bounds__(TW * HW * 64, 2) void swr_uni_bwd_kernel(Params p) 
 #pragma unroll
             for (int m = 0; m < CPL; ++m) s_x[buf].wf[wv][n * CPL + m] = Fl[m][3];
         }
-        __syncthreads();
+        lds_barrier();
         float pinE[CPL], sF[CPL];
 #pragma unroll
         for (int m = 0; m < CPL; ++m) { pinE[m] = 0.f; sF[m] = 0.f; }
