@@ -351,6 +351,9 @@ def main():
     ap.add_argument("--paper-shape", action="store_true",
                     help="forward-only sweep at the paper's own mixer-timing shape (B=1, D=2048 as "
                          "H=128 heads of d=16, block 16, bf16) over T = 1K .. 512K")
+    ap.add_argument("--channels", type=int, default=0,
+                    help="channels per head d (any multiple of 16 up to 256) in place of the workload's, "
+                         "with B, T, H and the rest of the recipe unchanged")
     ap.add_argument("--no-carriers", action="store_true",
                     help="the jagged window without saved block carriers: the forward keeps none "
                          "and the backward recomputes them (the problem statement's call shape)")
@@ -402,6 +405,11 @@ def main():
                   file=sys.stderr)
             return 2
         cfg = cfg.with_(name=cfg.name + f"_gates{groups}")
+    if args.channels:
+        if exact or uniform or groups:
+            print("--channels applies to the jagged window's own entry points only", file=sys.stderr)
+            return 2
+        cfg = cfg.with_(D=args.channels, name=cfg.name.replace(f"_d{cfg.D}", f"_d{args.channels}"))
     nocar = args.no_carriers
     if nocar:
         if exact or uniform or groups:
