@@ -89,7 +89,7 @@ def contraction_flops(cfg, backward, uniform=False):
 
 # The sources that decide what a launch does (kernels, grid policy): the
 # recorded traffic is stale once any of them changes.
-KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_groups.hip", "swr_device.h", "swr_api.cpp",
+KERNEL_SOURCES = ("swr_kernels.hip", "swr_uniform.hip", "swr_groups.hip", "swr_chain.hip", "swr_device.h", "swr_api.cpp",
                   "swr_launch.h")
 
 

@@ -193,8 +193,14 @@ int swr_abi_version(void);
  * state.  This is the recurrence that the jagged window approximates; with
  * h0 and h_last it also chains a long sequence processed in pieces, and a
  * single-token piece is the recurrent decoding step.  Stages I and III both
- * read x, b and a, so the exact forward moves about 1.5x the bytes of
- * swr_forward (the backward about 1.25x).
+ * read their inputs, so the three stages move about 1.5x the bytes of
+ * swr_forward (the backward about 1.25x).  With one decay per head (unless
+ * heads of 16 or 32 channels, stored next to each other, run packed four or
+ * two to a 64-channel group on the per-channel kernels), the forward instead
+ * runs the three stages in one pass over chunks of 128 tokens, each chunk
+ * composing the published aggregates of the chunks before it (a look-back
+ * between workgroups in a fixed pattern, so that repeated calls give the same
+ * bits): it reads every input once.
  *
  * Everything in swr_problem_t keeps its meaning except that `block` only sets
  * the length of the exact block carriers; every flag applies (with
@@ -231,13 +237,15 @@ int swr_exact_forward(const swr_problem_t* problem, const void* x, const void* a
  * bytes, one per GPU, held from the library's first use of that GPU until the
  * process ends; its address is looked up once per device, on the first call
  * on it.  A problem whose swr_exact_workspace_bytes exceeds that size is
- * rejected with SWR_ERR_SCRATCH before any HIP runtime call.  The kernels
- * write every workspace entry they read, so nothing is cleared between calls.
+ * rejected with SWR_ERR_SCRATCH before any HIP runtime call.  The one-pass
+ * forward's publication flags and ticket counters at the start of the array
+ * are zeroed by a fill kernel on `stream` at the start of every call (no
+ * memset); every other entry is written before it is read.
  * All calls on one GPU share its array: calls whose work overlaps in time on
  * one GPU (different streams, or host threads racing on the same stream)
  * race on it and give wrong results; calls ordered on one stream are safe.
  * Launches go to the device of `stream` (NULL: the current device). */
-#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)16 << 20)
+#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)32 << 20)
 int swr_exact_forward_noalloc(const swr_problem_t* problem, const void* x, const void* a,
                               const void* b, const void* c, const float* h0, void* y,
                               float* carriers, float* h_last, void* stream);

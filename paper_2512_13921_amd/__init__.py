@@ -37,7 +37,7 @@ SWR_FLAG_PER_CHANNEL_DECAY = 2
 SWR_FLAG_SIGMOID_DECAY = 4
 SWR_FLAG_SIGMOID_PREGATE = 8
 SWR_ERR_SCRATCH = -10
-SWR_NOALLOC_SCRATCH_BYTES = 16 << 20
+SWR_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class SwrProblem(ctypes.Structure):

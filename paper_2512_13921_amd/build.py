@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libswr.so")
 SOURCES = [os.path.join(CSRC, n) for n in ("swr_api.cpp", "swr_kernels.hip", "swr_uniform.hip", "swr_groups.hip",
-                                            "swr_noalloc.hip")]
+                                            "swr_noalloc.hip", "swr_chain.hip")]
 HEADERS = [os.path.join(CSRC, "swr_launch.h"), os.path.join(CSRC, "swr_device.h"),
            os.path.join(CSRC, "swr_internal.h"),
            os.path.join(os.path.dirname(HERE), "include", "swr.h")]

@@ -424,6 +424,51 @@ ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
 
 
 
+// The exact forward in one pass (swr_chain.hip), for one decay per head on
+// the MFMA kernels.  A float32 head of 128 channels runs as two virtual heads
+// of 64, each its own chain of chunks: the lighter wave lets two workgroups
+// share a compute unit, which hides the look-back's latency; a bf16 head of
+// 128 stays whole (16-byte row slices a lane).  Workspace: two ticket counters
+// (padded to 16 floats), then per chunk of chain_tokens() tokens of every
+// virtual sequence a flag and a decay product, then per chunk an aggregate
+// end state and an inclusive end state (a virtual head's channels each).
+#ifndef SWR_EXACT_CHAIN
+#define SWR_EXACT_CHAIN 1
+#endif
+
+struct ChainWs {
+    int cpl;          // channels per lane of the launch
+    int hs;           // log2 of the virtual heads per head
+    int64_t nch;      // chunks per sequence
+    int64_t n;        // chunks of the (virtual) sequences
+    int64_t floats;   // float32 elements
+};
+
+ChainWs chain_ws(const swr_problem_t* p) {
+    ChainWs c;
+    c.cpl = (int)std::min<int64_t>(p->D / 16, p->dtype == 1 ? 8 : 4);
+    const int64_t ct = swr::chain_tokens();
+    c.hs = 0;
+    while ((16 * c.cpl) << c.hs < p->D) ++c.hs;
+    c.nch = (p->T + ct - 1) / ct;
+    c.n = (p->B * p->H << c.hs) * c.nch;
+    // ticket counters, a flag and a decay product per chunk, two D-vectors per real chunk
+    c.floats = 16 + 2 * c.n + 2 * (c.n >> c.hs) * p->D;
+    return c;
+}
+
+// The tickets are 32-bit counters (each workgroup takes one past the last chunk).
+bool use_chain(const swr_problem_t* p, const Resolved& r) {
+    return SWR_EXACT_CHAIN && !r.pc && r.pack == 1 && !r.empty && chain_ws(p).n < ((int64_t)1 << 30);
+}
+
+// Workspace of the exact calls for one plan: the three-stage arrays (the
+// backward's, and the forward's when it does not run in one pass) or the
+// one-pass forward's, whichever is larger.
+int64_t exact_ws_floats(const swr_problem_t* p, const Resolved& r) {
+    return std::max(exact_ws(p, r).floats, use_chain(p, r) ? chain_ws(p).floats : (int64_t)0);
+}
+
 // Pointers into the workspace for one launch.
 void exact_arrays(const swr_problem_t* p, const ExactWs& w, void* ws, float** v, float** carry, float** prod) {
     float* f = (float*)ws;
@@ -445,7 +490,7 @@ int64_t swr_exact_workspace_bytes(const swr_problem_t* problem) {
     if (rc != SWR_OK) return rc;
     if (!r.natural) return SWR_ERR_UNSUPPORTED;
     if ((rc = resolve(problem, &u, false)) != SWR_OK) return rc;
-    return std::max(exact_ws(problem, r).floats, exact_ws(problem, u).floats) * 4;
+    return std::max(exact_ws_floats(problem, r), exact_ws_floats(problem, u)) * 4;
 }
 
 int swr_exact_forward(const swr_problem_t* p, const void* x, const void* a, const void* b,
@@ -464,14 +509,15 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     if (rc != SWR_OK) return rc;
     if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
+    const int64_t wfloats = exact_ws_floats(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
     if (!r.empty && (!x || !a || !b || !c || !y)) return SWR_ERR_NULL;
     if (scratch) {
         // the library's own array: disjoint from every caller buffer, located later
-        if (w.floats * 4 > scratch_bytes) return SWR_ERR_SCRATCH;
+        if (wfloats * 4 > scratch_bytes) return SWR_ERR_SCRATCH;
         workspace = nullptr;
-    } else if (w.floats > 0 && !workspace) {
+    } else if (wfloats > 0 && !workspace) {
         return SWR_ERR_NULL;
     }
     for (const void* q : {(const void*)h0, (const void*)h_last, (const void*)carriers, (const void*)workspace})
@@ -485,7 +531,7 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     const Span ins[5] = {span(x, r.xspan), span(b, r.xspan), span(c, r.xspan), span(a, r.aspan * r.es),
                          span(h0, h0 ? sbytes : 0)};
     const Span outs[4] = {span(y, r.xspan), span(carriers, carriers ? r.carriers * 4 : 0),
-                          span(h_last, h_last ? sbytes : 0), span(workspace, workspace ? w.floats * 4 : 0)};
+                          span(h_last, h_last ? sbytes : 0), span(workspace, workspace ? wfloats * 4 : 0)};
     for (int i = 0; i < 4; ++i) {
         for (const Span& s : ins)
             if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
@@ -493,7 +539,26 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
             if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
     }
 
-    if (scratch && w.floats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
+    if (scratch && wfloats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
+    if (use_chain(p, r)) {   // one pass: chained chunks with a look-back
+        const ChainWs cw = chain_ws(p);
+        float* f = (float*)workspace;
+        swr::Params k = make_params(p, r, false);
+        k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers; k.h0 = h0; k.h_last = h_last;
+        k.chain_ctr = (int32_t*)f;
+        k.chain_flags = (int32_t*)(f + 16);
+        k.agg_p = f + 16 + cw.n;
+        k.agg_v = f + 16 + 2 * cw.n;
+        k.chain_incl = k.agg_v + (cw.n >> cw.hs) * p->D;
+        k.hshift = cw.hs;
+        k.Hv = p->H << cw.hs;
+        k.dh = (int32_t)p->D;
+        k.dv = (int32_t)(16 * cw.cpl);
+        k.nruns = cw.nch;
+        // persistent workgroups: as many as the compute units hold at once
+        k.nwork = std::min<int64_t>(cw.n, 256 * (cw.cpl == 8 ? 1 : cw.cpl == 1 ? 3 : 2));
+        return swr::launch_chain_forward(k, p->dtype, cw.cpl, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    }
     float *wv = nullptr, *wc = nullptr, *wp = nullptr;
     if (w.floats > 0) exact_arrays(p, w, workspace, &wv, &wc, &wp);
     swr::Params k = make_params(p, r, false);

@@ -1,0 +1,342 @@
+// swr_chain.hip -- the exact (untruncated) recurrence's forward in one pass.
+//
+// The three-stage evaluation of the hierarchical decomposition (Alg.
+// "Hierarchical Block Parallel Inference": local solves, the carrier
+// recurrence, reconstruction) reads x, b and a twice.  Here the carrier
+// recurrence is resolved while the chunks are processed, by a look-back
+// between workgroups: each chunk of 128 tokens of a sequence is solved locally
+// from zero, which gives its aggregate, the end state V and decay product P of
+// the chunk started from zero.  The state entering chunk c is then
+//   S_c = P_{c-1} ( ... P_{k+1} (P_k S_k' + V_k) ...) + V_{c-1},
+// composed from the inclusive end state S_k' of the last boundary chunk k
+// before c (chunks 15, 31, 47, ...; before the first one, the initial state)
+// and the aggregates of the chunks in between.  Boundary chunks publish their
+// inclusive end state P S + V, the others their aggregate.  The composition
+// always takes the same chunks in the same pattern, so the results do not
+// depend on the order in which workgroups reach them; the outputs then follow
+// from the chunk's local solves, kept in registers.  Every input is read once.
+//
+// Chunks are handed out in order by a ticket counter (chunk-major over the
+// sequences), so a chunk only ever waits for chunks of lower tickets, whose
+// workgroups are already running.  A wait is bounded: past kSpinLimit polls
+// the chunk counts the time-out and proceeds from a NaN state, so that a lost
+// publication (never expected) shows in every output that depends on it
+// instead of passing as a plausible value.
+//
+// Publication uses device-coherent (agent-scope) stores, and a wait for
+// their completion before the flag that announces them; readers load the flag
+// and then the data with device-coherent loads.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "swr_device.h"
+#include "swr_launch.h"
+
+namespace swr {
+namespace {
+
+constexpr int kChainTW = 8;                // waves per workgroup, one sub-block each
+constexpr int kChainTok = kChainTW * SB;   // tokens per chunk
+constexpr int kFlagAgg = 1, kFlagIncl = 2;
+// Chunks kChainK - 1, 2 kChainK - 1, ... of a sequence publish their inclusive
+// end state, the others their aggregate; every chunk composes the aggregates
+// since the last such boundary, kChainQ per lane group (four groups).
+constexpr int kChainQ = 4;
+constexpr int kChainK = 4 * kChainQ;
+// device-coherent (sc1) vector loads of published values
+constexpr int kCoherent = 16;
+constexpr int kSpinLimit = 1 << 16;
+
+__device__ inline void put_coherent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void put_flag(int32_t* p, int v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline int get_flag(const int32_t* p) {
+    return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until this wave's memory writes are complete (vmcnt(0)); the
+// compiler moves no memory access across it.
+__device__ inline void writes_complete() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <class IO, int CPL, bool FEAT>
+__global__ __launch_bounds__(kChainTW * 64, 1) void swr_fwd_chain_kernel(Params p) {
+    constexpr int TW = kChainTW;
+    constexpr int TOK = kChainTok;
+    constexpr int D = CPL * SB;
+    constexpr int ES = IO::ES;
+    using RW = Row<IO, CPL>;
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
+    __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
+    __shared__ float s_c[TW];       // decay product of each sub-block
+    __shared__ float s_pre[D];      // the exact state entering the chunk
+    __shared__ int64_t s_ticket[2];
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    // (virtual) sequences: a head of p.dh channels is 2^hshift virtual heads of D
+    const int64_t S = p.B * p.Hv, nch = p.nruns, N = S * nch;
+    const int hmask = (1 << p.hshift) - 1;
+    const int64_t DH = p.dh;
+    const int64_t rs = p.sx_t * ES, as = p.sa_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const int smask = p.block / SB - 1;
+
+    // Tickets pass through LDS; two slots, so that a slot is only rewritten
+    // after a later barrier has ordered every wave's read of it.
+    int par = 0;
+    auto grab = [&]() {
+        if (threadIdx.x == 0) s_ticket[par] = atomicAdd(p.chain_ctr, 1);
+        lds_barrier();
+        const int64_t t = s_ticket[par];
+        par ^= 1;
+        return t;
+    };
+    int64_t ticket = grab();
+    for (;;) {
+        if (ticket >= N) break;
+        const int64_t seq = ticket % S, ch = ticket / S;   // chunk-major: earlier chunks first
+        const int64_t slot = seq * nch + ch;
+        const int64_t rseq = seq >> p.hshift;   // the real (batch, head) sequence
+        const int64_t coff = (int64_t)(seq & hmask) * D;   // its first channel here
+        const int64_t xo = (rseq / p.H * p.sx_b + rseq % p.H * p.sx_h + coff) * ES;
+        const int64_t t0 = ch * TOK, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+
+        // ---- the sub-block's local solve W = L u ----------------------------------
+        RW xr[4], br[4], cr[4];
+        {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
+                                         rb = rsrc((const char*)p.b + xo + r0 * rs),
+                                         rc = rsrc((const char*)p.c + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
+                xr[r].template load<kFwdLoad>(rx, o);
+                br[r].template load<kFwdLoad>(rb, o);
+                cr[r].template load<kFwdLoad>(rc, o);
+            }
+        }
+        const bool a_ok = r0 + n < p.T;
+        float a_n = load_scalar<IO, kFwdDecay>(
+            rsrc((const char*)p.a + (rseq / p.H * p.sa_b + rseq % p.H * p.sa_h) * ES + r0 * as), in_range(a_ok, aoff));
+        if (sig_a) a_n = sigmoid(a_n);
+        if (!a_ok) a_n = 1.0f;   // past the sequence's end the state is carried unchanged
+        const Decay dk = build_decay(a_n, grp, n);
+        f32x4 W[CPL];
+        {
+            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                float u[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
+                W[m] = Contract<IO>::run(A, u);
+            }
+        }
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_wl[tw][n * CPL + m] = W[m][3];
+        }
+        if (lane == 63) s_c[tw] = dk.c;
+        lds_barrier();
+
+        // ---- wave 0: the chunk's aggregate, the look-back, the inclusive state -----
+        if (tw == 0) {
+            float V[CPL], P = 1.0f;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) V[m] = 0.f;
+#pragma unroll 1
+            for (int r = 0; r < TW; ++r) {
+                const float c_ = s_c[r];
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) V[m] = __builtin_fmaf(c_, V[m], s_wl[r][n * CPL + m]);
+                P *= c_;
+            }
+            const uint32_t vch = (uint32_t)(n * CPL);
+            const int64_t slot0 = seq * nch;
+            const bool boundary = ch % kChainK == kChainK - 1;
+            // the last boundary chunk before this one (or none), and the chunks in between
+            const int64_t kb = ch / kChainK * kChainK - 1;
+            const int cnt = (int)(ch - 1 - kb);
+            if (!boundary && ch + 1 < nch) {   // later chunks of the group compose this aggregate
+                if (grp == 0) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) put_coherent(p.agg_v + slot * D + vch + m, V[m]);
+                }
+                if (lane == 0) put_coherent(p.agg_p + slot, P);
+                writes_complete();
+                if (lane == 0) put_flag(p.chain_flags + slot, kFlagAgg);
+            }
+            // wait until the boundary's inclusive state and the aggregates in
+            // between are published: lane i < cnt polls chunk kb + 1 + i, lane 63 the boundary
+            bool timed_out = false;
+            int spins = 0;
+#pragma unroll 1
+            for (;;) {
+                bool ok = true;
+                if (lane < cnt)
+                    ok = get_flag(p.chain_flags + slot0 + kb + 1 + lane) == kFlagAgg;
+                else if (lane == 63 && kb >= 0)
+                    ok = get_flag(p.chain_flags + slot0 + kb) == kFlagIncl;
+                if (__all(ok)) break;
+                if (++spins > kSpinLimit) {   // never expected: count it, poison the outputs
+                    if (lane == 0) atomicAdd(p.chain_ctr + 1, 1);
+                    timed_out = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            // compose in a fixed pattern, so that the result does not depend on
+            // timing: lane group g folds chunks kb+1+Q*g ... kb+Q*(g+1) in order,
+            // then the groups' compositions are applied to the boundary state in order
+            float gV[CPL], gP = 1.0f;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) gV[m] = 0.f;
+            {
+                Row<IoF32, CPL> rv[kChainQ];
+                float pj[kChainQ];
+                const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0);
+#pragma unroll
+                for (int q = 0; q < kChainQ; ++q) {
+                    const int i = grp * kChainQ + q;
+                    const int64_t j = kb + 1 + i;
+                    rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
+                    pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                          rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
+                }
+#pragma unroll
+                for (int q = 0; q < kChainQ; ++q) {
+                    const float pq = grp * kChainQ + q < cnt ? pj[q] : 1.0f;
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
+                    gP *= pq;
+                }
+            }
+            float pre[CPL];
+            if (kb >= 0) {
+                Row<IoF32, CPL> ri;
+                ri.template load<kCoherent>(rsrc(p.chain_incl + slot0 * D), (uint32_t)(kb * D + vch) * 4u);
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) pre[m] = ri.get(m);
+            } else {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) pre[m] = p.h0 ? p.h0[rseq * DH + coff + vch + m] : 0.f;
+            }
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int src = g * 16 + n;
+                const float pg = __shfl(gP, src);
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg, pre[m], __shfl(gV[m], src));
+            }
+            if (timed_out) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) pre[m] = __builtin_nanf("");
+            }
+            float I[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P, pre[m], V[m]);
+            if (boundary && ch + 1 < nch) {
+                if (grp == 0) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) put_coherent(p.chain_incl + slot * D + vch + m, I[m]);
+                }
+                writes_complete();
+                if (lane == 0) put_flag(p.chain_flags + slot, kFlagIncl);
+            }
+            if (grp == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
+                if (p.h_last && ch == nch - 1) {
+#pragma unroll
+                    for (int m = 0; m < CPL; ++m) p.h_last[rseq * DH + coff + vch + m] = I[m];
+                }
+            }
+        }
+        lds_barrier();
+
+        // ---- outputs: the state entering this wave's sub-block, y, block carriers -----
+        float e[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) e[m] = s_pre[n * CPL + m];
+#pragma unroll 1
+        for (int r = 0; r < tw; ++r) {
+            const float c_ = s_c[r];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) e[m] = __builtin_fmaf(c_, e[m], s_wl[r][n * CPL + m]);
+        }
+        const __amdgpu_buffer_rsrc_t ry = rsrc((char*)p.y + xo + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float yv[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                yv[m] = cr[r].get(m) * __builtin_fmaf(dk.G[r], e[m], W[m][r]);
+                if (p.residual) yv[m] += xr[r].get(m);
+            }
+            store_row<IO, CPL, kFwdStore>(ry, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)), yv);
+        }
+        // the exact state at the end of a block that ends with this sub-block
+        // (a block longer than a chunk that the sequence's end cuts short ends in the last chunk)
+        if (p.carriers && (((ch * TW + tw) & smask) == smask || (ch == nch - 1 && tw == TW - 1))) {
+            const int64_t blk = r0 >> p.lshift;
+            float v[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) v[m] = __builtin_fmaf(dk.c, e[m], s_wl[tw][n * CPL + m]);
+            store_row<IoF32, CPL>(rsrc(p.carriers + (rseq * p.nblocks * DH + coff)),
+                                  in_range(grp == 0 && blk < p.nblocks, (uint32_t)(blk * DH + n * CPL) * 4u), v);
+        }
+        ticket = grab();
+    }
+}
+
+// Zeroes the chunk flags and the ticket counters before a launch.
+__global__ __launch_bounds__(256) void swr_chain_reset_kernel(int32_t* flags, int64_t n, int32_t* ctr) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) flags[i] = 0;
+    if (blockIdx.x == 0 && threadIdx.x < 2) ctr[threadIdx.x] = 0;
+}
+
+template <class IO, int CPL>
+hipError_t launch_chain_cpl(const Params& p, hipStream_t st) {
+    const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
+    if (p.sig_a || p.sig_b)
+        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, true>), grid, block, 0, st, p);
+    else
+        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, false>), grid, block, 0, st, p);
+    return hipGetLastError();
+}
+
+template <class IO>
+hipError_t launch_chain_io(const Params& p, int cpl, hipStream_t st) {
+    switch (cpl) {
+        case 1: return launch_chain_cpl<IO, 1>(p, st);
+        case 2: return launch_chain_cpl<IO, 2>(p, st);
+        case 4: return launch_chain_cpl<IO, 4>(p, st);
+        case 8: return launch_chain_cpl<IO, 8>(p, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+int chain_tokens() { return kChainTok; }
+
+hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* stream) {
+    const hipStream_t st = (hipStream_t)stream;
+    const int64_t n = p.B * p.Hv * p.nruns;
+    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(swr_chain_reset_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, st,
+                       p.chain_flags, n, p.chain_ctr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n == 0) return e;
+    return dtype == 1 ? launch_chain_io<IoBf16>(p, cpl, st) : launch_chain_io<IoF32>(p, cpl, st);
+}
+
+}  // namespace swr

@@ -61,6 +61,15 @@ struct Params {
     int64_t group;
     int64_t sg_b, sg_t, sg_h;
     float* gws;
+    // Exact forward in one pass (swr_chain.hip), over the B * Hv virtual
+    // sequences of dv channels (dh = D): per chunk of a sequence a
+    // publication flag, the chunk's aggregate (agg_v [.][nchunks][dv], agg_p
+    // [.][nchunks]) or its inclusive end state; a ticket counter hands out
+    // the chunks in order (nruns = chunks per sequence).
+    int32_t* chain_flags;   // [B*Hv][nchunks]
+    int32_t* chain_ctr;     // [2]: next ticket, look-back time-outs
+    float* chain_incl;      // [B*Hv][nchunks][dv]
+    float* h_last;          // [B][H][D] or NULL
 };
 
 // What a forward or backward launch computes.
@@ -172,6 +181,12 @@ hipError_t launch(const Params& p, int dtype, int D, const Shape& shape, bool ba
                   int pack, int mode, void* stream);
 
 hipError_t launch_scan(const ScanParams& q, void* stream);
+
+// The exact recurrence's forward in one pass over chunks of chain_tokens()
+// tokens (one decay per head): p.nruns chunks per sequence, p.nwork
+// persistent workgroups; the workspace arrays of p are reset first.
+int chain_tokens();
+hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* stream);
 
 // Uniform window of block tokens (the window length): forward or backward
 // over 2^hshift virtual heads of 16 * cpl channels per head; the workgroups

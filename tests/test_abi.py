@@ -323,8 +323,19 @@ def test_exact_workspace_bytes():
     nr = max(-(-16384 // info["fwd_run_len"]), -(-16384 // info["bwd_run_len"]),
              _agg_runs(16384, 8 * 16, info["bwd_run_len"]))
     assert nr == 16           # 1024-token aggregate runs: 2048 stage-I groups
-    # per (batch, head) and run: aggregate end state, entering state (D each), decay product
-    assert swr.swr_exact_workspace_bytes(p) == 8 * 16 * nr * (2 * 128 + 1) * 4
+    # the three-stage backward: per (batch, head) and run, aggregate end state,
+    # entering state (D each), decay product; the one-pass forward: two counters
+    # (16 floats), then per 128-token chunk a flag, a decay product and two end
+    # states (D each) -- the larger of the two
+    stages = 8 * 16 * nr * (2 * 128 + 1)
+    chunks = 8 * 16 * (16384 // 128)
+    chain = 16 + 2 * chunks + 2 * chunks * 128
+    assert swr.swr_exact_workspace_bytes(p) == max(stages, chain) * 4 == chain * 4
+    # float32 heads of 128 run the one-pass forward as two virtual heads of 64:
+    # a flag and a decay product per chunk of each half
+    pf = problem(B=8, T=16384, H=16, D=128, block=128, dtype=F32)
+    chain32 = 16 + 2 * (2 * chunks) + 2 * chunks * 128
+    assert swr.swr_exact_workspace_bytes(pf) == max(stages, chain32) * 4
     assert swr.swr_exact_workspace_bytes(problem(T=0)) == 0
     lib = swr.load()
     # a per-channel decay keeps one run decay product per channel
@@ -385,14 +396,14 @@ def test_exact_forward_noalloc_validation():
     assert nfwd(p, hl=H0) == E_ALIAS and nfwd(p, hl=V) == E_ALIAS and nfwd(p, y=X) == E_ALIAS
     assert nfwd(problem(D=48)) == E_UNSUP and nfwd(problem(block=48)) == E_BLOCK
     # a problem whose workspace exceeds the static array is refused with its own code
-    assert swr.SWR_NOALLOC_SCRATCH_BYTES == 16 << 20
-    assert "#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)16 << 20)" in open(HEADER).read()
-    big = problem(B=128, T=128, H=128, D=128, block=128)
+    assert swr.SWR_NOALLOC_SCRATCH_BYTES == 32 << 20
+    assert "#define SWR_NOALLOC_SCRATCH_BYTES ((int64_t)32 << 20)" in open(HEADER).read()
+    big = problem(B=128, T=256, H=128, D=128, block=128)
     assert swr.swr_exact_workspace_bytes(big) > swr.SWR_NOALLOC_SCRATCH_BYTES
     assert nfwd(big) == E_SCRATCH
     assert "SWR_NOALLOC_SCRATCH_BYTES" in swr.swr_error_string(E_SCRATCH)
     # the headline shape fits
-    assert swr.swr_exact_workspace_bytes(problem(B=8, T=16384, H=16, D=128, block=128)) <= 16 << 20
+    assert swr.swr_exact_workspace_bytes(problem(B=8, T=16384, H=16, D=128, block=128)) <= 32 << 20
     # nothing to do for an empty batch or head set, even with NULL pointers
     for kw in (dict(B=0), dict(H=0)):
         assert nfwd(problem(**kw), 0, 0, 0, 0, 0, 0, 0, 0) == OK

@@ -268,3 +268,43 @@ def test_exact_full_size_whole_tensors(swr, cid):
     outs += [("dh0", grads[4], 1, 1), ("carriers", v, 1, 1)]
     _say(f"[exact config {cid}] comparing whole tensors with the oracle")
     compare_whole(f"exact config {cid} {cfg.name}", cfg.dtype, cfg.B, cfg.H, outs, ref_chunk)
+
+CHAINED = [
+    # (B, T, H, D, block, dtype): sequences of more than 16 chunks of 128 tokens,
+    # so that the one-pass forward's boundary chunks (every 16th) publish
+    # inclusive states that the chunks after them start from
+    (1, 5000, 2, 128, 128, "f32"),   # ragged tail; float32 heads of 128 as two halves of 64
+    (2, 4500, 3, 64, 64, "bf16"),
+    (1, 4096, 1, 128, 128, "bf16"),  # the last chunk is a boundary chunk
+    (1, 2049, 2, 32, 32, "bf16"),    # the last chunk starts right after the first boundary
+    (1, 6000, 1, 16, 16, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype", CHAINED)
+def test_exact_forward_across_boundary_chunks(swr, B, T, H, D, block, dtype):
+    prob = W.random_problem(91 + T + D, B, T, H, D, block, dtype, "sigmoid", 3.0)
+    rng = np.random.default_rng(T + 7)
+    h0 = _state(rng, prob.cfg)
+    _say(f"[exact chained] B={B} T={T} H={H} D={D} l={block} {dtype}")
+    y, v, hl, _ = run_exact(swr, prob, h0, None, backward=False)
+    check_exact(prob, h0, None, y, v, hl, None, what=f"chained {B}x{T}x{H}x{D} l{block} {dtype}")
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype", [(1, 65536, 2, 64, 128, "bf16"), (1, 20000, 2, 128, 128, "f32"),
+                                                 (2, 16384, 2, 128, 64, "bf16")])
+def test_exact_forward_is_deterministic(swr, B, T, H, D, block, dtype):
+    # the chunks compose their predecessors in a fixed pattern, whatever order
+    # the workgroups reach them in: repeated calls agree bit for bit
+    prob = W.random_problem(95, B, T, H, D, block, dtype, "sigmoid", 4.0)
+    x, a, b, c = (to_device(getattr(prob, n), dtype) for n in "xabc")
+    h0 = torch.from_numpy(_state(np.random.default_rng(5), prob.cfg)).cuda()
+    _say(f"[exact determinism] B={B} T={T} H={H} D={D} l={block} {dtype}")
+    first = swr.swr_exact_forward(x, a, b, c, block, h0=h0, save_carriers=True, want_h_last=True)
+    for _ in range(3):
+        again = swr.swr_exact_forward(x, a, b, c, block, h0=h0, save_carriers=True, want_h_last=True)
+        torch.cuda.synchronize()
+        for name, u, w in zip(("y", "carriers", "h_last"), again, first):
+            assert torch.equal(u, w), name
+    ref_y, ref_hl = oracle.exact_forward(prob.x, prob.a, prob.b, prob.c, to_host(h0))
+    assert_close(to_host(first[2]), ref_hl, "bf16" if dtype == "bf16" else "f32", "determinism h_last")

@@ -77,8 +77,8 @@ def test_noalloc_after_a_larger_call_on_another_stream(swr):
 
 def test_noalloc_refuses_problems_beyond_the_static_array(swr):
     # refused during validation, before any HIP call
-    x = torch.zeros((128, 128, 128, 128), dtype=torch.bfloat16, device="cuda")
-    a = torch.zeros((128, 128, 128), dtype=torch.bfloat16, device="cuda")
+    x = torch.zeros((128, 256, 128, 128), dtype=torch.bfloat16, device="cuda")
+    a = torch.zeros((128, 256, 128), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(swr.SwrError) as err:
         swr.swr_exact_forward_noalloc(x, a, x, x, 128, y=torch.empty_like(x))
     assert err.value.code == swr.SWR_ERR_SCRATCH
