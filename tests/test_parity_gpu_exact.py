@@ -308,3 +308,70 @@ def test_exact_forward_is_deterministic(swr, B, T, H, D, block, dtype):
             assert torch.equal(u, w), name
     ref_y, ref_hl = oracle.exact_forward(prob.x, prob.a, prob.b, prob.c, to_host(h0))
     assert_close(to_host(first[2]), ref_hl, "bf16" if dtype == "bf16" else "f32", "determinism h_last")
+
+
+def _bhtd(t):
+    # stored as [B, H, T, ...], handed over as a strided [B, T, H, ...] view
+    if t.dim() == 4:
+        return t.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    return t.permute(0, 2, 1).contiguous().permute(0, 2, 1)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_forward_chained_strided_featurised_residual(swr, dtype):
+    # more than 16 chunks of 128 tokens, a [B, H, T, d] layout, the fused
+    # sigmoids and the residual, on the one-pass forward
+    prob = W.random_problem(97, 2, 2500, 3, 128, 64, dtype, "sigmoid", 3.0, logits=True)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    x, a, b, c = (_bhtd(to_device(getattr(prob, n), dtype)) for n in "xabc")
+    assert x.stride() != x.contiguous().stride()
+    h0 = _state(np.random.default_rng(11), prob.cfg)
+    _say(f"[exact chained strided] 2x2500x3x128 l64 {dtype}")
+    y, v, hl = swr.swr_exact_forward(x, a, b, c, 64, h0=torch.from_numpy(h0).cuda(), residual=True,
+                                     save_carriers=True, want_h_last=True, **feat)
+    torch.cuda.synchronize()
+    check_exact(prob, h0, None, y, v, hl, None, residual=True, what=f"chained strided {dtype}", **feat)
+
+
+def test_exact_forward_chained_optional_outputs(swr):
+    # y alone, then y with h_last alone: the same y bits as with every output
+    prob = W.random_problem(98, 1, 3000, 2, 64, 128, "bf16", "sigmoid", 3.0)
+    x, a, b, c = (to_device(getattr(prob, n), "bf16") for n in "xabc")
+    y_all, v, hl = swr.swr_exact_forward(x, a, b, c, 128, save_carriers=True, want_h_last=True)
+    y_only = swr.swr_exact_forward(x, a, b, c, 128)
+    y_hl, hl2 = swr.swr_exact_forward(x, a, b, c, 128, want_h_last=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y_only, y_all) and torch.equal(y_hl, y_all) and torch.equal(hl2, hl)
+    check_exact(prob, None, None, y_all, v, hl, None, what="chained all outputs")
+
+
+def test_exact_in_a_captured_graph(swr):
+    # forward (one pass) and backward captured once in a HIP graph, replayed
+    # with eager work between replays: every replay gives the eager results
+    prob = W.random_problem(99, 2, 2300, 2, 64, 64, "bf16", "sigmoid", 3.0)
+    x, a, b, c, dy = (to_device(getattr(prob, n), "bf16") for n in ("x", "a", "b", "c", "dy"))
+    h0 = torch.from_numpy(_state(np.random.default_rng(3), prob.cfg)).cuda()
+    y_e, v_e, hl_e = swr.swr_exact_forward(x, a, b, c, 64, h0=h0, save_carriers=True, want_h_last=True)
+    g_e = swr.swr_exact_backward(x, a, b, c, dy, v_e, 64, h0=h0, dh_last=hl_e, want_dh0=True)
+    torch.cuda.synchronize()
+    y, v, hl = torch.empty_like(y_e), torch.empty_like(v_e), torch.empty_like(hl_e)
+    outs = tuple(torch.empty_like(t) for t in g_e[:4])
+    graph = torch.cuda.CUDAGraph()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            swr.swr_exact_forward(x, a, b, c, 64, h0=h0, y=y, carriers=v, h_last=hl)
+            swr.swr_exact_backward(x, a, b, c, dy, v, 64, h0=h0, dh_last=hl, outputs=outs)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (y, v, hl) + outs:
+            t.fill_(7.0)
+        swr.swr_exact_forward(c, a, b, x, 64)   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_e) and torch.equal(v, v_e) and torch.equal(hl, hl_e), rep
+        for p_, q_ in zip(outs, g_e[:4]):
+            assert torch.equal(p_, q_), rep

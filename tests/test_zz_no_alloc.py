@@ -83,3 +83,33 @@ def test_noalloc_refuses_problems_beyond_the_static_array(swr):
         swr.swr_exact_forward_noalloc(x, a, x, x, 128, y=torch.empty_like(x))
     assert err.value.code == swr.SWR_ERR_SCRATCH
     assert "SWR_NOALLOC_SCRATCH_BYTES" in str(err.value)
+
+
+def test_noalloc_in_a_captured_graph(swr):
+    # the allocation-free exact forward captured once in a HIP graph (its
+    # flags are cleared by a kernel, not a memset) and replayed, with an eager
+    # call of another size between replays that leaves other contents in the
+    # static array: every replay gives the eager result bit for bit
+    prob = W.random_problem(90, 2, 2600, 2, 128, 128, "bf16", "sigmoid", 3.0)
+    x, a, b, c = (to_device(getattr(prob, n), "bf16") for n in "xabc")
+    other = W.random_problem(91, 1, 5000, 3, 64, 64, "bf16", "sigmoid", 3.0)
+    xo, ao, bo, co = (to_device(getattr(other, n), "bf16") for n in "xabc")
+    y_e, v_e, hl_e = swr.swr_exact_forward(x, a, b, c, 128, save_carriers=True, want_h_last=True)
+    torch.cuda.synchronize()
+    y, v, hl = torch.empty_like(y_e), torch.empty_like(v_e), torch.empty_like(hl_e)
+    graph = torch.cuda.CUDAGraph()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            swr.swr_exact_forward_noalloc(x, a, b, c, 128, y=y, carriers=v, h_last=hl)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (y, v, hl):
+            t.fill_(7.0)
+        swr.swr_exact_forward_noalloc(xo, ao, bo, co, 64)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_e) and torch.equal(v, v_e) and torch.equal(hl, hl_e), rep
