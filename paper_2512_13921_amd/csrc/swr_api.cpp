@@ -428,7 +428,8 @@ ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
 // the MFMA kernels.  A float32 head of 128 channels runs as two virtual heads
 // of 64, each its own chain of chunks: the lighter wave lets two workgroups
 // share a compute unit, which hides the look-back's latency; a bf16 head of
-// 128 stays whole (16-byte row slices a lane).  Workspace: two ticket counters
+// 128 stays whole (16-byte row slices a lane; the kernel keeps its local
+// solutions in LDS to fit two workgroups a compute unit).  Workspace: two ticket counters
 // (padded to 16 floats), then per chunk of chain_tokens() tokens of every
 // virtual sequence a flag and a decay product, then per chunk an aggregate
 // end state and an inclusive end state (a virtual head's channels each).
@@ -555,8 +556,12 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
         k.dh = (int32_t)p->D;
         k.dv = (int32_t)(16 * cw.cpl);
         k.nruns = cw.nch;
-        // persistent workgroups: as many as the compute units hold at once
-        k.nwork = std::min<int64_t>(cw.n, 256 * (cw.cpl == 8 ? 1 : cw.cpl == 1 ? 3 : 2));
+        // persistent workgroups: as many as the 256 compute units hold at once
+        // (registers: bf16 with 16 or 8 channels a lane 2 or 3, float32 with
+        // 8 channels 2, 2 and 1 channels 2 and 3)
+        const bool bf16 = p->dtype == 1;
+        const int per_cu = cw.cpl == 8 ? 2 : cw.cpl == 4 ? (bf16 ? 3 : 2) : cw.cpl == 1 ? 3 : 2;
+        k.nwork = std::min<int64_t>(cw.n, 256 * per_cu);
         return swr::launch_chain_forward(k, p->dtype, cw.cpl, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
     }
     float *wv = nullptr, *wc = nullptr, *wp = nullptr;

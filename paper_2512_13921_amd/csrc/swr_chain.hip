@@ -14,7 +14,8 @@
 // inclusive end state P S + V, the others their aggregate.  The composition
 // always takes the same chunks in the same pattern, so the results do not
 // depend on the order in which workgroups reach them; the outputs then follow
-// from the chunk's local solves, kept in registers.  Every input is read once.
+// from the chunk's local solves, kept in registers or LDS.  Every input is
+// read once (x twice with the residual and bf16 heads of 64 or 128).
 //
 // Chunks are handed out in order by a ticket counter (chunk-major over the
 // sequences), so a chunk only ever waits for chunks of lower tickets, whose
@@ -38,11 +39,12 @@ namespace {
 constexpr int kChainTW = 8;                // waves per workgroup, one sub-block each
 constexpr int kChainTok = kChainTW * SB;   // tokens per chunk
 constexpr int kFlagAgg = 1, kFlagIncl = 2;
-// Chunks kChainK - 1, 2 kChainK - 1, ... of a sequence publish their inclusive
-// end state, the others their aggregate; every chunk composes the aggregates
-// since the last such boundary, kChainQ per lane group (four groups).
-constexpr int kChainQ = 4;
-constexpr int kChainK = 4 * kChainQ;
+// Chunks K - 1, 2 K - 1, ... of a sequence publish their inclusive end state,
+// the others their aggregate; every chunk composes the aggregates since the
+// last such boundary, Q per lane group (four groups, K = 4 Q).  Q = 2 where
+// the kernel is held to 80 registers, else 4.
+template <int CPL, bool WL>
+constexpr int chain_q() { return WL && CPL <= 4 ? 2 : 4; }
 // device-coherent (sc1) vector loads of published values
 constexpr int kCoherent = 16;
 constexpr int kSpinLimit = 1 << 16;
@@ -64,17 +66,29 @@ __device__ inline void writes_complete() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// bf16 lanes of 8 or 16 channels (heads of 64 and 128): the local solutions
+// wait for the look-back in LDS instead of registers, and x is loaded again
+// for the residual, so that the kernel fits 127 registers (two workgroups a
+// compute unit) or 80 (three); the launcher sizes its grid to match.
+template <class IO, int CPL>
+constexpr bool chain_w_in_lds() { return (CPL == 8 || CPL == 4) && IO::ES == 2; }
+template <class IO, int CPL>
+constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL == 8 ? 4 : 6) : 1; }
+
 template <class IO, int CPL, bool FEAT>
-__global__ __launch_bounds__(kChainTW * 64, 1) void swr_fwd_chain_kernel(Params p) {
+__global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) void swr_fwd_chain_kernel(Params p) {
     constexpr int TW = kChainTW;
     constexpr int TOK = kChainTok;
     constexpr int D = CPL * SB;
     constexpr int ES = IO::ES;
     using RW = Row<IO, CPL>;
+    constexpr bool WL = chain_w_in_lds<IO, CPL>();
+    constexpr int kChainQ = chain_q<CPL, WL>(), kChainK = 4 * kChainQ;
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
     __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[TW];       // decay product of each sub-block
     __shared__ float s_pre[D];      // the exact state entering the chunk
+    __shared__ f32x4 s_W[WL ? TW : 1][WL ? CPL : 1][WL ? 64 : 1];   // WL: each lane's local solution
     __shared__ int64_t s_ticket[2];
 
     const Lanes ln = lanes();
@@ -112,14 +126,12 @@ __global__ __launch_bounds__(kChainTW * 64, 1) void swr_fwd_chain_kernel(Params 
         RW xr[4], br[4], cr[4];
         {
             const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
-                                         rb = rsrc((const char*)p.b + xo + r0 * rs),
-                                         rc = rsrc((const char*)p.c + xo + r0 * rs);
+                                         rb = rsrc((const char*)p.b + xo + r0 * rs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
                 xr[r].template load<kFwdLoad>(rx, o);
                 br[r].template load<kFwdLoad>(rb, o);
-                cr[r].template load<kFwdLoad>(rc, o);
             }
         }
         const bool a_ok = r0 + n < p.T;
@@ -144,6 +156,16 @@ __global__ __launch_bounds__(kChainTW * 64, 1) void swr_fwd_chain_kernel(Params 
             for (int m = 0; m < CPL; ++m) s_wl[tw][n * CPL + m] = W[m][3];
         }
         if (lane == 63) s_c[tw] = dk.c;
+        if constexpr (WL) {   // (read back by the same lane)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_W[tw][m][lane] = W[m];
+        }
+        {   // c is needed for the outputs only: its loads go out now and land during the look-back
+            const __amdgpu_buffer_rsrc_t rc = rsrc((const char*)p.c + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                cr[r].template load<kFwdLoad>(rc, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)));
+        }
         lds_barrier();
 
         // ---- wave 0: the chunk's aggregate, the look-back, the inclusive state -----
@@ -273,13 +295,29 @@ __global__ __launch_bounds__(kChainTW * 64, 1) void swr_fwd_chain_kernel(Params 
             for (int m = 0; m < CPL; ++m) e[m] = __builtin_fmaf(c_, e[m], s_wl[r][n * CPL + m]);
         }
         const __amdgpu_buffer_rsrc_t ry = rsrc((char*)p.y + xo + r0 * rs);
+        f32x4 Wo[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            if constexpr (WL) Wo[m] = s_W[tw][m][lane];
+            else Wo[m] = W[m];
+        }
+        RW xres[4];   // the residual's x: WL loads it again rather than keep it through the look-back
+        if constexpr (WL) {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                xres[r].template load<kFwdLoad>(rx, in_range(p.residual && tr0 + r < p.T, loff + (uint32_t)(r * rs)));
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) xres[r] = xr[r];
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             float yv[CPL];
 #pragma unroll
             for (int m = 0; m < CPL; ++m) {
-                yv[m] = cr[r].get(m) * __builtin_fmaf(dk.G[r], e[m], W[m][r]);
-                if (p.residual) yv[m] += xr[r].get(m);
+                yv[m] = cr[r].get(m) * __builtin_fmaf(dk.G[r], e[m], Wo[m][r]);
+                if (p.residual) yv[m] += xres[r].get(m);
             }
             store_row<IO, CPL, kFwdStore>(ry, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)), yv);
         }
