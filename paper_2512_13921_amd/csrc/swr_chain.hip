@@ -41,10 +41,14 @@ constexpr int kChainTok = kChainTW * SB;   // tokens per chunk
 constexpr int kFlagAgg = 1, kFlagIncl = 2;
 // Chunks K - 1, 2 K - 1, ... of a sequence publish their inclusive end state,
 // the others their aggregate; every chunk composes the aggregates since the
-// last such boundary, Q per lane group (four groups, K = 4 Q).  Q = 2 where
-// the kernel is held to 80 registers, else 4.
+// last such boundary, Q per lane group (four groups, K = 4 Q), loaded QB at a
+// time: 2 where the kernel is held to 80 registers, else 4.  A longer K
+// shortens the chain of boundaries; a second batch of loads lengthens every
+// chunk's look-back: Q = 2 (one batch) for the 80-register kernels on
+// sequences shorter than kLongChain chunks, else Q = 4.
+constexpr int64_t kLongChain = 256;
 template <int CPL, bool WL>
-constexpr int chain_q() { return WL && CPL <= 4 ? 2 : 4; }
+constexpr int chain_qb() { return WL && CPL <= 4 ? 2 : 4; }
 // device-coherent (sc1) vector loads of published values
 constexpr int kCoherent = 16;
 constexpr int kSpinLimit = 1 << 16;
@@ -75,7 +79,7 @@ constexpr bool chain_w_in_lds() { return (CPL == 8 || CPL == 4) && IO::ES == 2; 
 template <class IO, int CPL>
 constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL == 8 ? 4 : 6) : 1; }
 
-template <class IO, int CPL, bool FEAT>
+template <class IO, int CPL, bool FEAT, int Q>
 __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) void swr_fwd_chain_kernel(Params p) {
     constexpr int TW = kChainTW;
     constexpr int TOK = kChainTok;
@@ -83,7 +87,8 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
     constexpr int ES = IO::ES;
     using RW = Row<IO, CPL>;
     constexpr bool WL = chain_w_in_lds<IO, CPL>();
-    constexpr int kChainQ = chain_q<CPL, WL>(), kChainK = 4 * kChainQ;
+    constexpr int QB = chain_qb<CPL, WL>();
+    constexpr int kChainQ = Q, kChainK = 4 * Q;   // aggregates a lane group folds; the boundary interval
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
     __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[TW];       // decay product of each sub-block
@@ -222,34 +227,40 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
 #pragma unroll
             for (int m = 0; m < CPL; ++m) gV[m] = 0.f;
             {
-                Row<IoF32, CPL> rv[kChainQ];
-                float pj[kChainQ];
                 const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0);
 #pragma unroll
-                for (int q = 0; q < kChainQ; ++q) {
-                    const int i = grp * kChainQ + q;
-                    const int64_t j = kb + 1 + i;
-                    rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
-                    pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                          rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
-                }
+                for (int q0 = 0; q0 < kChainQ; q0 += QB) {   // QB aggregates in flight at a time
+                    Row<IoF32, CPL> rv[QB];
+                    float pj[QB];
 #pragma unroll
-                for (int q = 0; q < kChainQ; ++q) {
-                    const float pq = grp * kChainQ + q < cnt ? pj[q] : 1.0f;
+                    for (int q = 0; q < QB; ++q) {
+                        const int i = grp * kChainQ + q0 + q;
+                        const int64_t j = kb + 1 + i;
+                        rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
+                        pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                              rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
+                    }
 #pragma unroll
-                    for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
-                    gP *= pq;
+                    for (int q = 0; q < QB; ++q) {
+                        const float pq = grp * kChainQ + q0 + q < cnt ? pj[q] : 1.0f;
+#pragma unroll
+                        for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
+                        gP *= pq;
+                    }
+                    if constexpr (QB < kChainQ) __builtin_amdgcn_sched_barrier(0);   // one batch live at a time
                 }
             }
+            // the boundary's inclusive state, or the initial state (zero without h0)
             float pre[CPL];
-            if (kb >= 0) {
+            {
                 Row<IoF32, CPL> ri;
-                ri.template load<kCoherent>(rsrc(p.chain_incl + slot0 * D), (uint32_t)(kb * D + vch) * 4u);
+                if (kb >= 0)
+                    ri.template load<kCoherent>(rsrc(p.chain_incl + slot0 * D), (uint32_t)(kb * D + vch) * 4u);
+                else
+                    ri.load(rsrc(p.h0 ? p.h0 + rseq * DH + coff : p.chain_incl),
+                            in_range(p.h0 != nullptr, (uint32_t)vch * 4u));
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) pre[m] = ri.get(m);
-            } else {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) pre[m] = p.h0 ? p.h0[rseq * DH + coff + vch + m] : 0.f;
             }
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
@@ -276,11 +287,9 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
             if (grp == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
-                if (p.h_last && ch == nch - 1) {
-#pragma unroll
-                    for (int m = 0; m < CPL; ++m) p.h_last[rseq * DH + coff + vch + m] = I[m];
-                }
             }
+            store_row<IoF32, CPL>(rsrc(p.h_last ? p.h_last + rseq * DH + coff : p.chain_incl),
+                                  in_range(p.h_last && ch == nch - 1 && grp == 0, (uint32_t)vch * 4u), I);
         }
         lds_barrier();
 
@@ -341,14 +350,22 @@ __global__ __launch_bounds__(256) void swr_chain_reset_kernel(int32_t* flags, in
     if (blockIdx.x == 0 && threadIdx.x < 2) ctr[threadIdx.x] = 0;
 }
 
-template <class IO, int CPL>
-hipError_t launch_chain_cpl(const Params& p, hipStream_t st) {
+template <class IO, int CPL, int Q>
+hipError_t launch_chain_q(const Params& p, hipStream_t st) {
     const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
     if (p.sig_a || p.sig_b)
-        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, true>), grid, block, 0, st, p);
+        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, true, Q>), grid, block, 0, st, p);
     else
-        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, false>), grid, block, 0, st, p);
+        hipLaunchKernelGGL((swr_fwd_chain_kernel<IO, CPL, false, Q>), grid, block, 0, st, p);
     return hipGetLastError();
+}
+
+template <class IO, int CPL>
+hipError_t launch_chain_cpl(const Params& p, hipStream_t st) {
+    if constexpr (chain_qb<CPL, chain_w_in_lds<IO, CPL>()>() == 2) {
+        if (p.nruns < kLongChain) return launch_chain_q<IO, CPL, 2>(p, st);
+    }
+    return launch_chain_q<IO, CPL, 4>(p, st);
 }
 
 template <class IO>

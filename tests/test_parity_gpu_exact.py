@@ -271,12 +271,15 @@ def test_exact_full_size_whole_tensors(swr, cid):
 
 CHAINED = [
     # (B, T, H, D, block, dtype): sequences of more than 16 chunks of 128 tokens,
-    # so that the one-pass forward's boundary chunks (every 16th) publish
-    # inclusive states that the chunks after them start from
+    # so that the one-pass forward's boundary chunks (every 16th; every 8th for
+    # bf16 heads of 64 on sequences of fewer than 256 chunks) publish inclusive
+    # states that the chunks after them start from
     (1, 5000, 2, 128, 128, "f32"),   # ragged tail; float32 heads of 128 as two halves of 64
     (2, 4500, 3, 64, 64, "bf16"),
     (1, 4096, 1, 128, 128, "bf16"),  # the last chunk is a boundary chunk
+    (1, 3072, 2, 64, 64, "bf16"),    # the same with boundaries every 8th chunk
     (1, 2049, 2, 32, 32, "bf16"),    # the last chunk starts right after the first boundary
+    (1, 1025, 2, 64, 128, "bf16"),   # the same with boundaries every 8th chunk
     (1, 6000, 1, 16, 16, "f32"),
 ]
 
