@@ -463,6 +463,20 @@ bool use_chain(const swr_problem_t* p, const Resolved& r) {
     return SWR_EXACT_CHAIN && !r.pc && r.pack == 1 && !r.empty && chain_ws(p).n < ((int64_t)1 << 30);
 }
 
+// The backward in one pass, for heads of up to 64 channels on sequences of
+// 256 chunks or more, where it measured faster than the three stages (B1
+// T131072 H32 d64: 1047 -> 1000 us); on shorter sequences (B16 T8192 H32
+// d64: 957 -> 970 us) and with 128 channels (983 -> 1208 us: one workgroup a
+// compute unit, whose look-back nothing covers) it is slower.
+#ifndef SWR_EXACT_CHAIN_BWD
+#define SWR_EXACT_CHAIN_BWD 1
+#endif
+bool use_chain_bwd(const swr_problem_t* p, const Resolved& r) {
+    if (!SWR_EXACT_CHAIN_BWD || !use_chain(p, r)) return false;
+    const ChainWs cw = chain_ws(p);
+    return cw.hs == 0 && cw.cpl <= 4 && cw.nch >= 256;
+}
+
 // Workspace of the exact calls for one plan: the three-stage arrays (the
 // backward's, and the forward's when it does not run in one pass) or the
 // one-pass forward's, whichever is larger.
@@ -597,10 +611,11 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     if (rc != SWR_OK) return rc;
     if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
+    const int64_t wfloats = exact_ws_floats(p, r);
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
     if (!r.empty && (!x || !a || !b || !c || !dy || !carriers || !dx || !da || !db || !dc)) return SWR_ERR_NULL;
-    if (w.floats > 0 && !workspace) return SWR_ERR_NULL;
+    if (wfloats > 0 && !workspace) return SWR_ERR_NULL;
     for (const void* q : {(const void*)h0, (const void*)dh_last, (const void*)dh0, (const void*)carriers,
                           (const void*)workspace})
         if (q && !aligned(q, 16)) return SWR_ERR_ALIGN;
@@ -615,7 +630,7 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
                          span(a, r.aspan * r.es), span(carriers, carriers ? r.carriers * 4 : 0),
                          span(h0, h0 ? sbytes : 0), span(dh_last, dh_last ? sbytes : 0)};
     const Span outs[6] = {span(dx, r.xspan), span(db, r.xspan), span(dc, r.xspan), span(da, r.aspan * 4),
-                          span(dh0, dh0 ? sbytes : 0), span(workspace, w.floats * 4)};
+                          span(dh0, dh0 ? sbytes : 0), span(workspace, wfloats * 4)};
     for (int i = 0; i < 6; ++i) {
         for (const Span& s : ins)
             if (overlap(outs[i], s)) return SWR_ERR_ALIAS;
@@ -623,6 +638,23 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
             if (overlap(outs[i], outs[j])) return SWR_ERR_ALIAS;
     }
 
+    if (use_chain_bwd(p, r)) {   // one pass: chunks from the sequences' ends, chained by a look-back
+        const ChainWs cw = chain_ws(p);
+        float* f = (float*)workspace;
+        swr::Params k = make_params(p, r, true);
+        k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;
+        k.dx = dx; k.da = da; k.db = db; k.dc = dc;
+        k.carriers = const_cast<float*>(carriers); k.h0 = h0; k.dh_last = dh_last; k.dh0 = dh0;
+        k.chain_ctr = (int32_t*)f;
+        k.chain_flags = (int32_t*)(f + 16);
+        k.agg_p = f + 16 + cw.n;
+        k.agg_v = f + 16 + 2 * cw.n;
+        k.chain_incl = k.agg_v + cw.n * p->D;
+        k.nruns = cw.nch;
+        // persistent workgroups: as many as the 256 compute units hold at once
+        k.nwork = std::min<int64_t>(cw.n, 256 * (cw.cpl == 8 ? 1 : 2));
+        return swr::launch_chain_backward(k, p->dtype, cw.cpl, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    }
     float *wv = nullptr, *wc = nullptr, *wp = nullptr;
     if (w.floats > 0) exact_arrays(p, w, workspace, &wv, &wc, &wp);
     swr::Params k = make_params(p, r, true);

@@ -79,6 +79,115 @@ constexpr bool chain_w_in_lds() { return (CPL == 8 || CPL == 4) && IO::ES == 2; 
 template <class IO, int CPL>
 constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL == 8 ? 4 : 6) : 1; }
 
+// Wave 0's part in the chain for chunk ci of a sequence (chunks slot0 ...
+// slot0 + nch - 1 of the workspace arrays, in chain order): publish the
+// chunk's aggregate (V, P), wait for the last boundary's inclusive value and
+// the aggregates after it, compose them in a fixed pattern (lane group g
+// folds chunks kb+1+Q*g ... kb+Q*(g+1) in order, then the groups' results
+// are applied to the boundary value in order), and at a boundary publish the
+// chunk's own inclusive value.  `in` is the value entering the chain's first
+// chunk (this lane's slice; NULL for zero).  Returns the value entering the
+// chunk and the one leaving it (I = P in + V).
+template <int CPL, int Q, int QB>
+__device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, int64_t nch, const float (&V)[CPL],
+                                  float P, const float* in, int lane, int grp, int n, float (&pre)[CPL],
+                                  float (&I)[CPL]) {
+    constexpr int D = CPL * SB, K = 4 * Q;
+    const uint32_t vch = (uint32_t)(n * CPL);
+    const int64_t slot = slot0 + ci;
+    const bool boundary = ci % K == K - 1;
+    // the last boundary chunk before this one (or none), and the chunks in between
+    const int64_t kb = ci / K * K - 1;
+    const int cnt = (int)(ci - 1 - kb);
+    if (!boundary && ci + 1 < nch) {   // later chunks of the group compose this aggregate
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) put_coherent(p.agg_v + slot * D + vch + m, V[m]);
+        }
+        if (lane == 0) put_coherent(p.agg_p + slot, P);
+        writes_complete();
+        if (lane == 0) put_flag(p.chain_flags + slot, kFlagAgg);
+    }
+    // wait until the boundary's inclusive value and the aggregates in
+    // between are published: lane i < cnt polls chunk kb + 1 + i, lane 63 the boundary
+    bool timed_out = false;
+    int spins = 0;
+#pragma unroll 1
+    for (;;) {
+        bool ok = true;
+        if (lane < cnt)
+            ok = get_flag(p.chain_flags + slot0 + kb + 1 + lane) == kFlagAgg;
+        else if (lane == 63 && kb >= 0)
+            ok = get_flag(p.chain_flags + slot0 + kb) == kFlagIncl;
+        if (__all(ok)) break;
+        if (++spins > kSpinLimit) {   // never expected: count it, poison the outputs
+            if (lane == 0) atomicAdd(p.chain_ctr + 1, 1);
+            timed_out = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    float gV[CPL], gP = 1.0f;
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) gV[m] = 0.f;
+    {
+        const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0);
+#pragma unroll
+        for (int q0 = 0; q0 < Q; q0 += QB) {   // QB aggregates in flight at a time
+            Row<IoF32, CPL> rv[QB];
+            float pj[QB];
+#pragma unroll
+            for (int q = 0; q < QB; ++q) {
+                const int i = grp * Q + q0 + q;
+                const int64_t j = kb + 1 + i;
+                rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
+                pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                      rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
+            }
+#pragma unroll
+            for (int q = 0; q < QB; ++q) {
+                const float pq = grp * Q + q0 + q < cnt ? pj[q] : 1.0f;
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
+                gP *= pq;
+            }
+            if constexpr (QB < Q) __builtin_amdgcn_sched_barrier(0);   // one batch live at a time
+        }
+    }
+    // the boundary's inclusive value, or the chain's entering value (zero without one)
+    {
+        Row<IoF32, CPL> ri;
+        if (kb >= 0)
+            ri.template load<kCoherent>(rsrc(p.chain_incl + slot0 * D), (uint32_t)(kb * D + vch) * 4u);
+        else
+            ri.load(rsrc(in ? in : p.chain_incl), in_range(in != nullptr, vch * 4u));
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) pre[m] = ri.get(m);
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int src = g * 16 + n;
+        const float pg = __shfl(gP, src);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg, pre[m], __shfl(gV[m], src));
+    }
+    if (timed_out) {
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_nanf("");
+    }
+#pragma unroll
+    for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P, pre[m], V[m]);
+    if (boundary && ci + 1 < nch) {
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) put_coherent(p.chain_incl + slot * D + vch + m, I[m]);
+        }
+        writes_complete();
+        if (lane == 0) put_flag(p.chain_flags + slot, kFlagIncl);
+    }
+}
+
 template <class IO, int CPL, bool FEAT, int Q>
 __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) void swr_fwd_chain_kernel(Params p) {
     constexpr int TW = kChainTW;
@@ -88,7 +197,6 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
     using RW = Row<IO, CPL>;
     constexpr bool WL = chain_w_in_lds<IO, CPL>();
     constexpr int QB = chain_qb<CPL, WL>();
-    constexpr int kChainQ = Q, kChainK = 4 * Q;   // aggregates a lane group folds; the boundary interval
     const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
     __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
     __shared__ float s_c[TW];       // decay product of each sub-block
@@ -186,104 +294,9 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
                 P *= c_;
             }
             const uint32_t vch = (uint32_t)(n * CPL);
-            const int64_t slot0 = seq * nch;
-            const bool boundary = ch % kChainK == kChainK - 1;
-            // the last boundary chunk before this one (or none), and the chunks in between
-            const int64_t kb = ch / kChainK * kChainK - 1;
-            const int cnt = (int)(ch - 1 - kb);
-            if (!boundary && ch + 1 < nch) {   // later chunks of the group compose this aggregate
-                if (grp == 0) {
-#pragma unroll
-                    for (int m = 0; m < CPL; ++m) put_coherent(p.agg_v + slot * D + vch + m, V[m]);
-                }
-                if (lane == 0) put_coherent(p.agg_p + slot, P);
-                writes_complete();
-                if (lane == 0) put_flag(p.chain_flags + slot, kFlagAgg);
-            }
-            // wait until the boundary's inclusive state and the aggregates in
-            // between are published: lane i < cnt polls chunk kb + 1 + i, lane 63 the boundary
-            bool timed_out = false;
-            int spins = 0;
-#pragma unroll 1
-            for (;;) {
-                bool ok = true;
-                if (lane < cnt)
-                    ok = get_flag(p.chain_flags + slot0 + kb + 1 + lane) == kFlagAgg;
-                else if (lane == 63 && kb >= 0)
-                    ok = get_flag(p.chain_flags + slot0 + kb) == kFlagIncl;
-                if (__all(ok)) break;
-                if (++spins > kSpinLimit) {   // never expected: count it, poison the outputs
-                    if (lane == 0) atomicAdd(p.chain_ctr + 1, 1);
-                    timed_out = true;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-            __atomic_signal_fence(__ATOMIC_SEQ_CST);
-            // compose in a fixed pattern, so that the result does not depend on
-            // timing: lane group g folds chunks kb+1+Q*g ... kb+Q*(g+1) in order,
-            // then the groups' compositions are applied to the boundary state in order
-            float gV[CPL], gP = 1.0f;
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) gV[m] = 0.f;
-            {
-                const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0);
-#pragma unroll
-                for (int q0 = 0; q0 < kChainQ; q0 += QB) {   // QB aggregates in flight at a time
-                    Row<IoF32, CPL> rv[QB];
-                    float pj[QB];
-#pragma unroll
-                    for (int q = 0; q < QB; ++q) {
-                        const int i = grp * kChainQ + q0 + q;
-                        const int64_t j = kb + 1 + i;
-                        rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
-                        pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                              rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
-                    }
-#pragma unroll
-                    for (int q = 0; q < QB; ++q) {
-                        const float pq = grp * kChainQ + q0 + q < cnt ? pj[q] : 1.0f;
-#pragma unroll
-                        for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
-                        gP *= pq;
-                    }
-                    if constexpr (QB < kChainQ) __builtin_amdgcn_sched_barrier(0);   // one batch live at a time
-                }
-            }
-            // the boundary's inclusive state, or the initial state (zero without h0)
-            float pre[CPL];
-            {
-                Row<IoF32, CPL> ri;
-                if (kb >= 0)
-                    ri.template load<kCoherent>(rsrc(p.chain_incl + slot0 * D), (uint32_t)(kb * D + vch) * 4u);
-                else
-                    ri.load(rsrc(p.h0 ? p.h0 + rseq * DH + coff : p.chain_incl),
-                            in_range(p.h0 != nullptr, (uint32_t)vch * 4u));
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) pre[m] = ri.get(m);
-            }
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int src = g * 16 + n;
-                const float pg = __shfl(gP, src);
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg, pre[m], __shfl(gV[m], src));
-            }
-            if (timed_out) {
-#pragma unroll
-                for (int m = 0; m < CPL; ++m) pre[m] = __builtin_nanf("");
-            }
-            float I[CPL];
-#pragma unroll
-            for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P, pre[m], V[m]);
-            if (boundary && ch + 1 < nch) {
-                if (grp == 0) {
-#pragma unroll
-                    for (int m = 0; m < CPL; ++m) put_coherent(p.chain_incl + slot * D + vch + m, I[m]);
-                }
-                writes_complete();
-                if (lane == 0) put_flag(p.chain_flags + slot, kFlagIncl);
-            }
+            float pre[CPL], I[CPL];
+            chain_link<CPL, Q, QB>(p, seq * nch, ch, nch, V, P, p.h0 ? p.h0 + rseq * DH + coff : nullptr, lane, grp,
+                                   n, pre, I);
             if (grp == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
@@ -344,6 +357,226 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
     }
 }
 
+// The exact recurrence's backward in one pass (mirror of the forward above):
+// the chunks are taken from each sequence's end, chain index ci = nch - 1 -
+// chunk.  A chunk's aggregate is the adjoint its first token sends towards
+// the previous one when nothing enters from its end (the reverse local solve
+// D = L^T dh, dh = c * dy, composed over the sub-blocks) and its decay
+// product; the value entering a chunk is the adjoint entering from its end
+// (dh_last for the last chunk).  The forward states come from the exact
+// block carriers (h0 before the first block), as in the three-stage
+// backward, and the gradients of a token are those of Sec. 4.2.2 without the
+// window's truncation term:  du = D + R eps_in,  dx = b du,  db = x du,
+// dc = dy h,  da = sum over channels of h_{t-1} du.
+// Lanes of 8 or 16 channels park both local solutions in LDS through the
+// look-back (64 or 128 KB a workgroup): 16 channels to fit one workgroup a
+// compute unit without spilling, 8 to fit two.
+template <int CPL>
+constexpr bool chain_bwd_park() { return CPL >= 4; }
+
+template <class IO, int CPL, bool FEAT, int Q>
+__global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_chain_kernel(Params p) {
+    constexpr int TW = kChainTW;
+    constexpr int TOK = kChainTok;
+    constexpr int D = CPL * SB;
+    constexpr int ES = IO::ES;
+    constexpr bool PARK = chain_bwd_park<CPL>();
+    using RW = Row<IO, CPL>;
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
+    __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve L u
+    __shared__ float s_df[TW][D];   // a_0 * first row of each sub-block's L^T dh
+    __shared__ float s_c[TW];       // decay product of each sub-block
+    __shared__ float s_eps[D];      // the adjoint entering the chunk from its end
+    __shared__ f32x4 s_W[PARK ? TW : 1][PARK ? 2 * CPL : 1][PARK ? 64 : 1];   // PARK: W and Dl of each lane
+    __shared__ int64_t s_ticket[2];
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    const int64_t S = p.B * p.H, nch = p.nruns, N = S * nch;
+    const int64_t rs = p.sx_t * ES, as = p.sa_t * ES, das = p.sa_t * 4;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const uint32_t daoff = (uint32_t)(4 * grp) * (uint32_t)das;
+    const uint32_t vch = (uint32_t)(n * CPL);
+    const int base = lane & 48;   // first lane of this 16-lane row
+
+    int par = 0;
+    auto grab = [&]() {
+        if (threadIdx.x == 0) s_ticket[par] = atomicAdd(p.chain_ctr, 1);
+        lds_barrier();
+        const int64_t t = s_ticket[par];
+        par ^= 1;
+        return t;
+    };
+    int64_t ticket = grab();
+    for (;;) {
+        if (ticket >= N) break;
+        const int64_t seq = ticket % S, ci = ticket / S;   // chunk-major from the sequences' ends
+        const int64_t ch = nch - 1 - ci;
+        const int64_t xo = (seq / p.H * p.sx_b + seq % p.H * p.sx_h) * ES;
+        const int64_t ao = seq / p.H * p.sa_b + seq % p.H * p.sa_h;
+        const int64_t t0 = ch * TOK, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+
+        // ---- loads -------------------------------------------------------------------
+        RW xr[4], br[4], cr[4], dyr[4];
+        {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
+                                         rb = rsrc((const char*)p.b + xo + r0 * rs),
+                                         rc = rsrc((const char*)p.c + xo + r0 * rs),
+                                         rdy = rsrc((const char*)p.dy + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
+                xr[r].template load<kBwdLoad>(rx, o);
+                br[r].template load<kBwdLoad>(rb, o);
+                cr[r].template load<kBwdLoad>(rc, o);
+                dyr[r].template load<kBwdLoad>(rdy, o);
+            }
+        }
+        const bool a_ok = r0 + n < p.T;
+        float a_n = load_scalar<IO, kBwdDecay>(rsrc((const char*)p.a + ao * ES + r0 * as), in_range(a_ok, aoff));
+        float ds_n = 1.0f;   // d a / d(input) of token n: 1, or sigma'(z) for a logit z
+        if (sig_a) {
+            const SigSlope g = sigmoid_slope(a_n);
+            ds_n = g.ds;
+            a_n = g.s;
+        }
+        if (!a_ok) a_n = 1.0f;   // past the end the adjoint entering from the end passes intact
+
+        // ---- local solves: W = L (b x) and Dl = L^T dh ----------------------------------
+        const Decay dk = build_decay(a_n, grp, n);
+        f32x4 W[CPL], Dl[CPL];
+        {
+            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L);
+            float LT[4];
+            build_decay_transposed(a_n, grp, n, LT);
+            const typename Contract<IO>::A At = Contract<IO>::prep(LT);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                float u[4], d4[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
+                    d4[q] = dyr[q].get(m) * cr[q].get(m);   // dh = c dy
+                }
+                W[m] = Contract<IO>::run(A, u);
+                Dl[m] = Contract<IO>::run(At, d4);
+            }
+        }
+        const float a0 = shfl(a_n, 0);
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_wl[tw][n * CPL + m] = W[m][3];
+        }
+        if (grp == 0) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) s_df[tw][n * CPL + m] = a0 * Dl[m][0];
+        }
+        if (lane == 63) s_c[tw] = dk.c;
+        if constexpr (PARK) {   // (read back by the same lane)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { s_W[tw][m][lane] = W[m]; s_W[tw][CPL + m][lane] = Dl[m]; }
+        }
+        // the exact state entering the chunk (the carrier of the block before it,
+        // or h0): requested now, needed after the look-back
+        Row<IoF32, CPL> vr;
+        if (t0 == 0)
+            vr.load(rsrc(p.h0 ? p.h0 + seq * D : p.carriers), in_range(p.h0 != nullptr, vch * 4u));
+        else
+            vr.load(rsrc(p.carriers + seq * p.nblocks * D), (uint32_t)(((t0 >> p.lshift) - 1) * D + vch) * 4u);
+        lds_barrier();
+
+        // ---- wave 0: the chunk's reverse aggregate, the look-back, dh0 -------------------
+        if (tw == 0) {
+            float V[CPL], P = 1.0f;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) V[m] = 0.f;
+#pragma unroll 1
+            for (int r = TW - 1; r >= 0; --r) {
+                const float c_ = s_c[r];
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) V[m] = __builtin_fmaf(c_, V[m], s_df[r][n * CPL + m]);
+                P *= c_;
+            }
+            float pre[CPL], I[CPL];
+            chain_link<CPL, Q, 4>(p, seq * nch, ci, nch, V, P, p.dh_last ? p.dh_last + seq * D : nullptr, lane,
+                                  grp, n, pre, I);
+            if (grp == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) s_eps[vch + m] = pre[m];
+            }
+            store_row<IoF32, CPL>(rsrc(p.dh0 ? p.dh0 + seq * D : p.chain_incl),
+                                  in_range(p.dh0 && ch == 0 && grp == 0, vch * 4u), I);
+        }
+        lds_barrier();
+
+        // ---- the exact state entering this wave's sub-block, the adjoint entering it from its end
+        float ein[CPL], epsin[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) { ein[m] = vr.get(m); epsin[m] = s_eps[vch + m]; }
+#pragma unroll 1
+        for (int r = 0; r < tw; ++r) {
+            const float c_ = s_c[r];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) ein[m] = __builtin_fmaf(c_, ein[m], s_wl[r][n * CPL + m]);
+        }
+#pragma unroll 1
+        for (int r = TW - 1; r > tw; --r) {
+            const float c_ = s_c[r];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) epsin[m] = __builtin_fmaf(c_, epsin[m], s_df[r][n * CPL + m]);
+        }
+
+        // ---- gradients -------------------------------------------------------------------
+        if constexpr (PARK) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { W[m] = s_W[tw][m][lane]; Dl[m] = s_W[tw][CPL + m][lane]; }
+        }
+        // H = W + g * e_in: the exact state of each row
+#pragma unroll
+        for (int m = 0; m < CPL; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) W[m][r] = __builtin_fmaf(dk.G[r], ein[m], W[m][r]);
+        float hup[CPL];   // state entering this lane's first row
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) {
+            const float v = shfl(W[m][3], (lane - 16) & 63);
+            hup[m] = grp == 0 ? ein[m] : v;
+        }
+        float Rr[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Rr[r] = shfl(dk.L[r], base + 15);   // r_q = L[15][.] at this lane's rows
+        const __amdgpu_buffer_rsrc_t rdx = rsrc((char*)p.dx + xo + r0 * rs), rdb = rsrc((char*)p.db + xo + r0 * rs),
+                                     rdc = rsrc((char*)p.dc + xo + r0 * rs), rda = rsrc(p.da + ao + r0 * p.sa_t);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float vdx[CPL], vdb[CPL], vdc[CPL], acc = 0.0f;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const float dyv = dyr[r].get(m);
+                vdc[m] = dyv * W[m][r];
+                const float du = __builtin_fmaf(Rr[r], epsin[m], Dl[m][r]);   // adjoint of u
+                const float zb = FEAT ? fresh(br[r].get(m)) : br[r].get(m);
+                const SigSlope g = sig_b ? sigmoid_slope(zb) : SigSlope{zb, 1.0f};
+                vdx[m] = g.s * du;
+                if (p.residual) vdx[m] += dyv;
+                vdb[m] = xr[r].get(m) * du * g.ds;
+                acc = __builtin_fmaf(r == 0 ? hup[m] : W[m][r - 1], du, acc);
+            }
+            const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
+            const bool ok = tr0 + r < p.T;
+            const uint32_t o = in_range(ok, loff + (uint32_t)(r * rs));
+            store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
+            store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
+            store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, tot), rda,
+                                                  (int)in_range(n == 0 && ok, daoff + (uint32_t)(r * das)), 0,
+                                                  kBwdStore);
+        }
+        ticket = grab();
+    }
+}
+
 // Zeroes the chunk flags and the ticket counters before a launch.
 __global__ __launch_bounds__(256) void swr_chain_reset_kernel(int32_t* flags, int64_t n, int32_t* ctr) {
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) flags[i] = 0;
@@ -379,6 +612,34 @@ hipError_t launch_chain_io(const Params& p, int cpl, hipStream_t st) {
     }
 }
 
+template <class IO, int CPL>
+hipError_t launch_chain_bwd_cpl(const Params& p, hipStream_t st) {
+    const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
+    if (p.sig_a || p.sig_b)
+        hipLaunchKernelGGL((swr_bwd_chain_kernel<IO, CPL, true, 4>), grid, block, 0, st, p);
+    else
+        hipLaunchKernelGGL((swr_bwd_chain_kernel<IO, CPL, false, 4>), grid, block, 0, st, p);
+    return hipGetLastError();
+}
+
+template <class IO>
+hipError_t launch_chain_bwd_io(const Params& p, int cpl, hipStream_t st) {
+    switch (cpl) {
+        case 1: return launch_chain_bwd_cpl<IO, 1>(p, st);
+        case 2: return launch_chain_bwd_cpl<IO, 2>(p, st);
+        case 4: return launch_chain_bwd_cpl<IO, 4>(p, st);
+        case 8: return launch_chain_bwd_cpl<IO, 8>(p, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t reset_chain(const Params& p, hipStream_t st, int64_t n) {
+    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(swr_chain_reset_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, st,
+                       p.chain_flags, n, p.chain_ctr);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 int chain_tokens() { return kChainTok; }
@@ -386,12 +647,17 @@ int chain_tokens() { return kChainTok; }
 hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* stream) {
     const hipStream_t st = (hipStream_t)stream;
     const int64_t n = p.B * p.Hv * p.nruns;
-    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
-    hipLaunchKernelGGL(swr_chain_reset_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, st,
-                       p.chain_flags, n, p.chain_ctr);
-    hipError_t e = hipGetLastError();
+    hipError_t e = reset_chain(p, st, n);
     if (e != hipSuccess || n == 0) return e;
     return dtype == 1 ? launch_chain_io<IoBf16>(p, cpl, st) : launch_chain_io<IoF32>(p, cpl, st);
+}
+
+hipError_t launch_chain_backward(const Params& p, int dtype, int cpl, void* stream) {
+    const hipStream_t st = (hipStream_t)stream;
+    const int64_t n = p.B * p.H * p.nruns;
+    hipError_t e = reset_chain(p, st, n);
+    if (e != hipSuccess || n == 0) return e;
+    return dtype == 1 ? launch_chain_bwd_io<IoBf16>(p, cpl, st) : launch_chain_bwd_io<IoF32>(p, cpl, st);
 }
 
 }  // namespace swr

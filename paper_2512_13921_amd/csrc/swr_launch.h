@@ -70,6 +70,10 @@ struct Params {
     int32_t* chain_ctr;     // [2]: next ticket, look-back time-outs
     float* chain_incl;      // [B*Hv][nchunks][dv]
     float* h_last;          // [B][H][D] or NULL
+    // Exact backward in one pass: the gradient entering the final state, and
+    // the one leaving towards h0 (each [B][H][D] or NULL).
+    const float* dh_last;
+    float* dh0;
 };
 
 // What a forward or backward launch computes.
@@ -187,6 +191,10 @@ hipError_t launch_scan(const ScanParams& q, void* stream);
 // persistent workgroups; the workspace arrays of p are reset first.
 int chain_tokens();
 hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* stream);
+// The exact recurrence's backward in one pass over the same chunks, taken
+// from each sequence's end (heads of 16 * cpl channels, no virtual split;
+// p.carriers are the forward's exact block carriers).
+hipError_t launch_chain_backward(const Params& p, int dtype, int cpl, void* stream);
 
 // Uniform window of block tokens (the window length): forward or backward
 // over 2^hshift virtual heads of 16 * cpl channels per head; the workgroups

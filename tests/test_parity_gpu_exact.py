@@ -378,3 +378,23 @@ def test_exact_in_a_captured_graph(swr):
         assert torch.equal(y, y_e) and torch.equal(v, v_e) and torch.equal(hl, hl_e), rep
         for p_, q_ in zip(outs, g_e[:4]):
             assert torch.equal(p_, q_), rep
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype", [(1, 40000, 2, 64, 128, "bf16"), (1, 33000, 1, 32, 32, "f32"),
+                                                 (1, 32768, 1, 16, 16, "bf16")])
+def test_exact_backward_one_pass_long_sequences(swr, B, T, H, D, block, dtype):
+    # sequences of 256 chunks or more: the backward runs in one pass (chunks
+    # taken from the end, chained by the look-back); against the oracle, and
+    # repeated calls agree bit for bit
+    prob = W.random_problem(101 + D, B, T, H, D, block, dtype, "sigmoid", 4.0)
+    rng = np.random.default_rng(D)
+    h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
+    _say(f"[exact one-pass backward] B={B} T={T} H={H} D={D} l={block} {dtype}")
+    y, v, hl, grads = run_exact(swr, prob, h0, dhl)
+    check_exact(prob, h0, dhl, y, v, hl, grads, what=f"one-pass bwd {B}x{T}x{H}x{D} {dtype}")
+    x, a, b, c, dy = (to_device(getattr(prob, n), dtype) for n in ("x", "a", "b", "c", "dy"))
+    h0_t, dhl_t = torch.from_numpy(h0).cuda(), torch.from_numpy(dhl).cuda()
+    again = swr.swr_exact_backward(x, a, b, c, dy, v, block, h0=h0_t, dh_last=dhl_t, want_dh0=True)
+    torch.cuda.synchronize()
+    for name, u, w in zip(("dx", "da", "db", "dc", "dh0"), again, grads):
+        assert torch.equal(u, w), name
