@@ -406,8 +406,9 @@ def main():
             return 2
         cfg = cfg.with_(name=cfg.name + f"_gates{groups}")
     if args.channels:
-        if exact or uniform or groups:
-            print("--channels applies to the jagged window's own entry points only", file=sys.stderr)
+        if uniform or groups or (exact and args.channels not in (16, 32, 64, 128)):
+            print("--channels applies to the jagged window's own entry points, and to the exact "
+                  "recurrence with 16, 32, 64 or 128 channels", file=sys.stderr)
             return 2
         cfg = cfg.with_(D=args.channels, name=cfg.name.replace(f"_d{cfg.D}", f"_d{args.channels}"))
     nocar = args.no_carriers

@@ -424,34 +424,50 @@ ExactWs exact_ws(const swr_problem_t* p, const Resolved& r) {
 
 
 
-// The exact forward in one pass (swr_chain.hip), for one decay per head on
-// the MFMA kernels.  A float32 head of 128 channels runs as two virtual heads
-// of 64, each its own chain of chunks: the lighter wave lets two workgroups
-// share a compute unit, which hides the look-back's latency; a bf16 head of
-// 128 stays whole (16-byte row slices a lane; the kernel keeps its local
-// solutions in LDS to fit two workgroups a compute unit).  Workspace: two ticket counters
-// (padded to 16 floats), then per chunk of chain_tokens() tokens of every
-// virtual sequence a flag and a decay product, then per chunk an aggregate
-// end state and an inclusive end state (a virtual head's channels each).
+// The exact forward in one pass (swr_chain.hip).  With one decay per head
+// on the MFMA kernels a float32 head of 128 channels runs as two virtual
+// heads of 64, each its own chain of chunks: the lighter wave lets two
+// workgroups share a compute unit, which hides the look-back's latency; a
+// bf16 head of 128 stays whole (16-byte row slices a lane; the kernel keeps
+// its local solutions in LDS to fit two workgroups a compute unit).
+// Workspace: two ticket counters (padded to 16 floats), then per chunk of
+// chain_tokens() tokens of every virtual sequence a flag and a decay product,
+// then per chunk an aggregate end state and an inclusive end state (a
+// virtual head's channels each).  With a decay per channel the per-channel
+// kernels' virtual heads chain the same way with a decay product per channel:
+// the flags (padded to 4), then a decay product, an aggregate and an
+// inclusive state per chunk and channel.
 #ifndef SWR_EXACT_CHAIN
 #define SWR_EXACT_CHAIN 1
 #endif
 
 struct ChainWs {
     int cpl;          // channels per lane of the launch
-    int hs;           // log2 of the virtual heads per head
+    int hs;           // log2 of the virtual heads per head (shared decay)
+    bool pcp;         // decay products per channel (a decay per channel)
     int64_t nch;      // chunks per sequence
     int64_t n;        // chunks of the (virtual) sequences
+    int64_t dv;       // channels of a (virtual) sequence
     int64_t floats;   // float32 elements
 };
 
-ChainWs chain_ws(const swr_problem_t* p) {
+ChainWs chain_ws(const swr_problem_t* p, const Resolved& r) {
     ChainWs c;
-    c.cpl = (int)std::min<int64_t>(p->D / 16, p->dtype == 1 ? 8 : 4);
     const int64_t ct = swr::chain_tokens();
+    c.nch = (p->T + ct - 1) / ct;
+    c.pcp = r.pc;
+    if (c.pcp) {   // the per-channel kernels' virtual heads; a flag, then three values a channel
+        c.cpl = r.cpl;
+        c.hs = 0;
+        c.dv = 16 * r.cpl;
+        c.n = p->B * r.hv * c.nch;
+        c.floats = 16 + (c.n + 3) / 4 * 4 + 3 * c.n * c.dv;
+        return c;
+    }
+    c.cpl = (int)std::min<int64_t>(p->D / 16, p->dtype == 1 ? 8 : 4);
     c.hs = 0;
     while ((16 * c.cpl) << c.hs < p->D) ++c.hs;
-    c.nch = (p->T + ct - 1) / ct;
+    c.dv = 16 * c.cpl;
     c.n = (p->B * p->H << c.hs) * c.nch;
     // ticket counters, a flag and a decay product per chunk, two D-vectors per real chunk
     c.floats = 16 + 2 * c.n + 2 * (c.n >> c.hs) * p->D;
@@ -459,8 +475,11 @@ ChainWs chain_ws(const swr_problem_t* p) {
 }
 
 // The tickets are 32-bit counters (each workgroup takes one past the last chunk).
+// Packed small heads keep the three stages: at B8 T16384 H16 d16 (32 packed
+// sequences of 128 chunks) the chain's boundaries, not the bytes, set the
+// time (99 against 94 us).
 bool use_chain(const swr_problem_t* p, const Resolved& r) {
-    return SWR_EXACT_CHAIN && !r.pc && r.pack == 1 && !r.empty && chain_ws(p).n < ((int64_t)1 << 30);
+    return SWR_EXACT_CHAIN && !r.empty && r.pack == 1 && chain_ws(p, r).n < ((int64_t)1 << 30);
 }
 
 // The backward in one pass, for heads of up to 64 channels on sequences of
@@ -473,15 +492,15 @@ bool use_chain(const swr_problem_t* p, const Resolved& r) {
 #endif
 bool use_chain_bwd(const swr_problem_t* p, const Resolved& r) {
     if (!SWR_EXACT_CHAIN_BWD || !use_chain(p, r)) return false;
-    const ChainWs cw = chain_ws(p);
-    return cw.hs == 0 && cw.cpl <= 4 && cw.nch >= 256;
+    const ChainWs cw = chain_ws(p, r);
+    return !cw.pcp && cw.hs == 0 && cw.cpl <= 4 && cw.nch >= 256;
 }
 
 // Workspace of the exact calls for one plan: the three-stage arrays (the
 // backward's, and the forward's when it does not run in one pass) or the
 // one-pass forward's, whichever is larger.
 int64_t exact_ws_floats(const swr_problem_t* p, const Resolved& r) {
-    return std::max(exact_ws(p, r).floats, use_chain(p, r) ? chain_ws(p).floats : (int64_t)0);
+    return std::max(exact_ws(p, r).floats, use_chain(p, r) ? chain_ws(p, r).floats : (int64_t)0);
 }
 
 // Pointers into the workspace for one launch.
@@ -555,8 +574,23 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     }
 
     if (scratch && wfloats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
+    if (use_chain(p, r) && chain_ws(p, r).pcp) {   // one pass, a decay per channel
+        const ChainWs cw = chain_ws(p, r);
+        float* f = (float*)workspace;
+        swr::Params k = make_params(p, r, false);
+        k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers; k.h0 = h0; k.h_last = h_last;
+        k.chain_ctr = (int32_t*)f;
+        k.chain_flags = (int32_t*)(f + 16);
+        k.agg_p = f + 16 + (cw.n + 3) / 4 * 4;
+        k.agg_v = k.agg_p + cw.n * cw.dv;
+        k.chain_incl = k.agg_v + cw.n * cw.dv;
+        k.nruns = cw.nch;
+        // persistent workgroups: as many as the 256 compute units hold at once
+        k.nwork = std::min<int64_t>(cw.n, 256 * (cw.cpl == 1 ? 3 : 2));
+        return swr::launch_chain_forward_pc(k, p->dtype, cw.cpl, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    }
     if (use_chain(p, r)) {   // one pass: chained chunks with a look-back
-        const ChainWs cw = chain_ws(p);
+        const ChainWs cw = chain_ws(p, r);
         float* f = (float*)workspace;
         swr::Params k = make_params(p, r, false);
         k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers; k.h0 = h0; k.h_last = h_last;
@@ -639,7 +673,7 @@ int swr_exact_backward(const swr_problem_t* p, const void* x, const void* a, con
     }
 
     if (use_chain_bwd(p, r)) {   // one pass: chunks from the sequences' ends, chained by a look-back
-        const ChainWs cw = chain_ws(p);
+        const ChainWs cw = chain_ws(p, r);
         float* f = (float*)workspace;
         swr::Params k = make_params(p, r, true);
         k.x = x; k.a = a; k.b = b; k.c = c; k.dy = dy;

@@ -86,13 +86,15 @@ constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL =
 // folds chunks kb+1+Q*g ... kb+Q*(g+1) in order, then the groups' results
 // are applied to the boundary value in order), and at a boundary publish the
 // chunk's own inclusive value.  `in` is the value entering the chain's first
-// chunk (this lane's slice; NULL for zero).  Returns the value entering the
-// chunk and the one leaving it (I = P in + V).
-template <int CPL, int Q, int QB>
+// chunk (this lane's slice at in + n * CPL; NULL for zero).  Returns the
+// value entering the chunk and the one leaving it (I = P in + V).  PCP: the
+// decay product P is per channel (agg_p holds D values a chunk), else one
+// value a chunk.
+template <int CPL, int Q, int QB, bool PCP>
 __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, int64_t nch, const float (&V)[CPL],
-                                  float P, const float* in, int lane, int grp, int n, float (&pre)[CPL],
-                                  float (&I)[CPL]) {
-    constexpr int D = CPL * SB, K = 4 * Q;
+                                  const float (&P)[PCP ? CPL : 1], const float* in, int lane, int grp, int n,
+                                  float (&pre)[CPL], float (&I)[CPL]) {
+    constexpr int D = CPL * SB, K = 4 * Q, NP = PCP ? CPL : 1, PD = PCP ? D : 1;
     const uint32_t vch = (uint32_t)(n * CPL);
     const int64_t slot = slot0 + ci;
     const bool boundary = ci % K == K - 1;
@@ -103,8 +105,12 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
         if (grp == 0) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) put_coherent(p.agg_v + slot * D + vch + m, V[m]);
+            if constexpr (PCP) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) put_coherent(p.agg_p + slot * D + vch + m, P[m]);
+            }
         }
-        if (lane == 0) put_coherent(p.agg_p + slot, P);
+        if (!PCP && lane == 0) put_coherent(p.agg_p + slot, P[0]);
         writes_complete();
         if (lane == 0) put_flag(p.chain_flags + slot, kFlagAgg);
     }
@@ -128,29 +134,34 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
         __builtin_amdgcn_s_sleep(1);
     }
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    float gV[CPL], gP = 1.0f;
+    float gV[CPL], gP[NP];
 #pragma unroll
     for (int m = 0; m < CPL; ++m) gV[m] = 0.f;
+#pragma unroll
+    for (int m = 0; m < NP; ++m) gP[m] = 1.0f;
     {
-        const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0);
+        const __amdgpu_buffer_rsrc_t rav = rsrc(p.agg_v + slot0 * D), rap = rsrc(p.agg_p + slot0 * PD);
 #pragma unroll
         for (int q0 = 0; q0 < Q; q0 += QB) {   // QB aggregates in flight at a time
             Row<IoF32, CPL> rv[QB];
-            float pj[QB];
+            Row<IoF32, NP> rp[QB];
 #pragma unroll
             for (int q = 0; q < QB; ++q) {
                 const int i = grp * Q + q0 + q;
                 const int64_t j = kb + 1 + i;
                 rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
-                pj[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                      rap, (int)in_range(i < cnt, (uint32_t)j * 4u), 0, kCoherent));
+                rp[q].template load<kCoherent>(rap, in_range(i < cnt, (uint32_t)(j * PD + (PCP ? vch : 0u)) * 4u));
             }
 #pragma unroll
             for (int q = 0; q < QB; ++q) {
-                const float pq = grp * Q + q0 + q < cnt ? pj[q] : 1.0f;
+                const bool live = grp * Q + q0 + q < cnt;
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
-                gP *= pq;
+                for (int m = 0; m < CPL; ++m) {
+                    const float pq = live ? rp[q].get(PCP ? m : 0) : 1.0f;
+                    gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
+                }
+#pragma unroll
+                for (int m = 0; m < NP; ++m) gP[m] *= live ? rp[q].get(m) : 1.0f;
             }
             if constexpr (QB < Q) __builtin_amdgcn_sched_barrier(0);   // one batch live at a time
         }
@@ -168,16 +179,18 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         const int src = g * 16 + n;
-        const float pg = __shfl(gP, src);
+        float pg[NP];
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg, pre[m], __shfl(gV[m], src));
+        for (int m = 0; m < NP; ++m) pg[m] = __shfl(gP[m], src);
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg[PCP ? m : 0], pre[m], __shfl(gV[m], src));
     }
     if (timed_out) {
 #pragma unroll
         for (int m = 0; m < CPL; ++m) pre[m] = __builtin_nanf("");
     }
 #pragma unroll
-    for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P, pre[m], V[m]);
+    for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P[PCP ? m : 0], pre[m], V[m]);
     if (boundary && ci + 1 < nch) {
         if (grp == 0) {
 #pragma unroll
@@ -295,8 +308,9 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
             }
             const uint32_t vch = (uint32_t)(n * CPL);
             float pre[CPL], I[CPL];
-            chain_link<CPL, Q, QB>(p, seq * nch, ch, nch, V, P, p.h0 ? p.h0 + rseq * DH + coff : nullptr, lane, grp,
-                                   n, pre, I);
+            const float Pv[1] = {P};
+            chain_link<CPL, Q, QB, false>(p, seq * nch, ch, nch, V, Pv, p.h0 ? p.h0 + rseq * DH + coff : nullptr,
+                                          lane, grp, n, pre, I);
             if (grp == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
@@ -352,6 +366,179 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
             for (int m = 0; m < CPL; ++m) v[m] = __builtin_fmaf(dk.c, e[m], s_wl[tw][n * CPL + m]);
             store_row<IoF32, CPL>(rsrc(p.carriers + (rseq * p.nblocks * DH + coff)),
                                   in_range(grp == 0 && blk < p.nblocks, (uint32_t)(blk * DH + n * CPL) * 4u), v);
+        }
+        ticket = grab();
+    }
+}
+
+// The exact forward in one pass with a decay per channel (heads of 128 as
+// two virtual heads of 64).  The chunks' local solves are the per-lane scans
+// of the per-channel sweep kernels (whose lane geometry, Geo, also covers
+// packed small heads: PK heads of 64 / PK channels a virtual head); the chain
+// is that of swr_fwd_chain_kernel with the decay products kept per channel.
+// (Lanes of 4 channels park their local solution and prefix products in LDS
+// through the look-back, 64 KB a workgroup, so that two workgroups share a
+// compute unit.)
+template <class IO, int CPL, bool FEAT, int PK, int Q>
+__global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 2)) void swr_fwd_chain_pc_kernel(Params p) {
+    constexpr int TW = kChainTW;
+    constexpr int TOK = kChainTok;
+    constexpr int D = CPL * SB;
+    constexpr int ES = IO::ES;
+    constexpr bool PARK = CPL == 4;
+    using RW = Row<IO, CPL>;
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
+    __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
+    __shared__ float s_cc[TW][D];   // each sub-block's decay product, per channel
+    __shared__ float s_pre[D];      // the exact state entering the chunk
+    __shared__ f32x4 s_WG[PARK ? TW : 1][PARK ? 2 * CPL : 1][PARK ? 64 : 1];
+    __shared__ int64_t s_ticket[2];
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    const int64_t S = p.B * p.Hv, nch = p.nruns, N = S * nch;
+    const int64_t rs = p.sx_t * ES, as = PK > 1 ? p.sa_t * ES : rs;
+    const uint32_t vch = (uint32_t)(n * CPL);
+    const int smask = p.block / SB - 1;
+
+    int par = 0;
+    auto grab = [&]() {
+        if (threadIdx.x == 0) s_ticket[par] = atomicAdd(p.chain_ctr, 1);
+        lds_barrier();
+        const int64_t t = s_ticket[par];
+        par ^= 1;
+        return t;
+    };
+    int64_t ticket = grab();
+    for (;;) {
+        if (ticket >= N) break;
+        const int64_t seq = ticket % S, ch = ticket / S;   // chunk-major: earlier chunks first
+        const int64_t bi = seq / p.Hv, vh = seq % p.Hv;
+        const Geo<PK, CPL> geo(vh, p, n);
+        const int64_t hb = bi * p.H + geo.head;   // first real (batch, head) of the virtual head
+        const int64_t xo = (bi * p.sx_b + geo.head * p.sx_h + geo.coff) * ES;
+        const char* ab = PK > 1 ? (const char*)p.a + (bi * p.sa_b + geo.head * p.sa_h) * ES : (const char*)p.a + xo;
+        const uint32_t loff = in_range(geo.ok, (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(n * CPL * ES));
+        const uint32_t aoffp = (uint32_t)(4 * grp) * (uint32_t)as + (uint32_t)(geo.lh * p.sa_h * ES);
+        const int64_t t0 = ch * TOK, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+
+        // ---- the sub-block's local solve: per-lane scans ------------------------------
+        RW xr[4], br[4], cr[4];
+        float av[4][CPL];
+        {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
+                                         rb = rsrc((const char*)p.b + xo + r0 * rs),
+                                         ra = rsrc(ab + r0 * as);
+            RW ar[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
+                xr[r].template load<kFwdLoad>(rx, o);
+                br[r].template load<kFwdLoad>(rb, o);
+                if constexpr (PK == 1) ar[r].template load<kFwdLoad>(ra, o);
+            }
+            if constexpr (PK > 1) {
+                float az[4];
+                decay_rows_packed<IO, CPL, kFwdDecay>(ra, aoffp, (uint32_t)as, tr0, 0, p.T, p.T, sig_a, az, av);
+            } else {
+                decay_rows<IO, CPL>(ar, tr0, 0, p.T, p.T, sig_a, av);   // 1 past the end
+            }
+        }
+        float W[4][CPL], G[4][CPL];
+        {
+            float u[4][CPL];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) u[r][m] = xr[r].get(m) * pregate(br[r].get(m), sig_b);
+            chan_scan_fwd<CPL>(av, u, W, G, grp, lane);
+        }
+        if (grp == 3) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_wl[tw][vch + m] = W[3][m];
+                s_cc[tw][vch + m] = G[3][m];
+            }
+        }
+        if constexpr (PARK) {   // (read back by the same lane)
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                s_WG[tw][m][lane] = f32x4{W[0][m], W[1][m], W[2][m], W[3][m]};
+                s_WG[tw][CPL + m][lane] = f32x4{G[0][m], G[1][m], G[2][m], G[3][m]};
+            }
+        }
+        {   // c is needed for the outputs only: its loads land during the look-back
+            const __amdgpu_buffer_rsrc_t rc = rsrc((const char*)p.c + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                cr[r].template load<kFwdLoad>(rc, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)));
+        }
+        lds_barrier();
+
+        // ---- wave 0: the chunk's aggregate, the look-back, the inclusive state -----
+        if (tw == 0) {
+            float V[CPL], P[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) { V[m] = 0.f; P[m] = 1.0f; }
+#pragma unroll 1
+            for (int r = 0; r < TW; ++r) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) {
+                    const float c_ = s_cc[r][vch + m];
+                    V[m] = __builtin_fmaf(c_, V[m], s_wl[r][vch + m]);
+                    P[m] *= c_;
+                }
+            }
+            float pre[CPL], I[CPL];
+            const int64_t so = hb * geo.Dr + geo.coff;   // the virtual head's slice of [B][H][D] states
+            chain_link<CPL, Q, 2, true>(p, seq * nch, ch, nch, V, P, p.h0 ? p.h0 + so : nullptr, lane, grp, n, pre,
+                                        I);
+            if (grp == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
+            }
+            store_row<IoF32, CPL>(rsrc(p.h_last ? p.h_last + so : p.chain_incl),
+                                  in_range(p.h_last && ch == nch - 1 && grp == 0, vch * 4u), I);
+        }
+        lds_barrier();
+
+        // ---- outputs: the state entering this wave's sub-block, y, block carriers -----
+        float e[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) e[m] = s_pre[vch + m];
+#pragma unroll 1
+        for (int r = 0; r < tw; ++r) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) e[m] = __builtin_fmaf(s_cc[r][vch + m], e[m], s_wl[r][vch + m]);
+        }
+        if constexpr (PARK) {
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const f32x4 w4 = s_WG[tw][m][lane], g4 = s_WG[tw][CPL + m][lane];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) { W[r][m] = w4[r]; G[r][m] = g4[r]; }
+            }
+        }
+        const __amdgpu_buffer_rsrc_t ry = rsrc((char*)p.y + xo + r0 * rs);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float yv[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                yv[m] = cr[r].get(m) * __builtin_fmaf(G[r][m], e[m], W[r][m]);
+                if (p.residual) yv[m] += xr[r].get(m);
+            }
+            store_row<IO, CPL, kFwdStore>(ry, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)), yv);
+        }
+        // the exact state at the end of a block that ends with this sub-block
+        // (a block longer than a chunk that the sequence's end cuts short ends in the last chunk)
+        if (p.carriers && (((ch * TW + tw) & smask) == smask || (ch == nch - 1 && tw == TW - 1))) {
+            const int64_t blk = r0 >> p.lshift;
+            float v[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) v[m] = __builtin_fmaf(s_cc[tw][vch + m], e[m], s_wl[tw][vch + m]);
+            store_row<IoF32, CPL>(rsrc(p.carriers + hb * p.nblocks * geo.Dr),
+                                  in_range(grp == 0 && geo.ok && blk < p.nblocks, geo.off(p.nblocks, blk) * 4u), v);
         }
         ticket = grab();
     }
@@ -499,8 +686,9 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
                 P *= c_;
             }
             float pre[CPL], I[CPL];
-            chain_link<CPL, Q, 4>(p, seq * nch, ci, nch, V, P, p.dh_last ? p.dh_last + seq * D : nullptr, lane,
-                                  grp, n, pre, I);
+            const float Pv[1] = {P};
+            chain_link<CPL, Q, 4, false>(p, seq * nch, ci, nch, V, Pv, p.dh_last ? p.dh_last + seq * D : nullptr,
+                                         lane, grp, n, pre, I);
             if (grp == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) s_eps[vch + m] = pre[m];
@@ -612,6 +800,31 @@ hipError_t launch_chain_io(const Params& p, int cpl, hipStream_t st) {
     }
 }
 
+template <class IO, int CPL, int PK, int Q>
+hipError_t launch_chain_pc_q(const Params& p, hipStream_t st) {
+    const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
+    if (p.sig_a || p.sig_b)
+        hipLaunchKernelGGL((swr_fwd_chain_pc_kernel<IO, CPL, true, PK, Q>), grid, block, 0, st, p);
+    else
+        hipLaunchKernelGGL((swr_fwd_chain_pc_kernel<IO, CPL, false, PK, Q>), grid, block, 0, st, p);
+    return hipGetLastError();
+}
+
+template <class IO, int CPL, int PK>
+hipError_t launch_chain_pc_cpl(const Params& p, hipStream_t st) {
+    return p.nruns < kLongChain ? launch_chain_pc_q<IO, CPL, PK, 2>(p, st) : launch_chain_pc_q<IO, CPL, PK, 4>(p, st);
+}
+
+template <class IO>
+hipError_t launch_chain_pc_io(const Params& p, int cpl, hipStream_t st) {
+    switch (cpl) {
+        case 1: return launch_chain_pc_cpl<IO, 1, 1>(p, st);
+        case 2: return launch_chain_pc_cpl<IO, 2, 1>(p, st);
+        case 4: return launch_chain_pc_cpl<IO, 4, 1>(p, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 template <class IO, int CPL>
 hipError_t launch_chain_bwd_cpl(const Params& p, hipStream_t st) {
     const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
@@ -628,7 +841,6 @@ hipError_t launch_chain_bwd_io(const Params& p, int cpl, hipStream_t st) {
         case 1: return launch_chain_bwd_cpl<IO, 1>(p, st);
         case 2: return launch_chain_bwd_cpl<IO, 2>(p, st);
         case 4: return launch_chain_bwd_cpl<IO, 4>(p, st);
-        case 8: return launch_chain_bwd_cpl<IO, 8>(p, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -650,6 +862,14 @@ hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* strea
     hipError_t e = reset_chain(p, st, n);
     if (e != hipSuccess || n == 0) return e;
     return dtype == 1 ? launch_chain_io<IoBf16>(p, cpl, st) : launch_chain_io<IoF32>(p, cpl, st);
+}
+
+hipError_t launch_chain_forward_pc(const Params& p, int dtype, int cpl, void* stream) {
+    const hipStream_t st = (hipStream_t)stream;
+    const int64_t n = p.B * p.Hv * p.nruns;
+    hipError_t e = reset_chain(p, st, n);
+    if (e != hipSuccess || n == 0) return e;
+    return dtype == 1 ? launch_chain_pc_io<IoBf16>(p, cpl, st) : launch_chain_pc_io<IoF32>(p, cpl, st);
 }
 
 hipError_t launch_chain_backward(const Params& p, int dtype, int cpl, void* stream) {

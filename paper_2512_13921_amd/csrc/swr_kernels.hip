@@ -1126,43 +1126,6 @@ __global__ __launch_bounds__(256) void swr_state_kernel(StateParams q) {
 // head of D = 128 channels is processed as two independent halves ("virtual
 // heads" of 64 channels), which keeps the per-channel products in registers.
 
-// Forward local solve of one sub-block, per channel:  w_k = a_k w_{k-1} + u_k
-// and G_k = a_k G_{k-1} (w_{-1} = 0, G_{-1} = 1) for this lane's tokens
-// k = 4*grp + r.  A state is carried through a stretch of tokens by
-// s -> G s + w, so stretches compose as (G1, w1) then (G2, w2) =
-// (G1 G2, G2 w1 + w2).
-// Every multiply-add is one explicit fused operation, so that the same scan
-// rounds identically in every kernel it is inlined into (the backward's
-// recomputation of a block carrier matches the forward's bit for bit).
-template <int CPL>
-__device__ inline void chan_scan_fwd(const float (&a)[4][CPL], const float (&u)[4][CPL],
-                                     float (&w)[4][CPL], float (&G)[4][CPL], int grp, int lane) {
-#pragma unroll
-    for (int m = 0; m < CPL; ++m) {
-        G[0][m] = a[0][m];
-        w[0][m] = u[0][m];
-#pragma unroll
-        for (int r = 1; r < 4; ++r) {
-            G[r][m] = a[r][m] * G[r - 1][m];
-            w[r][m] = __builtin_fmaf(a[r][m], w[r - 1][m], u[r][m]);
-        }
-        // Inclusive scan of the row totals over rows 0..grp.
-        float tg = G[3][m], tw = w[3][m];
-        float pg = shfl(tg, (lane - 16) & 63), pw = shfl(tw, (lane - 16) & 63);
-        if (grp >= 1) { tw = __builtin_fmaf(tg, pw, tw); tg = pg * tg; }
-        pg = shfl(tg, (lane - 32) & 63); pw = shfl(tw, (lane - 32) & 63);
-        if (grp >= 2) { tw = __builtin_fmaf(tg, pw, tw); tg = pg * tg; }
-        // Exclusive: the stretch from the sub-block start to this row.
-        pg = shfl(tg, (lane - 16) & 63); pw = shfl(tw, (lane - 16) & 63);
-        const float gin = grp >= 1 ? pg : 1.0f, win = grp >= 1 ? pw : 0.0f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            w[r][m] = __builtin_fmaf(G[r][m], win, w[r][m]);
-            G[r][m] *= gin;
-        }
-    }
-}
-
 // Reverse local solve of one sub-block, per channel:  D_k = dh_k + a_{k+1} D_{k+1}
 // (D_16 = 0), i.e. D = L^T dh, and R_k = a_{k+1} ... a_15 (R_15 = 1).  It runs
 // on E_k = a_k D_k, the adjoint leaving token k towards k-1, so that each row
@@ -1198,75 +1161,6 @@ __device__ inline void chan_scan_rev(const float (&a)[4][CPL], const float (&dh)
             Dv[r][m] += R[r][m] * lam;
             R[r][m] *= qin;
         }
-    }
-}
-
-// The decays of one row slice as floats: the loaded values (through the
-// sigmoid when they are logits) for tokens in [t_lo, t_hi), 0 before or after
-// that range, and 1 past the end of the sequence, so that a partial last
-// block's carrier is the state at its last token.
-template <class IO, int CPL>
-__device__ inline void decay_rows(const Row<IO, CPL> (&ar)[4], int64_t tr0, int64_t t_lo, int64_t t_hi,
-                                  int64_t T, int sig, float (&av)[4][CPL]) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int64_t t = tr0 + r;
-#pragma unroll
-        for (int m = 0; m < CPL; ++m) {
-            const float z = ar[r].get(m);
-            av[r][m] = t >= T ? 1.0f : (t >= t_lo && t < t_hi) ? (sig ? sigmoid(z) : z) : 0.0f;
-        }
-    }
-}
-
-// Where a lane's channels live in the per-channel kernels.  A kernel "head"
-// (virtual head) is D = CPL * 16 channels.  With a per-channel decay it is
-// one real head or one half of it (2^hshift halves).  With packed heads
-// (PK > 1: a decay per token and head, heads of 64 / PK channels stored next
-// to each other) it is PK adjacent real heads; lane n then holds channels
-// (n % (16/PK)) * CPL ... of real head n / (16/PK).  Small heads are
-// processed this way because a lane slice of one such head is only 2 or 4
-// bytes, while a lane slice of the packed row is 8 or 16.
-template <int PK, int CPL>
-struct Geo {
-    static constexpr int LPH = 16 / PK;   // lanes per real head when packed
-    int64_t head;   // first real head of the virtual head
-    int64_t coff;   // first channel of the virtual head within its real head
-    int64_t Dr;     // channels of a real head (the row length of carriers and states)
-    int lh;         // real head of this lane within the virtual head
-    int lch;        // first channel of this lane within its real head
-    bool ok;        // the lane holds channels (a virtual head of p.dv < D channels
-                    // leaves lanes n >= p.nlane idle)
-    __device__ Geo(int64_t vh, const Params& p, int n) {
-        constexpr int D = CPL * SB;
-        if constexpr (PK > 1) {
-            head = vh * PK; coff = 0; Dr = D / PK; lh = n / LPH; lch = (n % LPH) * CPL; ok = true;
-        } else {
-            head = vh >> p.hshift; coff = (vh & ((1 << p.hshift) - 1)) * (int64_t)p.dv; Dr = p.dh;
-            lh = 0; lch = (int)coff + n * CPL; ok = n < p.nlane;
-        }
-    }
-    // Offset (in float32 elements) of this lane's slice of row `row` of a
-    // per-head array [B*H][rows][Dr], from the start of the virtual head's first head.
-    __device__ uint32_t off(int64_t rows, int64_t row) const {
-        return (uint32_t)((lh * rows + row) * Dr + lch);
-    }
-};
-
-// Decays of one row slice for packed heads: one scalar per lane (its real
-// head's decay), with the conventions of decay_rows.
-template <class IO, int CPL, int POL>
-__device__ inline void decay_rows_packed(__amdgpu_buffer_rsrc_t ra, uint32_t aoff, uint32_t astep, int64_t tr0,
-                                         int64_t t_lo, int64_t t_hi, int64_t T, int sig, float (&az)[4],
-                                         float (&av)[4][CPL]) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int64_t t = tr0 + r;
-        const bool ok = t >= t_lo && t < t_hi;
-        az[r] = load_scalar<IO, POL>(ra, in_range(ok, aoff + (uint32_t)r * astep));
-        const float v = t >= T ? 1.0f : ok ? (sig ? sigmoid(az[r]) : az[r]) : 0.0f;
-#pragma unroll
-        for (int m = 0; m < CPL; ++m) av[r][m] = v;
     }
 }
 

@@ -398,3 +398,43 @@ def test_exact_backward_one_pass_long_sequences(swr, B, T, H, D, block, dtype):
     torch.cuda.synchronize()
     for name, u, w in zip(("dx", "da", "db", "dc", "dh0"), again, grads):
         assert torch.equal(u, w), name
+
+
+CHAINED_PC = [
+    # (B, T, H, D, block, dtype, per-channel decay): the one-pass forward with a
+    # decay product per channel (a decay per channel) on sequences of more than
+    # 16 chunks; small heads stored next to each other (packed four or two to a
+    # 64-channel group) run the three stages, checked the same way
+    (1, 3000, 2, 128, 128, "bf16", True),   # heads of 128 as two halves of 64
+    (1, 2500, 3, 64, 64, "f32", True),
+    (2, 2049, 2, 32, 32, "bf16", True),
+    (1, 2300, 1, 16, 16, "f32", True),
+    (1, 3000, 4, 16, 16, "bf16", False),     # packed four to a group
+    (2, 2600, 2, 32, 32, "f32", False),      # packed two to a group
+    (1, 33000, 1, 64, 64, "bf16", True),     # 258 chunks: boundaries every 16
+]
+
+
+@pytest.mark.parametrize("B,T,H,D,block,dtype,pc", CHAINED_PC)
+def test_exact_forward_chained_per_channel_products(swr, B, T, H, D, block, dtype, pc):
+    prob = W.random_problem(111 + T + D, B, T, H, D, block, dtype, "sigmoid", 3.0, per_channel=pc)
+    rng = np.random.default_rng(T + 9)
+    h0 = _state(rng, prob.cfg)
+    _say(f"[exact chained pc] B={B} T={T} H={H} D={D} l={block} {dtype} per_channel={pc}")
+    y, v, hl, _ = run_exact(swr, prob, h0, None, backward=False)
+    check_exact(prob, h0, None, y, v, hl, None, what=f"chained pc {B}x{T}x{H}x{D} {dtype} pc={pc}")
+    x, a, b, c = (to_device(getattr(prob, n), dtype) for n in "xabc")
+    again = swr.swr_exact_forward(x, a, b, c, block, h0=torch.from_numpy(h0).cuda(), save_carriers=True,
+                                  want_h_last=True)
+    torch.cuda.synchronize()
+    for name, u, w in zip(("y", "carriers", "h_last"), again, (y, v, hl)):
+        assert torch.equal(u, w), name
+
+
+def test_exact_forward_chained_per_channel_featurised_residual(swr):
+    prob = W.random_problem(113, 2, 2200, 2, 128, 64, "bf16", "sigmoid", 3.0, per_channel=True, logits=True)
+    rng = np.random.default_rng(13)
+    h0 = _state(rng, prob.cfg)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    y, v, hl, _ = run_exact(swr, prob, h0, None, residual=True, backward=False, **feat)
+    check_exact(prob, h0, None, y, v, hl, None, residual=True, what="chained pc residual+sigmoid", **feat)
