@@ -194,10 +194,10 @@ int swr_abi_version(void);
  * h0 and h_last it also chains a long sequence processed in pieces, and a
  * single-token piece is the recurrent decoding step.  Stages I and III both
  * read their inputs, so the three stages move about 1.5x the bytes of
- * swr_forward (the backward about 1.25x).  With one decay per head (unless
- * heads of 16 or 32 channels, stored next to each other, run packed four or
- * two to a 64-channel group on the per-channel kernels), the forward instead
- * runs the three stages in one pass over chunks of 128 tokens, each chunk
+ * swr_forward (the backward about 1.25x).  Unless heads of 16 or 32
+ * channels, stored next to each other with one decay per head, run packed
+ * four or two to a 64-channel group, the forward instead runs the three
+ * stages in one pass over chunks of 128 tokens, each chunk
  * composing the published aggregates of the chunks before it (a look-back
  * between workgroups in a fixed pattern, so that repeated calls give the same
  * bits): it reads every input once.  The backward does the same, from each
