@@ -72,7 +72,7 @@ __device__ inline void writes_complete() {
 
 // bf16 lanes of 8 or 16 channels (heads of 64 and 128): the local solutions
 // wait for the look-back in LDS instead of registers, and x is loaded again
-// for the residual, so that the kernel fits 127 registers (two workgroups a
+// for the residual, so that the kernel fits 128 registers (two workgroups a
 // compute unit) or 80 (three); the launcher sizes its grid to match.
 template <class IO, int CPL>
 constexpr bool chain_w_in_lds() { return (CPL == 8 || CPL == 4) && IO::ES == 2; }

@@ -344,6 +344,12 @@ def test_exact_workspace_bytes():
     nr = max(-(-256 // info["fwd_run_len"]), -(-256 // info["bwd_run_len"]),
              _agg_runs(256, 2 * 4, info["bwd_run_len"]))
     assert swr.swr_exact_workspace_bytes(pc) == 2 * 4 * nr * (3 * 64) * 4
+    # ... and its one-pass forward, per 128-token chunk of each 64-channel half
+    # of a head, a flag (padded to 4) and a decay product, an aggregate and an
+    # inclusive state per channel -- larger than the stages at the headline shape
+    pcl = problem(B=8, T=16384, H=16, D=128, block=128, per_channel=True)
+    n = 8 * 16 * 2 * 128
+    assert swr.swr_exact_workspace_bytes(pcl) == (16 + n + 3 * n * 64) * 4
     assert lib.swr_exact_workspace_bytes(ctypes.byref(problem(block=48))) == E_BLOCK
 
 
