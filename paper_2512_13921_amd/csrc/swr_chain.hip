@@ -1,4 +1,6 @@
-// swr_chain.hip -- the exact (untruncated) recurrence's forward in one pass.
+// swr_chain.hip -- the exact (untruncated) recurrence in one pass: the
+// forward (a decay per head or per channel), and the backward on long
+// sequences of small heads.
 //
 // The three-stage evaluation of the hierarchical decomposition (Alg.
 // "Hierarchical Block Parallel Inference": local solves, the carrier
@@ -9,8 +11,8 @@
 // the chunk started from zero.  The state entering chunk c is then
 //   S_c = P_{c-1} ( ... P_{k+1} (P_k S_k' + V_k) ...) + V_{c-1},
 // composed from the inclusive end state S_k' of the last boundary chunk k
-// before c (chunks 15, 31, 47, ...; before the first one, the initial state)
-// and the aggregates of the chunks in between.  Boundary chunks publish their
+// before c (every 16th chunk, or every 8th; before the first one, the
+// initial state) and the aggregates of the chunks in between.  Boundary chunks publish their
 // inclusive end state P S + V, the others their aggregate.  The composition
 // always takes the same chunks in the same pattern, so the results do not
 // depend on the order in which workgroups reach them; the outputs then follow
@@ -26,7 +28,9 @@
 //
 // Publication uses device-coherent (agent-scope) stores, and a wait for
 // their completion before the flag that announces them; readers load the flag
-// and then the data with device-coherent loads.
+// and then the data with device-coherent loads.  The backward runs the same
+// chain from each sequence's end, on the adjoint entering a chunk from its
+// end.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -555,9 +559,10 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 2)) void swr_fwd_cha
 // backward, and the gradients of a token are those of Sec. 4.2.2 without the
 // window's truncation term:  du = D + R eps_in,  dx = b du,  db = x du,
 // dc = dy h,  da = sum over channels of h_{t-1} du.
-// Lanes of 8 or 16 channels park both local solutions in LDS through the
-// look-back (64 or 128 KB a workgroup): 16 channels to fit one workgroup a
-// compute unit without spilling, 8 to fit two.
+// Lanes of 4 channels park both local solutions in LDS through the
+// look-back (64 KB a workgroup), to fit two workgroups a compute unit.  (The
+// launcher takes lanes of up to 4 channels: with 8, the kernel needs more
+// than 256 registers and measured slower than the three stages.)
 template <int CPL>
 constexpr bool chain_bwd_park() { return CPL >= 4; }
 
