@@ -238,8 +238,10 @@ int swr_exact_forward(const swr_problem_t* problem, const void* x, const void* a
  * routine).  The array is a static device array of SWR_NOALLOC_SCRATCH_BYTES
  * bytes, one per GPU, held from the library's first use of that GPU until the
  * process ends; its address is looked up once per device, on the first call
- * on it.  A problem whose swr_exact_workspace_bytes exceeds that size is
- * rejected with SWR_ERR_SCRATCH before any HIP runtime call.  The one-pass
+ * on it.  Where the one-pass forward's workspace exceeds that size and the
+ * three stages' does not, the call runs the three stages (the same result up
+ * to rounding); a problem for which both exceed it is rejected with
+ * SWR_ERR_SCRATCH before any HIP runtime call.  The one-pass
  * forward's publication flags and ticket counters at the start of the array
  * are zeroed by a fill kernel on `stream` at the start of every call (no
  * memset); every other entry is written before it is read.

@@ -543,7 +543,10 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     if (rc != SWR_OK) return rc;
     if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
-    const int64_t wfloats = exact_ws_floats(p, r);
+    // the library's static array may hold the three stages' arrays but not the
+    // one pass's: the allocation-free call then runs the three stages
+    const bool chain = use_chain(p, r) && (!scratch || chain_ws(p, r).floats * 4 <= scratch_bytes);
+    const int64_t wfloats = chain ? chain_ws(p, r).floats : w.floats;
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
     if (!r.empty && (!x || !a || !b || !c || !y)) return SWR_ERR_NULL;
@@ -574,7 +577,7 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     }
 
     if (scratch && wfloats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
-    if (use_chain(p, r) && chain_ws(p, r).pcp) {   // one pass, a decay per channel
+    if (chain && chain_ws(p, r).pcp) {   // one pass, a decay per channel
         const ChainWs cw = chain_ws(p, r);
         float* f = (float*)workspace;
         swr::Params k = make_params(p, r, false);
@@ -589,7 +592,7 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
         k.nwork = std::min<int64_t>(cw.n, 256 * (cw.cpl == 1 ? 3 : 2));
         return swr::launch_chain_forward_pc(k, p->dtype, cw.cpl, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
     }
-    if (use_chain(p, r)) {   // one pass: chained chunks with a look-back
+    if (chain) {   // one pass: chained chunks with a look-back
         const ChainWs cw = chain_ws(p, r);
         float* f = (float*)workspace;
         swr::Params k = make_params(p, r, false);

@@ -76,13 +76,32 @@ def test_noalloc_after_a_larger_call_on_another_stream(swr):
 
 
 def test_noalloc_refuses_problems_beyond_the_static_array(swr):
-    # refused during validation, before any HIP call
-    x = torch.zeros((128, 256, 128, 128), dtype=torch.bfloat16, device="cuda")
-    a = torch.zeros((128, 256, 128), dtype=torch.bfloat16, device="cuda")
+    # refused during validation, before any HIP call: 65536 (batch, head)
+    # sequences need more than the array for the one pass and the three stages
+    x = torch.zeros((512, 64, 128, 128), dtype=torch.bfloat16, device="cuda")
+    a = torch.zeros((512, 64, 128), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(swr.SwrError) as err:
         swr.swr_exact_forward_noalloc(x, a, x, x, 128, y=torch.empty_like(x))
     assert err.value.code == swr.SWR_ERR_SCRATCH
     assert "SWR_NOALLOC_SCRATCH_BYTES" in str(err.value)
+
+
+def test_noalloc_falls_back_to_the_three_stages(swr):
+    # B16 T16384 H16 d128: the one pass needs 33.8 MB of workspace, more than
+    # the static array, the three stages about 4 MB; the allocation-free call
+    # runs the three stages and agrees with the one pass up to rounding
+    g = torch.Generator(device="cuda").manual_seed(92)
+    shape = (16, 16384, 16, 128)
+    x, b, c = (torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16) for _ in range(3))
+    a = torch.sigmoid(2.0 + torch.randn(shape[:3], generator=g, device="cuda")).to(torch.bfloat16)
+    y1, hl1 = swr.swr_exact_forward(x, a, b, c, 128, want_h_last=True)
+    y2, hl2 = swr.swr_exact_forward_noalloc(x, a, b, c, 128, want_h_last=True)
+    torch.cuda.synchronize()
+    for name, u, w in (("y", y2, y1), ("h_last", hl2, hl1)):
+        assert torch.isfinite(u).all(), name
+        assert_close(to_host(u[:1]) if u.dim() == 4 else to_host(u), to_host(w[:1]) if w.dim() == 4 else to_host(w),
+                     "bf16", "fallback " + name)
+    del x, b, c, y1, y2
 
 
 def test_noalloc_in_a_captured_graph(swr):
