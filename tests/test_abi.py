@@ -15,6 +15,11 @@ BF16, F32 = swr.SWR_DTYPE_BF16, swr.SWR_DTYPE_F32
 OK, E_NULL, E_SHAPE, E_DTYPE, E_BLOCK, E_ALIGN, E_ALIAS, E_UNSUP, E_HIP, E_VER, E_SCRATCH = (
     0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10)
 
+# Where a GPU is visible, a call that passes validation with the fake
+# addresses below would launch kernels on them: such calls are skipped there.
+NO_GPU = not os.path.exists("/dev/kfd")
+reaches_launch = pytest.mark.skipif(not NO_GPU, reason="fake device addresses would reach a kernel launch")
+
 # Fake, well-aligned "device" addresses far apart: validation never dereferences them.
 GB = 1 << 30
 X, A, B_, C, Y, DY, DX, DA, DB, DC, V = (GB * (i + 1) for i in range(11))
@@ -94,6 +99,7 @@ def test_shape_validation(kw, code):
     assert fwd(p) == code and bwd(p) == code and car(p) == code
 
 
+@reaches_launch
 @pytest.mark.parametrize("D", [48, 80, 96, 112, 144, 160, 192, 208, 240, 256])
 @pytest.mark.parametrize("per_channel", [False, True])
 def test_any_multiple_of_16_up_to_256(D, per_channel):
@@ -154,6 +160,7 @@ def test_null_pointers_backward(which):
     assert bwd(problem(), *ptrs) == E_NULL
 
 
+@reaches_launch
 @pytest.mark.parametrize("kw", [dict(), dict(D=128, block=128), dict(dtype=F32, per_channel=True),
                                 dict(D=16, block=16, T=1000)])
 def test_backward_without_carriers_passes_validation(kw):
@@ -412,7 +419,8 @@ def test_exact_forward_noalloc_validation():
     # HIP runtime, which this machine lacks)
     mid = problem(B=16, T=16384, H=16, D=128, block=128)
     assert swr.swr_exact_workspace_bytes(mid) > swr.SWR_NOALLOC_SCRATCH_BYTES
-    assert nfwd(mid) in (OK, E_HIP)
+    if NO_GPU:
+        assert nfwd(mid) in (OK, E_HIP)
     assert "SWR_NOALLOC_SCRATCH_BYTES" in swr.swr_error_string(E_SCRATCH)
     # the headline shape fits
     assert swr.swr_exact_workspace_bytes(problem(B=8, T=16384, H=16, D=128, block=128)) <= 32 << 20
