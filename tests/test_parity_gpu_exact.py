@@ -174,9 +174,11 @@ def test_exact_residual_and_featurisation(swr, dtype):
 
 
 @pytest.mark.parametrize("value", [0.0, 1.0])
-def test_exact_decay_closed_forms(swr, value):
-    # a == 0: y = c*b*x (h0 forgotten at once); a == 1: a running sum from h0.
-    prob = W.random_problem(43, 1, 300, 2, 64, 64, "f32")
+@pytest.mark.parametrize("T", [300, 5000])
+def test_exact_decay_closed_forms(swr, value, T):
+    # a == 0: y = c*b*x (h0 forgotten at once); a == 1: a running sum from h0
+    # (T = 5000: 40 chunks, so the one-pass forward chains through boundaries)
+    prob = W.random_problem(43, 1, T, 2, 64, 64, "f32")
     prob.a[...] = value
     rng = np.random.default_rng(2)
     h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
