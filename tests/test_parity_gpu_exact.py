@@ -440,3 +440,25 @@ def test_exact_forward_chained_per_channel_featurised_residual(swr):
     feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
     y, v, hl, _ = run_exact(swr, prob, h0, None, residual=True, backward=False, **feat)
     check_exact(prob, h0, None, y, v, hl, None, residual=True, what="chained pc residual+sigmoid", **feat)
+
+
+def test_exact_forward_many_chained_sequences(swr):
+    # 512 sequences of 18 chunks (9216 chunks, several per workgroup): repeated
+    # calls agree bit for bit, and sampled sequences match the oracle
+    prob = W.random_problem(121, 16, 2200, 32, 64, 64, "bf16", "sigmoid", 3.0, with_dy=False)
+    x, a, b, c = (to_device(getattr(prob, n), "bf16") for n in "xabc")
+    h0 = _state(np.random.default_rng(17), prob.cfg)
+    h0_t = torch.from_numpy(h0).cuda()
+    first = swr.swr_exact_forward(x, a, b, c, 64, h0=h0_t, save_carriers=True, want_h_last=True)
+    for _ in range(2):
+        again = swr.swr_exact_forward(x, a, b, c, 64, h0=h0_t, save_carriers=True, want_h_last=True)
+        torch.cuda.synchronize()
+        for name, u, w in zip(("y", "carriers", "h_last"), again, first):
+            assert torch.equal(u, w), name
+    y = to_host(first[0])
+    hl = to_host(first[2])
+    for bi, hi in ((0, 0), (15, 31), (7, 13), (3, 30)):
+        sl = lambda t: t[bi:bi + 1, :, hi:hi + 1]
+        ref_y, ref_hl = oracle.exact_forward(sl(prob.x), sl(prob.a), sl(prob.b), sl(prob.c), h0[bi:bi + 1, hi:hi + 1])
+        assert_close(sl(y), ref_y, "bf16", f"many chains y ({bi}, {hi})")
+        assert_close(hl[bi:bi + 1, hi:hi + 1], ref_hl, "bf16", f"many chains h_last ({bi}, {hi})")
