@@ -496,11 +496,27 @@ bool use_chain_bwd(const swr_problem_t* p, const Resolved& r) {
     return !cw.pcp && cw.hs == 0 && cw.cpl <= 4 && cw.nch >= 256;
 }
 
+// The one-pass forward of bf16 heads of 64 channels taken two at a time
+// (16-byte lane slices): the per-channel layout over the pairs' 128 channels.
+int64_t chain_pair_floats(const swr_problem_t* p) {
+    const int64_t ct = swr::chain_tokens();
+    const int64_t n = p->B * (p->H / 2) * ((p->T + ct - 1) / ct);
+    return 16 + (n + 3) / 4 * 4 + 3 * n * 128;
+}
+// Whether the problem's shape and strides let heads run in pairs (the
+// pointers are checked where there are any: resolve_for).
+bool shape_pairs(const swr_problem_t* p) {
+    Resolved t;
+    return resolve(p, &t, true, true) == SWR_OK && t.pair && !t.empty && t.hv < ((int64_t)1 << 30);
+}
+
 // Workspace of the exact calls for one plan: the three-stage arrays (the
 // backward's, and the forward's when it does not run in one pass) or the
 // one-pass forward's, whichever is larger.
 int64_t exact_ws_floats(const swr_problem_t* p, const Resolved& r) {
-    return std::max(exact_ws(p, r).floats, use_chain(p, r) ? chain_ws(p, r).floats : (int64_t)0);
+    int64_t f = std::max(exact_ws(p, r).floats, use_chain(p, r) ? chain_ws(p, r).floats : (int64_t)0);
+    if (use_chain(p, r) && !r.pc && shape_pairs(p)) f = std::max(f, chain_pair_floats(p));
+    return f;
 }
 
 // Pointers into the workspace for one launch.
@@ -544,9 +560,16 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     if (!r.natural) return SWR_ERR_UNSUPPORTED;
     const ExactWs w = exact_ws(p, r);
     // the library's static array may hold the three stages' arrays but not the
-    // one pass's: the allocation-free call then runs the three stages
-    const bool chain = use_chain(p, r) && (!scratch || chain_ws(p, r).floats * 4 <= scratch_bytes);
-    const int64_t wfloats = chain ? chain_ws(p, r).floats : w.floats;
+    // one pass's: the allocation-free call then runs the three stages.  bf16
+    // heads of 64 channels run in pairs where the pointers and strides allow.
+#ifndef SWR_EXACT_CHAIN_PAIR
+#define SWR_EXACT_CHAIN_PAIR 1
+#endif
+    Resolved rp;
+    const bool pair = SWR_EXACT_CHAIN_PAIR && use_chain(p, r) && !r.pc && resolve_for(p, &rp, {x, b, c, (const void*)y}, true) == SWR_OK &&
+                      rp.pair && (!scratch || chain_pair_floats(p) * 4 <= scratch_bytes);
+    const bool chain = !pair && use_chain(p, r) && (!scratch || chain_ws(p, r).floats * 4 <= scratch_bytes);
+    const int64_t wfloats = pair ? chain_pair_floats(p) : chain ? chain_ws(p, r).floats : w.floats;
     const int64_t seqs = p->B * p->H, sbytes = seqs * p->D * 4;
     if (seqs == 0) return SWR_OK;
     if (!r.empty && (!x || !a || !b || !c || !y)) return SWR_ERR_NULL;
@@ -577,6 +600,21 @@ int swr::exact_forward_impl(const swr_problem_t* p, const void* x, const void* a
     }
 
     if (scratch && wfloats > 0 && !(workspace = scratch(stream))) return SWR_ERR_HIP;
+    if (pair) {   // one pass, heads of 64 channels two at a time
+        const int64_t nch = (p->T + swr::chain_tokens() - 1) / swr::chain_tokens();
+        const int64_t n = p->B * (p->H / 2) * nch;
+        float* f = (float*)workspace;
+        swr::Params k = make_params(p, r, false);
+        k.x = x; k.a = a; k.b = b; k.c = c; k.y = y; k.carriers = carriers; k.h0 = h0; k.h_last = h_last;
+        k.chain_ctr = (int32_t*)f;
+        k.chain_flags = (int32_t*)(f + 16);
+        k.agg_p = f + 16 + (n + 3) / 4 * 4;
+        k.agg_v = k.agg_p + n * 128;
+        k.chain_incl = k.agg_v + n * 128;
+        k.nruns = nch;
+        k.nwork = std::min<int64_t>(n, 512);   // two workgroups a compute unit
+        return swr::launch_chain_forward_pair(k, stream) == hipSuccess ? SWR_OK : SWR_ERR_HIP;
+    }
     if (chain && chain_ws(p, r).pcp) {   // one pass, a decay per channel
         const ChainWs cw = chain_ws(p, r);
         float* f = (float*)workspace;

@@ -83,6 +83,11 @@ constexpr bool chain_w_in_lds() { return (CPL == 8 || CPL == 4) && IO::ES == 2; 
 template <class IO, int CPL>
 constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL == 8 ? 4 : 6) : 1; }
 
+// How a chunk's decay product is kept: one value a chunk (a decay per head),
+// one per lane column (heads taken two at a time: lanes n < 8 and n >= 8
+// belong to different heads), or one per channel (a decay per channel).
+enum ChainP { kPChunk, kPLane, kPChannel };
+
 // Wave 0's part in the chain for chunk ci of a sequence (chunks slot0 ...
 // slot0 + nch - 1 of the workspace arrays, in chain order): publish the
 // chunk's aggregate (V, P), wait for the last boundary's inclusive value and
@@ -91,15 +96,17 @@ constexpr int chain_waves_per_simd() { return chain_w_in_lds<IO, CPL>() ? (CPL =
 // are applied to the boundary value in order), and at a boundary publish the
 // chunk's own inclusive value.  `in` is the value entering the chain's first
 // chunk (this lane's slice at in + n * CPL; NULL for zero).  Returns the
-// value entering the chunk and the one leaving it (I = P in + V).  PCP: the
-// decay product P is per channel (agg_p holds D values a chunk), else one
-// value a chunk.
-template <int CPL, int Q, int QB, bool PCP>
+// value entering the chunk and the one leaving it (I = P in + V).  P holds
+// CPL values with kPChannel, else one.
+template <int CPL, int Q, int QB, int PM>
 __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, int64_t nch, const float (&V)[CPL],
-                                  const float (&P)[PCP ? CPL : 1], const float* in, int lane, int grp, int n,
-                                  float (&pre)[CPL], float (&I)[CPL]) {
-    constexpr int D = CPL * SB, K = 4 * Q, NP = PCP ? CPL : 1, PD = PCP ? D : 1;
+                                  const float (&P)[PM == kPChannel ? CPL : 1], const float* in, int lane, int grp,
+                                  int n, float (&pre)[CPL], float (&I)[CPL]) {
+    constexpr int D = CPL * SB, K = 4 * Q;
+    constexpr int NP = PM == kPChannel ? CPL : 1;                      // values a lane keeps
+    constexpr int PD = PM == kPChannel ? D : PM == kPLane ? SB : 1;    // values a chunk stores
     const uint32_t vch = (uint32_t)(n * CPL);
+    const uint32_t pch = PM == kPChannel ? vch : PM == kPLane ? (uint32_t)n : 0u;   // this lane's first
     const int64_t slot = slot0 + ci;
     const bool boundary = ci % K == K - 1;
     // the last boundary chunk before this one (or none), and the chunks in between
@@ -109,12 +116,12 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
         if (grp == 0) {
 #pragma unroll
             for (int m = 0; m < CPL; ++m) put_coherent(p.agg_v + slot * D + vch + m, V[m]);
-            if constexpr (PCP) {
+            if constexpr (PM != kPChunk) {
 #pragma unroll
-                for (int m = 0; m < CPL; ++m) put_coherent(p.agg_p + slot * D + vch + m, P[m]);
+                for (int m = 0; m < NP; ++m) put_coherent(p.agg_p + slot * PD + pch + m, P[m]);
             }
         }
-        if (!PCP && lane == 0) put_coherent(p.agg_p + slot, P[0]);
+        if (PM == kPChunk && lane == 0) put_coherent(p.agg_p + slot, P[0]);
         writes_complete();
         if (lane == 0) put_flag(p.chain_flags + slot, kFlagAgg);
     }
@@ -154,14 +161,14 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
                 const int i = grp * Q + q0 + q;
                 const int64_t j = kb + 1 + i;
                 rv[q].template load<kCoherent>(rav, in_range(i < cnt, (uint32_t)(j * D + vch) * 4u));
-                rp[q].template load<kCoherent>(rap, in_range(i < cnt, (uint32_t)(j * PD + (PCP ? vch : 0u)) * 4u));
+                rp[q].template load<kCoherent>(rap, in_range(i < cnt, (uint32_t)(j * PD + pch) * 4u));
             }
 #pragma unroll
             for (int q = 0; q < QB; ++q) {
                 const bool live = grp * Q + q0 + q < cnt;
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) {
-                    const float pq = live ? rp[q].get(PCP ? m : 0) : 1.0f;
+                    const float pq = live ? rp[q].get(NP > 1 ? m : 0) : 1.0f;
                     gV[m] = __builtin_fmaf(pq, gV[m], rv[q].get(m));
                 }
 #pragma unroll
@@ -187,14 +194,14 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
 #pragma unroll
         for (int m = 0; m < NP; ++m) pg[m] = __shfl(gP[m], src);
 #pragma unroll
-        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg[PCP ? m : 0], pre[m], __shfl(gV[m], src));
+        for (int m = 0; m < CPL; ++m) pre[m] = __builtin_fmaf(pg[NP > 1 ? m : 0], pre[m], __shfl(gV[m], src));
     }
     if (timed_out) {
 #pragma unroll
         for (int m = 0; m < CPL; ++m) pre[m] = __builtin_nanf("");
     }
 #pragma unroll
-    for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P[PCP ? m : 0], pre[m], V[m]);
+    for (int m = 0; m < CPL; ++m) I[m] = __builtin_fmaf(P[NP > 1 ? m : 0], pre[m], V[m]);
     if (boundary && ci + 1 < nch) {
         if (grp == 0) {
 #pragma unroll
@@ -313,7 +320,7 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
             const uint32_t vch = (uint32_t)(n * CPL);
             float pre[CPL], I[CPL];
             const float Pv[1] = {P};
-            chain_link<CPL, Q, QB, false>(p, seq * nch, ch, nch, V, Pv, p.h0 ? p.h0 + rseq * DH + coff : nullptr,
+            chain_link<CPL, Q, QB, kPChunk>(p, seq * nch, ch, nch, V, Pv, p.h0 ? p.h0 + rseq * DH + coff : nullptr,
                                           lane, grp, n, pre, I);
             if (grp == 0) {
 #pragma unroll
@@ -370,6 +377,174 @@ __global__ __launch_bounds__(kChainTW * 64, (chain_waves_per_simd<IO, CPL>())) v
             for (int m = 0; m < CPL; ++m) v[m] = __builtin_fmaf(dk.c, e[m], s_wl[tw][n * CPL + m]);
             store_row<IoF32, CPL>(rsrc(p.carriers + (rseq * p.nblocks * DH + coff)),
                                   in_range(grp == 0 && blk < p.nblocks, (uint32_t)(blk * DH + n * CPL) * 4u), v);
+        }
+        ticket = grab();
+    }
+}
+
+// The exact forward in one pass for bf16 heads of 64 channels taken two at a
+// time (adjacent heads h, h+1 of an even head count): lanes n < 8 hold
+// head h's channels and n >= 8 head h+1's, so that every lane moves a
+// 16-byte row slice, as in the jagged window's paired forward.  Each head
+// has its own decay operator (two MFMA solves, each lane keeping its head's
+// result) and decay products; the chain runs over the pair with a decay
+// product per channel.  The local solutions wait for the look-back in LDS
+// (two workgroups a compute unit).
+template <bool FEAT, int Q>
+__global__ __launch_bounds__(kChainTW * 64, 4) void swr_fwd_chain_pair_kernel(Params p) {
+    using IO = IoBf16;
+    constexpr int CPL = 8;
+    constexpr int TW = kChainTW;
+    constexpr int TOK = kChainTok;
+    constexpr int D = CPL * SB;   // the pair's 128 channels
+    constexpr int DH = D / 2;     // channels of one head
+    constexpr int ES = IO::ES;
+    using RW = Row<IO, CPL>;
+    const int sig_a = FEAT ? p.sig_a : 0, sig_b = FEAT ? p.sig_b : 0;
+    __shared__ float s_wl[TW][D];   // last row of each sub-block's local solve
+    __shared__ float s_c[TW][2];    // decay product of each sub-block, per head
+    __shared__ float s_pre[D];      // the exact state entering the chunk
+    __shared__ f32x4 s_W[TW][CPL][64];
+    __shared__ int64_t s_ticket[2];
+
+    const Lanes ln = lanes();
+    const int lane = ln.lane, tw = ln.wv, grp = ln.grp, n = ln.n;
+    const int hsel = n >> 3;   // this lane's head of the pair
+    const int64_t HP = p.H / 2, S = p.B * HP, nch = p.nruns, N = S * nch;
+    const int64_t rs = p.sx_t * ES, as = p.sa_t * ES;
+    const uint32_t loff = (uint32_t)(4 * grp) * (uint32_t)rs + (uint32_t)(hsel * p.sx_h * ES) +
+                          (uint32_t)((n & 7) * CPL * ES);
+    const uint32_t aoff = (uint32_t)n * (uint32_t)as;
+    const uint32_t vch = (uint32_t)(n * CPL);   // this lane's slice of the pair's [2][64] states
+    const int smask = p.block / SB - 1;
+
+    int par = 0;
+    auto grab = [&]() {
+        if (threadIdx.x == 0) s_ticket[par] = atomicAdd(p.chain_ctr, 1);
+        lds_barrier();
+        const int64_t t = s_ticket[par];
+        par ^= 1;
+        return t;
+    };
+    int64_t ticket = grab();
+    for (;;) {
+        if (ticket >= N) break;
+        const int64_t seq = ticket % S, ch = ticket / S;   // chunk-major: earlier chunks first
+        const int64_t bi = seq / HP, h0 = 2 * (seq % HP);  // the pair's first head
+        const int64_t xo = (bi * p.sx_b + h0 * p.sx_h) * ES;
+        const int64_t t0 = ch * TOK, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+
+        // ---- the sub-block's local solves, one operator per head ----------------------
+        RW xr[4], br[4], cr[4];
+        {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs),
+                                         rb = rsrc((const char*)p.b + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
+                xr[r].template load<kFwdLoad>(rx, o);
+                br[r].template load<kFwdLoad>(rb, o);
+            }
+        }
+        const bool a_ok = r0 + n < p.T;
+        const char* ab = (const char*)p.a + (bi * p.sa_b + h0 * p.sa_h) * ES + r0 * as;
+        float a_n = load_scalar<IO, kFwdDecay>(rsrc(ab), in_range(a_ok, aoff));
+        float a_n1 = load_scalar<IO, kFwdDecay>(rsrc(ab + p.sa_h * ES), in_range(a_ok, aoff));
+        if (sig_a) { a_n = sigmoid(a_n); a_n1 = sigmoid(a_n1); }
+        if (!a_ok) { a_n = 1.0f; a_n1 = 1.0f; }   // past the sequence's end the state is carried unchanged
+        const Decay dk = build_decay(a_n, grp, n), dk1 = build_decay(a_n1, grp, n);
+        float Gl[4];   // this lane's head's prefix products at its rows
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Gl[r] = hsel ? dk1.G[r] : dk.G[r];
+        const float cl = hsel ? dk1.c : dk.c;
+        {
+            const typename Contract<IO>::A A = Contract<IO>::prep(dk.L), A1 = Contract<IO>::prep(dk1.L);
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                float u[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) u[q] = xr[q].get(m) * pregate(br[q].get(m), sig_b);
+                const f32x4 W0 = Contract<IO>::run(A, u), W1 = Contract<IO>::run(A1, u);
+                const f32x4 W = hsel ? W1 : W0;   // each lane keeps its own head's result
+                if (grp == 3) s_wl[tw][vch + m] = W[3];
+                s_W[tw][m][lane] = W;             // (read back by the same lane)
+            }
+        }
+        if (lane == 63) { s_c[tw][0] = dk.c; s_c[tw][1] = dk1.c; }
+        {   // c is needed for the outputs only: its loads land during the look-back
+            const __amdgpu_buffer_rsrc_t rc = rsrc((const char*)p.c + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                cr[r].template load<kFwdLoad>(rc, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)));
+        }
+        lds_barrier();
+
+        // ---- wave 0: the chunk's aggregate, the look-back, the inclusive state -----
+        if (tw == 0) {
+            float V[CPL], P = 1.0f;
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) V[m] = 0.f;
+#pragma unroll 1
+            for (int r = 0; r < TW; ++r) {
+                const float c_ = s_c[r][hsel];
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) V[m] = __builtin_fmaf(c_, V[m], s_wl[r][vch + m]);
+                P *= c_;
+            }
+            const float Pv[1] = {P};
+            float pre[CPL], I[CPL];
+            const int64_t so = (bi * p.H + h0) * DH;   // the pair's two [64] state rows, adjacent
+            chain_link<CPL, Q, 2, kPLane>(p, seq * nch, ch, nch, V, Pv, p.h0 ? p.h0 + so : nullptr, lane, grp, n,
+                                          pre, I);
+            if (grp == 0) {
+#pragma unroll
+                for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
+            }
+            store_row<IoF32, CPL>(rsrc(p.h_last ? p.h_last + so : p.chain_incl),
+                                  in_range(p.h_last && ch == nch - 1 && grp == 0, vch * 4u), I);
+        }
+        lds_barrier();
+
+        // ---- outputs: the state entering this wave's sub-block, y, block carriers -----
+        float e[CPL];
+#pragma unroll
+        for (int m = 0; m < CPL; ++m) e[m] = s_pre[vch + m];
+#pragma unroll 1
+        for (int r = 0; r < tw; ++r) {
+            const float c_ = s_c[r][hsel];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) e[m] = __builtin_fmaf(c_, e[m], s_wl[r][vch + m]);
+        }
+        const __amdgpu_buffer_rsrc_t ry = rsrc((char*)p.y + xo + r0 * rs);
+        RW xres[4];   // the residual's x, loaded again rather than kept through the look-back
+        {
+            const __amdgpu_buffer_rsrc_t rx = rsrc((const char*)p.x + xo + r0 * rs);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                xres[r].template load<kFwdLoad>(rx, in_range(p.residual && tr0 + r < p.T, loff + (uint32_t)(r * rs)));
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float yv[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) {
+                const f32x4 W = s_W[tw][m][lane];
+                yv[m] = cr[r].get(m) * __builtin_fmaf(Gl[r], e[m], W[r]);
+                if (p.residual) yv[m] += xres[r].get(m);
+            }
+            store_row<IO, CPL, kFwdStore>(ry, in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs)), yv);
+        }
+        // the exact state at the end of a block that ends with this sub-block
+        // (a block longer than a chunk that the sequence's end cuts short ends in the last chunk)
+        if (p.carriers && (((ch * TW + tw) & smask) == smask || (ch == nch - 1 && tw == TW - 1))) {
+            const int64_t blk = r0 >> p.lshift;
+            float v[CPL];
+#pragma unroll
+            for (int m = 0; m < CPL; ++m) v[m] = __builtin_fmaf(cl, e[m], s_wl[tw][vch + m]);
+            // each head's rows [nblocks][64]; this lane's head's, then its block's, slice
+            store_row<IoF32, CPL>(rsrc(p.carriers + (bi * p.H + h0) * p.nblocks * DH),
+                                  in_range(grp == 0 && blk < p.nblocks,
+                                           (uint32_t)((hsel * p.nblocks + blk) * DH + (n & 7) * CPL) * 4u), v);
         }
         ticket = grab();
     }
@@ -495,8 +670,8 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 2)) void swr_fwd_cha
             }
             float pre[CPL], I[CPL];
             const int64_t so = hb * geo.Dr + geo.coff;   // the virtual head's slice of [B][H][D] states
-            chain_link<CPL, Q, 2, true>(p, seq * nch, ch, nch, V, P, p.h0 ? p.h0 + so : nullptr, lane, grp, n, pre,
-                                        I);
+            chain_link<CPL, Q, 2, kPChannel>(p, seq * nch, ch, nch, V, P, p.h0 ? p.h0 + so : nullptr, lane, grp, n,
+                                             pre, I);
             if (grp == 0) {
 #pragma unroll
                 for (int m = 0; m < CPL; ++m) s_pre[vch + m] = pre[m];
@@ -692,7 +867,7 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
             }
             float pre[CPL], I[CPL];
             const float Pv[1] = {P};
-            chain_link<CPL, Q, 4, false>(p, seq * nch, ci, nch, V, Pv, p.dh_last ? p.dh_last + seq * D : nullptr,
+            chain_link<CPL, Q, 4, kPChunk>(p, seq * nch, ci, nch, V, Pv, p.dh_last ? p.dh_last + seq * D : nullptr,
                                          lane, grp, n, pre, I);
             if (grp == 0) {
 #pragma unroll
@@ -805,6 +980,16 @@ hipError_t launch_chain_io(const Params& p, int cpl, hipStream_t st) {
     }
 }
 
+template <int Q>
+hipError_t launch_chain_pair_q(const Params& p, hipStream_t st) {
+    const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
+    if (p.sig_a || p.sig_b)
+        hipLaunchKernelGGL((swr_fwd_chain_pair_kernel<true, Q>), grid, block, 0, st, p);
+    else
+        hipLaunchKernelGGL((swr_fwd_chain_pair_kernel<false, Q>), grid, block, 0, st, p);
+    return hipGetLastError();
+}
+
 template <class IO, int CPL, int PK, int Q>
 hipError_t launch_chain_pc_q(const Params& p, hipStream_t st) {
     const dim3 grid((unsigned)p.nwork), block(kChainTW * 64);
@@ -875,6 +1060,14 @@ hipError_t launch_chain_forward_pc(const Params& p, int dtype, int cpl, void* st
     hipError_t e = reset_chain(p, st, n);
     if (e != hipSuccess || n == 0) return e;
     return dtype == 1 ? launch_chain_pc_io<IoBf16>(p, cpl, st) : launch_chain_pc_io<IoF32>(p, cpl, st);
+}
+
+hipError_t launch_chain_forward_pair(const Params& p, void* stream) {
+    const hipStream_t st = (hipStream_t)stream;
+    const int64_t n = p.B * (p.H / 2) * p.nruns;
+    hipError_t e = reset_chain(p, st, n);
+    if (e != hipSuccess || n == 0) return e;
+    return p.nruns < kLongChain ? launch_chain_pair_q<2>(p, st) : launch_chain_pair_q<4>(p, st);
 }
 
 hipError_t launch_chain_backward(const Params& p, int dtype, int cpl, void* stream) {

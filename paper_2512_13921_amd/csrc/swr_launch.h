@@ -191,6 +191,9 @@ hipError_t launch_scan(const ScanParams& q, void* stream);
 // persistent workgroups; the workspace arrays of p are reset first.
 int chain_tokens();
 hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void* stream);
+// The same for bf16 heads of 64 channels taken two at a time (H even; the
+// pair's chain uses the per-channel workspace layout with 128 channels).
+hipError_t launch_chain_forward_pair(const Params& p, void* stream);
 // The same with a decay per channel (virtual heads of 16 * cpl channels).
 hipError_t launch_chain_forward_pc(const Params& p, int dtype, int cpl, void* stream);
 // The exact recurrence's backward in one pass over the same chunks, taken

@@ -88,6 +88,12 @@ hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void*) {
     return hipErrorNoDevice;
 }
 
+hipError_t launch_chain_forward_pair(const Params& p, void*) {
+    require(p.H % 2 == 0 && p.nruns == (p.T + 127) / 128 && p.nwork >= 1, "pairs and chunks");
+    require(p.chain_flags && p.chain_ctr && p.chain_incl && p.agg_v && p.agg_p, "workspace arrays");
+    return hipErrorNoDevice;
+}
+
 hipError_t launch_chain_forward_pc(const Params& p, int dtype, int cpl, void*) {
     require(dtype == SWR_DTYPE_F32 || dtype == SWR_DTYPE_BF16, "dtype");
     require(cpl == 1 || cpl == 2 || cpl == 4, "channels per lane");

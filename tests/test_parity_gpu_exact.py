@@ -462,3 +462,21 @@ def test_exact_forward_many_chained_sequences(swr):
         ref_y, ref_hl = oracle.exact_forward(sl(prob.x), sl(prob.a), sl(prob.b), sl(prob.c), h0[bi:bi + 1, hi:hi + 1])
         assert_close(sl(y), ref_y, "bf16", f"many chains y ({bi}, {hi})")
         assert_close(hl[bi:bi + 1, hi:hi + 1], ref_hl, "bf16", f"many chains h_last ({bi}, {hi})")
+
+
+@pytest.mark.parametrize("layout", ["bthd", "bhtd"])
+def test_exact_forward_paired_heads(swr, layout):
+    # bf16 heads of 64 channels run two at a time in the one-pass forward
+    # (lanes 0-7 one head, 8-15 the other), with the fused sigmoids, the
+    # residual and h0, in both layouts, on sequences of more than 16 chunks
+    prob = W.random_problem(131, 2, 2300, 4, 64, 64, "bf16", "sigmoid", 3.0, logits=True)
+    feat = dict(sigmoid_decay=True, sigmoid_pregate=True)
+    x, a, b, c = (to_device(getattr(prob, n), "bf16") for n in "xabc")
+    if layout == "bhtd":
+        x, a, b, c = (_bhtd(t) for t in (x, a, b, c))
+    h0 = _state(np.random.default_rng(19), prob.cfg)
+    _say(f"[exact paired] 2x2300x4x64 l64 {layout}")
+    y, v, hl = swr.swr_exact_forward(x, a, b, c, 64, h0=torch.from_numpy(h0).cuda(), residual=True,
+                                     save_carriers=True, want_h_last=True, **feat)
+    torch.cuda.synchronize()
+    check_exact(prob, h0, None, y, v, hl, None, residual=True, what=f"paired {layout}", **feat)
