@@ -36,10 +36,11 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
 
 # Kernels that must compile without register spills: the forward sweeps copy
 # their next tiles straight into LDS, and a forward instantiation that spilled
-# was once measured writing wrong outputs; the one-pass exact forward is held
-# to a register cap (two or three workgroups a compute unit) that a spill
-# would silently turn into scratch traffic.  The build refuses any such spill.
-NO_SPILL = ("swr_fwd_kernel", "swr_fwd_chain_kernel")
+# was once measured writing wrong outputs; the one-pass exact forwards are
+# held to register caps (two or three workgroups a compute unit) that a
+# spill would silently turn into scratch traffic.  The build refuses any such
+# spill.
+NO_SPILL = ("swr_fwd_kernel", "swr_fwd_chain_kernel", "swr_fwd_chain_pair_kernel", "swr_fwd_chain_pc_kernel")
 NO_SPILL_SOURCES = ("swr_kernels.hip", "swr_chain.hip")
 RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
 
