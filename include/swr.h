@@ -201,8 +201,7 @@ int swr_abi_version(void);
  * composing the published aggregates of the chunks before it (a look-back
  * between workgroups in a fixed pattern, so that repeated calls give the same
  * bits): it reads every input once.  The backward does the same, from each
- * sequence's end, for heads of up to 64 channels on sequences of 256 chunks
- * (32768 tokens) or more.
+ * sequence's end, for heads of up to 64 channels (one decay per head).
  *
  * Everything in swr_problem_t keeps its meaning except that `block` only sets
  * the length of the exact block carriers; every flag applies (with

@@ -482,18 +482,17 @@ bool use_chain(const swr_problem_t* p, const Resolved& r) {
     return SWR_EXACT_CHAIN && !r.empty && r.pack == 1 && chain_ws(p, r).n < ((int64_t)1 << 30);
 }
 
-// The backward in one pass, for heads of up to 64 channels on sequences of
-// 256 chunks or more, where it measured faster than the three stages (B1
-// T131072 H32 d64: 1047 -> 1000 us); on shorter sequences (B16 T8192 H32
-// d64: 957 -> 970 us) and with 128 channels (983 -> 1208 us: one workgroup a
-// compute unit, whose look-back nothing covers) it is slower.
+// The backward in one pass, for heads of up to 64 channels, where it
+// measured faster than the three stages (B1 T131072 H32 d64: 1047 -> 928 us;
+// B16 T8192 H32 d64: 960 -> 895 us); with 128 channels it is slower (983 ->
+// 1208 us: one workgroup a compute unit, whose look-back nothing covers).
 #ifndef SWR_EXACT_CHAIN_BWD
 #define SWR_EXACT_CHAIN_BWD 1
 #endif
 bool use_chain_bwd(const swr_problem_t* p, const Resolved& r) {
     if (!SWR_EXACT_CHAIN_BWD || !use_chain(p, r)) return false;
     const ChainWs cw = chain_ws(p, r);
-    return !cw.pcp && cw.hs == 0 && cw.cpl <= 4 && cw.nch >= 256;
+    return !cw.pcp && cw.hs == 0 && cw.cpl <= 4;
 }
 
 // The one-pass forward of bf16 heads of 64 channels taken two at a time

@@ -1,6 +1,6 @@
 // swr_chain.hip -- the exact (untruncated) recurrence in one pass: the
-// forward (a decay per head or per channel), and the backward on long
-// sequences of small heads.
+// forward (a decay per head or per channel), and the backward for heads of
+// up to 64 channels.
 //
 // The three-stage evaluation of the hierarchical decomposition (Alg.
 // "Hierarchical Block Parallel Inference": local solves, the carrier
@@ -783,6 +783,11 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
         const int64_t xo = (seq / p.H * p.sx_b + seq % p.H * p.sx_h) * ES;
         const int64_t ao = seq / p.H * p.sa_b + seq % p.H * p.sa_h;
         const int64_t t0 = ch * TOK, r0 = t0 + tw * SB, tr0 = r0 + 4 * grp;
+        // the rows' offsets, recomputed every chunk (an add each) rather than
+        // kept across the loop, which spilled registers: an empty asm hides
+        // that lo equals loff
+        uint32_t lo = loff, dao = daoff, ao_ = aoff;
+        asm volatile("" : "+v"(lo), "+v"(dao), "+v"(ao_));
 
         // ---- loads -------------------------------------------------------------------
         RW xr[4], br[4], cr[4], dyr[4];
@@ -793,7 +798,7 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
                                          rdy = rsrc((const char*)p.dy + xo + r0 * rs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const uint32_t o = in_range(tr0 + r < p.T, loff + (uint32_t)(r * rs));
+                const uint32_t o = in_range(tr0 + r < p.T, lo + (uint32_t)(r * rs));
                 xr[r].template load<kBwdLoad>(rx, o);
                 br[r].template load<kBwdLoad>(rb, o);
                 cr[r].template load<kBwdLoad>(rc, o);
@@ -801,7 +806,7 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
             }
         }
         const bool a_ok = r0 + n < p.T;
-        float a_n = load_scalar<IO, kBwdDecay>(rsrc((const char*)p.a + ao * ES + r0 * as), in_range(a_ok, aoff));
+        float a_n = load_scalar<IO, kBwdDecay>(rsrc((const char*)p.a + ao * ES + r0 * as), in_range(a_ok, ao_));
         float ds_n = 1.0f;   // d a / d(input) of token n: 1, or sigma'(z) for a logit z
         if (sig_a) {
             const SigSlope g = sigmoid_slope(a_n);
@@ -933,12 +938,12 @@ __global__ __launch_bounds__(kChainTW * 64, (CPL == 4 ? 4 : 1)) void swr_bwd_cha
             }
             const float tot = row_sum(acc) * shfl(ds_n, base + 4 * grp + r);
             const bool ok = tr0 + r < p.T;
-            const uint32_t o = in_range(ok, loff + (uint32_t)(r * rs));
+            const uint32_t o = in_range(ok, lo + (uint32_t)(r * rs));
             store_row<IO, CPL, kBwdStore>(rdx, o, vdx);
             store_row<IO, CPL, kBwdStore>(rdb, o, vdb);
             store_row<IO, CPL, kBwdStore>(rdc, o, vdc);
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, tot), rda,
-                                                  (int)in_range(n == 0 && ok, daoff + (uint32_t)(r * das)), 0,
+                                                  (int)in_range(n == 0 && ok, dao + (uint32_t)(r * das)), 0,
                                                   kBwdStore);
         }
         ticket = grab();

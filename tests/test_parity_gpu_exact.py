@@ -385,9 +385,9 @@ def test_exact_in_a_captured_graph(swr):
 @pytest.mark.parametrize("B,T,H,D,block,dtype", [(1, 40000, 2, 64, 128, "bf16"), (1, 33000, 1, 32, 32, "f32"),
                                                  (1, 32768, 1, 16, 16, "bf16")])
 def test_exact_backward_one_pass_long_sequences(swr, B, T, H, D, block, dtype):
-    # sequences of 256 chunks or more: the backward runs in one pass (chunks
-    # taken from the end, chained by the look-back); against the oracle, and
-    # repeated calls agree bit for bit
+    # long sequences (256 chunks and more) through the one-pass backward
+    # (chunks taken from the end, chained by the look-back): against the
+    # oracle, and repeated calls agree bit for bit
     prob = W.random_problem(101 + D, B, T, H, D, block, dtype, "sigmoid", 4.0)
     rng = np.random.default_rng(D)
     h0, dhl = _state(rng, prob.cfg), _state(rng, prob.cfg)
