@@ -190,6 +190,10 @@ __global__ __launch_bounds__(TW * HW * 64, 3) void swr_fwd_kernel(Params p) {
         const __amdgpu_buffer_rsrc_t ry = rsrc(yb + r0 * rs);
         RW xr[4], br[4], cr[4];
         if constexpr (PREFETCH) {
+            // The copies into the slot have landed: an explicit wait rather than
+            // the compiler's own tracking of copies into LDS, which was seen to
+            // let a read of such a tile go ahead of them in another kernel.
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 LR::read(s_tile[wv][0][r], lane, xr[r].w);
