@@ -201,7 +201,13 @@ int swr_abi_version(void);
  * composing the published aggregates of the chunks before it (a look-back
  * between workgroups in a fixed pattern, so that repeated calls give the same
  * bits): it reads every input once.  The backward does the same, from each
- * sequence's end, for heads of up to 64 channels (one decay per head).
+ * sequence's end, for heads of up to 64 channels (one decay per head).  A
+ * chunk waits only for chunks that are already running, and gives up after
+ * 65536 polls (never expected): it then adds one to the workspace's second
+ * 32-bit integer and continues from NaN, so that every output depending on
+ * it is NaN rather than a plausible value.  The environment variable
+ * SWR_CHAIN_SPIN_LIMIT (read at every call, 0 to 65535) lowers that limit,
+ * to exercise this path; it cannot raise it.
  *
  * Everything in swr_problem_t keeps its meaning except that `block` only sets
  * the length of the exact block carriers; every flag applies (with
@@ -213,7 +219,9 @@ int swr_abi_version(void);
  * Workspace: swr_exact_workspace_bytes(problem) bytes of device memory
  * (16-byte aligned, owned by the caller, needing no initialisation; it may be
  * NULL when that size is 0).  Its contents are scratch and are overwritten;
- * two calls in flight at once need two workspaces.
+ * two calls in flight at once need two workspaces.  After a one-pass call's
+ * work has completed, its second 32-bit integer holds the number of waits
+ * that gave up (see above; 0 in every correct run).
  * ------------------------------------------------------------------------ */
 
 /* Bytes of workspace swr_exact_forward / swr_exact_backward need for this

@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <initializer_list>
 
 #include "../../include/swr.h"
@@ -237,6 +238,21 @@ Span span(const void* p, int64_t bytes) { return {(uintptr_t)p, (uintptr_t)p + (
 
 bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
 
+// Polls a chunk of the one-pass exact recurrence makes before it gives up
+// waiting for an earlier chunk's publication: 2^16, unless the environment
+// variable SWR_CHAIN_SPIN_LIMIT (read at every call) lowers it, so that tests
+// can force the time-out path; it can never raise it.
+int32_t chain_spin_limit() {
+    constexpr long kDefault = 1L << 16;
+    const char* s = std::getenv("SWR_CHAIN_SPIN_LIMIT");
+    if (s && *s) {
+        char* end = nullptr;
+        const long v = std::strtol(s, &end, 10);
+        if (*end == '\0' && v >= 0 && v < kDefault) return (int32_t)v;
+    }
+    return (int32_t)kDefault;
+}
+
 swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward) {
     swr::Params k{};
     k.B = p->B; k.T = p->T; k.H = p->H;
@@ -256,6 +272,7 @@ swr::Params make_params(const swr_problem_t* p, const Resolved& r, bool backward
     k.nruns = backward ? r.nruns : r.nruns_f;
     k.nwork = backward ? r.nwork : r.nwork_f;
     k.nblocks = r.nblocks;
+    k.spin_limit = chain_spin_limit();
     return k;
 }
 

@@ -21,10 +21,10 @@
 //
 // Chunks are handed out in order by a ticket counter (chunk-major over the
 // sequences), so a chunk only ever waits for chunks of lower tickets, whose
-// workgroups are already running.  A wait is bounded: past kSpinLimit polls
-// the chunk counts the time-out and proceeds from a NaN state, so that a lost
-// publication (never expected) shows in every output that depends on it
-// instead of passing as a plausible value.
+// workgroups are already running.  A wait is bounded: past p.spin_limit polls
+// (2^16 unless the host lowers it) the chunk counts the time-out and proceeds
+// from a NaN state, so that a lost publication (never expected) shows in
+// every output that depends on it instead of passing as a plausible value.
 //
 // Publication uses device-coherent (agent-scope) stores, and a wait for
 // their completion before the flag that announces them; readers load the flag
@@ -55,7 +55,6 @@ template <int CPL, bool WL>
 constexpr int chain_qb() { return WL && CPL <= 4 ? 2 : 4; }
 // device-coherent (sc1) vector loads of published values
 constexpr int kCoherent = 16;
-constexpr int kSpinLimit = 1 << 16;
 
 __device__ inline void put_coherent(float* p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -137,7 +136,7 @@ __device__ inline void chain_link(const Params& p, int64_t slot0, int64_t ci, in
         else if (lane == 63 && kb >= 0)
             ok = get_flag(p.chain_flags + slot0 + kb) == kFlagIncl;
         if (__all(ok)) break;
-        if (++spins > kSpinLimit) {   // never expected: count it, poison the outputs
+        if (++spins > p.spin_limit) {   // never expected: count it, poison the outputs
             if (lane == 0) atomicAdd(p.chain_ctr + 1, 1);
             timed_out = true;
             break;

@@ -68,6 +68,7 @@ struct Params {
     // the chunks in order (nruns = chunks per sequence).
     int32_t* chain_flags;   // [B*Hv][nchunks]
     int32_t* chain_ctr;     // [2]: next ticket, look-back time-outs
+    int32_t spin_limit;     // polls before a look-back wait gives up
     float* chain_incl;      // [B*Hv][nchunks][dv]
     float* h_last;          // [B][H][D] or NULL
     // Exact backward in one pass: the gradient entering the final state, and

@@ -480,3 +480,60 @@ def test_exact_forward_paired_heads(swr, layout):
                                      save_carriers=True, want_h_last=True, **feat)
     torch.cuda.synchronize()
     check_exact(prob, h0, None, y, v, hl, None, residual=True, what=f"paired {layout}", **feat)
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_exact_one_pass_time_out_path(swr, monkeypatch, D):
+    # The look-back's failure path, forced from the host: with
+    # SWR_CHAIN_SPIN_LIMIT=0 a chunk gives up at its first poll that finds a
+    # publication missing.  Every kernel still ends; each wait that gave up is
+    # counted in the workspace's second int32, and the outputs that depend on
+    # it are NaN; every finite output equals the normal call's bit for bit;
+    # the next call with the default limit counts nothing and gives the
+    # normal results.  Two long sequences (128 chunks each, one workgroup per
+    # chunk), so that chunks are waiting while their predecessors compute.
+    # d = 64 runs the paired-head forward and the one-pass backward.
+    prob = W.random_problem(131 + D, 1, 128 * 128, 2, D, 128, "bf16", "sigmoid", 3.0)
+    x, a, b, c, dy = (to_device(getattr(prob, n), "bf16") for n in ("x", "a", "b", "c", "dy"))
+    ws = torch.zeros(8 << 20, dtype=torch.int32, device="cuda")
+
+    def forward():
+        out = swr.swr_exact_forward(x, a, b, c, 128, save_carriers=True, want_h_last=True, workspace=ws)
+        torch.cuda.synchronize()
+        return out, int(ws[1].item())
+
+    def backward(v):
+        out = swr.swr_exact_backward(x, a, b, c, dy, v, 128, workspace=ws)
+        torch.cuda.synchronize()
+        return out, int(ws[1].item())
+
+    def check(name, got, ref, count):
+        for i, (u, w) in enumerate(zip(got, ref)):
+            fin = torch.isfinite(u)
+            assert torch.equal(u[fin], w[fin]), (name, i)
+            if count == 0:
+                assert bool(fin.all()), (name, i)
+
+    _say(f"[exact time-out path] D={D} normal")
+    ref_f, n0 = forward()
+    assert n0 == 0
+    ref_b, n0 = backward(ref_f[1]) if D <= 64 else (None, 0)
+    assert n0 == 0
+    monkeypatch.setenv("SWR_CHAIN_SPIN_LIMIT", "0")
+    _say(f"[exact time-out path] D={D} spin limit 0")
+    got_f, nf = forward()
+    _say(f"[exact time-out path] forward waits given up: {nf}")
+    check("forward", got_f, ref_f, nf)
+    if nf > 0:
+        assert not bool(torch.isfinite(got_f[0]).all())
+    if D <= 64:
+        got_b, nb = backward(ref_f[1])
+        _say(f"[exact time-out path] backward waits given up: {nb}")
+        check("backward", got_b, ref_b, nb)
+        if nb > 0:
+            assert not bool(torch.isfinite(got_b[0]).all())
+    monkeypatch.delenv("SWR_CHAIN_SPIN_LIMIT")
+    again_f, n1 = forward()
+    assert n1 == 0
+    for u, w in zip(again_f, ref_f):
+        assert torch.equal(u, w)
