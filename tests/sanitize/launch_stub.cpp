@@ -35,6 +35,14 @@ void check_params(const swr::Params& p, int D) {
     require(p.Hv >= 1, "virtual heads");
 }
 
+// The one-pass chains' poll limit: never above its default of 2^16.  A test
+// states the value it expects through SWR_STUB_EXPECT_SPIN_LIMIT.
+void check_spin_limit(const swr::Params& p) {
+    require(p.spin_limit >= 0 && p.spin_limit <= 65536, "look-back poll limit");
+    const char* want = getenv("SWR_STUB_EXPECT_SPIN_LIMIT");
+    if (want && *want) require(p.spin_limit == atoi(want), "look-back poll limit not the expected one");
+}
+
 }  // namespace
 
 namespace swr {
@@ -85,12 +93,14 @@ hipError_t launch_chain_forward(const Params& p, int dtype, int cpl, void*) {
     require(cpl == 1 || cpl == 2 || cpl == 4 || cpl == 8, "channels per lane");
     require(p.nruns == (p.T + 127) / 128 && p.nwork >= 1, "chunks");
     require(p.chain_flags && p.chain_ctr && p.chain_incl && p.agg_v && p.agg_p, "workspace arrays");
+    check_spin_limit(p);
     return hipErrorNoDevice;
 }
 
 hipError_t launch_chain_forward_pair(const Params& p, void*) {
     require(p.H % 2 == 0 && p.nruns == (p.T + 127) / 128 && p.nwork >= 1, "pairs and chunks");
     require(p.chain_flags && p.chain_ctr && p.chain_incl && p.agg_v && p.agg_p, "workspace arrays");
+    check_spin_limit(p);
     return hipErrorNoDevice;
 }
 
@@ -100,6 +110,7 @@ hipError_t launch_chain_forward_pc(const Params& p, int dtype, int cpl, void*) {
     require(p.hshift == 0 || cpl == 4, "virtual heads");
     require(p.nruns == (p.T + 127) / 128 && p.nwork >= 1, "chunks");
     require(p.chain_flags && p.chain_ctr && p.chain_incl && p.agg_v && p.agg_p, "workspace arrays");
+    check_spin_limit(p);
     return hipErrorNoDevice;
 }
 
@@ -108,6 +119,7 @@ hipError_t launch_chain_backward(const Params& p, int dtype, int cpl, void*) {
     require(cpl == 1 || cpl == 2 || cpl == 4 || cpl == 8, "channels per lane");
     require(p.nruns == (p.T + 127) / 128 && p.nwork >= 1, "chunks");
     require(p.chain_flags && p.chain_ctr && p.chain_incl && p.agg_v && p.agg_p, "workspace arrays");
+    check_spin_limit(p);
     return hipErrorNoDevice;
 }
 
